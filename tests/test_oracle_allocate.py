@@ -1,0 +1,181 @@
+"""Pins of the oracle's tree-aware allocation (Eq. 2, Eq. 3, KKT view, Alg. 2).
+
+* brute force over the global scale alpha: Eq. 2 and Eq. 3 evaluated literally
+  (clip, floor, min/max) in exact rational arithmetic at every breakpoint,
+  keeping the largest alpha whose total fits the budget;
+* Alg. 2's Pressure loop run literally, one token at a time, lowest priority
+  first (with the termination fix: nodes at their minimum are skipped);
+* the KKT closed form of the relaxed program, solved by a root finder;
+* invariants: budget conservation, active-path protection, floors, caps,
+  maximality, monotonicity in the budget.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy.optimize import brentq
+
+from oracle import arbor_oracle as O
+from paper_2605_22106_amd import synth
+
+BASE = dict(alpha_max=math.inf, gamma=2.0, lambda_d=0.1, lambda_delta=0.5, eta=0.8,
+            r_min=0.05, k_min=2, l_tail=3)
+
+
+def weight(s, d, delta, p):
+    return float(np.float64(p["eta"]) * np.power(np.float64(s), p["gamma"])
+                 * np.exp(-p["lambda_d"] * d) * np.exp(-p["lambda_delta"] * delta))
+
+
+def brute_force(parent, n_full, n_kept, active, budget, s, p):
+    V = len(parent)
+    d, on_path, delta = O.geometry(parent, active)     # geometry is pinned separately
+    off = [i for i in range(V) if not on_path[i]]
+    b_off = budget - sum(n_full[i] for i in range(V) if on_path[i])
+    W = {i: Fraction(weight(s[i], d[i], delta[i], p)) for i in off}
+    rmin = Fraction(p["r_min"])
+
+    def keep(i, alpha):
+        r = min(Fraction(1), max(rmin, alpha * W[i]))
+        kk = max(p["k_min"], min(p["l_tail"], n_full[i]), math.floor(r * n_full[i]))
+        return min(n_kept[i], min(n_full[i], kk))
+
+    cands = [Fraction(0)]
+    for i in off:
+        if W[i] > 0:
+            cands += [Fraction(j) / (W[i] * n_full[i]) for j in range(1, n_full[i] + 1)]
+    if math.isfinite(p["alpha_max"]):
+        amax = Fraction(p["alpha_max"])
+        cands = [a for a in cands if a <= amax] + [amax]
+    best = None
+    for a in sorted(set(cands)):
+        tot = sum(keep(i, a) for i in off)
+        if tot <= b_off:
+            best = a
+    k = np.zeros(V, dtype=np.int64)
+    for i in range(V):
+        k[i] = n_full[i] if on_path[i] else 0
+    if best is not None:
+        for i in off:
+            k[i] = keep(i, best)
+        return k, O.OK
+    # Pressure (Alg. 2): floors first, then lower the lowest-priority node by one
+    for i in off:
+        k[i] = keep(i, Fraction(0))
+    prio = {i: weight(s[i], d[i], delta[i], p) for i in off}
+    while sum(k[i] for i in off) > b_off:
+        movable = [i for i in off if k[i] > min(p["k_min"], n_kept[i])]
+        if not movable:
+            return k, O.OVER_BUDGET
+        j = min(movable, key=lambda i: (prio[i], i))
+        k[j] = max(min(p["k_min"], n_kept[j]), k[j] - 1)
+    return k, O.OK
+
+
+def random_case(seed, V=12, max_n=14):
+    rng = np.random.default_rng(seed)
+    parent, n_full = synth.random_tree(V, max_n, seed, min_tokens=1)
+    n_kept = [int(rng.integers(0, n + 1)) if rng.random() < 0.4 else n for n in n_full]
+    leaves = [i for i in range(V) if i not in parent]
+    active = sorted(rng.choice(leaves, size=min(2, len(leaves)), replace=False).tolist())
+    s = rng.random(V).astype(np.float32)
+    s[rng.integers(0, V)] = 0.0
+    return parent, n_full, n_kept, active, s
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_allocate_matches_brute_force(seed):
+    parent, n_full, n_kept, active, s = random_case(seed)
+    p = dict(BASE)
+    if seed % 4 == 1:
+        p["alpha_max"] = 0.7
+    if seed % 4 == 2:
+        p.update(gamma=1.0, lambda_d=-0.2)
+    total = sum(n_full)
+    for rho in (0.2, 0.45, 0.7, 1.0):
+        budget = int(rho * total)
+        k, delta, on_path, status = O.allocate(parent, n_full, n_kept, active, budget, s, p)
+        kb, sb = brute_force(parent, n_full, n_kept, active, budget, s, p)
+        assert status == sb
+        assert k.tolist() == kb.tolist(), (rho, k, kb)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_allocate_invariants(seed):
+    parent, n_full, n_kept, active, s = random_case(seed + 100, V=20, max_n=30)
+    p = dict(BASE)
+    V = len(parent)
+    prev = None
+    for rho in np.linspace(0.1, 1.0, 10):
+        budget = int(rho * sum(n_full))
+        k, delta, on_path, status = O.allocate(parent, n_full, n_kept, active, budget, s, p)
+        path = [i for i in range(V) if on_path[i]]
+        for i in path:
+            assert k[i] == n_full[i]                               # invariant (i)
+        for i in range(V):
+            if not on_path[i]:
+                assert k[i] <= n_kept[i]                            # no re-growth off-path
+                assert k[i] >= min(p["k_min"], n_kept[i])           # invariant (ii)
+        if status == O.OK:
+            assert k.sum() <= budget
+        floors = {i: O.floor_count(n_full[i], n_kept[i], p) for i in range(V) if not on_path[i]}
+        if sum(floors.values()) <= budget - sum(n_full[i] for i in path):
+            assert status == O.OK
+            for i, f in floors.items():
+                assert k[i] >= f                                  # Eq. 3 floors hold
+        if prev is not None and status == O.OK:
+            assert np.all(k >= prev)                                # monotone in budget
+        prev = k if status == O.OK else None
+
+
+def test_allocate_maximality():
+    """No single extra tie group of prices fits: the next breakpoint overflows."""
+    parent, n_full = synth.complete_tree(3, 2, 40, 25)
+    rng = np.random.default_rng(3)
+    s = rng.random(len(parent)).astype(np.float32)
+    p = dict(BASE)
+    for budget in range(120, 400, 17):          # path 90 + floors 30 and up
+        k, _, on_path, st = O.allocate(parent, n_full, n_full, [4], budget, s, p)
+        assert st == O.OK and k.sum() <= budget
+        kb, _ = brute_force(parent, n_full, n_full, [4], budget, s, p)
+        assert k.tolist() == kb.tolist()
+
+
+def test_kkt_relaxed_solution():
+    """K_min = L_tail = r_min = 0 and long blocks: Eq. 2-3 at the budget-meeting
+    alpha reproduce the capped KKT allocation k_i = min(n_i, W_i / lambda) of the
+    relaxed program with weights W_i = w_i n_i, up to the floor."""
+    parent, n_full = synth.complete_tree(4, 2, 3000, 2000)
+    rng = np.random.default_rng(7)
+    s = (0.2 + 0.8 * rng.random(len(parent))).astype(np.float32)
+    p = dict(BASE, k_min=0, l_tail=0, r_min=0.0)
+    active = [5]
+    d, on_path, delta = O.geometry(parent, active)
+    budget = 3000 + 2000 * 2 + 9000
+    k, _, _, st = O.allocate(parent, n_full, n_full, active, budget, s, p)
+    assert st == O.OK
+    off = [i for i in range(len(parent)) if not on_path[i]]
+    Wt = np.array([weight(s[i], d[i], delta[i], p) * n_full[i] for i in off])
+    n = np.array([n_full[i] for i in off], dtype=np.float64)
+    b_off = budget - (3000 + 4000)
+    lam = brentq(lambda x: np.minimum(n, Wt / x).sum() - b_off, 1e-9, 1e9)
+    kstar = np.minimum(n, Wt / lam)
+    got = np.array([k[i] for i in off], dtype=np.float64)
+    # the discrete alpha is at least the relaxed one (floor(W/lambda) fits) ...
+    assert np.all(got >= np.floor(kstar) - 1e-9)
+    assert b_off - len(off) <= got.sum() <= b_off
+    # ... and one scalar alpha explains every count: got_i <= alpha W_i < got_i + 1
+    assert np.max(got / Wt) < np.min((got + 1) / Wt)
+
+
+def test_tiny_config_is_over_budget():
+    """The tiny configuration's path alone fills a 50 % budget."""
+    cfg = synth.CONFIGS["tiny"]
+    parent, n_full = synth.complete_tree(2, 2, 64, 32)
+    s = np.full(7, 0.5, np.float32)
+    k, delta, on_path, st = O.allocate(parent, n_full, n_full, [3], 128, s, cfg.params)
+    assert st == O.OVER_BUDGET
+    assert on_path.tolist() == [1, 1, 0, 1, 0, 0, 0]
+    assert k.tolist() == [64, 32, 2, 32, 2, 2, 2]
+    assert delta.tolist() == [2, 1, 3, 0, 2, 4, 4]
