@@ -1,0 +1,267 @@
+/*
+ * arbor.h -- C ABI of a gfx950 (MI355X) library for structure-aware KV eviction
+ * in Tree-of-Thoughts decoding, after ArborKV (arxiv 2605.22106).
+ *
+ * The library implements the data-parallel hot path of the method:
+ *   arbor_score             MSVE block score (Sec. 4): accumulated attention A_i(t)
+ *                           of later tokens, block attention a_i, s_i.
+ *   arbor_allocate          TAE keep-counts (Eq. 2, Eq. 3) under a global budget
+ *                           (KKT view of Sec. 4; Transition/Pressure of Alg. 2).
+ *   arbor_select            tail + heavy-hitter retained set per block (Sec. 4
+ *                           Execution; Alg. 1 Evict).
+ *   arbor_compact           token-extractive, order-preserving compaction of the
+ *                           retained K/V inside a paged tree KV pool (Sec. 4).
+ *   arbor_rehydrate         lazy rehydration of Path* blocks (Sec. 4; Alg. 2).
+ *   arbor_tree_decode_attn  decode attention of each active leaf over its
+ *                           ancestor chain (Sec. 1 and Sec. 3: the next step
+ *                           depends only on the chain).
+ *
+ * Conventions
+ *  - Every pointer is a DEVICE pointer unless marked (host) or (pinned host).
+ *    Struct arguments themselves are host memory, read during the call only.
+ *  - Every call enqueues work on `stream` and returns without synchronising.
+ *    The C return value reports host-side argument validation and launch
+ *    failures.  Outcomes that depend on device data are written to the device
+ *    int32 *status (read it after synchronising the stream).
+ *  - *status is sticky: a call does nothing on the device when *status < 0 on
+ *    entry, writes a negative code on error and ARBOR_OVER_BUDGET (1) as a
+ *    warning only over ARBOR_OK.  The caller zeroes it at the start of a
+ *    sequence of calls (one policy event).
+ *  - On any negative status every piece of pool/tree state (n_kept, page_table,
+ *    slot_pos, free_stack, free_top, K/V bytes of retained tokens) is unchanged;
+ *    pure outputs (k_out, sel_pos, out, ...) are then unspecified.
+ *  - The library allocates no memory.  The caller owns every buffer, including
+ *    the scratch `workspace` of `workspace_bytes` bytes (at least
+ *    arbor_workspace_size()).  Calls on distinct buffers are independent;
+ *    calls that share a workspace must be ordered (same stream).
+ *  - Node ids satisfy parent[0] = -1 and 0 <= parent[i] < i (creation order;
+ *    BFS order qualifies).  Depth of any node <= ARBOR_MAX_DEPTH.
+ *  - Positions are node-local: position p of node i is token a_i + p of the
+ *    paper's span x_{a_i:b_i}.  Per-token arrays (A, sel_pos) are indexed by
+ *    tok_off[i] + p.
+ */
+#ifndef ARBOR_H
+#define ARBOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARBOR_MAX_DEPTH 63
+
+typedef enum {
+  ARBOR_OK = 0,
+  ARBOR_OVER_BUDGET = 1,    /* warning: even the minimum counts exceed the budget  */
+  ARBOR_EINVAL = -1,        /* bad argument or malformed tree/selection            */
+  ARBOR_ENOPAGES = -2,      /* rehydration needs more pages than are free          */
+  ARBOR_EHIP = -3,          /* a HIP launch failed                                 */
+  ARBOR_EUNSUPPORTED = -4,  /* shape outside what the kernels implement            */
+  ARBOR_ENONFINITE = -5,    /* NaN in A or s                                       */
+  ARBOR_EWORKSPACE = -6,    /* workspace too small for this tree                   */
+  ARBOR_ECORRUPT = -7       /* pool bookkeeping inconsistent (free stack overflow) */
+} arbor_status_t;
+
+typedef enum { ARBOR_BF16 = 0, ARBOR_F32 = 1 } arbor_dtype_t;
+
+typedef enum { ARBOR_SELECT_TAIL_HEAVY = 0, ARBOR_SELECT_TAIL_ONLY = 1 } arbor_select_mode_t;
+
+/* (host) Shape of the KV pool.  head_dim in {64, 128}; page_size a multiple of
+ * 16 and at most 256; q_per_kv = G query heads share one KV head (query head h
+ * reads KV head h / G). */
+typedef struct {
+  int32_t num_layers;
+  int32_t num_kv_heads;
+  int32_t q_per_kv;
+  int32_t head_dim;
+  int32_t page_size;
+  int32_t dtype;            /* arbor_dtype_t of K, V, q_win and decode q */
+  int64_t num_pages;
+} arbor_geom_t;
+
+/* (host struct of device pointers) The thought tree T = (V, E) of Sec. 3. */
+typedef struct {
+  int32_t num_nodes;         /* V                                                 */
+  int64_t num_tokens;        /* N = tok_off[V]                                    */
+  const int32_t *parent;     /* [V]  parent[0] = -1                               */
+  const int32_t *n_full;     /* [V]  n_i = b_i - a_i + 1                          */
+  const int64_t *tok_off;    /* [V+1] prefix sum of n_full                        */
+  const int64_t *page_off;   /* [V+1] prefix sum of ceil(n_full / page_size)      */
+  int32_t *n_kept;           /* [V]  c_i, resident tokens (in/out)                */
+  int32_t *page_table;       /* [page_off[V]] physical page of logical page q of
+                                node i at page_off[i] + q; -1 = unused (in/out)   */
+} arbor_tree_t;
+
+/* (host struct of device pointers) The paged tree KV pool.  Slot s of node i
+ * lives in page page_table[page_off[i] + s / P] at row s % P; the resident
+ * slots of a node hold strictly increasing positions. */
+typedef struct {
+  void *k;                   /* [L][num_pages][Hkv][P][head_dim] dtype            */
+  void *v;                   /* same layout                                      */
+  int32_t *slot_pos;         /* [num_pages][P] position held by a slot, -1 empty  */
+  int32_t *free_stack;       /* [num_pages] free pages in [0, *free_top)          */
+  int32_t *free_top;         /* [1] number of free pages; the top is free_top-1   */
+} arbor_pool_t;
+
+/* (host) Parameter bundle of Alg. 1 / Alg. 2.  The paper prints no values. */
+typedef struct {
+  double alpha_max;          /* upper bound of the global scale alpha (Eq. 2); +inf
+                                means alpha is set by the budget alone (KKT view)   */
+  double gamma;              /* importance exponent (Eq. 2)                         */
+  double lambda_d;           /* depth decay (Eq. 2)                                 */
+  double lambda_delta;       /* distance-to-active-leaf decay (Eq. 2)               */
+  double eta;                /* off-path discount, 0 < eta <= 1 (Eq. 2)             */
+  double r_min;              /* ratio floor (Eq. 2)                                 */
+  int32_t k_min;             /* per-block minimum K_min (invariant (ii), Eq. 3)     */
+  int32_t l_tail;            /* tail window L_tail (Eq. 3, Sec. 4 Execution)        */
+  float theta[3];            /* MSVE weights on phi = [v, u, a]                     */
+  float softmax_scale;       /* score attention scale; <= 0 means 1/sqrt(head_dim)  */
+  int32_t select_mode;       /* arbor_select_mode_t                                 */
+  int32_t score_self_window; /* 0: credit proper ancestors only (u > b_i);
+                                1: also an observer's own earlier tokens            */
+} arbor_params_t;
+
+/* (host) Upper bounds used to size the workspace. */
+typedef struct {
+  int32_t num_nodes;         /* V                                                 */
+  int64_t num_tokens;        /* N                                                 */
+  int64_t max_context;       /* >= sum of n_full over any root-to-node chain      */
+  int32_t max_observers;     /* arbor_score: largest n_obs                        */
+  int32_t window;            /* arbor_score: W                                    */
+  int32_t n_slice;           /* arbor_score: slice layers per call                */
+  int32_t max_leaves;        /* arbor_tree_decode_attn: largest n_leaves          */
+  int32_t max_layers;        /* arbor_tree_decode_attn: largest layer_end-begin   */
+} arbor_sizes_t;
+
+/* Bytes of workspace that every call of the library needs for these bounds. */
+size_t arbor_workspace_size(const arbor_geom_t *geom, const arbor_sizes_t *sizes);
+
+/* Static text for a status code. */
+const char *arbor_strerror(int code);
+
+/*
+ * arbor_score -- MSVE scoring (Sec. 4 "Multi-Signal Value Estimation": the
+ * accumulated attention A_i(t) over a thin slice of layers and heads, the block
+ * attention a_i and s_i = clip(sigmoid(theta^T [v_i, u_i, a_i]), 0, 1);
+ * Alg. 1 MSVE).
+ *
+ * For each observer j = observers[o], slice layer slice_layers[s] and query
+ * head h, the window query of position u = n_j - w_j + t (t < w_j =
+ * min(window, n_j)) is q_win[o][s][h][t][:] (layout [n_obs][n_slice][Hq]
+ * [window][head_dim], dtype geom->dtype).  It attends (softmax, scale
+ * params->softmax_scale) over every resident token of j's proper ancestors and
+ * j's own resident tokens at positions <= u.  Its probability on each token of
+ * a proper ancestor of j (also on j's tokens p < u when score_self_window = 1)
+ * is added to A[tok_off[i] + p]; rows_seen[i] grows by the number of such rows
+ * that credited block i.  Then for every node
+ *   a_out[i] = sum_{p < n_i} A[tok_off[i] + p] / rows_seen[i]   (0 if never seen)
+ *   s_out[i] = clip(sigmoid(theta[0] v_in[i] + theta[1] u_in[i] + theta[2] a_out[i]), 0, 1).
+ * A is fp32 [N] (in/out), rows_seen int64 [V] (in/out), v_in/u_in/a_out/s_out
+ * fp32 [V].  slice_layers is a (host) array of n_slice (<= 8) layer ids.
+ * Results are bitwise reproducible run to run (no atomics in any sum).
+ * Errors: EINVAL (bad ids), EWORKSPACE, EUNSUPPORTED (page_size/head_dim).
+ */
+int arbor_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,
+                const int32_t *observers, int32_t n_obs, const void *q_win, int32_t window,
+                const int32_t *slice_layers, int32_t n_slice, const float *v_in,
+                const float *u_in, float *A, int64_t *rows_seen, float *a_out, float *s_out,
+                const arbor_params_t *params, int32_t *status, void *workspace,
+                size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * arbor_allocate -- tree-aware keep-counts (Eq. 2 and Eq. 3; the KKT view of
+ * Sec. 4; the Transition and Pressure branches of Alg. 2).
+ *
+ * Path* = union of the root-to-leaf chains of active[0 .. n_active) (device
+ * int32).  delta_out[i] = tree distance from i to the nearest active leaf,
+ * on_path_out[i] = 1 on Path* (uint8).  Path* nodes get k = n_i (invariant
+ * (i)).  Every other node i gets Eq. 3 at its Eq. 2 ratio
+ * r_i = clip(alpha w_i, r_min, 1), w_i = eta s_i^gamma e^{-lambda_d d_i}
+ * e^{-lambda_delta Delta_i}, capped at its resident count c_i (off-path blocks
+ * are only ever lowered), where alpha is the largest value <= alpha_max whose
+ * total fits budget_tokens.  Token j of block i is kept when
+ * alpha >= j / (w_i n_i) (its price, fp64); equal prices enter together.  If
+ * the Eq. 3 floors already exceed the budget (Pressure) blocks are lowered
+ * towards min(K_min, c_i) in ascending w_i (ties: lower id); if that is not
+ * enough *status gets ARBOR_OVER_BUDGET and k_out holds the lowered counts.
+ * s is fp32 [V] in [0, 1]; k_out int32 [V].  fp64 arithmetic, no contraction.
+ * Errors: EINVAL (malformed tree, bad leaf ids, n_active < 1), ENONFINITE (NaN s).
+ */
+int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_active,
+                   int64_t budget_tokens, const float *s, const arbor_params_t *params,
+                   int32_t *k_out, int32_t *delta_out, uint8_t *on_path_out, int32_t *status,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * arbor_select -- retained set of every block whose count drops (Sec. 4
+ * Execution: mandatory tail T_i and heavy hitters H_i by A_i(t), tail first on
+ * overlap; Alg. 1 Evict).
+ *
+ * For every node with k[i] < c_i: tail = resident positions >= n_i - L_tail.
+ * If k[i] <= |tail| or select_mode = TAIL_ONLY, the k[i] most recent resident
+ * positions are kept; otherwise the tail plus the k[i] - |tail| other resident
+ * positions with the largest A (fp32 compare, -0 == +0), ties to the lower
+ * position.  sel_pos[tok_off[i] + s] (s < k[i]) receives the kept positions in
+ * ascending order; entries of other nodes are not written.
+ * Errors: ENONFINITE (NaN in A over a changed block), EINVAL (k < 0).
+ */
+int arbor_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,
+                 const float *A, const int32_t *k, const arbor_params_t *params,
+                 int32_t *sel_pos, int32_t *status, hipStream_t stream);
+
+/*
+ * arbor_compact -- token-extractive compaction (Sec. 4 Execution: retained
+ * entries stay, the rest are freed).  For every node with k[i] < c_i, slot s
+ * (s < k[i]) afterwards holds position sel_pos[tok_off[i] + s], its K/V rows of
+ * every layer and KV head copied bitwise from the slot that held it (in place,
+ * order preserving).  The node keeps its first ceil(k[i]/P) pages; the rest go
+ * on the free stack in (node, page) order; vacated slots and freed pages get
+ * slot_pos = -1, unused page-table entries -1; n_kept[i] = k[i].
+ * Errors: EINVAL (selection not a strictly increasing subset of the resident
+ * positions), ECORRUPT (free stack would overflow).
+ */
+int arbor_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                  const int32_t *k, const int32_t *sel_pos, int32_t *status, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * arbor_rehydrate -- lazy rehydration (Sec. 4 "Lazy rehydration"; Alg. 2
+ * Transition): every node with on_path[i] != 0 and c_i < n_i is restored to
+ * full retention before the next decode step, in ascending id (root first).
+ * Its missing pages are popped from the top of the free stack in (node, page)
+ * order; afterwards slot p holds position p.  Resident rows move bitwise;
+ * evicted rows are copied bitwise from the token-span record host_k/host_v
+ * ((pinned host) or device, layout [N][L][Hkv][head_dim], dtype), read by the
+ * kernel over the host link.  Errors: ENOPAGES (checked before any change).
+ */
+int arbor_rehydrate(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                    const uint8_t *on_path, const void *host_k, const void *host_v,
+                    int32_t *status, void *workspace, size_t workspace_bytes,
+                    hipStream_t stream);
+
+/*
+ * arbor_tree_decode_attn -- decode attention of each active leaf over the
+ * resident tokens of its root-to-leaf chain (Sec. 1, Sec. 3).  For leaf
+ * leaves[b], layer l in [layer_begin, layer_end) and query head h:
+ *   out[b][l - layer_begin][h][:] = softmax(scale q K^T) V
+ * over every resident slot of every chain node (the leaf's newest token is the
+ * query's own position), q layout [n_leaves][Lr][Hq][head_dim] (dtype), out in
+ * out_dtype, lse_out [n_leaves][Lr][Hq] fp32 natural-log LSE (nullable).
+ * Each chain node is read once for all active leaves below it; partial results
+ * are merged per leaf root to leaf, so results are bitwise reproducible.
+ * Errors: EINVAL, EWORKSPACE, EUNSUPPORTED.
+ */
+int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
+                           const arbor_pool_t *pool, const int32_t *leaves, int32_t n_leaves,
+                           int32_t layer_begin, int32_t layer_end, const void *q, void *out,
+                           int32_t out_dtype, float *lse_out, float softmax_scale,
+                           int32_t *status, void *workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ARBOR_H */

@@ -1,0 +1,258 @@
+// arbor_compact: token-extractive, order-preserving compaction of the retained
+// K/V rows inside the paged tree KV pool (Sec. 4 Execution: retained entries
+// stay, the other entries are freed).
+//
+// Four launches on one stream:
+//   plan     one wave per node: validate the selection, locate each kept
+//            position's source slot, count the pages the node releases;
+//   scan     one workgroup: (node, page)-ordered free-stack offsets and the
+//            list of changed nodes;
+//   move     one wave per (changed node, layer, kv head) plane: rows move to
+//            lower slots only, so a wave stages a chunk of rows in registers
+//            (all loads of the chunk retire before its stores issue) and walks
+//            the chunks in ascending slot order -- in-place safe;
+//   finalize one wave per changed node: slot_pos, page table, free stack, c_i.
+#include "arbor_internal.h"
+
+namespace arbor {
+
+namespace {
+
+__device__ __forceinline__ int pos_at(const Tree &t, const Pool &pl, int64_t po, int s) {
+  const int page = t.page_table[po + s / pl.P];
+  return pl.slot_pos[(int64_t)page * pl.P + (s % pl.P)];
+}
+
+__global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32_t *__restrict__ k,
+                                                    const int32_t *__restrict__ sel_pos,
+                                                    int32_t *__restrict__ src_slot,
+                                                    int32_t *__restrict__ freed, int32_t *status) {
+  if (status_failed(status)) return;
+  const int lane = lane_id();
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= t.V) return;
+  const int c = t.n_kept[i];
+  const int ki = k[i];
+  if (ki >= c) {
+    if (lane == 0) freed[i] = 0;
+    return;
+  }
+  const int n = t.n_full[i];
+  const int64_t tb = t.tok_off[i];
+  const int64_t po = t.page_off[i];
+  bool bad = ki < 0;
+  for (int s = lane; s < ki; s += kWave) {
+    const int p = sel_pos[tb + s];
+    bad |= p < 0 || p >= n || (s > 0 && sel_pos[tb + s - 1] >= p);
+    // source slot: the resident positions ascend, and the kept ones are a
+    // subsequence, so the source of destination s lies in [s, c)
+    int lo = s, hi = c - 1, found = -1;
+    while (!bad && lo <= hi) {
+      const int mid = (lo + hi) >> 1;
+      const int pm = pos_at(t, pl, po, mid);
+      if (pm == p) {
+        found = mid;
+        break;
+      }
+      if (pm < p) lo = mid + 1;
+      else hi = mid - 1;
+    }
+    bad |= found < 0;
+    src_slot[tb + s] = found;
+  }
+  if (ballot(bad)) {
+    if (lane == 0) status_error(status, ARBOR_EINVAL);
+    return;
+  }
+  if (lane == 0) freed[i] = (c + pl.P - 1) / pl.P - (ki + pl.P - 1) / pl.P;
+}
+
+// meta[0] = number of changed nodes, meta[1] = free-stack top before pushes
+__global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int32_t *__restrict__ k,
+                                                     const int32_t *__restrict__ freed,
+                                                     int32_t *__restrict__ push_base,
+                                                     int32_t *__restrict__ changed,
+                                                     int32_t *__restrict__ meta, int32_t *status) {
+  __shared__ int64_t sm[17];
+  if (status_failed(status)) {
+    if (threadIdx.x == 0) meta[0] = 0;
+    return;
+  }
+  int64_t run_pages = 0, run_nodes = 0;
+  for (int base = 0; base < t.V; base += blockDim.x) {
+    const int i = base + threadIdx.x;
+    const bool in = i < t.V;
+    const bool ch = in && k[i] < t.n_kept[i];
+    const int64_t f = ch ? freed[i] : 0;
+    int64_t tot_p, tot_n;
+    const int64_t exp = block_exclusive_scan<int64_t>(f, sm, &tot_p);
+    const int64_t exn = block_exclusive_scan<int64_t>(ch ? 1 : 0, sm, &tot_n);
+    if (ch) {
+      push_base[i] = (int32_t)(run_pages + exp);
+      changed[run_nodes + exn] = i;
+    }
+    run_pages += tot_p;
+    run_nodes += tot_n;
+  }
+  if (threadIdx.x == 0) {
+    const int top = *pl.free_top;
+    if (top < 0 || (int64_t)top + run_pages > pl.num_pages) {
+      status_error(status, ARBOR_ECORRUPT);
+      meta[0] = 0;
+      return;
+    }
+    meta[0] = (int32_t)run_nodes;
+    meta[1] = top;
+    *pl.free_top = top + (int32_t)run_pages;
+  }
+}
+
+// Rows of one (layer, kv head) plane: LPR lanes per row, 16 bytes per lane.
+template <int LPR>
+__device__ void move_plane(const Tree &t, const Pool &pl, int i, int ki, int l, int g,
+                           const int32_t *__restrict__ src_slot, int lane) {
+  constexpr int RPP = kWave / LPR;   // rows per wave pass
+  constexpr int PASSES = 8;          // passes per chunk
+  constexpr int CH = RPP * PASSES;   // rows staged per chunk
+  const int64_t tb = t.tok_off[i];
+  const int64_t po = t.page_off[i];
+  // rows already in place form a prefix (src(s) = s); skip it
+  int s0 = ki;
+  for (int base = 0; base < ki; base += kWave) {
+    const int s = base + lane;
+    const uint64_t mv = ballot(s < ki && src_slot[tb + s] != s);
+    if (mv) {
+      s0 = base + __builtin_ctzll(mv);
+      break;
+    }
+  }
+  char *kb = static_cast<char *>(pl.k);
+  char *vb = static_cast<char *>(pl.v);
+  const int sub = lane % LPR;
+  const int rsel = lane / LPR;
+  for (int cbase = s0; cbase < ki; cbase += CH) {
+    uint4 kr[PASSES], vr[PASSES];
+    int64_t dst[PASSES];
+#pragma unroll
+    for (int ps = 0; ps < PASSES; ++ps) {
+      const int s = cbase + ps * RPP + rsel;
+      dst[ps] = -1;
+      if (s < ki) {
+        const int src = src_slot[tb + s];
+        const int64_t so = row_byte_offset(pl, l, t.page_table[po + src / pl.P], g, src % pl.P) +
+                           sub * 16;
+        kr[ps] = *reinterpret_cast<const uint4 *>(kb + so);
+        vr[ps] = *reinterpret_cast<const uint4 *>(vb + so);
+        dst[ps] = row_byte_offset(pl, l, t.page_table[po + s / pl.P], g, s % pl.P) + sub * 16;
+      }
+    }
+    // every lane's loads of this chunk have returned before any store below
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int ps = 0; ps < PASSES; ++ps) {
+      if (dst[ps] >= 0) {
+        *reinterpret_cast<uint4 *>(kb + dst[ps]) = kr[ps];
+        *reinterpret_cast<uint4 *>(vb + dst[ps]) = vr[ps];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+__global__ __launch_bounds__(256) void compact_move(Tree t, Pool pl, const int32_t *__restrict__ k,
+                                                    const int32_t *__restrict__ src_slot,
+                                                    const int32_t *__restrict__ changed,
+                                                    const int32_t *__restrict__ meta,
+                                                    int32_t *status) {
+  if (status_failed(status)) return;
+  const int lane = lane_id();
+  const int planes = pl.L * pl.Hkv;
+  const int64_t total = (int64_t)meta[0] * planes;
+  const int row_bytes = pl.D * pl.esize;
+  for (int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); w < total;
+       w += (int64_t)gridDim.x * 4) {
+    const int i = changed[w / planes];
+    const int rem = (int)(w % planes);
+    const int l = rem / pl.Hkv;
+    const int g = rem % pl.Hkv;
+    const int ki = k[i];
+    if (row_bytes == 128) move_plane<8>(t, pl, i, ki, l, g, src_slot, lane);
+    else if (row_bytes == 256) move_plane<16>(t, pl, i, ki, l, g, src_slot, lane);
+    else move_plane<32>(t, pl, i, ki, l, g, src_slot, lane);
+  }
+}
+
+__global__ __launch_bounds__(256) void compact_finalize(Tree t, Pool pl, const int32_t *__restrict__ k,
+                                                        const int32_t *__restrict__ sel_pos,
+                                                        const int32_t *__restrict__ push_base,
+                                                        const int32_t *__restrict__ changed,
+                                                        const int32_t *__restrict__ meta,
+                                                        int32_t *status) {
+  if (status_failed(status)) return;
+  const int lane = lane_id();
+  const int nch = meta[0];
+  const int top = meta[1];
+  const int P = pl.P;
+  for (int w = blockIdx.x * 4 + (threadIdx.x >> 6); w < nch; w += gridDim.x * 4) {
+    const int i = changed[w];
+    const int ki = k[i];
+    const int c = t.n_kept[i];
+    const int64_t tb = t.tok_off[i];
+    const int64_t po = t.page_off[i];
+    const int keep_pages = (ki + P - 1) / P;
+    const int old_pages = (c + P - 1) / P;
+    for (int s = lane; s < keep_pages * P; s += kWave) {
+      const int page = t.page_table[po + s / P];
+      pl.slot_pos[(int64_t)page * P + s % P] = s < ki ? sel_pos[tb + s] : -1;
+    }
+    const int nfree = old_pages - keep_pages;
+    for (int e = lane; e < nfree * P; e += kWave) {
+      const int q = keep_pages + e / P;
+      const int page = t.page_table[po + q];
+      pl.slot_pos[(int64_t)page * P + e % P] = -1;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int e = lane; e < nfree; e += kWave) {
+      const int q = keep_pages + e;
+      pl.free_stack[top + push_base[i] + e] = t.page_table[po + q];
+      t.page_table[po + q] = -1;
+    }
+    if (lane == 0) t.n_kept[i] = ki;
+  }
+}
+
+}  // namespace
+
+size_t compact_workspace(const arbor_sizes_t *sz) {
+  return (size_t)sz->num_tokens * 4 + (size_t)sz->num_nodes * 12 + 4096;
+}
+
+int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                   const int32_t *k, const int32_t *sel_pos, int32_t *status, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream) {
+  Tree t = make_tree(tree);
+  Pool pl = make_pool(geom, pool);
+  if (t.V <= 0) return ARBOR_OK;
+  Carve cv(workspace, workspace_bytes);
+  int32_t *src_slot = cv.take<int32_t>((size_t)t.N);
+  int32_t *freed = cv.take<int32_t>(t.V);
+  int32_t *push_base = cv.take<int32_t>(t.V);
+  int32_t *changed = cv.take<int32_t>(t.V);
+  int32_t *meta = cv.take<int32_t>(4);
+  if (!cv.ok) return ARBOR_EWORKSPACE;
+  const dim3 node_grid((t.V + 3) / 4);
+  hipLaunchKernelGGL(compact_plan, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos, src_slot,
+                     freed, status);
+  hipLaunchKernelGGL(compact_scan, dim3(1), dim3(1024), 0, stream, t, pl, k, freed, push_base,
+                     changed, meta, status);
+  const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
+  const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
+  hipLaunchKernelGGL(compact_move, dim3(move_blocks), dim3(256), 0, stream, t, pl, k, src_slot,
+                     changed, meta, status);
+  hipLaunchKernelGGL(compact_finalize, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos,
+                     push_base, changed, meta, status);
+  return hip_ok(hipGetLastError());
+}
+
+}  // namespace arbor
