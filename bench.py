@@ -1,0 +1,391 @@
+"""Benchmark of the ArborKV eviction hot path on one MI355X.
+
+One step = one eviction event on the Llama-3-8B-shaped synthetic tree (32
+layers, 8 KV heads, head_dim 128, bf16; root 1024 tokens, branching 4, depth 3,
+256 tokens per node; 4 active leaves; budget 25 % of all tokens):
+
+    arbor_score -> arbor_allocate -> arbor_select -> arbor_compact
+    -> arbor_tree_decode_attn (all 32 layers, the 4 active leaves)
+
+on inputs already resident in HBM.  Before every step the pristine pool and
+tree state are restored with an untimed device copy (which also flushes the
+256 MB last-level cache).  `value` is resident KV tokens per second of step
+time (tokens scored as keys, then kept or evicted, compacted, then decoded).
+
+Lazy rehydration reads the token-span record from pinned host memory, so its
+rate includes the host link; it is timed in the same run as a separate
+backtracking transition leg and reported under "rehydrate", never in `value`.
+
+Per-entry-point times come from HIP events recorded on the stream the kernels
+run on.  The CPU oracle is timed on a bounded sample of the same workload and
+reported as "cpu_baseline".
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2605_22106_amd import _lib as L  # noqa: E402
+from paper_2605_22106_amd import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+METRIC = "KV tokens scored+evicted+compacted/s; tree-decode attn HBM GB/s (% of peak)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="llama8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rehydrate-leg", action="store_true")
+    return ap.parse_args()
+
+
+class Event:
+    def __init__(self, kv, st, cfg):
+        self.kv = kv
+        self.st = st
+        self.cfg = cfg
+        V, N = kv.num_nodes, kv.num_tokens
+        dev = "cuda"
+        self.observers = st["observers"].to(dev)
+        self.q_win = st["q_win"].to(dev).contiguous()
+        self.v_sig = st["v_sig"].to(dev)
+        self.u_sig = st["u_sig"].to(dev)
+        self.A = torch.zeros(N, device=dev)
+        self.rows = torch.zeros(V, dtype=torch.int64, device=dev)
+        self.a = torch.empty(V, device=dev)
+        self.s = torch.empty(V, device=dev)
+        self.k = torch.empty(V, dtype=torch.int32, device=dev)
+        self.delta = torch.empty_like(self.k)
+        self.on_path = torch.empty(V, dtype=torch.uint8, device=dev)
+        self.sel = torch.empty(N, dtype=torch.int32, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.q_dec = st["q_dec"].to(dev).contiguous()
+        Hq = kv.kv_heads * kv.q_per_kv
+        self.out = torch.empty((st["active"].numel(), kv.layers, Hq, kv.head_dim),
+                               dtype=torch.bfloat16, device=dev)
+        self.lse = torch.empty((st["active"].numel(), kv.layers, Hq), device=dev)
+        chain_max = max(sum(int(st["n_full"][a]) for a in _chain(st["parent"].tolist(), j))
+                        for j in range(V))
+        nbytes = L.arbor_workspace_size(kv, max_context=chain_max,
+                                        max_observers=self.observers.numel(),
+                                        window=st["window"], n_slice=len(st["slice_layers"]),
+                                        max_leaves=64, max_layers=kv.layers)
+        self.ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self.params = dict(st["params"])
+
+    def check(self, rc):
+        if rc != L.OK:
+            raise RuntimeError(f"arbor call failed on the host: {L.arbor_strerror(rc)}")
+
+    def reset_scores(self):
+        self.A.zero_()
+        self.rows.zero_()
+        self.status.zero_()
+
+    def run(self, active, marks=None):
+        """score -> allocate -> select -> compact -> decode; `marks` records events."""
+        kv, st = self.kv, self.st
+        ev = (lambda: marks.append(torch.cuda.Event(enable_timing=True))) if marks is not None else None
+
+        def mark():
+            if ev is not None:
+                ev()
+                marks[-1].record()
+
+        mark()
+        self.check(L.arbor_score(kv, self.observers, self.q_win, st["window"], st["slice_layers"],
+                                 self.v_sig, self.u_sig, self.A, self.rows, self.a, self.s,
+                                 self.params, self.status, self.ws))
+        mark()
+        self.check(L.arbor_allocate(kv, active, st["budget"], self.s, self.params, self.k,
+                                    self.delta, self.on_path, self.status, self.ws))
+        mark()
+        self.check(L.arbor_select(kv, self.A, self.k, self.params, self.sel, self.status))
+        mark()
+        self.check(L.arbor_compact(kv, self.k, self.sel, self.status, self.ws))
+        mark()
+        self.check(L.arbor_tree_decode_attn(kv, active, 0, kv.layers, self.q_dec, self.out,
+                                            self.lse, 0.0, self.status, self.ws))
+        mark()
+
+
+def _chain(parent, j):
+    out = []
+    while j >= 0:
+        out.append(j)
+        j = parent[j]
+    return out
+
+
+def algorithmic_work(st, kv, k_after, n_kept_before, active):
+    """Bytes / flops each entry point must move or compute on this instance."""
+    parent = st["parent"].tolist()
+    n_full = st["n_full"].tolist()
+    Hkv, G, d, Lyr = kv.kv_heads, kv.q_per_kv, kv.head_dim, kv.layers
+    esz = 2 if kv.dtype == L.BF16 else 4
+    row_all_layers = Lyr * Hkv * d * esz * 2            # K + V of one token, all layers
+    S = len(st["slice_layers"])
+    W = st["window"]
+    # score: every (window row, context key) pair once
+    pairs = 0
+    for j in range(len(parent)):
+        ch = _chain(parent, j)
+        anc = sum(n_kept_before[a] for a in ch[1:])
+        wj = min(W, n_full[j])
+        own = sum(n_full[j] - wj + t + 1 for t in range(wj))
+        pairs += (anc * wj + own) * S * Hkv * G
+    score_flops = 2.0 * d * pairs
+    score_bytes = (sum(n_kept_before) * S * Hkv * d * esz + st["q_win"].numel() * esz
+                   + 4 * kv.num_tokens)
+    # compact: rows whose slot changes, read + write, every layer and KV head
+    moved = 0
+    sel = st.get("_sel_cpu")
+    tok_off = st["tok_off"].tolist()
+    for i in range(len(parent)):
+        if k_after[i] < n_kept_before[i]:
+            keep = sel[tok_off[i]:tok_off[i] + k_after[i]]
+            moved += int(np.sum(keep != np.arange(k_after[i])))
+    compact_bytes = 2.0 * moved * row_all_layers
+    # select: A of every candidate + one position per kept token
+    cand = sum(n_kept_before[i] for i in range(len(parent)) if k_after[i] < n_kept_before[i])
+    kept = sum(k_after[i] for i in range(len(parent)) if k_after[i] < n_kept_before[i])
+    select_bytes = 4.0 * cand + 4.0 * kept
+    # decode: K + V of the union of the active chains, every layer, + Q + O
+    union = set()
+    for l in active:
+        union.update(_chain(parent, l))
+    union_tok = sum(k_after[a] for a in union)
+    naive_tok = sum(k_after[a] for l in active for a in _chain(parent, l))
+    qo = 2 * len(active) * Lyr * Hkv * G * d * 2
+    decode_bytes = union_tok * row_all_layers + qo
+    decode_naive = naive_tok * row_all_layers + qo
+    return dict(score_flops=score_flops, score_bytes=score_bytes, score_pairs=pairs,
+                compact_bytes=compact_bytes, moved_rows=moved, select_bytes=select_bytes,
+                decode_bytes=decode_bytes, decode_naive_bytes=decode_naive,
+                union_tokens=union_tok)
+
+
+def cpu_baseline(st, kv_cpu_state, sel_budget_active, work):
+    """Time the oracle on a bounded sample and scale to one full step."""
+    from oracle import arbor_oracle as O
+
+    def np_float(t):
+        return t.detach().to("cpu", torch.float32).numpy()
+
+    def oracle_state(d):
+        out = {key: d[key].cpu().numpy().astype(np.int64) for key in
+               ("parent", "n_full", "tok_off", "page_off", "n_kept", "page_table", "slot_pos",
+                "free_stack")}
+        out.update(free_top=np.int64(int(d["free_top"].reshape(-1)[0])), k=np_float(d["k"]),
+                   v=np_float(d["v"]), page_size=int(d["page_size"]))
+        return out
+
+    t0 = time.perf_counter()
+    ost = oracle_state(kv_cpu_state)
+    t_conv = time.perf_counter() - t0
+    parent = st["parent"].numpy()
+    V = len(parent)
+    obs_all = st["observers"].tolist()
+    # sample: every 8th observer for the score
+    sample = obs_all[::8]
+    idx = [obs_all.index(j) for j in sample]
+    q = np_float(st["q_win"])[idx]
+    t0 = time.perf_counter()
+    O.score(ost, sample, q, st["window"], st["slice_layers"], st["q_per_kv"],
+            st["v_sig"].numpy(), st["u_sig"].numpy(), np.zeros(st["num_tokens"], np.float32),
+            np.zeros(V, np.int64), theta=st["params"]["theta"])
+    t_score_s = time.perf_counter() - t0
+    W, S, Hq = st["window"], len(st["slice_layers"]), st["kv_heads"] * st["q_per_kv"]
+    n_full = st["n_full"].tolist()
+    samp_pairs = 0
+    for j in sample:
+        ch = _chain(parent.tolist(), j)
+        anc = sum(n_full[a] for a in ch[1:])
+        wj = min(W, n_full[j])
+        samp_pairs += (anc * wj + sum(n_full[j] - wj + t + 1 for t in range(wj))) * S * Hq
+    t_score = t_score_s * work["score_pairs"] / samp_pairs
+    # full-size allocate / select / compact
+    s = np.random.default_rng(0).random(V).astype(np.float32)
+    active, budget, params = sel_budget_active
+    t0 = time.perf_counter()
+    k, _, _, _ = O.allocate(parent, ost["n_full"], ost["n_kept"], active, budget, s, params)
+    t_alloc = time.perf_counter() - t0
+    A = np.random.default_rng(1).random(st["num_tokens"]).astype(np.float32)
+    t0 = time.perf_counter()
+    sel, _ = O.select(ost, A, k, params["l_tail"])
+    t_select = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    new = O.compact(ost, k, sel)
+    t_compact = time.perf_counter() - t0
+    # decode: all active leaves, 2 of the layers, scaled to all layers
+    Lyr = st["layers"]
+    qd = np_float(st["q_dec"])[:, :2]
+    t0 = time.perf_counter()
+    O.tree_decode_attn(new, active, 0, 2, qd, st["q_per_kv"])
+    t_dec = (time.perf_counter() - t0) * Lyr / 2
+    total = t_score + t_alloc + t_select + t_compact + t_dec
+    cores = len(os.sched_getaffinity(0))
+    return {"value": st["num_tokens"] / total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"oracle score on {len(sample)} of {len(obs_all)} observers "
+                       f"({t_score_s:.1f} s, scaled by scored pairs), full allocate/select/"
+                       f"compact ({t_alloc + t_select + t_compact:.1f} s), decode of all "
+                       f"{len(active)} leaves on 2 of {Lyr} layers ({t_dec * 2 / Lyr:.1f} s, "
+                       f"scaled); estimated {total:.1f} s per step"),
+            "stage_s": {"score": t_score, "allocate": t_alloc, "select": t_select,
+                        "compact": t_compact, "decode": t_dec, "state_to_numpy": t_conv}}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "subtree sharding of this path is a design note, not a measured configuration.",
+              file=sys.stderr)
+        sys.exit(2)
+    cfg = synth.CONFIGS[args.config]
+    torch.cuda.init()
+    st = synth.build_config(cfg, device="cuda")
+    kv = L.kv_state_from(st, "cuda")
+    pristine = kv.clone()
+    ev = Event(kv, st, cfg)
+    active = st["active"].cuda()
+    stages = ["score", "allocate", "select", "compact", "decode"]
+
+    # warmup
+    for _ in range(args.warmup):
+        kv.copy_from(pristine)
+        ev.reset_scores()
+        ev.run(active)
+    torch.cuda.synchronize()
+    if int(ev.status) < 0:
+        raise RuntimeError(f"device status {int(ev.status)}: {L.arbor_strerror(int(ev.status))}")
+
+    # timed steps
+    per_stage = {s: [] for s in stages}
+    step_ms = []
+    wall = 0.0
+    for _ in range(args.steps):
+        kv.copy_from(pristine)
+        ev.reset_scores()
+        torch.cuda.synchronize()
+        marks = []
+        t0 = time.perf_counter()
+        ev.run(active, marks)
+        torch.cuda.synchronize()
+        wall += time.perf_counter() - t0
+        for si, s in enumerate(stages):
+            per_stage[s].append(marks[si].elapsed_time(marks[si + 1]))
+        step_ms.append(marks[0].elapsed_time(marks[-1]))
+    status = int(ev.status)
+    if status < 0:
+        raise RuntimeError(f"device status {status}: {L.arbor_strerror(status)}")
+    ms = float(np.mean(step_ms))
+    N_event = int(pristine.n_kept.sum())
+    value = N_event / (ms * 1e-3)
+
+    # algorithmic work of this instance (from the last step's outputs)
+    k_after = ev.k.cpu().tolist()
+    st["_sel_cpu"] = ev.sel.cpu().numpy()
+    work = algorithmic_work(st, kv, k_after, pristine.n_kept.cpu().tolist(), st["active"].tolist())
+    mean = {s: float(np.mean(v)) for s, v in per_stage.items()}
+    rates = {
+        "score": {"bound": "mfma", "achieved": work["score_flops"] / (mean["score"] * 1e-3) / 1e12,
+                  "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"},
+        "compact": {"bound": "hbm", "achieved": work["compact_bytes"] / (mean["compact"] * 1e-3) / 1e9,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+        "decode": {"bound": "hbm", "achieved": work["decode_bytes"] / (mean["decode"] * 1e-3) / 1e9,
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+        "select": {"bound": "hbm", "achieved": work["select_bytes"] / (mean["select"] * 1e-3) / 1e9,
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+    }
+    for r in rates.values():
+        r["frac"] = r["achieved"] / r["peak"]
+    dominant = max(["score", "compact", "decode", "select"], key=lambda s: mean[s])
+    roof = dict(rates[dominant])
+    roof["kernel"] = {"score": "arbor_score", "compact": "arbor_compact",
+                      "decode": "arbor_tree_decode_attn", "select": "arbor_select"}[dominant]
+    roof["traffic"] = None
+
+    result = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": (f"{cfg.name}: {cfg.layers} layers, {cfg.kv_heads} KV heads, "
+                                f"{cfg.q_heads} q heads, head_dim {cfg.head_dim}, {cfg.dtype}; "
+                                f"root {cfg.root_tokens}, branching {cfg.branching}, depth "
+                                f"{cfg.depth}, {cfg.node_tokens} tokens/node "
+                                f"({kv.num_nodes} nodes, {kv.num_tokens} tokens); "
+                                f"{cfg.n_active} active leaves; budget {cfg.rho:.0%}; window "
+                                f"{cfg.window}"),
+                   "tokens_per_step": N_event, "parallelism": "single GPU"},
+        "roofline": roof,
+        "stages_ms": mean,
+        "rates": rates,
+        "decode_hbm_gbs": rates["decode"]["achieved"],
+        "decode_hbm_frac": rates["decode"]["frac"],
+        "decode_union_vs_naive_bytes": [work["decode_bytes"], work["decode_naive_bytes"]],
+        "compact_moved_rows": work["moved_rows"],
+        "wall_ms_per_step": wall / args.steps * 1e3,
+        "status": status,
+    }
+
+    # backtracking transition with lazy rehydration from pinned host memory
+    if not args.no_rehydrate_leg:
+        kv.copy_from(pristine)
+        ev.reset_scores()
+        ev.run(active)
+        parent = st["parent"].tolist()
+        leaves = [i for i in range(kv.num_nodes) if i not in parent]
+        a0 = set(st["active"].tolist())
+        alt = [l for l in leaves if l not in a0]
+        a1 = torch.tensor([alt[(j * len(alt)) // len(a0) + 3] for j in range(len(a0))],
+                          dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        n_kept_before = kv.n_kept.cpu().numpy()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        ev.check(L.arbor_allocate(kv, a1, st["budget"], ev.s, ev.params, ev.k, ev.delta,
+                                  ev.on_path, ev.status, ev.ws))
+        e[1].record()
+        ev.check(L.arbor_rehydrate(kv, ev.on_path, st["host_k"], st["host_v"], ev.status, ev.ws))
+        e[2].record()
+        torch.cuda.synchronize()
+        onp = ev.on_path.cpu().numpy().astype(bool)
+        nf = st["n_full"].numpy()
+        restored = int(np.sum((nf - n_kept_before)[onp]))
+        row_bytes = kv.layers * kv.kv_heads * kv.head_dim * 2 * 2
+        t_re = e[1].elapsed_time(e[2])
+        result["rehydrate"] = {"ms": t_re, "tokens_from_host": restored,
+                               "host_link_gbs": restored * row_bytes / (t_re * 1e-3) / 1e9,
+                               "nodes": int(np.sum(onp & (n_kept_before < nf))),
+                               "status": int(ev.status),
+                               "note": "pinned host -> HBM, PCIe-inclusive; not part of value"}
+
+    if not args.no_cpu_baseline:
+        cpu_state = {k: (v.cpu() if isinstance(v, torch.Tensor) else v) for k, v in st.items()
+                     if k not in ("host_k", "host_v")}
+        cpu_state.update(k=pristine.k.cpu(), v=pristine.v.cpu(), n_kept=pristine.n_kept.cpu(),
+                         page_table=pristine.page_table.cpu(), slot_pos=pristine.slot_pos.cpu(),
+                         free_stack=pristine.free_stack.cpu(), free_top=pristine.free_top.cpu())
+        result["cpu_baseline"] = cpu_baseline(st, cpu_state, (st["active"].tolist(), st["budget"],
+                                                                st["params"]), work)
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()
