@@ -64,19 +64,39 @@ __device__ int count_prefix(int F, int c, double W, Pred pred) {
   return ans - F;
 }
 
-// Histogram increment aggregated over the lanes of a wave holding the same bin.
-__device__ __forceinline__ void wave_hist_add(unsigned *hist, int bin, bool active, unsigned w) {
-  uint64_t pending = ballot(active);
-  const int lane = lane_id();
-  while (pending) {
-    const int leader = __builtin_ctzll(pending);
-    const int lb = __shfl(bin, leader, kWave);
-    const bool same = active && bin == lb && ((pending >> lane) & 1ull);
-    const uint64_t grp = ballot(same);
-    const unsigned sum = (unsigned)wave_sum<int>(same ? (int)w : 0);
-    if (lane == leader) atomicAdd(&hist[lb], sum);
-    pending &= ~grp;
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+#pragma unroll
+  for (int d = kWave / 2; d > 0; d >>= 1) {
+    const uint64_t o = __shfl_xor(v, d, kWave);
+    v = o < v ? o : v;
   }
+  return v;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int d = kWave / 2; d > 0; d >>= 1) {
+    const uint64_t o = __shfl_xor(v, d, kWave);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+__device__ uint64_t block_min_u64(uint64_t v, uint64_t *sm) {
+  v = wave_min_u64(v);
+  if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t r = sm[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = sm[w] < r ? sm[w] : r;
+  __syncthreads();
+  return r;
+}
+__device__ uint64_t block_max_u64(uint64_t v, uint64_t *sm) {
+  v = wave_max_u64(v);
+  if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t r = sm[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = sm[w] > r ? sm[w] : r;
+  __syncthreads();
+  return r;
 }
 
 __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__restrict__ active,
@@ -88,9 +108,13 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
                                                       int32_t *status, AllocWs ws) {
   __shared__ int64_t sm[17];
   __shared__ int s_err;
-  __shared__ unsigned hist[256];
+  __shared__ unsigned hist4[4 * 256];
   __shared__ unsigned long long hist64[256];
   __shared__ unsigned s_ncand;
+  __shared__ uint64_t s_u64[17];
+  __shared__ int64_t s_wtot[4];
+  __shared__ int s_chosen;
+  __shared__ int64_t s_below;
   if (status_failed(status)) return;
   const int tid = threadIdx.x;
   const int V = t.V;
@@ -223,67 +247,83 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       run += tot;
     }
     __syncthreads();
-    // materialise the price bit patterns
-    for (int i = tid; i < V; i += AT) {
-      const int c = ws.cnt[i];
-      if (c == 0) continue;
-      const int64_t o = ws.cnt_off[i];
-      const double W = ws.W[i];
-      const int F = ws.F[i];
-      for (int j = 0; j < c; ++j) ws.buf0[o + j] = (uint64_t)__double_as_longlong(price(F + 1 + j, W));
+    // materialise the price bit patterns, one wave per node
+    {
+      const int wave = tid >> 6, lane = lane_id();
+      for (int i = wave; i < V; i += AT / kWave) {
+        const int c = ws.cnt[i];
+        if (c == 0) continue;
+        const int64_t o = ws.cnt_off[i];
+        const double W = ws.W[i];
+        const int F = ws.F[i];
+        for (int j = lane; j < c; j += kWave)
+          ws.buf0[o + j] = (uint64_t)__double_as_longlong(price(F + 1 + j, W));
+      }
     }
     __syncthreads();
-    // radix select of the element of rank E (0-based) in ascending order
-    uint64_t prefix = 0;
+    // the common high bits of all candidates need no pass
+    uint64_t kmin = ~0ull, kmax = 0ull;
+    for (int64_t e = tid; e < total; e += AT) {
+      const uint64_t key = ws.buf0[e];
+      kmin = key < kmin ? key : kmin;
+      kmax = key > kmax ? key : kmax;
+    }
+    kmin = block_min_u64(kmin, s_u64);
+    kmax = block_max_u64(kmax, s_u64);
+    uint64_t prefix = kmin;
     int64_t rank = E;
     int64_t ncand = total;
     uint64_t *src = ws.buf0, *dst = ws.buf1;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      for (int b = tid; b < 256; b += AT) hist[b] = 0;
-      __syncthreads();
-      for (int64_t e0 = 0; e0 < ncand; e0 += AT) {
-        const int64_t e = e0 + tid;
-        const bool v = e < ncand;
-        const uint64_t key = v ? src[e] : 0ull;
-        wave_hist_add(hist, (int)((key >> shift) & 255ull), v, 1u);
-      }
-      __syncthreads();
-      int chosen = 0;
-      int64_t below = 0;
-      {
-        // every thread scans the 256 bins (cheap, keeps the result uniform)
-        int64_t acc = 0;
-        for (int b = 0; b < 256; ++b) {
-          const int64_t h = hist[b];
-          if (acc + h > rank) {
-            chosen = b;
-            below = acc;
-            break;
+    if (kmin != kmax) {
+      const int top = 63 - __builtin_clzll(kmin ^ kmax);
+      int shift = (top / 8) * 8;
+      prefix = kmin & ~((shift + 8 >= 64) ? ~0ull : ((1ull << (shift + 8)) - 1ull));
+      for (; shift >= 0; shift -= 8) {
+        for (int b = tid; b < 4 * 256; b += AT) hist4[b] = 0;
+        __syncthreads();
+        unsigned *myh = hist4 + 256 * ((tid >> 6) & 3);
+        for (int64_t e = tid; e < ncand; e += AT)
+          atomicAdd(&myh[(src[e] >> shift) & 255ull], 1u);
+        __syncthreads();
+        // bin holding the element of rank `rank` (first 256 threads, 4 waves)
+        const unsigned h = tid < 256
+                               ? hist4[tid] + hist4[256 + tid] + hist4[512 + tid] + hist4[768 + tid]
+                               : 0u;
+        const int64_t inc = wave_inclusive_scan<int64_t>((int64_t)h);
+        if (tid < 256 && lane_id() == kWave - 1) s_wtot[tid >> 6] = inc;
+        __syncthreads();
+        if (tid < 256) {
+          int64_t base = 0;
+          for (int w = 0; w < (tid >> 6); ++w) base += s_wtot[w];
+          const int64_t ex = base + inc - (int64_t)h;
+          if (ex <= rank && rank < ex + (int64_t)h) {
+            s_chosen = tid;
+            s_below = ex;
           }
-          acc += h;
         }
+        __syncthreads();
+        const int chosen = s_chosen;
+        rank -= s_below;
+        prefix |= (uint64_t)chosen << shift;
+        if (shift == 0) break;
+        if (tid == 0) s_ncand = 0;
+        __syncthreads();
+        for (int64_t e0 = 0; e0 < ncand; e0 += AT) {
+          const int64_t e = e0 + tid;
+          const bool keep = e < ncand && (int)((src[e] >> shift) & 255ull) == chosen;
+          const uint64_t bk = ballot(keep);
+          unsigned base = 0;
+          if (lane_id() == 0 && bk) base = atomicAdd(&s_ncand, (unsigned)popc(bk));
+          base = __shfl(base, 0, kWave);
+          if (keep) dst[base + rank_below(bk, lane_id())] = src[e];
+        }
+        __syncthreads();
+        ncand = s_ncand;
+        uint64_t *tmp = src;
+        src = dst;
+        dst = tmp;
+        __syncthreads();
       }
-      rank -= below;
-      prefix |= (uint64_t)chosen << shift;
-      if (shift == 0) break;
-      // keep the candidates of the chosen bin
-      if (tid == 0) s_ncand = 0;
-      __syncthreads();
-      for (int64_t e0 = 0; e0 < ncand; e0 += AT) {
-        const int64_t e = e0 + tid;
-        const bool keep = e < ncand && (int)((src[e] >> shift) & 255ull) == chosen;
-        const uint64_t bk = ballot(keep);
-        unsigned base = 0;
-        if (lane_id() == 0 && bk) base = atomicAdd(&s_ncand, (unsigned)popc(bk));
-        base = __shfl(base, 0, kWave);
-        if (keep) dst[base + rank_below(bk, lane_id())] = src[e];
-      }
-      __syncthreads();
-      ncand = s_ncand;
-      uint64_t *tmp = src;
-      src = dst;
-      dst = tmp;
-      __syncthreads();
     }
     const double cut = __longlong_as_double((long long)prefix);
     for (int i = tid; i < V; i += AT) {

@@ -11,6 +11,8 @@
 // step is permuted so P needs no cross-lane movement.  Each unit writes an
 // unnormalised partial (max, sum, o); the merge kernel combines the partials of
 // a leaf in root-to-leaf order, so results are bitwise reproducible.
+#include <type_traits>
+
 #include "arbor_internal.h"
 #include "mfma_ops.h"
 
@@ -19,7 +21,7 @@ namespace arbor {
 namespace {
 
 constexpr int MAXD = ARBOR_MAX_DEPTH + 1;
-constexpr int CHUNK = 512;        // slots per work unit
+constexpr int CHUNK = 256;        // slots per work unit
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -46,6 +48,9 @@ struct DecArgs {
   const int32_t *lanc;        // [n_leaves][MAXD]
   const int32_t *ldepth;
   const int32_t *lrank;       // [n_leaves][MAXD]
+  const int32_t *leaf_np;     // partials of each leaf's chain
+  const int32_t *leaf_part;   // [n_leaves][max_parts]: first partial row of the leaf's heads
+  int max_parts;
   float *part;
   int64_t part_cap;
   int32_t *status;
@@ -57,7 +62,8 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
                                                     int32_t *node_leaf_off, int32_t *leaf_list,
                                                     int32_t *node_item0, int32_t *node_rowbase,
                                                     int32_t *lanc, int32_t *ldepth,
-                                                    int32_t *lrank) {
+                                                    int32_t *lrank, int32_t *leaf_np,
+                                                    int32_t *leaf_part) {
   __shared__ int64_t sm[17];
   __shared__ int s_err;
   if (status_failed(a.status)) {
@@ -162,9 +168,27 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     const int x = lanc[(int64_t)b * MAXD + d];
     leaf_list[node_leaf_off[x] + lrank[(int64_t)b * MAXD + d]] = b;
   }
+  __syncthreads();
+  // each leaf's partials, root first: the merge reads them without a chain walk
+  for (int b = threadIdx.x; b < a.n_leaves; b += blockDim.x) {
+    int np = 0;
+    for (int d = 0; d <= ldepth[b]; ++d) {
+      const int x = lanc[(int64_t)b * MAXD + d];
+      const int nch = (t.n_kept[x] + CHUNK - 1) / CHUNK;
+      const int r = lrank[(int64_t)b * MAXD + d] * G;
+      if (np + nch > a.max_parts) {  // more resident tokens than the workspace was sized for
+        atomicOr(&s_err, 4);
+        break;
+      }
+      for (int s = 0; s < nch; ++s, ++np)
+        leaf_part[(int64_t)b * a.max_parts + np] = item_rowbase[node_item0[x] + s] + r;
+    }
+    leaf_np[b] = np;
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
     const int64_t need = run_rows * a.Lr * a.pl.Hkv * (int64_t)(a.pl.D + 2);
-    if (run_item > a.max_items || need > a.part_cap) {
+    if (run_item > a.max_items || need > a.part_cap || s_err) {
       status_error(a.status, ARBOR_EWORKSPACE);
       meta[0] = meta[1] = meta[2] = 0;
       return;
@@ -176,16 +200,34 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   }
 }
 
-// One wave: one work unit, rows [rbase, rbase + 16 NB).
+// Column of head_dim that lane group g4 supplies at MFMA k-step ks.  K and Q
+// use the same map, so the dot product is unchanged; it makes the four lane
+// groups of one k-step read consecutive 16-byte pieces of a row.
+template <class T>
+__device__ __forceinline__ int frag_col(int ks, int g4) {
+  constexpr int VEC = 16 / (int)sizeof(T);          // elements per 16 bytes
+  constexpr int SPV = VEC / Op<T>::kPerStep;        // k-steps per 16 bytes
+  return (ks / SPV) * 4 * VEC + g4 * VEC + (ks % SPV) * Op<T>::kPerStep;
+}
+
+// One workgroup: one work unit (a CHUNK of a chain node's slots, one layer,
+// one kv head), rows [rbase, rbase + 16 NB).  Wave w takes the 16-slot
+// sub-pages w, w + 4, ... in groups of two whose K and V load together; the four
+// waves' (max, sum, o) are merged in LDS in wave order.
 template <class T, int D, int NB>
-__device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase) {
+__device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase, float *sm_o,
+                            float *sm_m, float *sm_l) {
   using O = Op<T>;
   constexpr int KS = D / 4 / O::kPerStep;  // MFMA k-steps over head_dim (S = K Q^T)
-  constexpr int QTR = D / 4;
   constexpr int NC = D / 16;               // output column chunks; lane owns NC columns
+  constexpr int GSP = 4 / NB;              // sub-pages per group (registers)
+  constexpr int RWS = 16 * NB;             // rows handled in this pass
+  typedef typename std::conditional<sizeof(T) == 2, __bf16, float>::type VT;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
+  const int tid = threadIdx.x;
   const int lane = lane_id();
+  const int wave = tid >> 6;
   const int rr = lane & 15;
   const int g4 = lane >> 4;
   const int G = pl.G;
@@ -201,7 +243,6 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   const int64_t po = t.page_off[node];
   const int loff = a.node_leaf_off[node];
 
-  // Q operand (S layout: lane owns row rbase + nb*16 + rr)
   typename O::reg q[NB][KS];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -209,9 +250,9 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
     if (r < R) {
       const int b = a.leaf_list[loff + r / G];
       const int h = g * G + r % G;
-      const T *qp = static_cast<const T *>(a.q) + (((int64_t)b * a.Lr + lr) * Hq + h) * D + g4 * QTR;
+      const T *qp = static_cast<const T *>(a.q) + (((int64_t)b * a.Lr + lr) * Hq + h) * D;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::load(qp + ks * O::kPerStep);
+      for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::load(qp + frag_col<T>(ks, g4));
     } else {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::zero();
@@ -228,43 +269,48 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   }
   const char *kb = static_cast<const char *>(pl.k);
   const char *vb = static_cast<const char *>(pl.v);
-  for (int gs = s_begin; gs < s_end; gs += 64) {
-    // phase A: logits of up to 4 sub-pages (64 keys)
-    float sv[4][NB][4];
+  const int n_sub = (s_end - s_begin + 15) / 16;
+  for (int base = wave; base < n_sub; base += 4 * GSP) {
+    typename O::reg kr[GSP][KS];
+    VT vr[GSP][4][NC];
+    int nval[GSP];
+#pragma unroll
+    for (int sp = 0; sp < GSP; ++sp) {
+      // clamp to a valid sub-page so every load is unconditional
+      const int sub = min(base + 4 * sp, n_sub - 1);
+      const int q0 = s_begin + sub * 16;
+      nval[sp] = base + 4 * sp < n_sub ? min(16, s_end - q0) : 0;
+      const int page = t.page_table[po + q0 / pl.P];
+      const int r0 = q0 % pl.P;
+      const T *kp = reinterpret_cast<const T *>(kb + row_byte_offset(pl, layer, page, g, r0 + rr));
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) kr[sp][ks] = O::load(kp + frag_col<T>(ks, g4));
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const VT *vp = reinterpret_cast<const VT *>(vb + row_byte_offset(pl, layer, page, g, r0 + 4 * g4 + ks)) + NC * rr;
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) vr[sp][ks][cc] = vp[cc];
+      }
+    }
+    float sv[GSP][NB][4];
     float gmax[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) gmax[nb] = -__builtin_inff();
 #pragma unroll
-    for (int sp = 0; sp < 4; ++sp) {
-      const int q0 = gs + sp * 16;
-      if (q0 >= s_end) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) sv[sp][nb][e] = -__builtin_inff();
-        continue;
-      }
-      const int page = t.page_table[po + q0 / pl.P];
-      const int r0 = q0 % pl.P;
-      const int nvalid = min(16, s_end - q0);
-      const T *kp = reinterpret_cast<const T *>(kb + row_byte_offset(pl, layer, page, g, r0 + rr)) + g4 * QTR;
-      typename O::reg kr[KS];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kr[ks] = O::load(kp + ks * O::kPerStep);
+    for (int sp = 0; sp < GSP; ++sp) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc = O::mma(kr[ks], q[nb][ks], acc);
+        for (int ks = 0; ks < KS; ++ks) acc = O::mma(kr[sp][ks], q[nb][ks], acc);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float z = (4 * g4 + e < nvalid) ? acc[e] * a.sl2 : -__builtin_inff();
+          const float z = (4 * g4 + e < nval[sp]) ? acc[e] * a.sl2 : -__builtin_inff();
           sv[sp][nb][e] = z;
           gmax[nb] = fmaxf(gmax[nb], z);
         }
       }
     }
-    // row max over the group; rescale the running state
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 16, kWave));
@@ -273,7 +319,6 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
       const float alpha = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
       m_run[nb] = mn;
       l_run[nb] *= alpha;
-      // O rows 4*g4+e take the factor of S-layout row 4*g4+e
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float fe = __shfl(alpha, 4 * g4 + e, kWave);
@@ -281,149 +326,215 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
         for (int cc = 0; cc < NC; ++cc) o[nb][cc][e] *= fe;
       }
     }
-    // phase B: probabilities and O += P V (key 4*g4 + ks of the sub-page in
-    // k-step ks, so P stays in the lane that computed it)
 #pragma unroll
-    for (int sp = 0; sp < 4; ++sp) {
-      const int q0 = gs + sp * 16;
-      if (q0 >= s_end) continue;
-      const int page = t.page_table[po + q0 / pl.P];
-      const int r0 = q0 % pl.P;
-      float vr[4][NC];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const T *vp = reinterpret_cast<const T *>(vb + row_byte_offset(pl, layer, page, g, r0 + 4 * g4 + ks)) + NC * rr;
-        load_row_f32<T, NC>(vp, vr[ks]);
-      }
+    for (int sp = 0; sp < GSP; ++sp) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         float p[4];
+        const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          p[e] = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(sv[sp][nb][e] - m_run[nb]) : 0.f;
+          p[e] = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
           l_run[nb] += p[e];
         }
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+        for (int ks = 0; ks < 4; ++ks) {
+          // a slot past the resident count may hold anything: its row is zeroed
+          const bool kv = 4 * g4 + ks < nval[sp];
 #pragma unroll
-          for (int cc = 0; cc < NC; ++cc) o[nb][cc] = mma_f32(p[ks], vr[ks][cc], o[nb][cc]);
+          for (int cc = 0; cc < NC; ++cc)
+            o[nb][cc] = mma_f32(p[ks], kv ? (float)vr[sp][ks][cc] : 0.f, o[nb][cc]);
+        }
       }
     }
   }
-  // write the unit's partial rows: [m, l, o(0..D-1)], o column NC*rr + cc
-  const int64_t stride = D + 2;
-  const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
-  float *base = a.part + (slab + a.item_rowbase[item]) * stride;
+  // merge the four waves in LDS: row maxima, then o accumulated wave by wave
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     float l = l_run[nb];
     l += __shfl_xor(l, 16, kWave);
     l += __shfl_xor(l, 32, kWave);
-    const int rs = rbase + nb * 16 + rr;
-    if (g4 == 0 && rs < R) {
-      base[rs * stride + 0] = m_run[nb];
-      base[rs * stride + 1] = l;
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int ro = rbase + nb * 16 + 4 * g4 + e;
-      if (ro < R) {
-        float *op = base + ro * stride + 2 + NC * rr;
-#pragma unroll
-        for (int cc = 0; cc < NC; ++cc) op[cc] = o[nb][cc][e];
-      }
+    if (g4 == 0) {
+      sm_m[wave * RWS + nb * 16 + rr] = m_run[nb];
+      sm_l[wave * RWS + nb * 16 + rr] = l;
     }
   }
+  __syncthreads();
+  float fo[NB][4];   // this wave's factor for its O-layout rows
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = nb * 16 + 4 * g4 + e;
+      float M = -__builtin_inff();
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w * RWS + r]);
+      const float mw = sm_m[wave * RWS + r];
+      fo[nb][e] = (mw > -__builtin_inff()) ? __builtin_amdgcn_exp2f(mw - M) : 0.f;
+    }
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float *dst = sm_o + (nb * 16 + 4 * g4 + e) * D + NC * rr;
+#pragma unroll
+          for (int cc = 0; cc < NC; ++cc)
+            dst[cc] = (w == 0 ? 0.f : dst[cc]) + o[nb][cc][e] * fo[nb][e];
+        }
+    }
+    __syncthreads();
+  }
+  // one partial row per query row: [m, l, o(0..D-1)]
+  const int64_t stride = D + 2;
+  const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
+  float *outp = a.part + (slab + a.item_rowbase[item]) * stride;
+  for (int r = wave; r < RWS; r += 4) {
+    const int row = rbase + r;
+    if (row >= R) continue;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w * RWS + r]);
+    float L = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = sm_m[w * RWS + r];
+      if (mw > -__builtin_inff()) L += sm_l[w * RWS + r] * __builtin_amdgcn_exp2f(mw - M);
+    }
+    float *op = outp + row * stride;
+    if (lane == 0) {
+      op[0] = M;
+      op[1] = L;
+    }
+    for (int d = lane; d < D; d += kWave) op[2 + d] = sm_o[r * D + d];
+  }
+  __syncthreads();
 }
 
 template <class T, int D, int NB>
 __global__ __launch_bounds__(256) void decode_attn(DecArgs a, int cls) {
-  if (status_failed(a.status)) return;
+  __shared__ float sm_o[16 * NB * D];
+  __shared__ float sm_m[4 * 16 * NB];
+  __shared__ float sm_l[4 * 16 * NB];
+  __shared__ int s_bad;
+  // the whole workgroup takes the same decision: the unit below synchronises
+  if (threadIdx.x == 0) s_bad = status_failed(a.status);
+  __syncthreads();
+  if (s_bad) return;
   const int n_items = a.meta[cls];
   const int planes = a.Lr * a.pl.Hkv;
   const int64_t total = (int64_t)n_items * planes;
-  for (int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); w < total;
-       w += (int64_t)gridDim.x * 4) {
+  for (int64_t w = blockIdx.x; w < total; w += gridDim.x) {
     const int item = a.cls_items[(int64_t)cls * a.max_items + w / planes];
     const int rem = (int)(w % planes);
     const int lr = rem / a.pl.Hkv;
     const int g = rem % a.pl.Hkv;
     const int R = a.node_nl[a.item_node[item]] * a.pl.G;
-    for (int rbase = 0; rbase < R; rbase += 16 * NB) decode_unit<T, D, NB>(a, item, lr, g, rbase);
+    for (int rbase = 0; rbase < R; rbase += 16 * NB)
+      decode_unit<T, D, NB>(a, item, lr, g, rbase, sm_o, sm_m, sm_l);
   }
 }
 
-// One wave per (leaf, layer, kv head): merge the chain's partials root first.
+// One wave per (leaf, layer, query head): merge the partials of the leaf's
+// chain.  Lane k holds partial k's (max, sum); the running max and the weights
+// come from fixed-order wave reductions, and o is accumulated in partial order,
+// so the result does not depend on scheduling.
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int out_dtype,
                                                     float *lse_out) {
   constexpr int EPL = D / 64;  // output columns per lane
+  constexpr int U = 4;         // partial rows loaded together
   if (status_failed(a.status)) return;
-  const Tree &t = a.t;
   const Pool &pl = a.pl;
   const int lane = lane_id();
   const int G = pl.G;
   const int Hq = pl.Hkv * G;
-  const int64_t total = (int64_t)a.n_leaves * a.Lr * pl.Hkv;
+  const int64_t total = (int64_t)a.n_leaves * a.Lr * Hq;
   const int64_t stride = D + 2;
   for (int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); w < total;
        w += (int64_t)gridDim.x * 4) {
-    const int b = (int)(w / (a.Lr * pl.Hkv));
-    const int rem = (int)(w % (a.Lr * pl.Hkv));
-    const int lr = rem / pl.Hkv;
-    const int g = rem % pl.Hkv;
-    const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
-    const int dep = a.ldepth[b];
-    for (int hl = 0; hl < G; ++hl) {
-      float M = -__builtin_inff(), L = 0.f, ov[EPL];
+    const int b = (int)(w / (a.Lr * Hq));
+    const int rem = (int)(w % (a.Lr * Hq));
+    const int lr = rem / Hq;
+    const int h = rem % Hq;
+    const int g = h / G;
+    const int hl = h % G;
+    const float *base = a.part + (((int64_t)lr * pl.Hkv + g) * a.meta[3] + hl) * stride;
+    const int32_t *lp = a.leaf_part + (int64_t)b * a.max_parts;
+    const int np = a.leaf_np[b];
+    // global max over the chain's partials
+    float M = -__builtin_inff();
+    for (int k0 = 0; k0 < np; k0 += kWave) {
+      const int k = k0 + lane;
+      const float m = k < np ? base[(int64_t)lp[k] * stride] : -__builtin_inff();
+      M = fmaxf(M, m);
+    }
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) ov[e] = 0.f;
-      for (int d = 0; d <= dep; ++d) {
-        const int x = a.lanc[(int64_t)b * MAXD + d];
-        const int row = a.lrank[(int64_t)b * MAXD + d] * G + hl;
-        const int nch = (t.n_kept[x] + CHUNK - 1) / CHUNK;
-        const int it0 = a.node_item0[x];
-        for (int s = 0; s < nch; ++s) {
-          const float *pp = a.part + (slab + a.item_rowbase[it0 + s] + row) * stride;
-          const float m = pp[0];
-          if (!(m > -__builtin_inff())) continue;
-          const float l = pp[1];
-          const float mn = fmaxf(M, m);
-          const float fa = (M > -__builtin_inff()) ? __builtin_amdgcn_exp2f(M - mn) : 0.f;
-          const float fb = __builtin_amdgcn_exp2f(m - mn);
-          L = L * fa + l * fb;
+    for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+    float L = 0.f, ov[EPL];
 #pragma unroll
-          for (int e = 0; e < EPL; ++e) ov[e] = ov[e] * fa + pp[2 + 64 * e + lane] * fb;
-          M = mn;
+    for (int e = 0; e < EPL; ++e) ov[e] = 0.f;
+    if (M > -__builtin_inff()) {
+      for (int k0 = 0; k0 < np; k0 += kWave) {
+        const int k = k0 + lane;
+        int64_t off = 0;
+        float f = 0.f, lk = 0.f;
+        if (k < np) {
+          off = (int64_t)lp[k] * stride;
+          const float m = base[off];
+          lk = base[off + 1];
+          f = m > -__builtin_inff() ? __builtin_amdgcn_exp2f(m - M) : 0.f;
+        }
+        L += wave_sum(lk * f);
+        const int nk = min(kWave, np - k0);
+        for (int j0 = 0; j0 < nk; j0 += U) {
+          float xv[U][EPL], fj[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const int j = min(j0 + u, nk - 1);
+            const int64_t oj = __shfl(off, j, kWave);
+            fj[u] = j0 + u < nk ? __shfl(f, j, kWave) : 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) xv[u][e] = base[oj + 2 + 64 * e + lane];
+          }
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) ov[e] += (fj[u] > 0.f ? xv[u][e] * fj[u] : 0.f);
         }
       }
-      const int h = g * G + hl;
-      const int64_t oi = (((int64_t)b * a.Lr + lr) * Hq + h) * D;
-      const float inv = L > 0.f ? 1.0f / L : 0.f;
-      if (out_dtype == ARBOR_BF16) {
-        __bf16 *op = static_cast<__bf16 *>(out) + oi;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) op[64 * e + lane] = (__bf16)(ov[e] * inv);
-      } else {
-        float *op = static_cast<float *>(out) + oi;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) op[64 * e + lane] = ov[e] * inv;
-      }
-      if (lse_out && lane == 0)
-        lse_out[((int64_t)b * a.Lr + lr) * Hq + h] =
-            L > 0.f ? (M + __log2f(L)) * kLn2 : -__builtin_inff();
     }
+    const int64_t oi = (((int64_t)b * a.Lr + lr) * Hq + h) * D;
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+    if (out_dtype == ARBOR_BF16) {
+      __bf16 *op = static_cast<__bf16 *>(out) + oi;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) op[64 * e + lane] = (__bf16)(ov[e] * inv);
+    } else {
+      float *op = static_cast<float *>(out) + oi;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) op[64 * e + lane] = ov[e] * inv;
+    }
+    if (lse_out && lane == 0)
+      lse_out[((int64_t)b * a.Lr + lr) * Hq + h] =
+          L > 0.f ? (M + __log2f(L)) * kLn2 : -__builtin_inff();
   }
 }
 
 template <class T, int D>
 void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *lse_out,
                            hipStream_t stream) {
-  const int grid = 2048;
+  const int grid = 8192;
+  // rows of a work unit are at most n_leaves * G: only the row classes that
+  // can occur are launched
+  const int max_rows = a.n_leaves * a.pl.G;
   hipLaunchKernelGGL((decode_attn<T, D, 1>), dim3(grid), dim3(256), 0, stream, a, 0);
-  hipLaunchKernelGGL((decode_attn<T, D, 2>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
-  hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
-  const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv;
+  if (max_rows > 16)
+    hipLaunchKernelGGL((decode_attn<T, D, 2>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
+  if (max_rows > 32)
+    hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
+  const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv * a.pl.G;
   const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
   hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
                      lse_out);
@@ -435,14 +546,20 @@ static size_t decode_max_items(const arbor_sizes_t *sz) {
   return (size_t)sz->num_nodes + (size_t)(sz->num_tokens / CHUNK) + 1;
 }
 
+// partials along one chain: at most one ragged chunk per chain node
+static size_t decode_max_parts(const arbor_sizes_t *sz) {
+  return (size_t)(sz->num_tokens / CHUNK) + MAXD + 1;
+}
+
 size_t decode_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t V = (size_t)sz->num_nodes;
   const size_t nl = (size_t)(sz->max_leaves > 0 ? sz->max_leaves : 1);
   const size_t items = decode_max_items(sz);
   const size_t per_leaf = (size_t)(sz->max_context / CHUNK) + MAXD + 1;
   const size_t rows = nl * per_leaf * g->q_per_kv;
-  size_t b = 16 * 256;
+  size_t b = 18 * 256;
   b += 3 * items * 4 + 3 * items * 4 + V * 4 * 4 + nl * MAXD * 4 * 3 + nl * 4 + nl * MAXD * 4;
+  b += nl * 4 + nl * decode_max_parts(sz) * 4;
   b += rows * (size_t)sz->max_layers * g->num_kv_heads * (g->head_dim + 2) * 4;
   return b;
 }
@@ -486,6 +603,9 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   int32_t *lanc = cv.take<int32_t>((size_t)n_leaves * MAXD);
   int32_t *ldepth = cv.take<int32_t>(n_leaves);
   int32_t *lrank = cv.take<int32_t>((size_t)n_leaves * MAXD);
+  const int max_parts = (int)decode_max_parts(&sz);
+  int32_t *leaf_np = cv.take<int32_t>(n_leaves);
+  int32_t *leaf_part = cv.take<int32_t>((size_t)n_leaves * max_parts);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   a.meta = meta;
   a.cls_items = cls_items;
@@ -500,11 +620,14 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   a.lanc = lanc;
   a.ldepth = ldepth;
   a.lrank = lrank;
+  a.leaf_np = leaf_np;
+  a.leaf_part = leaf_part;
+  a.max_parts = max_parts;
   a.part = reinterpret_cast<float *>(cv.rest());
   a.part_cap = (int64_t)(cv.remaining() / 4);
   hipLaunchKernelGGL(decode_plan, dim3(1), dim3(1024), 0, stream, a, meta, cls_items, item_node,
                      item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list, node_item0,
-                     node_rowbase, lanc, ldepth, lrank);
+                     node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part);
   if (geom->dtype == ARBOR_BF16) {
     if (geom->head_dim == 128) launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, stream);
     else launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, stream);

@@ -54,44 +54,128 @@ struct ScoreArgs {
   int32_t *status;
 };
 
-// Chain of observer j in LDS, root first.
+// Chain of observer j in LDS, root first, with a table of its 16-slot
+// sub-pages so the key loop needs no dependent page-table load.
+constexpr int SPCAP = 512;
 struct ChainLds {
   int node[MAXD];
   int c[MAXD];
   int64_t po[MAXD];
-  int ctx[MAXD];      // context offset of the node's first slot
+  int ctx[MAXD];       // context offset of the node's first slot
   int sp_off[MAXD + 1];
   int depth;
+  int sp_row[SPCAP];   // page * Hkv * P + r0: row of the sub-page within a (layer, kv head) plane
+  int sp_slot[SPCAP];  // page * P + r0: index into slot_pos
+  int sp_ctx[SPCAP];   // context position of the sub-page's first slot
+  int sp_meta[SPCAP];  // chain depth | valid slots << 8
 };
 
-__device__ void build_chain(const Tree &t, int j, ChainLds &ch) {
-  int d = 0;
-  for (int x = t.parent[j]; x >= 0 && d < MAXD - 1; x = t.parent[x]) ++d;
-  ch.depth = d;
-  int e = d;
-  for (int x = j; x >= 0 && e >= 0; x = t.parent[x]) ch.node[e--] = x;
-  int ctx = 0, sp = 0;
-  for (e = 0; e <= d; ++e) {
-    const int x = ch.node[e];
-    const int c = t.n_kept[x];
-    ch.c[e] = c;
-    ch.po[e] = t.page_off[x];
-    ch.ctx[e] = ctx;
-    ch.sp_off[e] = sp;
-    ctx += c;
-    sp += (c + 15) / 16;
+__device__ void build_chain(const Tree &t, const Pool &pl, int j, ChainLds &ch) {
+  if (threadIdx.x == 0) {
+    int d = 0;
+    for (int x = t.parent[j]; x >= 0 && d < MAXD - 1; x = t.parent[x]) ++d;
+    ch.depth = d;
+    int e = d;
+    for (int x = j; x >= 0 && e >= 0; x = t.parent[x]) ch.node[e--] = x;
+    int ctx = 0, sp = 0;
+    for (e = 0; e <= d; ++e) {
+      const int x = ch.node[e];
+      const int c = t.n_kept[x];
+      ch.c[e] = c;
+      ch.po[e] = t.page_off[x];
+      ch.ctx[e] = ctx;
+      ch.sp_off[e] = sp;
+      ctx += c;
+      sp += (c + 15) / 16;
+    }
+    ch.sp_off[d + 1] = sp;
   }
-  ch.sp_off[d + 1] = sp;
+  __syncthreads();
+  const int n_sp = min(ch.sp_off[ch.depth + 1], SPCAP);
+  for (int sp = threadIdx.x; sp < n_sp; sp += blockDim.x) {
+    int d = 0;
+    while (sp >= ch.sp_off[d + 1]) ++d;
+    const int q0 = (sp - ch.sp_off[d]) * 16;
+    const int page = t.page_table[ch.po[d] + q0 / pl.P];
+    const int r0 = q0 % pl.P;
+    ch.sp_row[sp] = page * pl.Hkv * pl.P + r0;
+    ch.sp_slot[sp] = page * pl.P + r0;
+    ch.sp_ctx[sp] = ch.ctx[d] + q0;
+    ch.sp_meta[sp] = d | (min(16, ch.c[d] - q0) << 8);
+  }
+  __syncthreads();
 }
 
-template <int PASS, class T, int D, int NB>
+struct SubPage {
+  int row, slot, ctx, d, nvalid;
+};
+
+__device__ __forceinline__ SubPage sub_page(const Tree &t, const Pool &pl, const ChainLds &ch,
+                                            int sp) {
+  SubPage r;
+  if (sp < SPCAP) {
+    r.row = ch.sp_row[sp];
+    r.slot = ch.sp_slot[sp];
+    r.ctx = ch.sp_ctx[sp];
+    r.d = ch.sp_meta[sp] & 255;
+    r.nvalid = ch.sp_meta[sp] >> 8;
+  } else {
+    int d = 0;
+    while (sp >= ch.sp_off[d + 1]) ++d;
+    const int q0 = (sp - ch.sp_off[d]) * 16;
+    const int page = t.page_table[ch.po[d] + q0 / pl.P];
+    const int r0 = q0 % pl.P;
+    r.row = page * pl.Hkv * pl.P + r0;
+    r.slot = page * pl.P + r0;
+    r.ctx = ch.ctx[d] + q0;
+    r.d = d;
+    r.nvalid = min(16, ch.c[d] - q0);
+  }
+  return r;
+}
+
+// Sub-page staging: the workgroup loads each 16-key sub-page of K once into an
+// LDS ring; every wave then reads the operand of its own lanes.  Unit u =
+// blk * 64 + lane is 16 bytes: key (lane % 16), quarter (lane / 16), bytes
+// [16 blk, 16 blk + 16) of that quarter row.
+__device__ __forceinline__ int sub_meta(const ChainLds &ch, const Tree &t, const Pool &pl, int sp) {
+  if (sp < SPCAP) return ch.sp_meta[sp];
+  const SubPage s = sub_page(t, pl, ch, sp);
+  return s.d | (s.nvalid << 8);
+}
+
+__device__ __forceinline__ void sub_row_slot(const ChainLds &ch, const Tree &t, const Pool &pl,
+                                             int sp, int &row, int &slot) {
+  if (sp < SPCAP) {
+    row = ch.sp_row[sp];
+    slot = ch.sp_slot[sp];
+  } else {
+    const SubPage s = sub_page(t, pl, ch, sp);
+    row = s.row;
+    slot = s.slot;
+  }
+}
+
+template <class T, int D>
+struct Stage {
+  static constexpr int QB = D / 4 * (int)sizeof(T);  // bytes of a quarter row
+  static constexpr int NBLK = QB / 16;                // 16-byte units per lane
+  static constexpr int UNITS = NBLK * kWave;          // units per sub-page
+  static constexpr int UPT = (UNITS + 255) / 256;     // units per thread (256 threads)
+  static constexpr int BYTES = UNITS * 16;
+};
+
+template <int PASS, class T, int D, int NBW, int GS>
 __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
   using O = Op<T>;
+  using SG = Stage<T, D>;
   constexpr int KS = D / 4 / O::kPerStep;  // MFMA k-steps over head_dim
-  constexpr int QTR = D / 4;               // elements of a row per lane group
+  constexpr int RW = 64 * NBW;             // rows of the workgroup's row group
+  constexpr int RING = 2;                  // stages of GS sub-pages in LDS
   __shared__ ChainLds ch;
-  __shared__ float sm_m[4][16 * NB];
-  __shared__ float sm_l[4][16 * NB];
+  __shared__ __attribute__((aligned(16))) char ring[RING][GS][SG::BYTES];
+  __shared__ __attribute__((aligned(16))) int ring_pos[RING][GS][16];
+  __shared__ float red[RING][GS][4][16];
   if (status_failed(a.status)) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
@@ -102,10 +186,10 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
   const int g = slg % pl.Hkv;
   const int layer = a.slice[si];
   const int j = a.obs[o];
-  if (threadIdx.x == 0) build_chain(t, j, ch);
-  __syncthreads();
+  build_chain(t, pl, j, ch);
+  const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = threadIdx.x >> 6;
+  const int wave = tid >> 6;
   const int rr = lane & 15;
   const int g4 = lane >> 4;
   const int G = pl.G;
@@ -113,89 +197,223 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
   const int wj = min(a.W, nj);
   const int rows_total = G * a.W;
   const int own_d = ch.depth;
+  const int row0 = rg * RW + wave * 16 * NBW;   // first row of this wave
 
-  // Q operand rows (query row of this lane in block nb: rg*16NB + nb*16 + rr)
-  typename O::reg q[NB][KS];
+  // Q operand: query row row0 + nb*16 + rr of block nb
+  typename O::reg q[NBW][KS];
   const T *qbase = static_cast<const T *>(a.q_win) +
                    ((((int64_t)o * a.S + si) * (pl.Hkv * G) + (int64_t)g * G) * a.W) * D;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int r = rg * 16 * NB + nb * 16 + rr;
+  for (int nb = 0; nb < NBW; ++nb) {
+    const int r = row0 + nb * 16 + rr;
     const bool rv = r < rows_total;
-    const T *rp = qbase + (int64_t)(rv ? r : 0) * D + g4 * QTR;
+    const T *rp = qbase + (int64_t)(rv ? r : 0) * D + g4 * (D / 4);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) q[nb][ks] = rv ? O::load(rp + ks * O::kPerStep) : O::zero();
   }
-  // window position u of a row, or -1 for an unused row
   auto row_u = [&](int r) -> int {
     if (r >= rows_total) return -1;
     const int tt = r % a.W;
     return tt < wj ? nj - wj + tt : -1;
   };
+  const int64_t lse_base = (((int64_t)o * a.S + si) * pl.Hkv + g) * ((int64_t)a.n_rg * RW) +
+                           (int64_t)rg * RW;
+  const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
+  const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
+  const int n_sp = (PASS == 1 && !a.self_window) ? ch.sp_off[own_d] : ch.sp_off[own_d + 1];
+  const int n_st = (n_sp + GS - 1) / GS;   // stages
 
-  const int64_t lse_base = ((((int64_t)o * a.S + si) * pl.Hkv + g) * a.n_rg + rg) * (16 * NB);
-  const char *kbase = static_cast<const char *>(pl.k);
-  const int esz = sizeof(T);
-
-  if (PASS == 0) {
-    int urow[NB];
-    float m[NB], l[NB];
+  // Staging: two register sets alternate by stage parity, so a load has a full
+  // stage of compute to land before it is written to the LDS ring.  Loads are
+  // unconditional (indices are clamped to the last sub-page) so the number of
+  // loads in flight is the same on every path.
+  struct Staged {
+    uint4 u[GS][SG::UPT];
+    int pos[GS];
+  };
+  int unit_off[SG::UPT];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      urow[nb] = row_u(rg * 16 * NB + nb * 16 + rr);
-      m[nb] = -__builtin_inff();
-      l[nb] = 0.f;
+  for (int e = 0; e < SG::UPT; ++e) {
+    const int u = (tid + 256 * e) % SG::UNITS;
+    const int ul = u & 63, blk = u >> 6;
+    unit_off[e] = (ul & 15) * D * (int)sizeof(T) + (ul >> 4) * SG::QB + blk * 16;
+  }
+  auto fetch = [&](int st_idx) -> Staged {
+    Staged sv;
+#pragma unroll
+    for (int k = 0; k < GS; ++k) {
+      const int sp = min(st_idx * GS + k, n_sp - 1);
+      int row, slot;
+      sub_row_slot(ch, t, pl, sp, row, slot);
+      const char *src = kplane + (int64_t)row * (D * (int)sizeof(T));
+#pragma unroll
+      for (int e = 0; e < SG::UPT; ++e) sv.u[k][e] = *reinterpret_cast<const uint4 *>(src + unit_off[e]);
+      sv.pos[k] = pl.slot_pos[slot + (tid & 15)];
     }
-    const int n_sp = ch.sp_off[own_d + 1];
-    int d = 0;
-    for (int sp = wave; sp < n_sp; sp += 4) {
-      while (sp >= ch.sp_off[d + 1]) ++d;
-      const int q0 = (sp - ch.sp_off[d]) * 16;      // first slot of the sub-page
-      const int page = t.page_table[ch.po[d] + q0 / pl.P];
-      const int r0 = q0 % pl.P;
-      const int nvalid = min(16, ch.c[d] - q0);
-      const bool own = d == own_d;
-      // K operand: key rr of the sub-page
-      typename O::reg kr[KS];
-      const T *kp = reinterpret_cast<const T *>(kbase + row_byte_offset(pl, layer, page, g, r0 + rr)) +
-                    g4 * QTR;
+    return sv;
+  };
+  auto commit = [&](int slot, const Staged sv) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kr[ks] = O::load(kp + ks * O::kPerStep);
-      int kpos[4] = {0, 0, 0, 0};
-      if (own) {
-        const int4 pv = *reinterpret_cast<const int4 *>(pl.slot_pos + (int64_t)page * pl.P + r0 + 4 * g4);
-        kpos[0] = pv.x;
-        kpos[1] = pv.y;
-        kpos[2] = pv.z;
-        kpos[3] = pv.w;
+    for (int k = 0; k < GS; ++k) {
+#pragma unroll
+      for (int e = 0; e < SG::UPT; ++e) {
+        const int u = tid + 256 * e;
+        if (u < SG::UNITS) reinterpret_cast<uint4 *>(ring[slot][k])[u] = sv.u[k][e];
+      }
+      if (tid < 16) ring_pos[slot][k][tid] = sv.pos[k];
+    }
+  };
+  auto operand = [&](const char *buf, typename O::reg (&kr)[KS]) {
+    const char *base = buf + lane * 16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int byte = ks * O::kPerStep * (int)sizeof(T);   // within the quarter row
+      kr[ks] = O::load(reinterpret_cast<const T *>(base + (byte / 16) * (kWave * 16) + byte % 16));
+    }
+  };
+
+  float m[NBW], l[NBW];
+  int urow[NBW];
+  float nlse[NBW][4];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    m[nb] = -__builtin_inff();
+    l[nb] = 0.f;
+    urow[nb] = row_u(row0 + nb * 16 + rr);
+    if (PASS == 1) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) nlse[nb][e] = -a.lse[lse_base + wave * 16 * NBW + nb * 16 + 4 * g4 + e];
+    }
+  }
+  float *pout = PASS == 1 ? a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o] : nullptr;
+
+  // One stage: all MFMAs of its GS sub-pages first, then one softmax update
+  // (pass 0) or the column sums (pass 1).
+  auto compute = [&](int st_idx, int slot) {
+    f32x4 acc[GS][NBW];
+    int meta[GS];
+#pragma unroll
+    for (int k = 0; k < GS; ++k) {
+      const int sp = st_idx * GS + k;
+      meta[k] = sp < n_sp ? sub_meta(ch, t, pl, sp) : 0;
+      typename O::reg kr[KS];
+      operand(ring[slot][k], kr);
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) {
+        acc[k][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          acc[k][nb] = PASS == 0 ? O::mma(kr[ks], q[nb][ks], acc[k][nb])
+                                 : O::mma(q[nb][ks], kr[ks], acc[k][nb]);
+      }
+    }
+    if (PASS == 0) {
+#pragma unroll
+      for (int k = 0; k < GS; ++k) {
+        const int d = meta[k] & 255, nvalid = meta[k] >> 8;
+        const bool own = d == own_d;
+        if (own || nvalid < 16) {
+          int kpos[4] = {0, 0, 0, 0};
+          if (own) {
+            const int4 pv = *reinterpret_cast<const int4 *>(&ring_pos[slot][k][4 * g4]);
+            kpos[0] = pv.x;
+            kpos[1] = pv.y;
+            kpos[2] = pv.z;
+            kpos[3] = pv.w;
+          }
+#pragma unroll
+          for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bool ok = 4 * g4 + e < nvalid && (!own || kpos[e] <= urow[nb]);
+              acc[k][nb][e] = ok ? acc[k][nb][e] : -__builtin_inff();
+            }
+        }
       }
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc = O::mma(kr[ks], q[nb][ks], acc);
-        float z[4];
+      for (int nb = 0; nb < NBW; ++nb) {
         float mx = -__builtin_inff();
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = 4 * g4 + e;
-          const bool ok = key < nvalid && (!own || kpos[e] <= urow[nb]);
-          z[e] = ok ? acc[e] * a.sl2 : -__builtin_inff();
-          mx = fmaxf(mx, z[e]);
-        }
+        for (int k = 0; k < GS; ++k)
+          mx = fmaxf(mx, fmaxf(fmaxf(acc[k][nb][0], acc[k][nb][1]), fmaxf(acc[k][nb][2], acc[k][nb][3])));
+        mx *= a.sl2;
         if (mx > m[nb]) {
-          if (m[nb] > -__builtin_inff()) l[nb] *= __builtin_amdgcn_exp2f(m[nb] - mx);
+          l[nb] *= __builtin_amdgcn_exp2f(m[nb] - mx);
           m[nb] = mx;
         }
-        if (m[nb] > -__builtin_inff()) {
+        const float nm = m[nb] > -__builtin_inff() ? -m[nb] : 0.f;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) l[nb] += __builtin_amdgcn_exp2f(z[e] - m[nb]);
+        for (int k = 0; k < GS; ++k)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) l[nb] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nm));
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < GS; ++k) {
+        const int d = meta[k] & 255;
+        const bool own = d == own_d && (st_idx * GS + k) < n_sp;
+        float colsum = 0.f;
+        if (own) {
+          const int kpos = ring_pos[slot][k][rr];
+#pragma unroll
+          for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float pz = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nlse[nb][e]));
+              colsum += (kpos < row_u(row0 + nb * 16 + 4 * g4 + e)) ? pz : 0.f;
+            }
+        } else {
+#pragma unroll
+          for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              colsum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nlse[nb][e]));
+        }
+        colsum += __shfl_xor(colsum, 16, kWave);
+        colsum += __shfl_xor(colsum, 32, kWave);
+        if (lane < 16) red[slot][k][wave][lane] = colsum;
+      }
+    }
+  };
+  auto finish = [&](int st_idx, int slot) {
+    if (PASS == 1 && tid < 16 * GS) {
+      const int k = tid >> 4, key = tid & 15;
+      const int sp = st_idx * GS + k;
+      if (sp < n_sp) {
+        const SubPage cur = sub_page(t, pl, ch, sp);
+        if (key < cur.nvalid) {
+          const float v = ((red[slot][k][0][key] + red[slot][k][1][key]) + red[slot][k][2][key]) +
+                          red[slot][k][3][key];
+          pout[cur.ctx + key] = v;
         }
       }
     }
-    // merge the four lane groups that share a query row, then the waves
+  };
+
+  if (n_st > 0) {
+    const int last = n_st - 1;
+    commit(0, fetch(0));
+    Staged s1 = fetch(min(1, last));
+    Staged s0 = fetch(min(2, last));
+    __syncthreads();
+    for (int st = 0; st < n_st; st += 2) {
+      // even stage: its successor sits in s1, the one after in s0
+      compute(st, 0);
+      if (st + 1 < n_st) commit(1, s1);
+      s1 = fetch(min(st + 3, last));
+      __syncthreads();
+      finish(st, 0);
+      const bool live = st + 1 < n_st;
+      if (live) compute(st + 1, 1);
+      if (st + 2 < n_st) commit(0, s0);
+      s0 = fetch(min(st + 4, last));
+      __syncthreads();
+      if (live) finish(st + 1, 1);
+    }
+  }
+  if (PASS == 0) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < NBW; ++nb) {
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1) {
         const float mo = __shfl_xor(m[nb], off, kWave);
@@ -210,68 +428,11 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
         l[nb] = ln;
       }
       if (g4 == 0) {
-        sm_m[wave][nb * 16 + rr] = m[nb];
-        sm_l[wave][nb * 16 + rr] = l[nb];
+        const int r = wave * 16 * NBW + nb * 16 + rr;
+        const bool valid = urow[nb] >= 0 && l[nb] > 0.f;
+        a.lse[lse_base + r] = valid ? m[nb] + __log2f(l[nb]) : __builtin_inff();
       }
     }
-    __syncthreads();
-    for (int r = threadIdx.x; r < 16 * NB; r += blockDim.x) {
-      float M = -__builtin_inff();
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w][r]);
-      float L = 0.f;
-      if (M > -__builtin_inff())
-        for (int w = 0; w < 4; ++w)
-          if (sm_m[w][r] > -__builtin_inff()) L += sm_l[w][r] * __builtin_amdgcn_exp2f(sm_m[w][r] - M);
-      const bool valid = row_u(rg * 16 * NB + r) >= 0 && L > 0.f;
-      a.lse[lse_base + r] = valid ? M + __log2f(L) : __builtin_inff();
-    }
-    return;
-  }
-
-  // ---- PASS 1: column sums of p = exp2(z - lse) over this row group -------
-  float lse[NB][4];
-  int urow[NB][4];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = nb * 16 + 4 * g4 + e;
-      lse[nb][e] = a.lse[lse_base + r];
-      urow[nb][e] = row_u(rg * 16 * NB + r);
-    }
-  const int n_sp = a.self_window ? ch.sp_off[own_d + 1] : ch.sp_off[own_d];
-  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
-  int d = 0;
-  for (int sp = wave; sp < n_sp; sp += 4) {
-    while (sp >= ch.sp_off[d + 1]) ++d;
-    const int q0 = (sp - ch.sp_off[d]) * 16;
-    const int page = t.page_table[ch.po[d] + q0 / pl.P];
-    const int r0 = q0 % pl.P;
-    const int nvalid = min(16, ch.c[d] - q0);
-    const bool own = d == own_d;
-    typename O::reg kr[KS];
-    const T *kp = reinterpret_cast<const T *>(kbase + row_byte_offset(pl, layer, page, g, r0 + rr)) +
-                  g4 * QTR;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kr[ks] = O::load(kp + ks * O::kPerStep);
-    const int kpos = own ? pl.slot_pos[(int64_t)page * pl.P + r0 + rr] : 0;
-    const bool kvalid = rr < nvalid;
-    float colsum = 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = O::mma(q[nb][ks], kr[ks], acc);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool ok = kvalid && (!own || kpos < urow[nb][e]);
-        const float pz = __builtin_amdgcn_exp2f(acc[e] * a.sl2 - lse[nb][e]);
-        colsum += ok ? pz : 0.f;
-      }
-    }
-    colsum += __shfl_xor(colsum, 16, kWave);
-    colsum += __shfl_xor(colsum, 32, kWave);
-    if (g4 == 0 && kvalid) pout[ch.ctx[d] + q0 + rr] = colsum;
   }
 }
 
@@ -279,6 +440,7 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
 __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__restrict__ obs, int n_obs,
                                                    int S, int Hkv, int n_rg, int64_t part_cap,
                                                    int64_t *__restrict__ pbase,
+                                                   int64_t *__restrict__ fbase,
                                                    int32_t *__restrict__ ctxlen,
                                                    int32_t *__restrict__ odepth,
                                                    int32_t *__restrict__ anc, int32_t *status) {
@@ -294,7 +456,7 @@ __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__rest
     if (!ok || c < 0 || c > t.n_full[i]) atomicOr(&s_err, 1);
   }
   __syncthreads();
-  int64_t run = 0;
+  int64_t run = 0, frun = 0;
   for (int base = 0; base < n_obs; base += blockDim.x) {
     const int o = base + threadIdx.x;
     int64_t len = 0;
@@ -324,24 +486,53 @@ __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__rest
       }
       ctxlen[o] = (int32_t)len;
     }
-    int64_t tot;
+    int64_t tot, ftot;
     const int64_t ex = block_exclusive_scan<int64_t>(len * S * Hkv * n_rg, sm, &tot);
-    if (o < n_obs) pbase[o] = run + ex;
+    const int64_t fx = block_exclusive_scan<int64_t>(len, sm, &ftot);
+    if (o < n_obs) {
+      pbase[o] = run + ex;
+      fbase[o] = frun + fx;
+    }
     run += tot;
+    frun += ftot;
   }
   __syncthreads();
+  // the folded sums live after the partials in the same buffer
+  for (int o = threadIdx.x; o < n_obs; o += blockDim.x) fbase[o] += run;
   if (threadIdx.x == 0) {
     if (s_err & 1) status_error(status, ARBOR_EINVAL);
     else if (s_err & 2) status_error(status, ARBOR_EUNSUPPORTED);
-    else if (run > part_cap) status_error(status, ARBOR_EWORKSPACE);
+    else if (run + frun > part_cap) status_error(status, ARBOR_EWORKSPACE);
   }
 }
 
-// A += partials of every observer below block i; rows_seen_i grows.
-__global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, float *__restrict__ A,
+// Fold the (slice layer, kv head, row group) slabs of every observer: one
+// column sum per (observer, credited context key), summed in slab order.
+__global__ __launch_bounds__(256) void score_fold(ScoreArgs a, float *__restrict__ fold,
+                                                  const int64_t *__restrict__ fbase) {
+  if (status_failed(a.status)) return;
+  const int o = blockIdx.x;
+  const int len = a.ctxlen[o];
+  const int own_c = a.t.n_kept[a.obs[o]];
+  const int credited = a.self_window ? len : len - own_c;
+  const int nslab = a.S * a.pl.Hkv * a.n_rg;
+  const float *src = a.part + a.pbase[o];
+  float *dst = fold + fbase[o];
+  for (int x = blockIdx.y * blockDim.x + threadIdx.x; x < credited; x += gridDim.y * blockDim.x) {
+    float acc = 0.f;
+    for (int sl = 0; sl < nslab; ++sl) acc += src[(int64_t)sl * len + x];
+    dst[x] = acc;
+  }
+}
+
+// A += folded sums of every observer below block i (observer order, fp64);
+// rows_seen_i grows.  The four waves of a workgroup split the observers of a
+// 64-slot chunk and are combined in wave order.
+__global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const float *__restrict__ fold,
+                                                    const int64_t *__restrict__ fbase,
+                                                    float *__restrict__ A,
                                                     int64_t *__restrict__ rows_seen) {
-  __shared__ int hits[256];
-  __shared__ int s_nh;
+  __shared__ int64_t hbase[256];
   __shared__ int s_wcnt[4];
   __shared__ double s_acc[4][64];
   if (status_failed(a.status)) return;
@@ -351,18 +542,16 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, float *__restri
   const int c = t.n_kept[i];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
-  // depth and context offset of block i
   int di = 0, ctxoff = 0;
   for (int x = t.parent[i]; x >= 0 && di < MAXD; x = t.parent[x]) {
     ++di;
     ctxoff += t.n_kept[x];
   }
-  const int nslab = a.S * pl.Hkv * a.n_rg;
   const int64_t tb = t.tok_off[i];
   const int64_t po = t.page_off[i];
   int64_t rows_add = 0;
+  const int nchunk = (c + 63) / 64;
   for (int ob = 0; ob < a.n_obs; ob += 256) {
-    // observers that credit block i, in observer order
     const int o = ob + threadIdx.x;
     bool hit = false;
     if (o < a.n_obs) {
@@ -374,40 +563,46 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, float *__restri
     __syncthreads();
     int before = 0;
     for (int w = 0; w < wave; ++w) before += s_wcnt[w];
-    if (hit) hits[before + rank_below(bm, lane)] = o;
-    if (threadIdx.x == 0) s_nh = s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
-    __syncthreads();
-    const int nh = s_nh;
-    if (blockIdx.y == 0 && threadIdx.x == 0) {
-      for (int h = 0; h < nh; ++h) {
-        const int jj = a.obs[hits[h]];
-        rows_add += (int64_t)a.S * pl.Hkv * pl.G * min(a.W, t.n_full[jj]);
-      }
+    const int nh = s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
+    if (hit) {
+      hbase[before + rank_below(bm, lane)] = fbase[o] + ctxoff;
+      if (blockIdx.y == 0) rows_add += (int64_t)a.S * pl.Hkv * pl.G * min(a.W, t.n_full[a.obs[o]]);
     }
-    // chunks of 64 slots; the 4 waves split the (hit, slab) pairs
-    for (int chk = blockIdx.y; chk * 64 < c; chk += gridDim.y) {
-      const int s = chk * 64 + lane;
-      double acc = 0.0;
-      if (s < c) {
-        for (int e = wave; e < nh * nslab; e += 4) {
-          const int h = e / nslab;
-          const int sl = e % nslab;
-          const int oo = hits[h];
-          acc += (double)a.part[a.pbase[oo] + (int64_t)sl * a.ctxlen[oo] + ctxoff + s];
+    __syncthreads();
+    if (nh > 0) {
+      for (int chk = blockIdx.y; chk < nchunk; chk += gridDim.y) {
+        const int s = chk * 64 + lane;
+        double acc = 0.0;
+        if (s < c) {
+          int h = wave;
+          for (; h + 12 < nh; h += 16) {
+            const float f0 = fold[hbase[h] + s];
+            const float f1 = fold[hbase[h + 4] + s];
+            const float f2 = fold[hbase[h + 8] + s];
+            const float f3 = fold[hbase[h + 12] + s];
+            acc += (double)f0;
+            acc += (double)f1;
+            acc += (double)f2;
+            acc += (double)f3;
+          }
+          for (; h < nh; h += 4) acc += (double)fold[hbase[h] + s];
         }
+        s_acc[wave][lane] = acc;
+        __syncthreads();
+        if (wave == 0 && s < c) {
+          const double tot = ((s_acc[0][lane] + s_acc[1][lane]) + s_acc[2][lane]) + s_acc[3][lane];
+          const int page = t.page_table[po + s / pl.P];
+          const int pos = pl.slot_pos[(int64_t)page * pl.P + s % pl.P];
+          A[tb + pos] = (float)((double)A[tb + pos] + tot);
+        }
+        __syncthreads();
       }
-      s_acc[wave][lane] = acc;
-      __syncthreads();
-      if (wave == 0 && s < c) {
-        const double tot = ((s_acc[0][lane] + s_acc[1][lane]) + s_acc[2][lane]) + s_acc[3][lane];
-        const int page = t.page_table[po + s / pl.P];
-        const int pos = pl.slot_pos[(int64_t)page * pl.P + s % pl.P];
-        A[tb + pos] = (float)((double)A[tb + pos] + tot);
-      }
-      __syncthreads();
     }
   }
-  if (blockIdx.y == 0 && threadIdx.x == 0) rows_seen[i] += rows_add;
+  if (blockIdx.y == 0) {
+    rows_add = block_sum<int64_t>(rows_add, reinterpret_cast<int64_t *>(&s_acc[0][0]));
+    if (threadIdx.x == 0) rows_seen[i] += rows_add;
+  }
 }
 
 // a_i and s_i from the updated A (one wave per block).
@@ -437,47 +632,51 @@ __global__ __launch_bounds__(256) void score_final(Tree t, const float *__restri
   }
 }
 
+#ifndef ARBOR_SCORE_STAGE
+#define ARBOR_SCORE_STAGE 2
+#endif
+constexpr int kStageSub = ARBOR_SCORE_STAGE;   // sub-pages staged per barrier
+
 template <int PASS, class T, int D>
-void launch_pass_nb(int NB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
-  switch (NB) {
-    case 1: hipLaunchKernelGGL((score_pass<PASS, T, D, 1>), grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((score_pass<PASS, T, D, 2>), grid, dim3(256), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((score_pass<PASS, T, D, 4>), grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL((score_pass<PASS, T, D, 8>), grid, dim3(256), 0, stream, a); break;
+void launch_pass_nb(int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  switch (NBW) {
+    case 1: hipLaunchKernelGGL((score_pass<PASS, T, D, 1, kStageSub>), grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((score_pass<PASS, T, D, 2, kStageSub>), grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL((score_pass<PASS, T, D, 4, kStageSub>), grid, dim3(256), 0, stream, a); break;
   }
 }
 
 template <int PASS>
-void launch_pass(int dtype, int D, int NB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+void launch_pass(int dtype, int D, int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
   if (dtype == ARBOR_BF16) {
-    if (D == 128) launch_pass_nb<PASS, __bf16, 128>(NB, grid, stream, a);
-    else launch_pass_nb<PASS, __bf16, 64>(NB, grid, stream, a);
+    if (D == 128) launch_pass_nb<PASS, __bf16, 128>(NBW, grid, stream, a);
+    else launch_pass_nb<PASS, __bf16, 64>(NBW, grid, stream, a);
   } else {
-    if (D == 128) launch_pass_nb<PASS, float, 128>(NB, grid, stream, a);
-    else launch_pass_nb<PASS, float, 64>(NB, grid, stream, a);
+    if (D == 128) launch_pass_nb<PASS, float, 128>(NBW, grid, stream, a);
+    else launch_pass_nb<PASS, float, 64>(NBW, grid, stream, a);
   }
 }
 
-int rows_per_group(int rows_total) {
-  int nb = (rows_total + 15) / 16;
-  if (nb <= 1) return 1;
-  if (nb <= 2) return 2;
-  if (nb <= 4) return 4;
-  return 8;
+// Row blocks per wave: the workgroup (4 waves) covers 64 * NBW query rows.
+int blocks_per_wave(int rows_total) {
+  if (rows_total <= 64) return 1;
+  if (rows_total <= 128) return 2;
+  return 4;
 }
 
 }  // namespace
 
 size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const int rows_total = g->q_per_kv * sz->window;
-  const int NB = rows_per_group(rows_total);
+  const int NB = 4 * blocks_per_wave(rows_total);
   const int n_rg = (rows_total + 16 * NB - 1) / (16 * NB);
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
   b += nobs * 8 + nobs * 4 * 2 + nobs * MAXD * 4 + 4 * 256;
   b += nobs * slabs * 16 * NB * 4 + 256;
-  b += nobs * slabs * (size_t)sz->max_context * 4 + 256;
+  b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
+  b += nobs * 8 + 256;
   return b;
 }
 
@@ -490,6 +689,7 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   Tree t = make_tree(tree);
   Pool pl = make_pool(geom, pool);
   if (t.V <= 0) return ARBOR_OK;
+  if ((int64_t)pl.num_pages * pl.Hkv * pl.P >= ((int64_t)1 << 31)) return ARBOR_EUNSUPPORTED;
   ScoreArgs a;
   a.t = t;
   a.pl = pl;
@@ -500,7 +700,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.S = n_slice;
   for (int e = 0; e < 8; ++e) a.slice[e] = e < n_slice ? slice_layers[e] : 0;
   const int rows_total = pl.G * window;
-  const int NB = rows_per_group(rows_total);
+  const int NBW = blocks_per_wave(rows_total);
+  const int NB = 4 * NBW;
   a.n_rg = (rows_total + 16 * NB - 1) / (16 * NB);
   const float scale = params->softmax_scale > 0.f ? params->softmax_scale
                                                   : 1.0f / sqrtf((float)geom->head_dim);
@@ -510,6 +711,7 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   Carve cv(workspace, workspace_bytes);
   const size_t nobs = n_obs > 0 ? (size_t)n_obs : 1;
   int64_t *pbase = cv.take<int64_t>(nobs);
+  int64_t *fbase = cv.take<int64_t>(nobs);
   int32_t *ctxlen = cv.take<int32_t>(nobs);
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
@@ -526,11 +728,13 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.anc = anc;
   if (n_obs > 0) {
     hipLaunchKernelGGL(score_plan, dim3(1), dim3(1024), 0, stream, t, observers, n_obs, n_slice,
-                       pl.Hkv, a.n_rg, part_cap, pbase, ctxlen, odepth, anc, status);
+                       pl.Hkv, a.n_rg, part_cap, pbase, fbase, ctxlen, odepth, anc, status);
     const dim3 grid(n_obs, n_slice * pl.Hkv, a.n_rg);
-    launch_pass<0>(geom->dtype, geom->head_dim, NB, grid, stream, a);
-    launch_pass<1>(geom->dtype, geom->head_dim, NB, grid, stream, a);
-    hipLaunchKernelGGL(score_reduce, dim3(t.V, 8), dim3(256), 0, stream, a, A, rows_seen);
+    launch_pass<0>(geom->dtype, geom->head_dim, NBW, grid, stream, a);
+    launch_pass<1>(geom->dtype, geom->head_dim, NBW, grid, stream, a);
+    hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, part, fbase);
+    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, part, fbase, A,
+                       rows_seen);
   }
   hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen,
                      v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out,

@@ -20,6 +20,161 @@ struct NodeView {
   }
 };
 
+constexpr int kCached = 8;   // resident slots per lane held in registers
+
+// Count, per 4-bit digit, the matching keys of one 64-wide chunk (ballots).
+__device__ __forceinline__ void digit_counts(bool match, uint32_t dig, int (&cnt)[16]) {
+  const uint64_t bm = ballot(match);
+  const uint64_t b0 = ballot(match && (dig & 1u));
+  const uint64_t b1 = ballot(match && (dig & 2u));
+  const uint64_t b2 = ballot(match && (dig & 4u));
+  const uint64_t b3 = ballot(match && (dig & 8u));
+#pragma unroll
+  for (int b = 0; b < 16; ++b) {
+    const uint64_t mm = bm & ((b & 1) ? b0 : ~b0) & ((b & 2) ? b1 : ~b1) &
+                        ((b & 4) ? b2 : ~b2) & ((b & 8) ? b3 : ~b3);
+    cnt[b] += popc(mm);
+  }
+}
+
+// Pick the digit holding the `remaining`-th largest key; updates remaining.
+__device__ __forceinline__ int pick_digit(const int (&cnt)[16], int &remaining) {
+  for (int b = 15; b >= 0; --b) {
+    if (cnt[b] >= remaining) return b;
+    remaining -= cnt[b];
+  }
+  return 0;
+}
+
+// Nodes with at most 64 * kCached resident slots: keys and positions stay in
+// registers for every radix pass.
+__device__ void select_cached(const NodeView &nv, const float *__restrict__ A, int c, int ki,
+                              int thr, int mode, int32_t *__restrict__ out, int32_t *status,
+                              int lane) {
+  uint32_t key[kCached];
+  int pos[kCached];
+  bool nan = false;
+  int n_head = 0;
+#pragma unroll
+  for (int r = 0; r < kCached; ++r) {
+    const int s = r * kWave + lane;
+    const bool v = s < c;
+    const int p = v ? nv.pos(s) : 0;
+    const float a = v ? A[p] : 0.f;
+    nan |= v && (a != a);
+    key[r] = ordered_key(a);
+    pos[r] = p;
+    if (r * kWave < c) n_head += popc(ballot(v && p < thr));
+  }
+  if (ballot(nan)) {
+    if (lane == 0) status_error(status, ARBOR_ENONFINITE);
+    return;
+  }
+  const int n_tail = c - n_head;
+  if (mode == ARBOR_SELECT_TAIL_ONLY || ki <= n_tail) {
+#pragma unroll
+    for (int r = 0; r < kCached; ++r) {
+      const int s = r * kWave + lane;
+      if (s >= c - ki && s < c) out[s - (c - ki)] = pos[r];
+    }
+    return;
+  }
+  const int m = ki - n_tail;
+  uint32_t prefix = 0, pmask = 0;
+  int remaining = m;
+  for (int shift = 28; shift >= 0; shift -= 4) {
+    int cnt[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b) cnt[b] = 0;
+#pragma unroll
+    for (int r = 0; r < kCached; ++r) {
+      if (r * kWave >= n_head) break;
+      const int s = r * kWave + lane;
+      const bool match = s < n_head && ((key[r] & pmask) == prefix);
+      digit_counts(match, (key[r] >> shift) & 15u, cnt);
+    }
+    prefix |= (uint32_t)pick_digit(cnt, remaining) << shift;
+    pmask |= 15u << shift;
+  }
+  int written = 0, ties = 0;
+#pragma unroll
+  for (int r = 0; r < kCached; ++r) {
+    if (r * kWave >= c) break;
+    const int s = r * kWave + lane;
+    const bool head = s < n_head;
+    const bool gt = head && key[r] > prefix;
+    const bool eq = head && key[r] == prefix;
+    const uint64_t beq = ballot(eq);
+    const bool take = gt || (eq && ties + rank_below(beq, lane) < remaining);
+    const uint64_t bt = ballot(take);
+    const int dst = written + rank_below(bt, lane);
+    if (take && dst < m) out[dst] = pos[r];
+    written += popc(bt);
+    ties += popc(beq);
+    if (s >= n_head && s < c) out[m + s - n_head] = pos[r];   // the tail, in order
+  }
+  if (written != m && lane == 0) status_error(status, ARBOR_ECORRUPT);
+}
+
+// Larger nodes: every pass streams the keys again (L2-resident).
+__device__ void select_streamed(const NodeView &nv, const float *__restrict__ A, int c, int ki,
+                                int thr, int mode, int32_t *__restrict__ out, int32_t *status,
+                                int lane) {
+  int n_head = 0;
+  bool nan = false;
+  for (int base = 0; base < c; base += kWave) {
+    const int s = base + lane;
+    const bool v = s < c;
+    const int p = v ? nv.pos(s) : 0;
+    const float a = v ? A[p] : 0.f;
+    nan |= v && (a != a);
+    n_head += popc(ballot(v && p < thr));
+  }
+  if (ballot(nan)) {
+    if (lane == 0) status_error(status, ARBOR_ENONFINITE);
+    return;
+  }
+  const int n_tail = c - n_head;
+  if (mode == ARBOR_SELECT_TAIL_ONLY || ki <= n_tail) {
+    for (int s = lane; s < ki; s += kWave) out[s] = nv.pos(c - ki + s);
+    return;
+  }
+  const int m = ki - n_tail;
+  uint32_t prefix = 0, pmask = 0;
+  int remaining = m;
+  for (int shift = 28; shift >= 0; shift -= 4) {
+    int cnt[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b) cnt[b] = 0;
+    for (int base = 0; base < n_head; base += kWave) {
+      const int s = base + lane;
+      const bool v = s < n_head;
+      const uint32_t key = v ? ordered_key(A[nv.pos(s)]) : 0u;
+      digit_counts(v && ((key & pmask) == prefix), (key >> shift) & 15u, cnt);
+    }
+    prefix |= (uint32_t)pick_digit(cnt, remaining) << shift;
+    pmask |= 15u << shift;
+  }
+  int written = 0, ties = 0;
+  for (int base = 0; base < n_head; base += kWave) {
+    const int s = base + lane;
+    const bool v = s < n_head;
+    const int p = v ? nv.pos(s) : 0;
+    const uint32_t key = v ? ordered_key(A[p]) : 0u;
+    const bool gt = v && key > prefix;
+    const bool eq = v && key == prefix;
+    const uint64_t beq = ballot(eq);
+    const bool take = gt || (eq && ties + rank_below(beq, lane) < remaining);
+    const uint64_t bt = ballot(take);
+    const int dst = written + rank_below(bt, lane);
+    if (take && dst < m) out[dst] = p;
+    written += popc(bt);
+    ties += popc(beq);
+  }
+  if (written != m && lane == 0) status_error(status, ARBOR_ECORRUPT);
+  for (int s = lane; s < n_tail; s += kWave) out[m + s] = nv.pos(n_head + s);
+}
+
 __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const float *__restrict__ A,
                                                      const int32_t *__restrict__ k, int l_tail,
                                                      int mode, int32_t *__restrict__ sel_pos,
@@ -38,87 +193,9 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
   const int n = t.n_full[i];
   const int64_t tb = t.tok_off[i];
   const NodeView nv{t.page_table, pl.slot_pos, t.page_off[i], pl.P};
-  const int thr = n - l_tail;
-
-  // Resident positions are ascending in slot order, so the tail is a suffix.
-  int n_head = 0;
-  bool nan = false;
-  for (int base = 0; base < c; base += kWave) {
-    const int s = base + lane;
-    const bool v = s < c;
-    const int p = v ? nv.pos(s) : 0;
-    const float a = v ? A[tb + p] : 0.f;
-    nan |= v && (a != a);
-    n_head += popc(ballot(v && p < thr));
-  }
-  if (ballot(nan)) {
-    if (lane == 0) status_error(status, ARBOR_ENONFINITE);
-    return;
-  }
-  const int n_tail = c - n_head;
   int32_t *out = sel_pos + tb;
-  if (mode == ARBOR_SELECT_TAIL_ONLY || ki <= n_tail) {
-    for (int s = lane; s < ki; s += kWave) out[s] = nv.pos(c - ki + s);
-    return;
-  }
-
-  // m-th largest key among the head slots [0, n_head).
-  const int m = ki - n_tail;
-  uint32_t prefix = 0, pmask = 0;
-  int remaining = m;
-  for (int shift = 28; shift >= 0; shift -= 4) {
-    int cnt[16];
-#pragma unroll
-    for (int b = 0; b < 16; ++b) cnt[b] = 0;
-    for (int base = 0; base < n_head; base += kWave) {
-      const int s = base + lane;
-      const bool v = s < n_head;
-      const uint32_t key = v ? ordered_key(A[tb + nv.pos(s)]) : 0u;
-      const bool match = v && ((key & pmask) == prefix);
-      const uint32_t dig = (key >> shift) & 15u;
-      const uint64_t bm = ballot(match);
-      const uint64_t b0 = ballot(match && (dig & 1u));
-      const uint64_t b1 = ballot(match && (dig & 2u));
-      const uint64_t b2 = ballot(match && (dig & 4u));
-      const uint64_t b3 = ballot(match && (dig & 8u));
-#pragma unroll
-      for (int b = 0; b < 16; ++b) {
-        const uint64_t mm = bm & ((b & 1) ? b0 : ~b0) & ((b & 2) ? b1 : ~b1) &
-                            ((b & 4) ? b2 : ~b2) & ((b & 8) ? b3 : ~b3);
-        cnt[b] += popc(mm);
-      }
-    }
-    int chosen = 0;
-    for (int b = 15; b >= 0; --b) {
-      if (cnt[b] >= remaining) {
-        chosen = b;
-        break;
-      }
-      remaining -= cnt[b];
-    }
-    prefix |= (uint32_t)chosen << shift;
-    pmask |= 15u << shift;
-  }
-
-  // Keys above the threshold, then `remaining` of the tied keys in slot order.
-  int written = 0, ties = 0;
-  for (int base = 0; base < n_head; base += kWave) {
-    const int s = base + lane;
-    const bool v = s < n_head;
-    const int p = v ? nv.pos(s) : 0;
-    const uint32_t key = v ? ordered_key(A[tb + p]) : 0u;
-    const bool gt = v && key > prefix;
-    const bool eq = v && key == prefix;
-    const uint64_t beq = ballot(eq);
-    const bool take = gt || (eq && ties + rank_below(beq, lane) < remaining);
-    const uint64_t bt = ballot(take);
-    const int dst = written + rank_below(bt, lane);
-    if (take && dst < m) out[dst] = p;
-    written += popc(bt);
-    ties += popc(beq);
-  }
-  if (written != m && lane == 0) status_error(status, ARBOR_ECORRUPT);
-  for (int s = lane; s < n_tail; s += kWave) out[m + s] = nv.pos(n_head + s);
+  if (c <= kWave * kCached) select_cached(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane);
+  else select_streamed(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane);
 }
 
 }  // namespace

@@ -321,6 +321,22 @@ def test_score_after_eviction():
     _close(s, so)
 
 
+def test_score_long_chain():
+    """Chains longer than the score kernel's in-LDS sub-page table."""
+    parent, n_full = [-1, 0, 1], [7000, 6000, 5003]
+    st = synth.build_state(parent, n_full, layers=1, kv_heads=1, q_per_kv=1, head_dim=64,
+                           dtype="bf16", seed=3, shuffle_pages=True, page_size=32, window=4,
+                           active=[2], heavy_frac=0.01)
+    kv = to_gpu(st)
+    ost = oracle_state(st)
+    A, rows, a, s, sg = _gpu_score(st, kv, PARAMS)
+    Ao, ro, ao, so = _oracle_score(st, ost, PARAMS)
+    assert sg == L.OK
+    _close(A, Ao)
+    assert np.array_equal(rows, ro)
+    _close(s, so)
+
+
 # --------------------------------------------------------------------------- decode
 def _gpu_decode(st, kv, leaves, l0, l1, q, out_dtype=torch.float32):
     n = leaves.numel()
