@@ -200,34 +200,130 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   }
 }
 
-// Column of head_dim that lane group g4 supplies at MFMA k-step ks.  K and Q
-// use the same map, so the dot product is unchanged; it makes the four lane
-// groups of one k-step read consecutive 16-byte pieces of a row.
-template <class T>
-__device__ __forceinline__ int frag_col(int ks, int g4) {
-  constexpr int VEC = 16 / (int)sizeof(T);          // elements per 16 bytes
-  constexpr int SPV = VEC / Op<T>::kPerStep;        // k-steps per 16 bytes
-  return (ks / SPV) * 4 * VEC + g4 * VEC + (ks % SPV) * Op<T>::kPerStep;
+// K and V of GSP consecutive 16-slot sub-pages of one unit, in MFMA operand
+// layout: lane (rr, g4) holds key row rr of each sub-page (S = K Q^T), and
+// value rows 4 g4 + e, columns NC rr .. NC rr + NC - 1 (O += P V).
+template <class T, int D, int GSP>
+struct KVFrag {
+  typedef typename std::conditional<sizeof(T) == 2, __bf16, float>::type VT;
+  static constexpr int KS = D / 4 / Op<T>::kPerStep;
+  static constexpr int NC = D / 16;
+  typename Op<T>::reg k[GSP][KS];
+  VT v[GSP][4][NC];
+  int nval[GSP];  // valid slots of each sub-page (0: padding, never counted)
+};
+
+template <class T, int D, int GSP>
+__device__ __forceinline__ KVFrag<T, D, GSP> fetch_kv(const Pool &pl, int pg, int layer, int g,
+                                                      int s_begin, int s_end, int n_sub, int sub0,
+                                                      int rr, int g4) {
+  typedef KVFrag<T, D, GSP> F;
+  F f;
+  const char *kb = static_cast<const char *>(pl.k);
+  const char *vb = static_cast<const char *>(pl.v);
+#pragma unroll
+  for (int sp = 0; sp < GSP; ++sp) {
+    // clamped to a valid sub-page so that every load is unconditional
+    const int sub = min(sub0 + sp, n_sub - 1);
+    const int q0 = s_begin + sub * 16;
+    f.nval[sp] = sub0 + sp < n_sub ? min(16, s_end - q0) : 0;
+    const int page = __shfl(pg, sub, kWave);  // lane j holds sub-page j's page
+    const int r0 = q0 % pl.P;
+    const T *kp = reinterpret_cast<const T *>(kb + row_byte_offset(pl, layer, page, g, r0 + rr));
+#pragma unroll
+    for (int ks = 0; ks < F::KS; ++ks) f.k[sp][ks] = Op<T>::load(kp + frag_col<T>(ks, g4));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const typename F::VT *vp = reinterpret_cast<const typename F::VT *>(
+                                     vb + row_byte_offset(pl, layer, page, g, r0 + 4 * g4 + e)) +
+                                 F::NC * rr;
+#pragma unroll
+      for (int cc = 0; cc < F::NC; ++cc) f.v[sp][e][cc] = vp[cc];
+    }
+  }
+  return f;
 }
 
-// One workgroup: one work unit (a CHUNK of a chain node's slots, one layer,
-// one kv head), rows [rbase, rbase + 16 NB).  Wave w takes the 16-slot
-// sub-pages w, w + 4, ... in groups of two whose K and V load together; the four
-// waves' (max, sum, o) are merged in LDS in wave order.
+// Online-softmax update of one wave's rows with one fragment.
+template <class T, int D, int NB, int GSP>
+__device__ __forceinline__ void attend(const KVFrag<T, D, GSP> &f,
+                                       const typename Op<T>::reg (&q)[NB][KVFrag<T, D, GSP>::KS],
+                                       float sl2, int g4, float (&m_run)[NB], float (&l_run)[NB],
+                                       f32x4 (&o)[NB][D / 16]) {
+  typedef KVFrag<T, D, GSP> F;
+  constexpr int NC = F::NC;
+  float sv[GSP][NB][4];
+  float gmax[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) gmax[nb] = -__builtin_inff();
+#pragma unroll
+  for (int sp = 0; sp < GSP; ++sp) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < F::KS; ++ks) acc = Op<T>::mma(f.k[sp][ks], q[nb][ks], acc);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float z = (4 * g4 + e < f.nval[sp]) ? acc[e] * sl2 : -__builtin_inff();
+        sv[sp][nb][e] = z;
+        gmax[nb] = fmaxf(gmax[nb], z);
+      }
+    }
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 16, kWave));
+    gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 32, kWave));
+    const float mn = fmaxf(m_run[nb], gmax[nb]);
+    const float alpha = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
+    m_run[nb] = mn;
+    l_run[nb] *= alpha;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float fe = __shfl(alpha, 4 * g4 + e, kWave);
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) o[nb][cc][e] *= fe;
+    }
+  }
+#pragma unroll
+  for (int sp = 0; sp < GSP; ++sp) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float p[4];
+      const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
+        l_run[nb] += p[e];
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        // a slot past the resident count may hold anything: its row is zeroed
+        const bool kv = 4 * g4 + ks < f.nval[sp];
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc)
+          o[nb][cc] = mma_f32(p[ks], kv ? (float)f.v[sp][ks][cc] : 0.f, o[nb][cc]);
+      }
+    }
+  }
+}
+
+// One wave: one work unit (a CHUNK of a chain node's slots, one layer, one kv
+// head), rows [rbase, rbase + 16 NB).  The unit's sub-pages are taken GSP at
+// a time; with DB the next fragment is in flight while the current one is
+// attended, so HBM streaming overlaps the MFMA work.
 template <class T, int D, int NB>
-__device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase, float *sm_o,
-                            float *sm_m, float *sm_l) {
+__device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase) {
   using O = Op<T>;
-  constexpr int KS = D / 4 / O::kPerStep;  // MFMA k-steps over head_dim (S = K Q^T)
-  constexpr int NC = D / 16;               // output column chunks; lane owns NC columns
-  constexpr int GSP = 4 / NB;              // sub-pages per group (registers)
-  constexpr int RWS = 16 * NB;             // rows handled in this pass
-  typedef typename std::conditional<sizeof(T) == 2, __bf16, float>::type VT;
+  constexpr int GSP = NB == 1 ? 2 : 1;
+  constexpr bool DB = NB <= 2;
+  typedef KVFrag<T, D, GSP> F;
+  constexpr int KS = F::KS;
+  constexpr int NC = F::NC;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
-  const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = tid >> 6;
   const int rr = lane & 15;
   const int g4 = lane >> 4;
   const int G = pl.G;
@@ -242,15 +338,26 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   const int Hq = pl.Hkv * G;
   const int64_t po = t.page_off[node];
   const int loff = a.node_leaf_off[node];
+  const int n_sub = (s_end - s_begin + 15) / 16;
+  const int n_grp = (n_sub + GSP - 1) / GSP;
+  // page ids of all sub-pages up front: a dependent load inside the pipeline
+  // would make every wait cover the fragment still in flight
+  static_assert(CHUNK / 16 <= kWave, "one lane per sub-page");
+  const int pg = lane < n_sub ? t.page_table[po + (s_begin + 16 * lane) / pl.P] : 0;
 
+  int qleaf[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int r = rbase + nb * 16 + rr;
+    qleaf[nb] = r < R ? a.leaf_list[loff + r / G] : -1;
+  }
   typename O::reg q[NB][KS];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int r = rbase + nb * 16 + rr;
-    if (r < R) {
-      const int b = a.leaf_list[loff + r / G];
+    if (qleaf[nb] >= 0) {
       const int h = g * G + r % G;
-      const T *qp = static_cast<const T *>(a.q) + (((int64_t)b * a.Lr + lr) * Hq + h) * D;
+      const T *qp = static_cast<const T *>(a.q) + (((int64_t)qleaf[nb] * a.Lr + lr) * Hq + h) * D;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::load(qp + frag_col<T>(ks, g4));
     } else {
@@ -258,6 +365,7 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
       for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::zero();
     }
   }
+  F cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, 0, rr, g4);
   float m_run[NB], l_run[NB];
   f32x4 o[NB][NC];
 #pragma unroll
@@ -267,172 +375,66 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) o[nb][cc] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const char *kb = static_cast<const char *>(pl.k);
-  const char *vb = static_cast<const char *>(pl.v);
-  const int n_sub = (s_end - s_begin + 15) / 16;
-  for (int base = wave; base < n_sub; base += 4 * GSP) {
-    typename O::reg kr[GSP][KS];
-    VT vr[GSP][4][NC];
-    int nval[GSP];
-#pragma unroll
-    for (int sp = 0; sp < GSP; ++sp) {
-      // clamp to a valid sub-page so every load is unconditional
-      const int sub = min(base + 4 * sp, n_sub - 1);
-      const int q0 = s_begin + sub * 16;
-      nval[sp] = base + 4 * sp < n_sub ? min(16, s_end - q0) : 0;
-      const int page = t.page_table[po + q0 / pl.P];
-      const int r0 = q0 % pl.P;
-      const T *kp = reinterpret_cast<const T *>(kb + row_byte_offset(pl, layer, page, g, r0 + rr));
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kr[sp][ks] = O::load(kp + frag_col<T>(ks, g4));
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const VT *vp = reinterpret_cast<const VT *>(vb + row_byte_offset(pl, layer, page, g, r0 + 4 * g4 + ks)) + NC * rr;
-#pragma unroll
-        for (int cc = 0; cc < NC; ++cc) vr[sp][ks][cc] = vp[cc];
-      }
+  if (DB) {
+    // two fragments alternate; the last prefetch of an odd count is a clamped
+    // re-read of the final sub-pages with no valid slots
+    for (int gi = 0; gi < n_grp; gi += 2) {
+      F nxt = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, (gi + 1) * GSP, rr, g4);
+      // keep the prefetch ahead of the work on the current fragment
+      __builtin_amdgcn_sched_barrier(0);
+      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
+      if (gi + 1 >= n_grp) break;
+      cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, (gi + 2) * GSP, rr, g4);
+      __builtin_amdgcn_sched_barrier(0);
+      attend<T, D, NB, GSP>(nxt, q, a.sl2, g4, m_run, l_run, o);
     }
-    float sv[GSP][NB][4];
-    float gmax[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) gmax[nb] = -__builtin_inff();
-#pragma unroll
-    for (int sp = 0; sp < GSP; ++sp) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc = O::mma(kr[sp][ks], q[nb][ks], acc);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float z = (4 * g4 + e < nval[sp]) ? acc[e] * a.sl2 : -__builtin_inff();
-          sv[sp][nb][e] = z;
-          gmax[nb] = fmaxf(gmax[nb], z);
-        }
-      }
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 16, kWave));
-      gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 32, kWave));
-      const float mn = fmaxf(m_run[nb], gmax[nb]);
-      const float alpha = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
-      m_run[nb] = mn;
-      l_run[nb] *= alpha;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float fe = __shfl(alpha, 4 * g4 + e, kWave);
-#pragma unroll
-        for (int cc = 0; cc < NC; ++cc) o[nb][cc][e] *= fe;
-      }
-    }
-#pragma unroll
-    for (int sp = 0; sp < GSP; ++sp) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        float p[4];
-        const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
-          l_run[nb] += p[e];
-        }
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          // a slot past the resident count may hold anything: its row is zeroed
-          const bool kv = 4 * g4 + ks < nval[sp];
-#pragma unroll
-          for (int cc = 0; cc < NC; ++cc)
-            o[nb][cc] = mma_f32(p[ks], kv ? (float)vr[sp][ks][cc] : 0.f, o[nb][cc]);
-        }
-      }
+  } else {
+    for (int gi = 0; gi < n_grp; ++gi) {
+      if (gi > 0) cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, gi * GSP, rr, g4);
+      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
     }
   }
-  // merge the four waves in LDS: row maxima, then o accumulated wave by wave
+  // partial rows [m, l, o(0..D-1)] of this unit
+  const int64_t stride = D + 2;
+  const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
+  float *outp = a.part + (slab + a.item_rowbase[item]) * stride;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     float l = l_run[nb];
     l += __shfl_xor(l, 16, kWave);
     l += __shfl_xor(l, 32, kWave);
-    if (g4 == 0) {
-      sm_m[wave * RWS + nb * 16 + rr] = m_run[nb];
-      sm_l[wave * RWS + nb * 16 + rr] = l;
+    const int row = rbase + nb * 16 + rr;
+    if (g4 == 0 && row < R) {
+      outp[row * stride] = m_run[nb];
+      outp[row * stride + 1] = l;
     }
-  }
-  __syncthreads();
-  float fo[NB][4];   // this wave's factor for its O-layout rows
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int r = nb * 16 + 4 * g4 + e;
-      float M = -__builtin_inff();
+      const int orow = rbase + nb * 16 + 4 * g4 + e;
+      if (orow < R) {
+        float *op = outp + orow * stride + 2 + NC * rr;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w * RWS + r]);
-      const float mw = sm_m[wave * RWS + r];
-      fo[nb][e] = (mw > -__builtin_inff()) ? __builtin_amdgcn_exp2f(mw - M) : 0.f;
+        for (int cc = 0; cc < NC; ++cc) op[cc] = o[nb][cc][e];
+      }
     }
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float *dst = sm_o + (nb * 16 + 4 * g4 + e) * D + NC * rr;
-#pragma unroll
-          for (int cc = 0; cc < NC; ++cc)
-            dst[cc] = (w == 0 ? 0.f : dst[cc]) + o[nb][cc][e] * fo[nb][e];
-        }
-    }
-    __syncthreads();
   }
-  // one partial row per query row: [m, l, o(0..D-1)]
-  const int64_t stride = D + 2;
-  const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
-  float *outp = a.part + (slab + a.item_rowbase[item]) * stride;
-  for (int r = wave; r < RWS; r += 4) {
-    const int row = rbase + r;
-    if (row >= R) continue;
-    float M = -__builtin_inff();
-#pragma unroll
-    for (int w = 0; w < 4; ++w) M = fmaxf(M, sm_m[w * RWS + r]);
-    float L = 0.f;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const float mw = sm_m[w * RWS + r];
-      if (mw > -__builtin_inff()) L += sm_l[w * RWS + r] * __builtin_amdgcn_exp2f(mw - M);
-    }
-    float *op = outp + row * stride;
-    if (lane == 0) {
-      op[0] = M;
-      op[1] = L;
-    }
-    for (int d = lane; d < D; d += kWave) op[2 + d] = sm_o[r * D + d];
-  }
-  __syncthreads();
 }
 
 template <class T, int D, int NB>
 __global__ __launch_bounds__(256) void decode_attn(DecArgs a, int cls) {
-  __shared__ float sm_o[16 * NB * D];
-  __shared__ float sm_m[4 * 16 * NB];
-  __shared__ float sm_l[4 * 16 * NB];
-  __shared__ int s_bad;
-  // the whole workgroup takes the same decision: the unit below synchronises
-  if (threadIdx.x == 0) s_bad = status_failed(a.status);
-  __syncthreads();
-  if (s_bad) return;
+  if (status_failed(a.status)) return;
   const int n_items = a.meta[cls];
   const int planes = a.Lr * a.pl.Hkv;
   const int64_t total = (int64_t)n_items * planes;
-  for (int64_t w = blockIdx.x; w < total; w += gridDim.x) {
+  // the wave index is wave-uniform: keep the unit's bookkeeping scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (int64_t w = (int64_t)blockIdx.x * 4 + wave; w < total; w += (int64_t)gridDim.x * 4) {
     const int item = a.cls_items[(int64_t)cls * a.max_items + w / planes];
     const int rem = (int)(w % planes);
     const int lr = rem / a.pl.Hkv;
     const int g = rem % a.pl.Hkv;
     const int R = a.node_nl[a.item_node[item]] * a.pl.G;
-    for (int rbase = 0; rbase < R; rbase += 16 * NB)
-      decode_unit<T, D, NB>(a, item, lr, g, rbase, sm_o, sm_m, sm_l);
+    for (int rbase = 0; rbase < R; rbase += 16 * NB) decode_unit<T, D, NB>(a, item, lr, g, rbase);
   }
 }
 
@@ -525,7 +527,7 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 template <class T, int D>
 void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *lse_out,
                            hipStream_t stream) {
-  const int grid = 8192;
+  const int grid = 2048;
   // rows of a work unit are at most n_leaves * G: only the row classes that
   // can occur are launched
   const int max_rows = a.n_leaves * a.pl.G;

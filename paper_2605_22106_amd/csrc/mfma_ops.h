@@ -49,6 +49,17 @@ struct Op<float> {
   static __device__ __forceinline__ reg zero() { return 0.0f; }
 };
 
+// Column of head_dim that lane group g4 supplies at MFMA k-step ks.  Both
+// operands of a dot product use the same map, so the result is unchanged; it
+// makes the four lane groups of one k-step read consecutive 16-byte pieces of
+// a row, so a 16-row fragment load touches 64 contiguous bytes of each row.
+template <class T>
+__device__ __forceinline__ int frag_col(int ks, int g4) {
+  constexpr int VEC = 16 / (int)sizeof(T);          // elements per 16 bytes
+  constexpr int SPV = VEC / Op<T>::kPerStep;        // k-steps per 16 bytes
+  return (ks / SPV) * 4 * VEC + g4 * VEC + (ks % SPV) * Op<T>::kPerStep;
+}
+
 // fp32 MFMA 16x16x4 (A, B scalars per lane), used for P V with fp32 P.
 __device__ __forceinline__ f32x4 mma_f32(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
