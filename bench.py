@@ -46,6 +46,132 @@ BF16_PEAK_TFLOPS = 2500.0
 METRIC = "KV tokens scored+evicted+compacted/s; tree-decode attn HBM GB/s (% of peak)"
 
 
+CSRC = os.path.join(ROOT, "paper_2605_22106_amd", "csrc")
+# kernels of each entry point (name prefix) and the source file that defines them
+ENTRY_KERNELS = {
+    "arbor_score": ("score_", "score.hip"),
+    "arbor_allocate": ("allocate_", "allocate.hip"),
+    "arbor_select": ("select_", "select.hip"),
+    "arbor_compact": ("compact_", "compact.hip"),
+    "arbor_tree_decode_attn": ("decode_", "decode.hip"),
+    "arbor_rehydrate": ("rehyd_", "rehydrate.hip"),
+}
+
+
+def short_kernel_name(name: str) -> str:
+    """'arbor::(anonymous namespace)::compact_move(...)' -> 'compact_move';
+    '_ZN5arbor12_GLOBAL__N_110score_passILi0EDF16bLi128ELi2ELi2EEEv...' -> 'score_pass<0,bf16,128,2,2>'."""
+    import re
+    m = re.search(r"_GLOBAL__N_1(\d+)", name)
+    if m and name.startswith("_Z"):
+        k = int(m.group(1))
+        start = m.end()
+        ident = name[start:start + k]
+        rest = name[start + k:]
+        if rest.startswith("I"):
+            args = []
+            for tok in re.finditer(r"Li(\d+)E|DF16b|(?<=[IE])f(?=[LE])", rest[:rest.find("EEv") + 1]):
+                t = tok.group(0)
+                args.append(tok.group(1) if tok.group(1) else ("bf16" if t == "DF16b" else "f32"))
+            return f"{ident}<{','.join(args)}>"
+        return ident
+    m = re.search(r"arbor::\(anonymous namespace\)::(?:void )?([A-Za-z_0-9]+(?:<[^>(]*>)?)\(", name)
+    if m:
+        return m.group(1)
+    m = re.search(r"void arbor::\(anonymous namespace\)::([A-Za-z_0-9]+(?:<[^>(]*>)?)\(", name)
+    return m.group(1) if m else name[:80]
+
+
+def source_sha256(fname: str) -> str:
+    import hashlib
+    with open(os.path.join(CSRC, fname), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def summarize_trace(db: str, title: str, command: str) -> str:
+    """Per-kernel calls / avg / min / max / total (us) of a rocprofv3 kernel-trace database."""
+    import collections
+    import sqlite3
+    c = sqlite3.connect(db)
+    d = collections.defaultdict(list)
+    for name, dur in c.execute("select name, duration from kernels"):
+        d[name].append(dur / 1000.0)
+    lines = [f"# {title}", f"# command: {command}",
+             "# durations from rocprofv3 --kernel-trace, microseconds",
+             f"{'calls':>5} {'avg_us':>9} {'min_us':>9} {'max_us':>9} {'total_us':>10}  kernel"]
+    rows = sorted(((short_kernel_name(n), v) for n, v in d.items() if "arbor" in n),
+                  key=lambda kv: -sum(kv[1]))
+    for name, v in rows:
+        lines.append(f"{len(v):5d} {sum(v) / len(v):9.2f} {min(v):9.2f} {max(v):9.2f} "
+                     f"{sum(v):10.1f}  {name}")
+    return "\n".join(lines) + "\n"
+
+
+def summarize_traffic(fetch_csv: str, write_csv: str, title: str, command: str,
+                      copy_bytes: int) -> str:
+    """HBM bytes per dispatch from FETCH_SIZE / WRITE_SIZE (KiB), each scaled by what the
+    counter reads for a plain device copy of `copy_bytes` (the last dispatches of the run)."""
+    import collections
+    import csv
+
+    def per_kernel(path, counter):
+        agg = collections.defaultdict(list)
+        copies = []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"])
+            if "arbor" in r["Kernel_Name"]:
+                agg[short_kernel_name(r["Kernel_Name"])].append(v)
+            elif "copyBuffer" in r["Kernel_Name"] or "copy" in r["Kernel_Name"].lower():
+                copies.append((int(r["Dispatch_Id"]), v))
+        copies.sort()
+        return agg, copies
+
+    fk, fcopy = per_kernel(fetch_csv, "FETCH_SIZE")
+    wk, wcopy = per_kernel(write_csv, "WRITE_SIZE")
+    kib = copy_bytes / 1024.0
+    # the calibration copies are the last three copy dispatches of the run
+    f_cal = float(np.mean([v for _, v in fcopy[-3:]]))
+    w_cal = float(np.mean([v for _, v in wcopy[-3:]]))
+    ff, wf = kib / f_cal, kib / w_cal
+    lines = [f"# {title}", f"# command (FETCH_SIZE): {command.format(counter='FETCH_SIZE')}",
+             f"# command (WRITE_SIZE): {command.format(counter='WRITE_SIZE')}",
+             f"# calibration: a plain device copy of {copy_bytes} bytes reads FETCH_SIZE "
+             f"{f_cal:.1f} KiB and WRITE_SIZE {w_cal:.1f} KiB; factors {ff:.4f} (fetch), "
+             f"{wf:.4f} (write)",
+             "# one JSON object per kernel: average counters per dispatch and scaled HBM bytes"]
+    src_of = {pre: src for pre, src in ENTRY_KERNELS.values()}
+    for name in sorted(set(fk) | set(wk)):
+        fkib = float(np.mean(fk.get(name, [0.0])))
+        wkib = float(np.mean(wk.get(name, [0.0])))
+        src = next((s for pre, s in src_of.items() if name.startswith(pre)), None)
+        lines.append(json.dumps({
+            "kernel": name, "fetch_kib": round(fkib, 3), "write_kib": round(wkib, 3),
+            "hbm_read_bytes": round(fkib * ff * 1024), "hbm_write_bytes": round(wkib * wf * 1024),
+            "source": src, "source_sha256": source_sha256(src) if src else None}))
+    lines.append(json.dumps({"calibration": {"copy_bytes": copy_bytes, "fetch_kib": f_cal,
+                                             "write_kib": w_cal, "fetch_factor": ff,
+                                             "write_factor": wf}}))
+    return "\n".join(lines) + "\n"
+
+
+def stored_traffic(workload: str, entry: str):
+    """HBM bytes per call of `entry` from the committed counter summary, or None when it is
+    missing or any of the entry point's kernels changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    prefix, src = ENTRY_KERNELS[entry]
+    rows = [json.loads(line) for line in open(path) if line.startswith("{")]
+    rows = [r for r in rows if r.get("kernel", "").startswith(prefix)]
+    if not rows or any(r["source_sha256"] != source_sha256(src) for r in rows):
+        return None
+    return {"read_bytes": sum(r["hbm_read_bytes"] for r in rows),
+            "write_bytes": sum(r["hbm_write_bytes"] for r in rows),
+            "kernels": [r["kernel"] for r in rows], "source": os.path.relpath(path, ROOT)}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -54,6 +180,13 @@ def parse():
     ap.add_argument("--config", default="llama8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rehydrate-leg", action="store_true")
+    ap.add_argument("--summarize-trace", metavar="DB",
+                    help="write a per-kernel summary of a rocprofv3 kernel-trace database and exit")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write per-kernel HBM bytes from FETCH_SIZE / WRITE_SIZE counter CSVs")
+    ap.add_argument("--title", default="")
+    ap.add_argument("--command", default="")
+    ap.add_argument("--out", default=None)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB device to device with "
                          "a plain copy kernel (a known-size reference for HBM byte counters)")
@@ -258,6 +391,17 @@ def cpu_baseline(st, kv_cpu_state, sel_budget_active, work):
 
 def main():
     args = parse()
+    if args.summarize_trace or args.summarize_traffic:
+        if args.summarize_trace:
+            text = summarize_trace(args.summarize_trace, args.title, args.command)
+        else:
+            text = summarize_traffic(args.summarize_traffic[0], args.summarize_traffic[1],
+                                     args.title, args.command, args.copy_calibration_mib << 20)
+        if args.out:
+            with open(args.out, "w") as f:
+                f.write(text)
+        print(text, end="")
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
               "subtree sharding of this path is a design note, not a measured configuration.",
@@ -323,13 +467,18 @@ def main():
         "select": {"bound": "hbm", "achieved": work["select_bytes"] / (mean["select"] * 1e-3) / 1e9,
                    "peak": HBM_PEAK_GBS, "unit": "GB/s"},
     }
-    for r in rates.values():
+    entry = {"score": "arbor_score", "compact": "arbor_compact",
+             "decode": "arbor_tree_decode_attn", "select": "arbor_select"}
+    for st_name, r in rates.items():
         r["frac"] = r["achieved"] / r["peak"]
+        r["kernel"] = entry[st_name]
+        r["ms_per_call"] = mean[st_name]
+        tr = stored_traffic(cfg.name, entry[st_name])
+        r["traffic"] = None if tr is None else tr["read_bytes"] + tr["write_bytes"]
+        if tr is not None:
+            r["traffic_kernels"] = tr["kernels"]
     dominant = max(["score", "compact", "decode", "select"], key=lambda s: mean[s])
     roof = dict(rates[dominant])
-    roof["kernel"] = {"score": "arbor_score", "compact": "arbor_compact",
-                      "decode": "arbor_tree_decode_attn", "select": "arbor_select"}[dominant]
-    roof["traffic"] = None
 
     result = {
         "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
