@@ -54,6 +54,15 @@ __device__ __forceinline__ int64_t row_byte_offset(const Pool &pl, int l, int64_
 }
 
 // ---- sticky device status ------------------------------------------------
+// 16-byte store with the non-temporal hint: rows a kernel moves are not read
+// again soon, and keeping them out of the caches spares the next kernel the
+// write-back of their dirty lines.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store16_nt(void *dst, uint4 v) {
+  const u32x4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, static_cast<u32x4 *>(dst));
+}
+
 __device__ __forceinline__ bool status_failed(const int32_t *st) {
   return *reinterpret_cast<const volatile int32_t *>(st) < 0;
 }

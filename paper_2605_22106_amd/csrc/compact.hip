@@ -23,9 +23,18 @@ __device__ __forceinline__ int pos_at(const Tree &t, const Pool &pl, int64_t po,
   return pl.slot_pos[(int64_t)page * pl.P + (s % pl.P)];
 }
 
+// Row of slot s of a node within every (layer, kv head) plane: page * Hkv * P
+// + s % P (the plane adds layer * num_pages * Hkv * P + g * P).
+__device__ __forceinline__ int plane_row(const Tree &t, const Pool &pl, int64_t po, int s) {
+  return t.page_table[po + s / pl.P] * pl.Hkv * pl.P + s % pl.P;
+}
+
 __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32_t *__restrict__ k,
                                                     const int32_t *__restrict__ sel_pos,
                                                     int32_t *__restrict__ src_slot,
+                                                    int32_t *__restrict__ mv_src,
+                                                    int32_t *__restrict__ mv_dst,
+                                                    int32_t *__restrict__ first_moved,
                                                     int32_t *__restrict__ freed, int32_t *status) {
   if (status_failed(status)) return;
   const int lane = lane_id();
@@ -59,12 +68,29 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
     }
     bad |= found < 0;
     src_slot[tb + s] = found;
+    if (!bad) {
+      mv_src[tb + s] = plane_row(t, pl, po, found);
+      mv_dst[tb + s] = plane_row(t, pl, po, s);
+    }
   }
   if (ballot(bad)) {
     if (lane == 0) status_error(status, ARBOR_EINVAL);
     return;
   }
-  if (lane == 0) freed[i] = (c + pl.P - 1) / pl.P - (ki + pl.P - 1) / pl.P;
+  // slots already holding their row form a prefix (sources ascend and src >= s)
+  int s0 = ki;
+  for (int base = 0; base < ki; base += kWave) {
+    const int s = base + lane;
+    const uint64_t mv = ballot(s < ki && src_slot[tb + s] != s);
+    if (mv) {
+      s0 = base + __builtin_ctzll(mv);
+      break;
+    }
+  }
+  if (lane == 0) {
+    freed[i] = (c + pl.P - 1) / pl.P - (ki + pl.P - 1) / pl.P;
+    first_moved[i] = s0;
+  }
 }
 
 // meta[0] = number of changed nodes, meta[1] = free-stack top before pushes
@@ -109,25 +135,16 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
 
 // Rows of one (layer, kv head) plane: LPR lanes per row, 16 bytes per lane.
 template <int LPR>
-__device__ void move_plane(const Tree &t, const Pool &pl, int i, int ki, int l, int g,
-                           const int32_t *__restrict__ src_slot, int lane) {
+__device__ void move_plane(const Pool &pl, int64_t tb, int s0, int ki, int l, int g,
+                           const int32_t *__restrict__ mv_src, const int32_t *__restrict__ mv_dst,
+                           int lane) {
   constexpr int RPP = kWave / LPR;   // rows per wave pass
   constexpr int PASSES = 8;          // passes per chunk
   constexpr int CH = RPP * PASSES;   // rows staged per chunk
-  const int64_t tb = t.tok_off[i];
-  const int64_t po = t.page_off[i];
-  // rows already in place form a prefix (src(s) = s); skip it
-  int s0 = ki;
-  for (int base = 0; base < ki; base += kWave) {
-    const int s = base + lane;
-    const uint64_t mv = ballot(s < ki && src_slot[tb + s] != s);
-    if (mv) {
-      s0 = base + __builtin_ctzll(mv);
-      break;
-    }
-  }
-  char *kb = static_cast<char *>(pl.k);
-  char *vb = static_cast<char *>(pl.v);
+  const int64_t plane = ((int64_t)l * pl.num_pages * pl.Hkv + g) * pl.P;
+  const int64_t row_bytes = (int64_t)pl.D * pl.esize;
+  char *kb = static_cast<char *>(pl.k) + plane * row_bytes;
+  char *vb = static_cast<char *>(pl.v) + plane * row_bytes;
   const int sub = lane % LPR;
   const int rsel = lane / LPR;
   for (int cbase = s0; cbase < ki; cbase += CH) {
@@ -138,12 +155,10 @@ __device__ void move_plane(const Tree &t, const Pool &pl, int i, int ki, int l, 
       const int s = cbase + ps * RPP + rsel;
       dst[ps] = -1;
       if (s < ki) {
-        const int src = src_slot[tb + s];
-        const int64_t so = row_byte_offset(pl, l, t.page_table[po + src / pl.P], g, src % pl.P) +
-                           sub * 16;
+        const int64_t so = (int64_t)mv_src[tb + s] * row_bytes + sub * 16;
         kr[ps] = *reinterpret_cast<const uint4 *>(kb + so);
         vr[ps] = *reinterpret_cast<const uint4 *>(vb + so);
-        dst[ps] = row_byte_offset(pl, l, t.page_table[po + s / pl.P], g, s % pl.P) + sub * 16;
+        dst[ps] = (int64_t)mv_dst[tb + s] * row_bytes + sub * 16;
       }
     }
     // every lane's loads of this chunk have returned before any store below
@@ -152,8 +167,8 @@ __device__ void move_plane(const Tree &t, const Pool &pl, int i, int ki, int l, 
 #pragma unroll
     for (int ps = 0; ps < PASSES; ++ps) {
       if (dst[ps] >= 0) {
-        *reinterpret_cast<uint4 *>(kb + dst[ps]) = kr[ps];
-        *reinterpret_cast<uint4 *>(vb + dst[ps]) = vr[ps];
+        store16_nt(kb + dst[ps], kr[ps]);
+        store16_nt(vb + dst[ps], vr[ps]);
       }
     }
     __builtin_amdgcn_wave_barrier();
@@ -161,25 +176,29 @@ __device__ void move_plane(const Tree &t, const Pool &pl, int i, int ki, int l, 
 }
 
 __global__ __launch_bounds__(256) void compact_move(Tree t, Pool pl, const int32_t *__restrict__ k,
-                                                    const int32_t *__restrict__ src_slot,
+                                                    const int32_t *__restrict__ mv_src,
+                                                    const int32_t *__restrict__ mv_dst,
+                                                    const int32_t *__restrict__ first_moved,
                                                     const int32_t *__restrict__ changed,
                                                     const int32_t *__restrict__ meta,
                                                     int32_t *status) {
   if (status_failed(status)) return;
   const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int planes = pl.L * pl.Hkv;
   const int64_t total = (int64_t)meta[0] * planes;
   const int row_bytes = pl.D * pl.esize;
-  for (int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); w < total;
-       w += (int64_t)gridDim.x * 4) {
+  for (int64_t w = (int64_t)blockIdx.x * 4 + wave; w < total; w += (int64_t)gridDim.x * 4) {
     const int i = changed[w / planes];
     const int rem = (int)(w % planes);
     const int l = rem / pl.Hkv;
     const int g = rem % pl.Hkv;
     const int ki = k[i];
-    if (row_bytes == 128) move_plane<8>(t, pl, i, ki, l, g, src_slot, lane);
-    else if (row_bytes == 256) move_plane<16>(t, pl, i, ki, l, g, src_slot, lane);
-    else move_plane<32>(t, pl, i, ki, l, g, src_slot, lane);
+    const int s0 = first_moved[i];
+    const int64_t tb = t.tok_off[i];
+    if (row_bytes == 128) move_plane<8>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
+    else if (row_bytes == 256) move_plane<16>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
+    else move_plane<32>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
   }
 }
 
@@ -225,7 +244,7 @@ __global__ __launch_bounds__(256) void compact_finalize(Tree t, Pool pl, const i
 }  // namespace
 
 size_t compact_workspace(const arbor_sizes_t *sz) {
-  return (size_t)sz->num_tokens * 4 + (size_t)sz->num_nodes * 12 + 4096;
+  return (size_t)sz->num_tokens * 12 + (size_t)sz->num_nodes * 16 + 4096;
 }
 
 int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
@@ -235,7 +254,11 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   Pool pl = make_pool(geom, pool);
   if (t.V <= 0) return ARBOR_OK;
   Carve cv(workspace, workspace_bytes);
+  if ((int64_t)pl.num_pages * pl.Hkv * pl.P >= ((int64_t)1 << 31)) return ARBOR_EUNSUPPORTED;
   int32_t *src_slot = cv.take<int32_t>((size_t)t.N);
+  int32_t *mv_src = cv.take<int32_t>((size_t)t.N);
+  int32_t *mv_dst = cv.take<int32_t>((size_t)t.N);
+  int32_t *first_moved = cv.take<int32_t>(t.V);
   int32_t *freed = cv.take<int32_t>(t.V);
   int32_t *push_base = cv.take<int32_t>(t.V);
   int32_t *changed = cv.take<int32_t>(t.V);
@@ -243,13 +266,13 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   if (!cv.ok) return ARBOR_EWORKSPACE;
   const dim3 node_grid((t.V + 3) / 4);
   hipLaunchKernelGGL(compact_plan, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos, src_slot,
-                     freed, status);
+                     mv_src, mv_dst, first_moved, freed, status);
   hipLaunchKernelGGL(compact_scan, dim3(1), dim3(1024), 0, stream, t, pl, k, freed, push_base,
                      changed, meta, status);
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
-  hipLaunchKernelGGL(compact_move, dim3(move_blocks), dim3(256), 0, stream, t, pl, k, src_slot,
-                     changed, meta, status);
+  hipLaunchKernelGGL(compact_move, dim3(move_blocks), dim3(256), 0, stream, t, pl, k, mv_src,
+                     mv_dst, first_moved, changed, meta, status);
   hipLaunchKernelGGL(compact_finalize, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos,
                      push_base, changed, meta, status);
   return hip_ok(hipGetLastError());
