@@ -2,7 +2,7 @@
 // K/V rows inside the paged tree KV pool (Sec. 4 Execution: retained entries
 // stay, the other entries are freed).
 //
-// Four launches on one stream:
+// Three launches on one stream:
 //   plan     one wave per node: validate the selection, locate each kept
 //            position's source slot, count the pages the node releases;
 //   scan     one workgroup: (node, page)-ordered free-stack offsets and the
@@ -10,8 +10,9 @@
 //   move     one wave per (changed node, layer, kv head) plane: rows move to
 //            lower slots only, so a wave stages a chunk of rows in registers
 //            (all loads of the chunk retire before its stores issue) and walks
-//            the chunks in ascending slot order -- in-place safe;
-//   finalize one wave per changed node: slot_pos, page table, free stack, c_i.
+//            the chunks in ascending slot order -- in-place safe; extra
+//            workgroups of the same launch finalize the changed nodes
+//            (slot_pos, page table, free stack, c_i).
 #include "arbor_internal.h"
 
 namespace arbor {
@@ -133,6 +134,46 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
   }
 }
 
+// Node bookkeeping of the changed nodes: slot_pos, page table, free stack, c_i.
+// It touches no K/V bytes and the moves read none of it (they use the plan's
+// tables), so it runs in the same launch as the moves.
+__device__ void finalize_nodes(const Tree &t, const Pool &pl, const int32_t *__restrict__ k,
+                               const int32_t *__restrict__ sel_pos,
+                               const int32_t *__restrict__ push_base,
+                               const int32_t *__restrict__ changed,
+                               const int32_t *__restrict__ meta, int wave0, int nwaves) {
+  const int lane = lane_id();
+  const int nch = meta[0];
+  const int top = meta[1];
+  const int P = pl.P;
+  for (int w = wave0; w < nch; w += nwaves) {
+    const int i = changed[w];
+    const int ki = k[i];
+    const int c = t.n_kept[i];
+    const int64_t tb = t.tok_off[i];
+    const int64_t po = t.page_off[i];
+    const int keep_pages = (ki + P - 1) / P;
+    const int old_pages = (c + P - 1) / P;
+    for (int s = lane; s < keep_pages * P; s += kWave) {
+      const int page = t.page_table[po + s / P];
+      pl.slot_pos[(int64_t)page * P + s % P] = s < ki ? sel_pos[tb + s] : -1;
+    }
+    const int nfree = old_pages - keep_pages;
+    for (int e = lane; e < nfree * P; e += kWave) {
+      const int q = keep_pages + e / P;
+      const int page = t.page_table[po + q];
+      pl.slot_pos[(int64_t)page * P + e % P] = -1;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int e = lane; e < nfree; e += kWave) {
+      const int q = keep_pages + e;
+      pl.free_stack[top + push_base[i] + e] = t.page_table[po + q];
+      t.page_table[po + q] = -1;
+    }
+    if (lane == 0) t.n_kept[i] = ki;
+  }
+}
+
 // Rows of one (layer, kv head) plane: LPR lanes per row, 16 bytes per lane.
 template <int LPR>
 __device__ void move_plane(const Pool &pl, int64_t tb, int s0, int ki, int l, int g,
@@ -179,16 +220,24 @@ __global__ __launch_bounds__(256) void compact_move(Tree t, Pool pl, const int32
                                                     const int32_t *__restrict__ mv_src,
                                                     const int32_t *__restrict__ mv_dst,
                                                     const int32_t *__restrict__ first_moved,
+                                                    const int32_t *__restrict__ sel_pos,
+                                                    const int32_t *__restrict__ push_base,
                                                     const int32_t *__restrict__ changed,
                                                     const int32_t *__restrict__ meta,
-                                                    int32_t *status) {
+                                                    int move_blocks, int32_t *status) {
   if (status_failed(status)) return;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if ((int)blockIdx.x >= move_blocks) {
+    const int fb = (int)blockIdx.x - move_blocks;
+    finalize_nodes(t, pl, k, sel_pos, push_base, changed, meta, fb * 4 + wave,
+                   ((int)gridDim.x - move_blocks) * 4);
+    return;
+  }
   const int planes = pl.L * pl.Hkv;
   const int64_t total = (int64_t)meta[0] * planes;
   const int row_bytes = pl.D * pl.esize;
-  for (int64_t w = (int64_t)blockIdx.x * 4 + wave; w < total; w += (int64_t)gridDim.x * 4) {
+  for (int64_t w = (int64_t)blockIdx.x * 4 + wave; w < total; w += (int64_t)move_blocks * 4) {
     const int i = changed[w / planes];
     const int rem = (int)(w % planes);
     const int l = rem / pl.Hkv;
@@ -199,45 +248,6 @@ __global__ __launch_bounds__(256) void compact_move(Tree t, Pool pl, const int32
     if (row_bytes == 128) move_plane<8>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
     else if (row_bytes == 256) move_plane<16>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
     else move_plane<32>(pl, tb, s0, ki, l, g, mv_src, mv_dst, lane);
-  }
-}
-
-__global__ __launch_bounds__(256) void compact_finalize(Tree t, Pool pl, const int32_t *__restrict__ k,
-                                                        const int32_t *__restrict__ sel_pos,
-                                                        const int32_t *__restrict__ push_base,
-                                                        const int32_t *__restrict__ changed,
-                                                        const int32_t *__restrict__ meta,
-                                                        int32_t *status) {
-  if (status_failed(status)) return;
-  const int lane = lane_id();
-  const int nch = meta[0];
-  const int top = meta[1];
-  const int P = pl.P;
-  for (int w = blockIdx.x * 4 + (threadIdx.x >> 6); w < nch; w += gridDim.x * 4) {
-    const int i = changed[w];
-    const int ki = k[i];
-    const int c = t.n_kept[i];
-    const int64_t tb = t.tok_off[i];
-    const int64_t po = t.page_off[i];
-    const int keep_pages = (ki + P - 1) / P;
-    const int old_pages = (c + P - 1) / P;
-    for (int s = lane; s < keep_pages * P; s += kWave) {
-      const int page = t.page_table[po + s / P];
-      pl.slot_pos[(int64_t)page * P + s % P] = s < ki ? sel_pos[tb + s] : -1;
-    }
-    const int nfree = old_pages - keep_pages;
-    for (int e = lane; e < nfree * P; e += kWave) {
-      const int q = keep_pages + e / P;
-      const int page = t.page_table[po + q];
-      pl.slot_pos[(int64_t)page * P + e % P] = -1;
-    }
-    __builtin_amdgcn_wave_barrier();
-    for (int e = lane; e < nfree; e += kWave) {
-      const int q = keep_pages + e;
-      pl.free_stack[top + push_base[i] + e] = t.page_table[po + q];
-      t.page_table[po + q] = -1;
-    }
-    if (lane == 0) t.n_kept[i] = ki;
   }
 }
 
@@ -271,10 +281,10 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
                      changed, meta, status);
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
-  hipLaunchKernelGGL(compact_move, dim3(move_blocks), dim3(256), 0, stream, t, pl, k, mv_src,
-                     mv_dst, first_moved, changed, meta, status);
-  hipLaunchKernelGGL(compact_finalize, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos,
-                     push_base, changed, meta, status);
+  const int fin_blocks = (t.V + 3) / 4;
+  hipLaunchKernelGGL(compact_move, dim3(move_blocks + fin_blocks), dim3(256), 0, stream, t, pl, k,
+                     mv_src, mv_dst, first_moved, sel_pos, push_base, changed, meta, move_blocks,
+                     status);
   return hip_ok(hipGetLastError());
 }
 

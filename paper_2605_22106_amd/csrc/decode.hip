@@ -21,6 +21,7 @@ namespace arbor {
 namespace {
 
 constexpr int MAXD = ARBOR_MAX_DEPTH + 1;
+static_assert(MAXD == kWave, "one wave covers a chain");
 constexpr int CHUNK = 256;        // slots per work unit
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -169,21 +170,32 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     leaf_list[node_leaf_off[x] + lrank[(int64_t)b * MAXD + d]] = b;
   }
   __syncthreads();
-  // each leaf's partials, root first: the merge reads them without a chain walk
-  for (int b = threadIdx.x; b < a.n_leaves; b += blockDim.x) {
-    int np = 0;
-    for (int d = 0; d <= ldepth[b]; ++d) {
-      const int x = lanc[(int64_t)b * MAXD + d];
-      const int nch = (t.n_kept[x] + CHUNK - 1) / CHUNK;
-      const int r = lrank[(int64_t)b * MAXD + d] * G;
-      if (np + nch > a.max_parts) {  // more resident tokens than the workspace was sized for
-        atomicOr(&s_err, 4);
-        break;
-      }
-      for (int s = 0; s < nch; ++s, ++np)
-        leaf_part[(int64_t)b * a.max_parts + np] = item_rowbase[node_item0[x] + s] + r;
+  // each leaf's partials, root first, so the merge needs no chain walk: one
+  // thread per (leaf, chain depth); the offsets come from a per-leaf scan of
+  // the chunk counts along the chain (at most MAXD entries)
+  for (int b0 = 0; b0 < a.n_leaves; b0 += blockDim.x / MAXD) {
+    const int b = b0 + (int)threadIdx.x / MAXD;
+    const int d = (int)threadIdx.x % MAXD;
+    const bool live = b < a.n_leaves && d <= ldepth[b];
+    int x = 0, nch = 0;
+    if (live) {
+      x = lanc[(int64_t)b * MAXD + d];
+      nch = (t.n_kept[x] + CHUNK - 1) / CHUNK;
     }
-    leaf_np[b] = np;
+    // inclusive scan over the MAXD threads of this leaf (MAXD = kWave)
+    const int incl = wave_inclusive_scan<int>(nch);
+    const int np = incl - nch;
+    if (live) {
+      const int r = lrank[(int64_t)b * MAXD + d] * G;
+      const int it0 = node_item0[x];
+      if (incl > a.max_parts) {
+        atomicOr(&s_err, 4);  // more resident tokens than the workspace was sized for
+      } else {
+        for (int s = 0; s < nch; ++s)
+          leaf_part[(int64_t)b * a.max_parts + np + s] = item_rowbase[it0 + s] + r;
+      }
+      if (d == ldepth[b]) leaf_np[b] = min(incl, a.max_parts);
+    }
   }
   __syncthreads();
   if (threadIdx.x == 0) {

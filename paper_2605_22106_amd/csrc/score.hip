@@ -189,14 +189,16 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
   build_chain(t, pl, j, ch);
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = tid >> 6;
+  // wave-uniform values live in scalar registers, so per-sub-page decisions
+  // below are branches instead of per-lane selects
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rr = lane & 15;
   const int g4 = lane >> 4;
   const int G = pl.G;
   const int nj = t.n_full[j];
   const int wj = min(a.W, nj);
   const int rows_total = G * a.W;
-  const int own_d = ch.depth;
+  const int own_d = __builtin_amdgcn_readfirstlane(ch.depth);
   const int row0 = rg * RW + wave * 16 * NBW;   // first row of this wave
 
   // Q operand: query row row0 + nb*16 + rr of block nb
@@ -220,7 +222,8 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
                            (int64_t)rg * RW;
   const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
   const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
-  const int n_sp = (PASS == 1 && !a.self_window) ? ch.sp_off[own_d] : ch.sp_off[own_d + 1];
+  const int n_sp = __builtin_amdgcn_readfirstlane(
+      (PASS == 1 && !a.self_window) ? ch.sp_off[own_d] : ch.sp_off[own_d + 1]);
   const int n_st = (n_sp + GS - 1) / GS;   // stages
 
   // Staging: two register sets alternate by stage parity, so a load has a full
@@ -295,7 +298,7 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
 #pragma unroll
     for (int k = 0; k < GS; ++k) {
       const int sp = st_idx * GS + k;
-      meta[k] = sp < n_sp ? sub_meta(ch, t, pl, sp) : 0;
+      meta[k] = __builtin_amdgcn_readfirstlane(sp < n_sp ? sub_meta(ch, t, pl, sp) : 0);
       typename O::reg kr[KS];
       operand(ring[slot][k], kr);
 #pragma unroll
