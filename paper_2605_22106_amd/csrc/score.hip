@@ -48,6 +48,8 @@ struct ScoreArgs {
   float *lse;       // [n_obs][S][Hkv][n_rg][16*NB]
   float *part;      // partial column sums
   const int64_t *pbase;   // [n_obs]
+  const int64_t *tbase;   // [n_obs]: float offset (in part) of the observer's sub-page table
+  const int32_t *nsp;     // [n_obs][2]: sub-pages of the chain, and of the credited part
   const int32_t *ctxlen;  // [n_obs]
   const int32_t *odepth;  // [n_obs]
   const int32_t *anc;     // [n_obs][MAXD]
@@ -70,7 +72,7 @@ struct ChainLds {
   int sp_meta[SPCAP];  // chain depth | valid slots << 8
 };
 
-__device__ void build_chain(const Tree &t, const Pool &pl, int j, ChainLds &ch) {
+__device__ __forceinline__ void build_chain(const Tree &t, const Pool &pl, int j, ChainLds &ch) {
   if (threadIdx.x == 0) {
     int d = 0;
     for (int x = t.parent[j]; x >= 0 && d < MAXD - 1; x = t.parent[x]) ++d;
@@ -439,11 +441,355 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused two-pass kernel.  Keys stream through a ring of RING stages of GS
+// sub-pages in LDS, filled by direct global->LDS loads; each wave owns 16 NBW
+// query rows and keeps their Q in registers for both passes:
+//   pass 0  C = K Q^T: running max / sum of each row over the chain -> lse;
+//   pass 1  C = Q K^T: per key, sum over the wave's rows of exp2(z - lse);
+//           the four waves' sums are added in wave order and stored as the
+//           row group's partial for that key.
+// One barrier per stage: a wave waits for its own loads of the stage, then the
+// barrier makes every wave's loads visible and frees the slot the next load
+// refills.  Ring slots are distinct LDS arrays (the loop is unrolled by RING),
+// so the compiler can tell a slot being filled from the one being read.
+constexpr int kGS = 4;     // sub-pages per stage
+constexpr int kRing = 3;   // stages in the ring
+
+// v_max3 without the quieting the IEEE maxnum lowering adds to each operand:
+// the operands are MFMA results or -inf, never signalling NaNs.
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// Direct global -> LDS loads: lane L's `size` bytes land at lds + size * L.
+__device__ __forceinline__ void load_to_lds16(const void *g, void *lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
+__device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
+  __builtin_amdgcn_global_load_lds(g, lds, 4, 0, 0);
+}
+
+template <class T, int D>
+struct Ring {
+  typedef Stage<T, D> SG;
+  __attribute__((aligned(16))) char k[kGS][SG::BYTES];
+  __attribute__((aligned(16))) int pos[kGS][16];
+};
+// per-stage column sums of the four waves (not a load target, so reading it
+// never has to wait for loads in flight)
+struct Red {
+  float v[kGS][4][16];
+};
+
+template <class T, int D, int NBW>
+__global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
+  using O = Op<T>;
+  using SG = Stage<T, D>;
+  constexpr int KS = D / 4 / O::kPerStep;   // MFMA k-steps over head_dim
+  constexpr int RW = 64 * NBW;              // rows of the workgroup
+  constexpr int DPW = kGS * SG::NBLK / 4;   // K loads per wave per stage
+  constexpr int VM = DPW + 1;               // vector-memory ops per wave per stage
+  static_assert(kGS == 4, "one position load per wave per stage");
+  static_assert((kRing - 2) * VM <= 15, "vmcnt immediate");
+  constexpr float kFloor = -1e30f;
+  __shared__ Ring<T, D> r0, r1, r2;
+  __shared__ Red d0, d1, d2;
+  __shared__ int s_bad;
+  if (threadIdx.x == 0) s_bad = status_failed(a.status);
+  __syncthreads();
+  if (s_bad) return;
+  const Tree &t = a.t;
+  const Pool &pl = a.pl;
+  const int o = blockIdx.x;
+  const int slg = blockIdx.y;
+  const int rg = blockIdx.z;
+  const int si = slg / pl.Hkv;
+  const int g = slg % pl.Hkv;
+  const int layer = a.slice[si];
+  const int j = a.obs[o];
+  // the chain's sub-page table, read with scalar loads (constant address space)
+  // entry sp: [4 sp] plane row, [4 sp + 1] slot, [4 sp + 2] context offset,
+  // [4 sp + 3] valid slots | own << 8
+  typedef const __attribute__((address_space(4))) int *TabPtr;
+  const TabPtr tab = (TabPtr)(a.part + a.tbase[o]);
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rr = lane & 15;
+  const int g4 = lane >> 4;
+  const int G = pl.G;
+  const int nj = t.n_full[j];
+  const int wj = min(a.W, nj);
+  const int rows_total = G * a.W;
+  const int row0 = rg * RW + wave * 16 * NBW;   // first row of this wave
+  const float sl2 = a.sl2;
+  auto row_u = [&](int r) __attribute__((always_inline)) -> int {
+    if (r >= rows_total) return -1;
+    const int tt = r % a.W;
+    return tt < wj ? nj - wj + tt : -1;
+  };
+
+  typename O::reg q[NBW][KS];
+  const T *qbase = static_cast<const T *>(a.q_win) +
+                   ((((int64_t)o * a.S + si) * (pl.Hkv * G) + (int64_t)g * G) * a.W) * D;
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    const int r = row0 + nb * 16 + rr;
+    const bool rv = r < rows_total;
+    const T *rp = qbase + (int64_t)(rv ? r : 0) * D + g4 * (D / 4);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) q[nb][ks] = rv ? O::load(rp + ks * O::kPerStep) : O::zero();
+  }
+  const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
+  const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
+  // this lane's 16-byte unit of a key tile: key rr, quarter g4
+  const int64_t lane_off = (int64_t)rr * (D * (int)sizeof(T)) + g4 * SG::QB;
+
+  // direct loads of stage st (sub-pages st*GS .. st*GS+GS-1, clamped) into R;
+  // all addresses are formed before the first load is issued
+  auto issue = [&](Ring<T, D> &R, int st, int n_sp) __attribute__((always_inline)) {
+    int rows[kGS], slots[kGS];
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) {
+      const int sp = min(st * kGS + k, n_sp - 1);
+      rows[k] = tab[4 * sp];
+      slots[k] = tab[4 * sp + 1];
+    }
+    int my_slot = slots[0];
+#pragma unroll
+    for (int k = 1; k < kGS; ++k) my_slot = wave == k ? slots[k] : my_slot;
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) {
+      const int u = wave + 4 * i;          // unit (sub-page k, 16-byte block blk)
+      const int k = u / SG::NBLK, blk = u % SG::NBLK;
+      int row = rows[0];
+#pragma unroll
+      for (int kk = 1; kk < kGS; ++kk) row = k == kk ? rows[kk] : row;
+      const char *src = kplane + (int64_t)row * (D * (int)sizeof(T)) + lane_off + blk * 16;
+      load_to_lds16(src, &R.k[k][blk * kWave * 16]);
+    }
+    if (lane < 16)
+      load_to_lds4(pl.slot_pos + my_slot + lane, &R.pos[wave][0]);
+  };
+  // my loads of the stage about to be computed are done; everyone's are visible
+  // (s_waitcnt immediate: vmcnt in bits 3:0, expcnt 6:4, lgkmcnt 11:8.)  The
+  // LDS writes of this wave are complete too (lgkmcnt 0), so no release fence
+  // is needed -- one would also wait for the loads still filling later slots.
+  auto stage_sync = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0x070 | ((kRing - 2) * VM));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
+  auto operand = [&](const Ring<T, D> &R, int k, typename O::reg (&kr)[KS]) __attribute__((always_inline)) {
+    const char *base = &R.k[k][0] + lane * 16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int byte = ks * O::kPerStep * (int)sizeof(T);   // within the quarter row
+      kr[ks] = O::load(reinterpret_cast<const T *>(base + (byte / 16) * (kWave * 16) + byte % 16));
+    }
+  };
+
+  // ---- pass 0: row log2-sum-exp ----
+  float m[NBW], l[NBW];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    m[nb] = kFloor;
+    l[nb] = 0.f;
+  }
+  auto lse_stage = [&](const Ring<T, D> &R, int st, int n_sp) __attribute__((always_inline)) {
+    f32x4 acc[kGS][NBW];
+    int meta[kGS];
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) {
+      const int sp = st * kGS + k;
+      meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
+      typename O::reg kr[KS];
+      operand(R, k, kr);
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) {
+        acc[k][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc[k][nb] = O::mma(kr[ks], q[nb][ks], acc[k][nb]);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) {
+      const int nvalid = meta[k] & 255;
+      const bool own = (meta[k] >> 8) != 0;
+      if (own || nvalid < 16) {
+        int kpos[4] = {0, 0, 0, 0};
+        if (own) {
+          const int4 pv = *reinterpret_cast<const int4 *>(&R.pos[k][4 * g4]);
+          kpos[0] = pv.x;
+          kpos[1] = pv.y;
+          kpos[2] = pv.z;
+          kpos[3] = pv.w;
+        }
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb) {
+          const int ur = row_u(row0 + nb * 16 + rr);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = 4 * g4 + e < nvalid && (!own || kpos[e] <= ur);
+            acc[k][nb][e] = ok ? acc[k][nb][e] : -__builtin_inff();
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+      float mx = m[nb];
+#pragma unroll
+      for (int k = 0; k < kGS; ++k) {
+        mx = max3f(mx, acc[k][nb][0], acc[k][nb][1]);
+        mx = max3f(mx, acc[k][nb][2], acc[k][nb][3]);
+      }
+      const float nm = -mx * sl2;
+      // (m - mx) is exactly 0 while the max is unchanged
+      float sum = l[nb] * __builtin_amdgcn_exp2f((m[nb] - mx) * sl2);
+#pragma unroll
+      for (int k = 0; k < kGS; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], sl2, nm));
+      l[nb] = sum;
+      m[nb] = mx;
+    }
+  };
+
+  // ---- pass 1: credited column sums ----
+  float nlse[NBW][4];
+  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
+  auto col_stage = [&](Ring<T, D> &R, Red &RD, int st, int n_sp) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) {
+      const int sp = st * kGS + k;
+      const int meta = sp < n_sp ? tab[4 * sp + 3] : 0;
+      const bool own = (meta >> 8) != 0;
+      typename O::reg kr[KS];
+      operand(R, k, kr);
+      f32x4 acc[NBW];
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) {
+        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc[nb] = O::mma(q[nb][ks], kr[ks], acc[nb]);
+      }
+      float colsum = 0.f;
+      if (own) {
+        // own tokens are credited only by later rows of the window
+        const int kp = R.pos[k][rr];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float pz = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
+            colsum += kp < row_u(row0 + nb * 16 + 4 * g4 + e) ? pz : 0.f;
+          }
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            colsum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
+      }
+      colsum += __shfl_xor(colsum, 16, kWave);
+      colsum += __shfl_xor(colsum, 32, kWave);
+      if (lane < 16) RD.v[k][wave][lane] = colsum;
+    }
+  };
+  // the previous stage's sums of all four waves, in wave order
+  auto finish = [&](const Red &RD, int st, int n_sp) __attribute__((always_inline)) {
+    if (wave == 0) {
+      // table entries by scalar loads (a per-lane load would wait behind the
+      // direct loads in flight)
+#pragma unroll
+      for (int k = 0; k < kGS; ++k) {
+        const int sp = st * kGS + k;
+        if (sp >= 0 && sp < n_sp) {
+          const int ctx = tab[4 * sp + 2], nvalid = tab[4 * sp + 3] & 255;
+          if ((lane >> 4) == k && rr < nvalid)
+            pout[ctx + rr] = ((RD.v[k][0][rr] + RD.v[k][1][rr]) + RD.v[k][2][rr]) + RD.v[k][3][rr];
+        }
+      }
+    }
+  };
+
+  // one pass over the chain's sub-pages with the ring; `work` computes a
+  // stage from a slot, `after` runs (for the previous stage) right after the
+  // stage barrier
+  auto run = [&](int n_sp, auto &&work, auto &&after) __attribute__((always_inline)) {
+    if (n_sp <= 0) return;
+    const int n_st = (n_sp + kGS - 1) / kGS;
+    issue(r0, 0, n_sp);
+    issue(r1, 1, n_sp);
+    // `after` of the previous stage runs once the current stage's operands
+    // are read: its data became visible at this stage's barrier
+    for (int st = 0;; st += 3) {
+      stage_sync();
+      issue(r2, st + 2, n_sp);
+      work(r0, d0, st, n_sp);
+      after(d2, st - 1, n_sp);   // nothing to finish before the first stage (st - 1 < 0)
+      if (st + 1 >= n_st) break;
+      stage_sync();
+      issue(r0, st + 3, n_sp);
+      work(r1, d1, st + 1, n_sp);
+      after(d0, st, n_sp);
+      if (st + 2 >= n_st) break;
+      stage_sync();
+      issue(r1, st + 4, n_sp);
+      work(r2, d2, st + 2, n_sp);
+      after(d1, st + 1, n_sp);
+      if (st + 3 >= n_st) break;
+    }
+    // drain: every load has landed and the last stage's results are visible
+    __builtin_amdgcn_s_waitcnt(0x070);
+    __syncthreads();
+    const int last = n_st - 1;
+    after(last % 3 == 0 ? d0 : (last % 3 == 1 ? d1 : d2), last, n_sp);
+    __syncthreads();
+  };
+  auto nothing = [](const Red &, int, int) __attribute__((always_inline)) {};
+
+  const int n_sp0 = a.nsp[2 * o];
+  run(n_sp0, [&](Ring<T, D> &R, Red &, int st, int n) __attribute__((always_inline)) { lse_stage(R, st, n); }, nothing);
+  // rows: lane groups merged (log2 units), then each lane takes the lse of
+  // the rows it holds in the pass-1 layout (rows 4 g4 + e of each block)
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    float mm = m[nb] > kFloor ? m[nb] * sl2 : -__builtin_inff();
+    float ll = l[nb];
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+      const float mo = __shfl_xor(mm, off, kWave);
+      const float lo = __shfl_xor(ll, off, kWave);
+      const float mn = fmaxf(mm, mo);
+      float ln = 0.f;
+      if (mn > -__builtin_inff())
+        ln = (mm > -__builtin_inff() ? ll * __builtin_amdgcn_exp2f(mm - mn) : 0.f) +
+             (mo > -__builtin_inff() ? lo * __builtin_amdgcn_exp2f(mo - mn) : 0.f);
+      mm = mn;
+      ll = ln;
+    }
+    const bool valid = row_u(row0 + nb * 16 + rr) >= 0 && ll > 0.f;
+    const float lse = valid ? mm + __log2f(ll) : __builtin_inff();
+#pragma unroll
+    for (int e = 0; e < 4; ++e) nlse[nb][e] = -__shfl(lse, 4 * g4 + e, kWave);
+  }
+  const int n_sp1 = a.nsp[2 * o + 1];
+  run(n_sp1, [&](Ring<T, D> &R, Red &RD, int st, int n) __attribute__((always_inline)) { col_stage(R, RD, st, n); },
+      [&](const Red &RD, int st, int n) __attribute__((always_inline)) { finish(RD, st, n); });
+}
+
 // Observer chains, partial offsets and validation (one workgroup).
 __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__restrict__ obs, int n_obs,
                                                    int S, int Hkv, int n_rg, int64_t part_cap,
                                                    int64_t *__restrict__ pbase,
                                                    int64_t *__restrict__ fbase,
+                                                   int64_t *__restrict__ tbase,
+                                                   int32_t *__restrict__ nsp, int self_window,
                                                    int32_t *__restrict__ ctxlen,
                                                    int32_t *__restrict__ odepth,
                                                    int32_t *__restrict__ anc, int32_t *status) {
@@ -459,10 +805,10 @@ __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__rest
     if (!ok || c < 0 || c > t.n_full[i]) atomicOr(&s_err, 1);
   }
   __syncthreads();
-  int64_t run = 0, frun = 0;
+  int64_t run = 0, frun = 0, trun = 0;
   for (int base = 0; base < n_obs; base += blockDim.x) {
     const int o = base + threadIdx.x;
-    int64_t len = 0;
+    int64_t len = 0, subs = 0;
     if (o < n_obs) {
       const int j = obs[o];
       if (j < 0 || j >= t.V) {
@@ -479,6 +825,7 @@ __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__rest
           }
           chainv[d++] = x;
           len += t.n_kept[x];
+          subs += (t.n_kept[x] + 15) / 16;
         }
         if (!ok) {
           atomicOr(&s_err, 2);
@@ -486,26 +833,56 @@ __global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__rest
         }
         odepth[o] = d - 1;
         for (int e = 0; e < d; ++e) anc[(int64_t)o * MAXD + e] = chainv[d - 1 - e];
+        const int own = ok ? (t.n_kept[j] + 15) / 16 : 0;
+        nsp[2 * o] = ok ? (int32_t)subs : 0;
+        nsp[2 * o + 1] = ok ? (int32_t)(self_window ? subs : subs - own) : 0;
       }
       ctxlen[o] = (int32_t)len;
     }
-    int64_t tot, ftot;
+    int64_t tot, ftot, ttot;
     const int64_t ex = block_exclusive_scan<int64_t>(len * S * Hkv * n_rg, sm, &tot);
     const int64_t fx = block_exclusive_scan<int64_t>(len, sm, &ftot);
+    const int64_t tx = block_exclusive_scan<int64_t>(subs, sm, &ttot);
     if (o < n_obs) {
       pbase[o] = run + ex;
       fbase[o] = frun + fx;
+      tbase[o] = 4 * (trun + tx);
     }
     run += tot;
     frun += ftot;
+    trun += ttot;
   }
   __syncthreads();
-  // the folded sums live after the partials in the same buffer
-  for (int o = threadIdx.x; o < n_obs; o += blockDim.x) fbase[o] += run;
+  // the folded sums live after the partials in the same buffer, then the
+  // sub-page tables (16-byte entries, 16-byte aligned)
+  const int64_t tab0 = (run + frun + 3) & ~(int64_t)3;
+  for (int o = threadIdx.x; o < n_obs; o += blockDim.x) {
+    fbase[o] += run;
+    tbase[o] += tab0;
+  }
   if (threadIdx.x == 0) {
     if (s_err & 1) status_error(status, ARBOR_EINVAL);
     else if (s_err & 2) status_error(status, ARBOR_EUNSUPPORTED);
-    else if (run + frun > part_cap) status_error(status, ARBOR_EWORKSPACE);
+    else if (tab0 + 4 * trun > part_cap) status_error(status, ARBOR_EWORKSPACE);
+  }
+}
+
+// One workgroup per observer: its chain's 16-slot sub-pages, root first, as
+// 16-byte entries (plane row, slot, context offset, valid slots | own << 8),
+// so the streaming kernel reads them with scalar loads.
+__global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
+  __shared__ ChainLds ch;
+  __shared__ int s_bad;
+  if (threadIdx.x == 0) s_bad = status_failed(a.status);
+  __syncthreads();
+  if (s_bad) return;
+  const int o = blockIdx.x;
+  build_chain(a.t, a.pl, a.obs[o], ch);
+  const int n = a.nsp[2 * o];
+  int4 *tab = reinterpret_cast<int4 *>(a.part + a.tbase[o]);
+  for (int sp = threadIdx.x; sp < n; sp += blockDim.x) {
+    const SubPage e = sub_page(a.t, a.pl, ch, sp);
+    tab[sp] = make_int4(e.row, e.slot, e.ctx, e.nvalid | ((e.d == ch.depth ? 1 : 0) << 8));
   }
 }
 
@@ -660,6 +1037,25 @@ void launch_pass(int dtype, int D, int NBW, dim3 grid, hipStream_t stream, const
   }
 }
 
+template <class T, int D>
+void launch_attn_nb(int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  switch (NBW) {
+    case 1: hipLaunchKernelGGL((score_attn<T, D, 1>), grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((score_attn<T, D, 2>), grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL((score_attn<T, D, 4>), grid, dim3(256), 0, stream, a); break;
+  }
+}
+
+void launch_attn(int dtype, int D, int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  if (dtype == ARBOR_BF16) {
+    if (D == 128) launch_attn_nb<__bf16, 128>(NBW, grid, stream, a);
+    else launch_attn_nb<__bf16, 64>(NBW, grid, stream, a);
+  } else {
+    if (D == 128) launch_attn_nb<float, 128>(NBW, grid, stream, a);
+    else launch_attn_nb<float, 64>(NBW, grid, stream, a);
+  }
+}
+
 // Row blocks per wave: the workgroup (4 waves) covers 64 * NBW query rows.
 int blocks_per_wave(int rows_total) {
   if (rows_total <= 64) return 1;
@@ -676,10 +1072,11 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
-  b += nobs * 8 + nobs * 4 * 2 + nobs * MAXD * 4 + 4 * 256;
+  b += nobs * 8 * 3 + nobs * 4 * 4 + nobs * MAXD * 4 + 5 * 256;
   b += nobs * slabs * 16 * NB * 4 + 256;
   b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
-  b += nobs * 8 + 256;
+  // sub-page tables: at most one ragged sub-page per chain node
+  b += nobs * ((size_t)sz->max_context / 16 + MAXD + 1) * 16 + 256;
   return b;
 }
 
@@ -715,6 +1112,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   const size_t nobs = n_obs > 0 ? (size_t)n_obs : 1;
   int64_t *pbase = cv.take<int64_t>(nobs);
   int64_t *fbase = cv.take<int64_t>(nobs);
+  int64_t *tbase = cv.take<int64_t>(nobs);
+  int32_t *nsp = cv.take<int32_t>(2 * nobs);
   int32_t *ctxlen = cv.take<int32_t>(nobs);
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
@@ -726,15 +1125,18 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.lse = lse;
   a.part = part;
   a.pbase = pbase;
+  a.tbase = tbase;
+  a.nsp = nsp;
   a.ctxlen = ctxlen;
   a.odepth = odepth;
   a.anc = anc;
   if (n_obs > 0) {
     hipLaunchKernelGGL(score_plan, dim3(1), dim3(1024), 0, stream, t, observers, n_obs, n_slice,
-                       pl.Hkv, a.n_rg, part_cap, pbase, fbase, ctxlen, odepth, anc, status);
+                       pl.Hkv, a.n_rg, part_cap, pbase, fbase, tbase, nsp, a.self_window, ctxlen,
+                       odepth, anc, status);
+    hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     const dim3 grid(n_obs, n_slice * pl.Hkv, a.n_rg);
-    launch_pass<0>(geom->dtype, geom->head_dim, NBW, grid, stream, a);
-    launch_pass<1>(geom->dtype, geom->head_dim, NBW, grid, stream, a);
+    launch_attn(geom->dtype, geom->head_dim, NBW, grid, stream, a);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, part, fbase);
     hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, part, fbase, A,
                        rows_seen);
