@@ -7,22 +7,21 @@
 // context (proper ancestors + own tokens up to the row), and the probability is
 // credited to tokens of proper ancestors (u > b_i).
 //
-// A row's normaliser spans its whole chain, so there are two passes over the
-// same (row, key) pairs, both as MFMA tiles of 16 keys (one 16-slot sub-page of
-// the paged pool) by 16 query rows:
-//   lse     C = K Q^T  (keys along M): each lane owns one query row and four
-//           keys, so the running max / sum stay in-lane; rows are merged over
-//           lane groups and waves at the end -> log2-sum-exp per row;
-//   colsum  C = Q K^T  (rows along M): each lane owns one key and four rows, so
-//           p = exp2(z - lse) sums over rows in-lane; one partial per
-//           (observer, slice layer, kv head, row group, context key), no atomics;
-//   reduce  per block i and 64-slot chunk: sum the partials of every observer
-//           below i in observer order (fp64) into A, rows_seen;
+// Launches on one stream:
+//   plan    (one workgroup) validate the tree, per-observer chain lengths,
+//           partial / table offsets;
+//   tables  one workgroup per observer: its chain's 16-slot sub-pages;
+//   attn    per (observer, slice layer, kv head, row group), two passes over
+//           the same (row, key) pairs as MFMA tiles of 16 keys x 16 rows:
+//           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
+//           sums of exp2(z - lse) -> one partial per credited context key;
+//   fold    per observer: sum its (slice layer, kv head, row group) partials;
+//   reduce  per block i and 64-slot chunk: sum the folded partials of every
+//           observer below i in observer order (fp64) into A, rows_seen;
 //   final   a_i = sum_p A_i(p) / rows_seen_i, s_i = clip(sigmoid(theta.phi)).
-// The Q operand of a wave stays in registers for the whole chain; keys are
-// split over the 4 waves of a workgroup by sub-page.  The reduction dimension
-// (head_dim) is permuted identically in both operands so that every lane reads
-// one contiguous quarter of a K or Q row (64 B for bf16 d=128).
+// No atomics anywhere, so A is bitwise reproducible.  The reduction dimension
+// (head_dim) is permuted identically in both MFMA operands so that every lane
+// reads one contiguous quarter of a K or Q row (64 B for bf16 d = 128).
 #include "arbor_internal.h"
 #include "mfma_ops.h"
 
@@ -136,310 +135,17 @@ __device__ __forceinline__ SubPage sub_page(const Tree &t, const Pool &pl, const
   return r;
 }
 
-// Sub-page staging: the workgroup loads each 16-key sub-page of K once into an
-// LDS ring; every wave then reads the operand of its own lanes.  Unit u =
-// blk * 64 + lane is 16 bytes: key (lane % 16), quarter (lane / 16), bytes
-// [16 blk, 16 blk + 16) of that quarter row.
-__device__ __forceinline__ int sub_meta(const ChainLds &ch, const Tree &t, const Pool &pl, int sp) {
-  if (sp < SPCAP) return ch.sp_meta[sp];
-  const SubPage s = sub_page(t, pl, ch, sp);
-  return s.d | (s.nvalid << 8);
-}
-
-__device__ __forceinline__ void sub_row_slot(const ChainLds &ch, const Tree &t, const Pool &pl,
-                                             int sp, int &row, int &slot) {
-  if (sp < SPCAP) {
-    row = ch.sp_row[sp];
-    slot = ch.sp_slot[sp];
-  } else {
-    const SubPage s = sub_page(t, pl, ch, sp);
-    row = s.row;
-    slot = s.slot;
-  }
-}
-
+// Layout of one 16-key sub-page of K in LDS: unit u = blk * 64 + lane is 16
+// bytes: key (lane % 16), quarter (lane / 16), bytes [16 blk, 16 blk + 16) of
+// that quarter row, so the MFMA operand of a k-step is one conflict-free
+// 16-byte read per lane.
 template <class T, int D>
 struct Stage {
   static constexpr int QB = D / 4 * (int)sizeof(T);  // bytes of a quarter row
   static constexpr int NBLK = QB / 16;                // 16-byte units per lane
   static constexpr int UNITS = NBLK * kWave;          // units per sub-page
-  static constexpr int UPT = (UNITS + 255) / 256;     // units per thread (256 threads)
   static constexpr int BYTES = UNITS * 16;
 };
-
-template <int PASS, class T, int D, int NBW, int GS>
-__global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
-  using O = Op<T>;
-  using SG = Stage<T, D>;
-  constexpr int KS = D / 4 / O::kPerStep;  // MFMA k-steps over head_dim
-  constexpr int RW = 64 * NBW;             // rows of the workgroup's row group
-  constexpr int RING = 2;                  // stages of GS sub-pages in LDS
-  __shared__ ChainLds ch;
-  __shared__ __attribute__((aligned(16))) char ring[RING][GS][SG::BYTES];
-  __shared__ __attribute__((aligned(16))) int ring_pos[RING][GS][16];
-  __shared__ float red[RING][GS][4][16];
-  if (status_failed(a.status)) return;
-  const Tree &t = a.t;
-  const Pool &pl = a.pl;
-  const int o = blockIdx.x;
-  const int slg = blockIdx.y;
-  const int rg = blockIdx.z;
-  const int si = slg / pl.Hkv;
-  const int g = slg % pl.Hkv;
-  const int layer = a.slice[si];
-  const int j = a.obs[o];
-  build_chain(t, pl, j, ch);
-  const int tid = threadIdx.x;
-  const int lane = lane_id();
-  // wave-uniform values live in scalar registers, so per-sub-page decisions
-  // below are branches instead of per-lane selects
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int rr = lane & 15;
-  const int g4 = lane >> 4;
-  const int G = pl.G;
-  const int nj = t.n_full[j];
-  const int wj = min(a.W, nj);
-  const int rows_total = G * a.W;
-  const int own_d = __builtin_amdgcn_readfirstlane(ch.depth);
-  const int row0 = rg * RW + wave * 16 * NBW;   // first row of this wave
-
-  // Q operand: query row row0 + nb*16 + rr of block nb
-  typename O::reg q[NBW][KS];
-  const T *qbase = static_cast<const T *>(a.q_win) +
-                   ((((int64_t)o * a.S + si) * (pl.Hkv * G) + (int64_t)g * G) * a.W) * D;
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    const int r = row0 + nb * 16 + rr;
-    const bool rv = r < rows_total;
-    const T *rp = qbase + (int64_t)(rv ? r : 0) * D + g4 * (D / 4);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) q[nb][ks] = rv ? O::load(rp + ks * O::kPerStep) : O::zero();
-  }
-  auto row_u = [&](int r) -> int {
-    if (r >= rows_total) return -1;
-    const int tt = r % a.W;
-    return tt < wj ? nj - wj + tt : -1;
-  };
-  const int64_t lse_base = (((int64_t)o * a.S + si) * pl.Hkv + g) * ((int64_t)a.n_rg * RW) +
-                           (int64_t)rg * RW;
-  const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
-  const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
-  const int n_sp = __builtin_amdgcn_readfirstlane(
-      (PASS == 1 && !a.self_window) ? ch.sp_off[own_d] : ch.sp_off[own_d + 1]);
-  const int n_st = (n_sp + GS - 1) / GS;   // stages
-
-  // Staging: two register sets alternate by stage parity, so a load has a full
-  // stage of compute to land before it is written to the LDS ring.  Loads are
-  // unconditional (indices are clamped to the last sub-page) so the number of
-  // loads in flight is the same on every path.
-  struct Staged {
-    uint4 u[GS][SG::UPT];
-    int pos[GS];
-  };
-  int unit_off[SG::UPT];
-#pragma unroll
-  for (int e = 0; e < SG::UPT; ++e) {
-    const int u = (tid + 256 * e) % SG::UNITS;
-    const int ul = u & 63, blk = u >> 6;
-    unit_off[e] = (ul & 15) * D * (int)sizeof(T) + (ul >> 4) * SG::QB + blk * 16;
-  }
-  auto fetch = [&](int st_idx) -> Staged {
-    Staged sv;
-#pragma unroll
-    for (int k = 0; k < GS; ++k) {
-      const int sp = min(st_idx * GS + k, n_sp - 1);
-      int row, slot;
-      sub_row_slot(ch, t, pl, sp, row, slot);
-      const char *src = kplane + (int64_t)row * (D * (int)sizeof(T));
-#pragma unroll
-      for (int e = 0; e < SG::UPT; ++e) sv.u[k][e] = *reinterpret_cast<const uint4 *>(src + unit_off[e]);
-      sv.pos[k] = pl.slot_pos[slot + (tid & 15)];
-    }
-    return sv;
-  };
-  auto commit = [&](int slot, const Staged sv) {
-#pragma unroll
-    for (int k = 0; k < GS; ++k) {
-#pragma unroll
-      for (int e = 0; e < SG::UPT; ++e) {
-        const int u = tid + 256 * e;
-        if (u < SG::UNITS) reinterpret_cast<uint4 *>(ring[slot][k])[u] = sv.u[k][e];
-      }
-      if (tid < 16) ring_pos[slot][k][tid] = sv.pos[k];
-    }
-  };
-  auto operand = [&](const char *buf, typename O::reg (&kr)[KS]) {
-    const char *base = buf + lane * 16;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int byte = ks * O::kPerStep * (int)sizeof(T);   // within the quarter row
-      kr[ks] = O::load(reinterpret_cast<const T *>(base + (byte / 16) * (kWave * 16) + byte % 16));
-    }
-  };
-
-  float m[NBW], l[NBW];
-  int urow[NBW];
-  float nlse[NBW][4];
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    m[nb] = -__builtin_inff();
-    l[nb] = 0.f;
-    urow[nb] = row_u(row0 + nb * 16 + rr);
-    if (PASS == 1) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) nlse[nb][e] = -a.lse[lse_base + wave * 16 * NBW + nb * 16 + 4 * g4 + e];
-    }
-  }
-  float *pout = PASS == 1 ? a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o] : nullptr;
-
-  // One stage: all MFMAs of its GS sub-pages first, then one softmax update
-  // (pass 0) or the column sums (pass 1).
-  auto compute = [&](int st_idx, int slot) {
-    f32x4 acc[GS][NBW];
-    int meta[GS];
-#pragma unroll
-    for (int k = 0; k < GS; ++k) {
-      const int sp = st_idx * GS + k;
-      meta[k] = __builtin_amdgcn_readfirstlane(sp < n_sp ? sub_meta(ch, t, pl, sp) : 0);
-      typename O::reg kr[KS];
-      operand(ring[slot][k], kr);
-#pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) {
-        acc[k][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          acc[k][nb] = PASS == 0 ? O::mma(kr[ks], q[nb][ks], acc[k][nb])
-                                 : O::mma(q[nb][ks], kr[ks], acc[k][nb]);
-      }
-    }
-    if (PASS == 0) {
-#pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int d = meta[k] & 255, nvalid = meta[k] >> 8;
-        const bool own = d == own_d;
-        if (own || nvalid < 16) {
-          int kpos[4] = {0, 0, 0, 0};
-          if (own) {
-            const int4 pv = *reinterpret_cast<const int4 *>(&ring_pos[slot][k][4 * g4]);
-            kpos[0] = pv.x;
-            kpos[1] = pv.y;
-            kpos[2] = pv.z;
-            kpos[3] = pv.w;
-          }
-#pragma unroll
-          for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bool ok = 4 * g4 + e < nvalid && (!own || kpos[e] <= urow[nb]);
-              acc[k][nb][e] = ok ? acc[k][nb][e] : -__builtin_inff();
-            }
-        }
-      }
-#pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) {
-        float mx = -__builtin_inff();
-#pragma unroll
-        for (int k = 0; k < GS; ++k)
-          mx = fmaxf(mx, fmaxf(fmaxf(acc[k][nb][0], acc[k][nb][1]), fmaxf(acc[k][nb][2], acc[k][nb][3])));
-        mx *= a.sl2;
-        if (mx > m[nb]) {
-          l[nb] *= __builtin_amdgcn_exp2f(m[nb] - mx);
-          m[nb] = mx;
-        }
-        const float nm = m[nb] > -__builtin_inff() ? -m[nb] : 0.f;
-#pragma unroll
-        for (int k = 0; k < GS; ++k)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) l[nb] += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nm));
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int d = meta[k] & 255;
-        const bool own = d == own_d && (st_idx * GS + k) < n_sp;
-        float colsum = 0.f;
-        if (own) {
-          const int kpos = ring_pos[slot][k][rr];
-#pragma unroll
-          for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float pz = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nlse[nb][e]));
-              colsum += (kpos < row_u(row0 + nb * 16 + 4 * g4 + e)) ? pz : 0.f;
-            }
-        } else {
-#pragma unroll
-          for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              colsum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], a.sl2, nlse[nb][e]));
-        }
-        colsum += __shfl_xor(colsum, 16, kWave);
-        colsum += __shfl_xor(colsum, 32, kWave);
-        if (lane < 16) red[slot][k][wave][lane] = colsum;
-      }
-    }
-  };
-  auto finish = [&](int st_idx, int slot) {
-    if (PASS == 1 && tid < 16 * GS) {
-      const int k = tid >> 4, key = tid & 15;
-      const int sp = st_idx * GS + k;
-      if (sp < n_sp) {
-        const SubPage cur = sub_page(t, pl, ch, sp);
-        if (key < cur.nvalid) {
-          const float v = ((red[slot][k][0][key] + red[slot][k][1][key]) + red[slot][k][2][key]) +
-                          red[slot][k][3][key];
-          pout[cur.ctx + key] = v;
-        }
-      }
-    }
-  };
-
-  if (n_st > 0) {
-    const int last = n_st - 1;
-    commit(0, fetch(0));
-    Staged s1 = fetch(min(1, last));
-    Staged s0 = fetch(min(2, last));
-    __syncthreads();
-    for (int st = 0; st < n_st; st += 2) {
-      // even stage: its successor sits in s1, the one after in s0
-      compute(st, 0);
-      if (st + 1 < n_st) commit(1, s1);
-      s1 = fetch(min(st + 3, last));
-      __syncthreads();
-      finish(st, 0);
-      const bool live = st + 1 < n_st;
-      if (live) compute(st + 1, 1);
-      if (st + 2 < n_st) commit(0, s0);
-      s0 = fetch(min(st + 4, last));
-      __syncthreads();
-      if (live) finish(st + 1, 1);
-    }
-  }
-  if (PASS == 0) {
-#pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-#pragma unroll
-      for (int off = 16; off <= 32; off <<= 1) {
-        const float mo = __shfl_xor(m[nb], off, kWave);
-        const float lo = __shfl_xor(l[nb], off, kWave);
-        const float mn = fmaxf(m[nb], mo);
-        float ln = 0.f;
-        if (mn > -__builtin_inff()) {
-          ln = (m[nb] > -__builtin_inff() ? l[nb] * __builtin_amdgcn_exp2f(m[nb] - mn) : 0.f) +
-               (mo > -__builtin_inff() ? lo * __builtin_amdgcn_exp2f(mo - mn) : 0.f);
-        }
-        m[nb] = mn;
-        l[nb] = ln;
-      }
-      if (g4 == 0) {
-        const int r = wave * 16 * NBW + nb * 16 + rr;
-        const bool valid = urow[nb] >= 0 && l[nb] > 0.f;
-        a.lse[lse_base + r] = valid ? m[nb] + __log2f(l[nb]) : __builtin_inff();
-      }
-    }
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Fused two-pass kernel.  Keys stream through a ring of RING stages of GS
@@ -454,6 +160,7 @@ __global__ __launch_bounds__(256) void score_pass(ScoreArgs a) {
 // refills.  Ring slots are distinct LDS arrays (the loop is unrolled by RING),
 // so the compiler can tell a slot being filled from the one being read.
 constexpr int kGS = 4;     // sub-pages per stage
+constexpr int kXcds = 8;   // accelerator dies of the device; workgroups go round-robin
 constexpr int kRing = 3;   // stages in the ring
 
 // v_max3 without the quieting the IEEE maxnum lowering adds to each operand:
@@ -470,6 +177,29 @@ __device__ __forceinline__ void load_to_lds16(const void *g, void *lds) {
 }
 __device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 4, 0, 0);
+}
+
+template <int N>
+__device__ __forceinline__ float tree_sum(const float (&v)[N]) {
+  static_assert((N & (N - 1)) == 0, "power of two");
+  float w[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) w[i] = v[i];
+#pragma unroll
+  for (int h = N / 2; h >= 1; h /= 2)
+#pragma unroll
+    for (int i = 0; i < h; ++i) w[i] = w[i] + w[i + h];
+  return w[0];
+}
+
+// max of v[] and m, three operands per instruction
+template <int N>
+__device__ __forceinline__ float tree_max(const float (&v)[N], float m) {
+  static_assert(N == 16, "one stage of a row block");
+  const float x0 = max3f(v[0], v[1], v[2]), x1 = max3f(v[3], v[4], v[5]);
+  const float x2 = max3f(v[6], v[7], v[8]), x3 = max3f(v[9], v[10], v[11]);
+  const float x4 = max3f(v[12], v[13], v[14]);
+  return max3f(max3f(x0, x1, x2), max3f(x3, x4, v[15]), m);
 }
 
 template <class T, int D>
@@ -498,14 +228,23 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   __shared__ Ring<T, D> r0, r1, r2;
   __shared__ Red d0, d1, d2;
   __shared__ int s_bad;
+  // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
+  // (slice layer, kv head, row group) planes p = x, x + 8, ... and, within a
+  // plane, the observers in id order -- siblings, which share their whole
+  // ancestor chain, run together and read those keys from the XCD's L2
+  const int n_planes = a.S * a.pl.Hkv * a.n_rg;
+  const int xcd = (int)blockIdx.x % kXcds;
+  const int idx = (int)blockIdx.x / kXcds;
+  const int o = idx % a.n_obs;
+  const int plane = (idx / a.n_obs) * kXcds + xcd;
+  if (plane >= n_planes) return;
   if (threadIdx.x == 0) s_bad = status_failed(a.status);
   __syncthreads();
   if (s_bad) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
-  const int o = blockIdx.x;
-  const int slg = blockIdx.y;
-  const int rg = blockIdx.z;
+  const int slg = plane / a.n_rg;
+  const int rg = plane % a.n_rg;
   const int si = slg / pl.Hkv;
   const int g = slg % pl.Hkv;
   const int layer = a.slice[si];
@@ -602,19 +341,21 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   auto lse_stage = [&](const Ring<T, D> &R, int st, int n_sp) __attribute__((always_inline)) {
     f32x4 acc[kGS][NBW];
     int meta[kGS];
+    typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int sp = st * kGS + k;
       meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
-      typename O::reg kr[KS];
-      operand(R, k, kr);
+      operand(R, k, kr[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < kGS; ++k)
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) {
         acc[k][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc[k][nb] = O::mma(kr[ks], q[nb][ks], acc[k][nb]);
+        for (int ks = 0; ks < KS; ++ks) acc[k][nb] = O::mma(kr[k][ks], q[nb][ks], acc[k][nb]);
       }
-    }
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int nvalid = meta[k] & 255;
@@ -641,20 +382,18 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
     }
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
-      float mx = m[nb];
-#pragma unroll
-      for (int k = 0; k < kGS; ++k) {
-        mx = max3f(mx, acc[k][nb][0], acc[k][nb][1]);
-        mx = max3f(mx, acc[k][nb][2], acc[k][nb][3]);
-      }
-      const float nm = -mx * sl2;
-      // (m - mx) is exactly 0 while the max is unchanged
-      float sum = l[nb] * __builtin_amdgcn_exp2f((m[nb] - mx) * sl2);
+      // reductions as trees: short dependency chains keep the VALU busy
+      float v[4 * kGS];
 #pragma unroll
       for (int k = 0; k < kGS; ++k)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[k][nb][e], sl2, nm));
-      l[nb] = sum;
+        for (int e = 0; e < 4; ++e) v[4 * k + e] = acc[k][nb][e];
+      const float mx = tree_max(v, m[nb]);
+      const float nm = -mx * sl2;
+#pragma unroll
+      for (int i = 0; i < 4 * kGS; ++i) v[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(v[i], sl2, nm));
+      // (m - mx) is exactly 0 while the max is unchanged
+      l[nb] = __builtin_fmaf(l[nb], __builtin_amdgcn_exp2f((m[nb] - mx) * sl2), tree_sum(v));
       m[nb] = mx;
     }
   };
@@ -663,38 +402,37 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   float nlse[NBW][4];
   float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
   auto col_stage = [&](Ring<T, D> &R, Red &RD, int st, int n_sp) __attribute__((always_inline)) {
+    typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int sp = st * kGS + k;
       const int meta = sp < n_sp ? tab[4 * sp + 3] : 0;
       const bool own = (meta >> 8) != 0;
-      typename O::reg kr[KS];
-      operand(R, k, kr);
       f32x4 acc[NBW];
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) {
         acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc[nb] = O::mma(q[nb][ks], kr[ks], acc[nb]);
+        for (int ks = 0; ks < KS; ++ks) acc[nb] = O::mma(q[nb][ks], kr[k][ks], acc[nb]);
       }
-      float colsum = 0.f;
+      float pz[4 * NBW];
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          pz[4 * nb + e] = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
       if (own) {
         // own tokens are credited only by later rows of the window
         const int kp = R.pos[k][rr];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float pz = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
-            colsum += kp < row_u(row0 + nb * 16 + 4 * g4 + e) ? pz : 0.f;
-          }
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
           for (int e = 0; e < 4; ++e)
-            colsum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
+            pz[4 * nb + e] = kp < row_u(row0 + nb * 16 + 4 * g4 + e) ? pz[4 * nb + e] : 0.f;
       }
+      float colsum = tree_sum(pz);
       colsum += __shfl_xor(colsum, 16, kWave);
       colsum += __shfl_xor(colsum, 32, kWave);
       if (lane < 16) RD.v[k][wave][lane] = colsum;
@@ -1012,31 +750,6 @@ __global__ __launch_bounds__(256) void score_final(Tree t, const float *__restri
   }
 }
 
-#ifndef ARBOR_SCORE_STAGE
-#define ARBOR_SCORE_STAGE 2
-#endif
-constexpr int kStageSub = ARBOR_SCORE_STAGE;   // sub-pages staged per barrier
-
-template <int PASS, class T, int D>
-void launch_pass_nb(int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
-  switch (NBW) {
-    case 1: hipLaunchKernelGGL((score_pass<PASS, T, D, 1, kStageSub>), grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((score_pass<PASS, T, D, 2, kStageSub>), grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL((score_pass<PASS, T, D, 4, kStageSub>), grid, dim3(256), 0, stream, a); break;
-  }
-}
-
-template <int PASS>
-void launch_pass(int dtype, int D, int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
-  if (dtype == ARBOR_BF16) {
-    if (D == 128) launch_pass_nb<PASS, __bf16, 128>(NBW, grid, stream, a);
-    else launch_pass_nb<PASS, __bf16, 64>(NBW, grid, stream, a);
-  } else {
-    if (D == 128) launch_pass_nb<PASS, float, 128>(NBW, grid, stream, a);
-    else launch_pass_nb<PASS, float, 64>(NBW, grid, stream, a);
-  }
-}
-
 template <class T, int D>
 void launch_attn_nb(int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
   switch (NBW) {
@@ -1135,7 +848,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
                        pl.Hkv, a.n_rg, part_cap, pbase, fbase, tbase, nsp, a.self_window, ctxlen,
                        odepth, anc, status);
     hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
-    const dim3 grid(n_obs, n_slice * pl.Hkv, a.n_rg);
+    const int n_planes = n_slice * pl.Hkv * a.n_rg;
+    const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     launch_attn(geom->dtype, geom->head_dim, NBW, grid, stream, a);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, part, fbase);
     hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, part, fbase, A,
