@@ -227,7 +227,11 @@ def build_state(parent, n_full, *, layers, kv_heads, q_per_kv, head_dim, dtype="
         # [L][N][Hkv][d] -> [N][L][Hkv][d]
         hk = k.permute(1, 3, 0, 2, 4)[pt, sl]
         hv = v.permute(1, 3, 0, 2, 4)[pt, sl]
-        if dev.type == "cuda":
+        if host_store == "device":
+            # the same token-major record kept in device memory (very large pools)
+            st["host_k"] = hk.contiguous()
+            st["host_v"] = hv.contiguous()
+        elif dev.type == "cuda":
             st["host_k"] = torch.empty(hk.shape, dtype=tdt, pin_memory=True)
             st["host_v"] = torch.empty(hv.shape, dtype=tdt, pin_memory=True)
             st["host_k"].copy_(hk)
