@@ -159,9 +159,11 @@ struct Stage {
 // barrier makes every wave's loads visible and frees the slot the next load
 // refills.  Ring slots are distinct LDS arrays (the loop is unrolled by RING),
 // so the compiler can tell a slot being filled from the one being read.
-constexpr int kGS = 4;     // sub-pages per stage
-constexpr int kXcds = 8;   // accelerator dies of the device; workgroups go round-robin
-constexpr int kRing = 3;   // stages in the ring
+constexpr int kGS = 4;         // sub-pages per stage
+constexpr int kRing = 3;       // stages in the ring
+constexpr int kXcds = 8;       // accelerator dies of the device; workgroups go round-robin
+template <int N>
+using Ic = std::integral_constant<int, N>;
 
 // v_max3 without the quieting the IEEE maxnum lowering adds to each operand:
 // the operands are MFMA results or -inf, never signalling NaNs.
@@ -297,9 +299,10 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
       rows[k] = tab[4 * sp];
       slots[k] = tab[4 * sp + 1];
     }
-    int my_slot = slots[0];
+    // lane L: position (L & 15) of sub-page L >> 4
+    int lane_slot = slots[0];
 #pragma unroll
-    for (int k = 1; k < kGS; ++k) my_slot = wave == k ? slots[k] : my_slot;
+    for (int k = 1; k < kGS; ++k) lane_slot = g4 == k ? slots[k] : lane_slot;
 #pragma unroll
     for (int i = 0; i < DPW; ++i) {
       const int u = wave + 4 * i;          // unit (sub-page k, 16-byte block blk)
@@ -310,15 +313,19 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
       const char *src = kplane + (int64_t)row * (D * (int)sizeof(T)) + lane_off + blk * 16;
       load_to_lds16(src, &R.k[k][blk * kWave * 16]);
     }
-    if (lane < 16)
-      load_to_lds4(pl.slot_pos + my_slot + lane, &R.pos[wave][0]);
+    // the key positions of all four sub-pages, loaded by every wave (the
+    // waves write the same values).  An unmasked load: a load under a lane
+    // mask gives the compiler paths with different numbers of loads in
+    // flight, and it then waits for all of them before each read of the ring.
+    load_to_lds4(pl.slot_pos + lane_slot + rr, &R.pos[0][0]);
   };
   // my loads of the stage about to be computed are done; everyone's are visible
   // (s_waitcnt immediate: vmcnt in bits 3:0, expcnt 6:4, lgkmcnt 11:8.)  The
   // LDS writes of this wave are complete too (lgkmcnt 0), so no release fence
   // is needed -- one would also wait for the loads still filling later slots.
-  auto stage_sync = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0x070 | ((kRing - 2) * VM));
+  // (`later`: how many stages' loads may stay in flight, a compile-time count)
+  auto stage_sync = [&](auto later) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0x070 | (decltype(later)::value * VM));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   };
@@ -338,15 +345,18 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
     m[nb] = kFloor;
     l[nb] = 0.f;
   }
-  auto lse_stage = [&](const Ring<T, D> &R, int st, int n_sp) __attribute__((always_inline)) {
+  auto lse_stage = [&](const Ring<T, D> &R, int st, int n_sp, auto &&between)
+                       __attribute__((always_inline)) {
     f32x4 acc[kGS][NBW];
     int meta[kGS];
     typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
 #pragma unroll
+    for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
+    between();
+#pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int sp = st * kGS + k;
       meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
-      operand(R, k, kr[k]);
     }
 #pragma unroll
     for (int k = 0; k < kGS; ++k)
@@ -401,10 +411,12 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   // ---- pass 1: credited column sums ----
   float nlse[NBW][4];
   float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
-  auto col_stage = [&](Ring<T, D> &R, Red &RD, int st, int n_sp) __attribute__((always_inline)) {
+  auto col_stage = [&](Ring<T, D> &R, Red &RD, int st, int n_sp, auto &&between)
+                       __attribute__((always_inline)) {
     typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
 #pragma unroll
     for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
+    between();
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int sp = st * kGS + k;
@@ -463,24 +475,35 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
     const int n_st = (n_sp + kGS - 1) / kGS;
     issue(r0, 0, n_sp);
     issue(r1, 1, n_sp);
-    // `after` of the previous stage runs once the current stage's operands
-    // are read: its data became visible at this stage's barrier
-    for (int st = 0;; st += 3) {
-      stage_sync();
-      issue(r2, st + 2, n_sp);
-      work(r0, d0, st, n_sp);
+    // A stage reads its operands from the slot first and only then issues the
+    // loads that refill the previous slot.  `after` of the previous stage runs
+    // once the current stage is computed: its data became visible at this
+    // stage's barrier.  Whole rounds of three stages run in a loop with one
+    // exit, so every path into a stage has the same loads in flight and the
+    // compiler keeps the partial waits.
+    int st = 0;
+    for (; st + 3 <= n_st; st += 3) {
+      stage_sync(Ic<kRing - 2>{});
+      work(r0, d0, st, n_sp, [&]() __attribute__((always_inline)) { issue(r2, st + 2, n_sp); });
       after(d2, st - 1, n_sp);   // nothing to finish before the first stage (st - 1 < 0)
-      if (st + 1 >= n_st) break;
-      stage_sync();
-      issue(r0, st + 3, n_sp);
-      work(r1, d1, st + 1, n_sp);
+      stage_sync(Ic<kRing - 2>{});
+      work(r1, d1, st + 1, n_sp, [&]() __attribute__((always_inline)) { issue(r0, st + 3, n_sp); });
       after(d0, st, n_sp);
-      if (st + 2 >= n_st) break;
-      stage_sync();
-      issue(r1, st + 4, n_sp);
-      work(r2, d2, st + 2, n_sp);
+      stage_sync(Ic<kRing - 2>{});
+      work(r2, d2, st + 2, n_sp, [&]() __attribute__((always_inline)) { issue(r1, st + 4, n_sp); });
       after(d1, st + 1, n_sp);
-      if (st + 3 >= n_st) break;
+    }
+    // the last one or two stages: their loads are already in flight
+    auto none = []() __attribute__((always_inline)) {};
+    if (st < n_st) {
+      stage_sync(Ic<1>{});
+      work(r0, d0, st, n_sp, none);
+      after(d2, st - 1, n_sp);
+      if (st + 1 < n_st) {
+        stage_sync(Ic<0>{});
+        work(r1, d1, st + 1, n_sp, none);
+        after(d0, st, n_sp);
+      }
     }
     // drain: every load has landed and the last stage's results are visible
     __builtin_amdgcn_s_waitcnt(0x070);
@@ -492,7 +515,11 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   auto nothing = [](const Red &, int, int) __attribute__((always_inline)) {};
 
   const int n_sp0 = a.nsp[2 * o];
-  run(n_sp0, [&](Ring<T, D> &R, Red &, int st, int n) __attribute__((always_inline)) { lse_stage(R, st, n); }, nothing);
+  run(n_sp0,
+      [&](Ring<T, D> &R, Red &, int st, int n, auto &&between) __attribute__((always_inline)) {
+        lse_stage(R, st, n, between);
+      },
+      nothing);
   // rows: lane groups merged (log2 units), then each lane takes the lse of
   // the rows it holds in the pass-1 layout (rows 4 g4 + e of each block)
 #pragma unroll
@@ -517,7 +544,10 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
     for (int e = 0; e < 4; ++e) nlse[nb][e] = -__shfl(lse, 4 * g4 + e, kWave);
   }
   const int n_sp1 = a.nsp[2 * o + 1];
-  run(n_sp1, [&](Ring<T, D> &R, Red &RD, int st, int n) __attribute__((always_inline)) { col_stage(R, RD, st, n); },
+  run(n_sp1,
+      [&](Ring<T, D> &R, Red &RD, int st, int n, auto &&between) __attribute__((always_inline)) {
+        col_stage(R, RD, st, n, between);
+      },
       [&](const Red &RD, int st, int n) __attribute__((always_inline)) { finish(RD, st, n); });
 }
 
