@@ -181,6 +181,17 @@ __device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 4, 0, 0);
 }
 
+// sum over the four 16-lane groups of the wave (lanes l, l ^ 16, l ^ 32,
+// l ^ 48), in every lane: two lane swaps across rows instead of LDS permutes
+__device__ __forceinline__ float group_sum(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const unsigned w = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 template <int N>
 __device__ __forceinline__ float tree_sum(const float (&v)[N]) {
   static_assert((N & (N - 1)) == 0, "power of two");
@@ -258,7 +269,8 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   const TabPtr tab = (TabPtr)(a.part + a.tbase[o]);
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // (& 3: four waves; lets the compiler resolve each load's sub-page statically)
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;
   const int rr = lane & 15;
   const int g4 = lane >> 4;
   const int G = pl.G;
@@ -366,11 +378,13 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) acc[k][nb] = O::mma(kr[k][ks], q[nb][ks], acc[k][nb]);
       }
+    // meta == 16: a full sub-page of ancestor keys, nothing to mask
+    const bool any_mask = ((meta[0] ^ 16) | (meta[1] ^ 16) | (meta[2] ^ 16) | (meta[3] ^ 16)) != 0;
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int nvalid = meta[k] & 255;
       const bool own = (meta[k] >> 8) != 0;
-      if (own || nvalid < 16) {
+      if (any_mask && (own || nvalid < 16)) {
         int kpos[4] = {0, 0, 0, 0};
         if (own) {
           const int4 pv = *reinterpret_cast<const int4 *>(&R.pos[k][4 * g4]);
@@ -417,11 +431,16 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
 #pragma unroll
     for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
     between();
+    int meta[kGS];
 #pragma unroll
     for (int k = 0; k < kGS; ++k) {
       const int sp = st * kGS + k;
-      const int meta = sp < n_sp ? tab[4 * sp + 3] : 0;
-      const bool own = (meta >> 8) != 0;
+      meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
+    }
+    const bool any_own = ((meta[0] | meta[1] | meta[2] | meta[3]) >> 8) != 0;
+#pragma unroll
+    for (int k = 0; k < kGS; ++k) {
+      const bool own = any_own && (meta[k] >> 8) != 0;
       f32x4 acc[NBW];
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) {
@@ -444,9 +463,7 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
           for (int e = 0; e < 4; ++e)
             pz[4 * nb + e] = kp < row_u(row0 + nb * 16 + 4 * g4 + e) ? pz[4 * nb + e] : 0.f;
       }
-      float colsum = tree_sum(pz);
-      colsum += __shfl_xor(colsum, 16, kWave);
-      colsum += __shfl_xor(colsum, 32, kWave);
+      const float colsum = group_sum(tree_sum(pz));
       if (lane < 16) RD.v[k][wave][lane] = colsum;
     }
   };
