@@ -6,16 +6,23 @@
 // Sec. 4 sets the one global scale alpha so that the total meets the budget.
 // Token j of block i is kept exactly when alpha >= j / (w_i n_i) ("price"), so
 // the largest feasible alpha keeps every price below the (E+1)-th smallest one,
-// E being the budget left after the floors.  That order statistic is found by
-// an MSB-first radix select over the fp64 bit patterns of the prices (positive
-// doubles order like their bits).  Path* nodes (Alg. 2 Transition) are pinned
-// at n_i; when the floors alone overflow (Alg. 2 Pressure) the lowest-priority
-// blocks are drained towards K_min, found by a weighted radix select over the
-// bit patterns of w_i.
+// E being the budget left after the floors.  Path* nodes (Alg. 2 Transition)
+// are pinned at n_i; when the floors alone overflow (Alg. 2 Pressure) the
+// lowest-priority blocks are drained towards K_min, found by a weighted radix
+// select over the bit patterns of w_i.
 //
-// Everything runs in one 1024-thread workgroup: the work is O(V + sum of
-// candidate tokens) and latency bound.  fp64, no contraction, so the prices
-// are the same IEEE quotients any fp64 implementation computes.
+// Finding the (E+1)-th smallest price without listing every token: the prices
+// of block i are j / W_i for consecutive j, so the number of prices up to x is
+// floor(x W_i) - F_i (clamped), exact up to rounding at the two ends.  A
+// search over x with that count brackets the order statistic between two
+// values whose exact counts lie on either side of E; only the few prices in
+// the bracket are listed, and an MSB-first radix select over their fp64 bit
+// patterns (positive doubles order like their bits) picks the exact one.
+//
+// Everything runs in one 1024-thread workgroup: the work is O(V) per search
+// step and latency bound.  Per-node state sits in LDS when the tree is small
+// enough, else in the workspace.  fp64, no contraction, so the prices are the
+// same IEEE quotients any fp64 implementation computes.
 #include "arbor_internal.h"
 
 #pragma clang fp contract(off)
@@ -25,22 +32,44 @@ namespace arbor {
 namespace {
 
 constexpr int AT = 1024;
+constexpr int kLdsNodes = 512;    // per-node state in LDS up to this many nodes
+constexpr int kCandLds = 1536;    // listed prices selected in LDS up to this many
+constexpr int kNodeBytes = 2 * 8 + 7 * 4 + 1;
+constexpr int kSearchWaves = AT / kWave / 2;   // test points per bracket end
+constexpr int kDecay = 128;                    // tabulated depths and distances
 
+// The decay factors exp(-lambda_d d) and exp(-lambda_Delta Delta) for small
+// integer d and Delta are tabulated per call by the host with the C library's
+// exp, the same doubles an fp64 reference on the host obtains, so that ties
+// between prices of different nodes break the same way (a device exp may
+// round the last bit differently).
 struct AllocParams {
   double alpha_max, gamma, lambda_d, lambda_delta, eta, r_min;
   int k_min, l_tail;
+  double dexp[kDecay], texp[kDecay];
+};
+
+// s^gamma; exact for the common gamma = 2 (s is an fp32 value, its square is
+// a double) and gamma = 1
+__device__ __forceinline__ double pow_gamma(double s, double gamma) {
+  if (gamma == 2.0) return s * s;
+  if (gamma == 1.0) return s;
+  return pow(s, gamma);
+}
+
+// Per-node working state.  parent / n_full / n_kept are the tree's arrays or
+// LDS copies of them; `path` is the on-path output or its LDS copy.
+struct Nodes {
+  int32_t *parent, *n_full, *n_kept;
+  int32_t *depth, *down, *F, *cnt;
+  double *W, *w;
+  uint8_t *path;
 };
 
 struct AllocWs {
-  int32_t *depth;
-  int32_t *down;
-  int32_t *F;
-  int32_t *cnt;        // eligible prices per node
-  int64_t *cnt_off;    // exclusive prefix of cnt
-  double *W;           // w_i * n_i
-  double *w;
-  uint64_t *buf0;
-  uint64_t *buf1;
+  int32_t *depth, *down, *F, *cnt;
+  double *W, *w;
+  uint64_t *buf0, *buf1;
   int64_t buf_cap;
 };
 
@@ -64,28 +93,36 @@ __device__ int count_prefix(int F, int c, double W, Pred pred) {
   return ans - F;
 }
 
+// Largest m in [F, F + cnt] with price(m) <= x (m = F: none), starting from
+// the rounded estimate floor(x W) and correcting it by exact comparisons.
+__device__ int last_le(double x, int F, int cnt, double W) {
+  double y = __builtin_floor(x * W);
+  y = y < (double)F ? (double)F : (y > (double)(F + cnt) ? (double)(F + cnt) : y);
+  int m = (int)y;
+  while (m < F + cnt && price(m + 1, W) <= x) ++m;
+  while (m > F && price(m, W) > x) --m;
+  return m;
+}
+
+// Rounded count of prices <= x of one node (exact up to one price at each end).
+__device__ __forceinline__ double approx_le(double x, int F, int cnt, double W) {
+  double y = __builtin_floor(x * W) - (double)F;
+  return y < 0.0 ? 0.0 : (y > (double)cnt ? (double)cnt : y);
+}
+
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-  for (int d = kWave / 2; d > 0; d >>= 1) {
-    const uint64_t o = __shfl_xor(v, d, kWave);
-    v = o < v ? o : v;
-  }
-  return v;
+  return wave_allreduce(v, [](uint64_t a, uint64_t b) { return a < b ? a : b; });
 }
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int d = kWave / 2; d > 0; d >>= 1) {
-    const uint64_t o = __shfl_xor(v, d, kWave);
-    v = o > v ? o : v;
-  }
-  return v;
+  return wave_allreduce(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
 }
+
+// block-wide min / max: wave partials in sm, then every wave combines them
 __device__ uint64_t block_min_u64(uint64_t v, uint64_t *sm) {
   v = wave_min_u64(v);
   if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
   __syncthreads();
-  uint64_t r = sm[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = sm[w] < r ? sm[w] : r;
+  const uint64_t r = wave_min_u64(lane_id() < (int)(blockDim.x >> 6) ? sm[lane_id()] : ~0ull);
   __syncthreads();
   return r;
 }
@@ -93,10 +130,144 @@ __device__ uint64_t block_max_u64(uint64_t v, uint64_t *sm) {
   v = wave_max_u64(v);
   if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
   __syncthreads();
-  uint64_t r = sm[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = sm[w] > r ? sm[w] : r;
+  const uint64_t r = wave_max_u64(lane_id() < (int)(blockDim.x >> 6) ? sm[lane_id()] : 0ull);
   __syncthreads();
   return r;
+}
+
+// three block-wide sums in one exchange; sm holds 48 values
+__device__ void block_sum3(int64_t (&v)[3], int64_t *sm) {
+  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+  for (int q = 0; q < 3; ++q) v[q] = wave_sum(v[q]);
+  if (lane == 0)
+#pragma unroll
+    for (int q = 0; q < 3; ++q) sm[16 * q + w] = v[q];
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 3; ++q) v[q] = wave_sum(lane < nw ? sm[16 * q + lane] : (int64_t)0);
+  __syncthreads();
+}
+
+__device__ __forceinline__ int64_t wave_min_i64(int64_t v) {
+  return wave_allreduce(v, [](int64_t a, int64_t b) { return a < b ? a : b; });
+}
+
+// block-wide sum of v[0] and minima of v[1], v[2] in one exchange
+__device__ void block_min_sum3(int64_t (&v)[3], int64_t *sm) {
+  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v[0] = wave_sum(v[0]);
+  v[1] = wave_min_i64(v[1]);
+  v[2] = wave_min_i64(v[2]);
+  if (lane == 0)
+#pragma unroll
+    for (int q = 0; q < 3; ++q) sm[16 * q + w] = v[q];
+  __syncthreads();
+  const bool in = lane < nw;
+  v[0] = wave_sum(in ? sm[lane] : (int64_t)0);
+  v[1] = wave_min_i64(in ? sm[16 + lane] : INT64_MAX);
+  v[2] = wave_min_i64(in ? sm[32 + lane] : INT64_MAX);
+  __syncthreads();
+}
+
+// The rank-th smallest (0-based) of the keys src[0, n), 0 <= rank < n: an
+// MSB-first radix select over 8-bit digits until at most 64 candidates are
+// left, which one wave then ranks directly.  src and dst (room for n keys) may
+// be LDS or global memory; both are overwritten.  Called by the whole block;
+// contains __syncthreads.
+__device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t rank) {
+  __shared__ unsigned hist4[4 * 256];
+  __shared__ int64_t s_wtot[4];
+  __shared__ int s_chosen;
+  __shared__ int64_t s_below;
+  __shared__ unsigned s_ncand;
+  __shared__ uint64_t s_mm[17];
+  __shared__ uint64_t s_key;
+  const int tid = threadIdx.x, lane = lane_id();
+  uint64_t cmin = ~0ull, cmax = 0ull;
+  for (int64_t e = tid; e < n; e += blockDim.x) {
+    const uint64_t key = src[e];
+    cmin = key < cmin ? key : cmin;
+    cmax = key > cmax ? key : cmax;
+  }
+  cmin = block_min_u64(cmin, s_mm);
+  cmax = block_max_u64(cmax, s_mm);
+  if (cmin == cmax) return cmin;
+  int64_t ncand = n;
+  const int top = 63 - __builtin_clzll(cmin ^ cmax);
+  int shift = (top / 8) * 8;
+  uint64_t prefix = cmin & ~((shift + 8 >= 64) ? ~0ull : ((1ull << (shift + 8)) - 1ull));
+  for (; ncand > kWave; shift -= 8) {
+    for (int bn = tid; bn < 4 * 256; bn += blockDim.x) hist4[bn] = 0;
+    __syncthreads();
+    unsigned *myh = hist4 + 256 * ((tid >> 6) & 3);
+    for (int64_t e = tid; e < ncand; e += blockDim.x)
+      atomicAdd(&myh[(src[e] >> shift) & 255ull], 1u);
+    __syncthreads();
+    // bin holding the element of rank `rank` (first 256 threads, 4 waves)
+    const unsigned h =
+        tid < 256 ? hist4[tid] + hist4[256 + tid] + hist4[512 + tid] + hist4[768 + tid] : 0u;
+    const int64_t inc = wave_inclusive_scan<int64_t>((int64_t)h);
+    if (tid < 256 && lane == kWave - 1) s_wtot[tid >> 6] = inc;
+    __syncthreads();
+    if (tid < 256) {
+      int64_t base = 0;
+      for (int w = 0; w < (tid >> 6); ++w) base += s_wtot[w];
+      const int64_t ex = base + inc - (int64_t)h;
+      if (ex <= rank && rank < ex + (int64_t)h) {
+        s_chosen = tid;
+        s_below = ex;
+      }
+    }
+    __syncthreads();
+    const int chosen = s_chosen;
+    rank -= s_below;
+    prefix |= (uint64_t)chosen << shift;
+    if (shift == 0) return prefix;
+    if (tid == 0) s_ncand = 0;
+    __syncthreads();
+    for (int64_t e0 = 0; e0 < ncand; e0 += blockDim.x) {
+      const int64_t e = e0 + tid;
+      const bool keep = e < ncand && (int)((src[e] >> shift) & 255ull) == chosen;
+      const uint64_t bk = ballot(keep);
+      unsigned base = 0;
+      if (lane == 0 && bk) base = atomicAdd(&s_ncand, (unsigned)popc(bk));
+      base = lane_value(base, 0);
+      if (keep) dst[base + rank_below(bk, lane)] = src[e];
+    }
+    __syncthreads();
+    ncand = s_ncand;
+    uint64_t *tmp = src;
+    src = dst;
+    dst = tmp;
+    __syncthreads();
+  }
+  // at most 64 left: lane l holds candidate l and counts the smaller ones
+  if (tid < kWave) {
+    const uint64_t k = lane < ncand ? src[lane] : ~0ull;
+    int less = 0, leq = 0;
+    for (int j = 0; j < (int)ncand; ++j) {
+      const uint64_t kj =
+          (uint64_t)(unsigned)__builtin_amdgcn_readlane((int)(unsigned)k, j) |
+          ((uint64_t)(unsigned)__builtin_amdgcn_readlane((int)(unsigned)(k >> 32), j) << 32);
+      less += kj < k ? 1 : 0;
+      leq += kj <= k ? 1 : 0;
+    }
+    if (lane < ncand && less <= rank && rank < leq) s_key = k;
+  }
+  __syncthreads();
+  return s_key;
+}
+
+__device__ __forceinline__ double key_value(uint64_t k) {
+  return __longlong_as_double((long long)k);
+}
+
+// test point q (0-based) of N splitting (lo, lo + span) into N + 1 parts
+template <int N>
+__device__ __forceinline__ uint64_t split_point(uint64_t lo, uint64_t span, int q) {
+  const uint64_t m = (uint64_t)(q + 1);
+  return lo + (span / (N + 1)) * m + ((span % (N + 1)) * m) / (N + 1);
 }
 
 __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__restrict__ active,
@@ -105,32 +276,65 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
                                                       int32_t *__restrict__ k_out,
                                                       int32_t *__restrict__ delta_out,
                                                       uint8_t *__restrict__ on_path,
-                                                      int32_t *status, AllocWs ws) {
-  __shared__ int64_t sm[17];
+                                                      int32_t *status, AllocWs ws, int in_lds) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  __shared__ int64_t sm[3 * 16];
   __shared__ int s_err;
-  __shared__ unsigned hist4[4 * 256];
   __shared__ unsigned long long hist64[256];
-  __shared__ unsigned s_ncand;
-  __shared__ uint64_t s_u64[17];
-  __shared__ int64_t s_wtot[4];
-  __shared__ int s_chosen;
-  __shared__ int64_t s_below;
+  __shared__ double s_cnt[2][2 * kSearchWaves];
   if (status_failed(status)) return;
   const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = lane_id();
   const int V = t.V;
   if (tid == 0) s_err = 0;
+
+  // listed prices: LDS after the node state when few enough, else workspace
+  uint64_t *const cand_lds =
+      reinterpret_cast<uint64_t *>(dyn + (in_lds ? ((size_t)V * kNodeBytes + 15) / 16 * 16 : 0));
+  Nodes nd;
+  if (in_lds) {
+    double *dp = reinterpret_cast<double *>(dyn);
+    nd.W = dp;
+    nd.w = dp + V;
+    int32_t *ip = reinterpret_cast<int32_t *>(dp + 2 * V);
+    nd.parent = ip;
+    nd.n_full = ip + V;
+    nd.n_kept = ip + 2 * V;
+    nd.depth = ip + 3 * V;
+    nd.down = ip + 4 * V;
+    nd.F = ip + 5 * V;
+    nd.cnt = ip + 6 * V;
+    nd.path = reinterpret_cast<uint8_t *>(ip + 7 * V);
+
+    for (int i = tid; i < V; i += AT) {
+      nd.parent[i] = t.parent[i];
+      nd.n_full[i] = t.n_full[i];
+      nd.n_kept[i] = t.n_kept[i];
+    }
+  } else {
+    nd.parent = const_cast<int32_t *>(t.parent);
+    nd.n_full = const_cast<int32_t *>(t.n_full);
+    nd.n_kept = t.n_kept;
+    nd.depth = ws.depth;
+    nd.down = ws.down;
+    nd.F = ws.F;
+    nd.cnt = ws.cnt;
+    nd.W = ws.W;
+    nd.w = ws.w;
+    nd.path = on_path;
+  }
   __syncthreads();
 
   // ---- geometry: validation, depth d_i, Path*, Delta_i (Sec. 3) ----------
   for (int i = tid; i < V; i += AT) {
-    const int par = t.parent[i];
-    const int n = t.n_full[i];
-    const int c = t.n_kept[i];
+    const int par = nd.parent[i];
+    const int n = nd.n_full[i];
+    const int c = nd.n_kept[i];
     bool ok = (i == 0) ? (par == -1) : (par >= 0 && par < i);
     ok = ok && n >= 0 && c >= 0 && c <= n;
     int d = 0;
     for (int a = i; ok && a > 0;) {
-      const int pa = t.parent[a];
+      const int pa = nd.parent[a];
       if (pa < 0 || pa >= a) {
         ok = false;
         break;
@@ -139,9 +343,9 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       ++d;
     }
     if (!ok) atomicOr(&s_err, 1);
-    ws.depth[i] = d;
-    ws.down[i] = 0x7fffffff;
-    on_path[i] = 0;
+    nd.depth[i] = d;
+    nd.down[i] = 0x7fffffff;
+    nd.path[i] = 0;
   }
   __syncthreads();
   if (n_active < 1) s_err = 1;
@@ -152,10 +356,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       atomicOr(&s_err, 1);
       continue;
     }
-    const int dl = ws.depth[l];
-    for (int a = l; a >= 0; a = t.parent[a]) {
-      on_path[a] = 1;
-      atomicMin(&ws.down[a], dl - ws.depth[a]);
+    const int dl = nd.depth[l];
+    for (int a = l; a >= 0; a = nd.parent[a]) {
+      nd.path[a] = 1;
+      atomicMin(&nd.down[a], dl - nd.depth[a]);
     }
   }
   __syncthreads();
@@ -168,20 +372,21 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   int64_t path_tok = 0, sum_F = 0, sum_red = 0;
   for (int i = tid; i < V; i += AT) {
     int best = 0x7fffffff;
-    const int di = ws.depth[i];
-    for (int a = i; a >= 0; a = t.parent[a]) {
-      const int dn = ws.down[a];
-      if (dn != 0x7fffffff) best = min(best, di - ws.depth[a] + dn);
+    const int di = nd.depth[i];
+    for (int a = i; a >= 0; a = nd.parent[a]) {
+      const int dn = nd.down[a];
+      if (dn != 0x7fffffff) best = min(best, di - nd.depth[a] + dn);
     }
     delta_out[i] = best;
-    const int n = t.n_full[i];
-    const int c = t.n_kept[i];
-    if (on_path[i]) {
+    const int n = nd.n_full[i];
+    const int c = nd.n_kept[i];
+    if (in_lds) on_path[i] = nd.path[i];
+    if (nd.path[i]) {
       k_out[i] = n;
       path_tok += n;
-      ws.F[i] = 0;
-      ws.W[i] = 0.0;
-      ws.w[i] = 0.0;
+      nd.F[i] = 0;
+      nd.W[i] = 0.0;
+      nd.w[i] = 0.0;
       continue;
     }
     const float sf = s_in[i];
@@ -191,20 +396,24 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     int f = max(p.k_min, min(p.l_tail, n));
     f = max(f, (int)floor(p.r_min * (double)n));
     f = min(c, min(n, f));
-    ws.F[i] = f;
+    nd.F[i] = f;
     // the off-path Eq. 2 weight without alpha, in the same operation order as
     // ((eta * s^gamma) * e^{-lambda_d d}) * e^{-lambda_Delta Delta}
-    double w = p.eta * pow(s, p.gamma);
-    w = w * exp(-p.lambda_d * (double)di);
-    w = w * exp(-p.lambda_delta * (double)best);
-    ws.w[i] = w;
-    ws.W[i] = w * (double)n;
+    double w = p.eta * pow_gamma(s, p.gamma);
+    w = w * (di < kDecay ? p.dexp[di] : exp(-p.lambda_d * (double)di));
+    w = w * (best < kDecay ? p.texp[best] : exp(-p.lambda_delta * (double)best));
+    nd.w[i] = w;
+    nd.W[i] = w * (double)n;
     sum_F += f;
     sum_red += f - min(p.k_min, c);
   }
-  path_tok = block_sum<int64_t>(path_tok, sm);
-  sum_F = block_sum<int64_t>(sum_F, sm);
-  sum_red = block_sum<int64_t>(sum_red, sm);
+  {
+    int64_t v3[3] = {path_tok, sum_F, sum_red};
+    block_sum3(v3, sm);
+    path_tok = v3[0];
+    sum_F = v3[1];
+    sum_red = v3[2];
+  }
   if (s_err) {
     if (tid == 0) status_error(status, ARBOR_ENONFINITE);
     return;
@@ -215,122 +424,177 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     // ---- budget mode: alpha from the price order statistic ---------------
     const int64_t E = b_off - sum_F;
     const double amax = p.alpha_max;
-    int64_t total = 0;
+    // eligible prices of each node (finite, at most alpha_max) and their range
+    int64_t total = 0, n_elig = 0;
+    uint64_t kmin = ~0ull, kmax = 0ull;
     for (int i = tid; i < V; i += AT) {
       int cnt = 0;
-      if (!on_path[i]) {
-        const double W = ws.W[i];
-        cnt = count_prefix(ws.F[i], t.n_kept[i], W,
+      if (!nd.path[i]) {
+        const double W = nd.W[i];
+        const int F = nd.F[i];
+        cnt = count_prefix(F, nd.n_kept[i], W,
                            [amax](double x) { return x <= amax && x < __builtin_inf(); });
+        if (cnt > 0) {
+          const uint64_t lo = (uint64_t)__double_as_longlong(price(F + 1, W));
+          const uint64_t hi = (uint64_t)__double_as_longlong(price(F + cnt, W));
+          kmin = lo < kmin ? lo : kmin;
+          kmax = hi > kmax ? hi : kmax;
+          ++n_elig;
+        }
       }
-      ws.cnt[i] = cnt;
+      nd.cnt[i] = cnt;
       total += cnt;
     }
     total = block_sum<int64_t>(total, sm);
     if (total <= E) {
       for (int i = tid; i < V; i += AT)
-        if (!on_path[i]) k_out[i] = ws.F[i] + ws.cnt[i];
+        if (!nd.path[i]) k_out[i] = nd.F[i] + nd.cnt[i];
       return;
     }
-    if (total > ws.buf_cap) {
+    {
+      // n_elig, kmin and kmax in one exchange (finite positive keys are below
+      // 2^63: the maximum is taken as the minimum of INT64_MAX - key)
+      int64_t v3[3] = {n_elig, kmin == ~0ull ? INT64_MAX : (int64_t)kmin,
+                       INT64_MAX - (int64_t)kmax};
+      block_min_sum3(v3, sm);
+      n_elig = v3[0];
+      kmin = (uint64_t)v3[1];
+      kmax = (uint64_t)(INT64_MAX - v3[2]);
+    }
+
+    // -- bracket: keys a (few prices <= a) and b (enough prices <= b) --------
+    // The rounded count is off by at most two prices per node, so
+    //   approx(a) <= E - 2 n_elig - 1  ->  exact(a) <= E - 1, and
+    //   approx(b) >= E + 2 n_elig + 1  ->  exact(b) >= E + 1:
+    // the order statistic lies in (a, b].  Each end has its own bracket
+    // [lo, hi] around the crossing of its threshold; waves 0..7 test eight
+    // points inside the bracket of a, waves 8..15 inside that of b.
+    const double t_lo = (double)(E - 2 * n_elig - 1);
+    const double t_hi = (double)(E + 2 * n_elig + 1);
+    // a: approx(a_lo) <= t_lo < approx(a_hi); b: approx(b_lo) < t_hi, and
+    // b_hi == kmax (exact count = total > E) or approx(b_hi) >= t_hi
+    // (a zero price -- W_i infinite -- leaves no key below the smallest one:
+    // then a stays "below everything" and every price up to b is listed)
+    const bool a_none = kmin == 0;
+    uint64_t a_lo = a_none ? 0 : kmin - 1, a_hi = kmax, b_lo = a_lo, b_hi = kmax;
+    double ca = 0.0, cb = (double)total;
+    bool a_done = a_none || t_lo < 0.0, b_done = a_none || t_hi > (double)total;
+    // stop once the bracket holds few prices: listing them costs less than
+    // another round
+    const double enough = 256.0 + 4.0 * (double)n_elig;
+    for (int round = 0; !(a_done && b_done) && cb - ca > enough; ++round) {
+      const bool end_b = wave >= kSearchWaves;
+      const int q = wave % kSearchWaves;
+      const uint64_t lo = end_b ? b_lo : a_lo;
+      const uint64_t x = split_point<kSearchWaves>(lo, (end_b ? b_hi : a_hi) - lo, q);
+      double c = 0.0;
+      if (!(end_b ? b_done : a_done)) {
+        const double xv = key_value(x);
+        for (int i = lane; i < V; i += kWave) {
+          const int cnt = nd.cnt[i];
+          if (cnt > 0) c += approx_le(xv, nd.F[i], cnt, nd.W[i]);
+        }
+        c = wave_sum(c);
+      }
+      if (lane == 0) s_cnt[round & 1][wave] = c;
+      __syncthreads();
+      // every thread narrows both brackets from the same counts, in the same order
+      if (!a_done) {
+        const uint64_t span_a = a_hi - a_lo;
+        uint64_t nlo = a_lo, nhi = a_hi;
+        double nca = ca;
+        for (int qq = 0; qq < kSearchWaves; ++qq) {
+          const uint64_t xq = split_point<kSearchWaves>(a_lo, span_a, qq);
+          const double cq = s_cnt[round & 1][qq];
+          if (cq <= t_lo) {
+            nlo = xq;
+            nca = cq;
+          } else if (xq < nhi) {
+            nhi = xq;
+          }
+        }
+        a_lo = nlo;
+        a_hi = nhi;
+        ca = nca;
+        if (a_hi - a_lo <= 1) a_done = true;
+      }
+      if (!b_done) {
+        const uint64_t span_b = b_hi - b_lo;
+        uint64_t nlo = b_lo, nhi = b_hi;
+        double ncb = cb;
+        for (int qq = kSearchWaves - 1; qq >= 0; --qq) {
+          const uint64_t xq = split_point<kSearchWaves>(b_lo, span_b, qq);
+          const double cq = s_cnt[round & 1][kSearchWaves + qq];
+          if (cq >= t_hi) {
+            nhi = xq;
+            ncb = cq;
+          } else if (xq > nlo) {
+            nlo = xq;
+          }
+        }
+        b_lo = nlo;
+        b_hi = nhi;
+        cb = ncb;
+        if (b_hi - b_lo <= 1) b_done = true;
+      }
+    }
+    const uint64_t a = a_lo, b = b_hi;
+
+    // -- list the prices in (a, b] and count those <= a exactly -------------
+    // per node: first listed j - 1 in depth[], how many in down[], offset in
+    // cnt[] (the geometry fields are no longer needed)
+    const double av = key_value(a), bv = key_value(b);
+    int64_t below = 0, run = 0;
+    for (int base = 0; base < V; base += AT) {
+      const int i = base + tid;
+      int m_lo = 0, m_hi = 0;
+      if (i < V) {
+        const int cnt = nd.cnt[i];
+        if (cnt > 0) {
+          const int F = nd.F[i];
+          const double W = nd.W[i];
+          m_lo = a_none ? F : last_le(av, F, cnt, W);
+          m_hi = last_le(bv, F, cnt, W);
+          below += m_lo - F;
+        }
+      }
+      int64_t tot;
+      const int64_t ex = block_exclusive_scan<int64_t>((int64_t)(m_hi - m_lo), sm, &tot);
+      if (i < V) {
+        nd.depth[i] = m_lo;
+        nd.down[i] = m_hi - m_lo;
+        nd.cnt[i] = (int)(run + ex);
+      }
+      run += tot;
+    }
+    below = block_sum<int64_t>(below, sm);
+    const int64_t total_c = run;
+    if (total_c > ws.buf_cap || total_c > 0x7fffffff) {
       if (tid == 0) status_error(status, ARBOR_EWORKSPACE);
       return;
     }
-    // node offsets of the eligible prices
-    int64_t run = 0;
-    for (int base = 0; base < V; base += AT) {
-      const int i = base + tid;
-      const int64_t c = i < V ? ws.cnt[i] : 0;
-      int64_t tot;
-      const int64_t ex = block_exclusive_scan<int64_t>(c, sm, &tot);
-      if (i < V) ws.cnt_off[i] = run + ex;
-      run += tot;
+    const bool c_lds = total_c <= kCandLds;
+    uint64_t *const cand = c_lds ? cand_lds : ws.buf0;
+    uint64_t *const cand2 = c_lds ? cand_lds + kCandLds : ws.buf1;
+    // one wave per node, lanes over its listed prices
+    for (int i = wave; i < V; i += AT / kWave) {
+      const int nl = nd.down[i];
+      if (nl <= 0) continue;
+      const int m_lo = nd.depth[i], o = nd.cnt[i];
+      const double W = nd.W[i];
+      for (int j = lane; j < nl; j += kWave)
+        cand[o + j] = (uint64_t)__double_as_longlong(price(m_lo + 1 + j, W));
     }
     __syncthreads();
-    // materialise the price bit patterns, one wave per node
-    {
-      const int wave = tid >> 6, lane = lane_id();
-      for (int i = wave; i < V; i += AT / kWave) {
-        const int c = ws.cnt[i];
-        if (c == 0) continue;
-        const int64_t o = ws.cnt_off[i];
-        const double W = ws.W[i];
-        const int F = ws.F[i];
-        for (int j = lane; j < c; j += kWave)
-          ws.buf0[o + j] = (uint64_t)__double_as_longlong(price(F + 1 + j, W));
-      }
-    }
-    __syncthreads();
-    // the common high bits of all candidates need no pass
-    uint64_t kmin = ~0ull, kmax = 0ull;
-    for (int64_t e = tid; e < total; e += AT) {
-      const uint64_t key = ws.buf0[e];
-      kmin = key < kmin ? key : kmin;
-      kmax = key > kmax ? key : kmax;
-    }
-    kmin = block_min_u64(kmin, s_u64);
-    kmax = block_max_u64(kmax, s_u64);
-    uint64_t prefix = kmin;
-    int64_t rank = E;
-    int64_t ncand = total;
-    uint64_t *src = ws.buf0, *dst = ws.buf1;
-    if (kmin != kmax) {
-      const int top = 63 - __builtin_clzll(kmin ^ kmax);
-      int shift = (top / 8) * 8;
-      prefix = kmin & ~((shift + 8 >= 64) ? ~0ull : ((1ull << (shift + 8)) - 1ull));
-      for (; shift >= 0; shift -= 8) {
-        for (int b = tid; b < 4 * 256; b += AT) hist4[b] = 0;
-        __syncthreads();
-        unsigned *myh = hist4 + 256 * ((tid >> 6) & 3);
-        for (int64_t e = tid; e < ncand; e += AT)
-          atomicAdd(&myh[(src[e] >> shift) & 255ull], 1u);
-        __syncthreads();
-        // bin holding the element of rank `rank` (first 256 threads, 4 waves)
-        const unsigned h = tid < 256
-                               ? hist4[tid] + hist4[256 + tid] + hist4[512 + tid] + hist4[768 + tid]
-                               : 0u;
-        const int64_t inc = wave_inclusive_scan<int64_t>((int64_t)h);
-        if (tid < 256 && lane_id() == kWave - 1) s_wtot[tid >> 6] = inc;
-        __syncthreads();
-        if (tid < 256) {
-          int64_t base = 0;
-          for (int w = 0; w < (tid >> 6); ++w) base += s_wtot[w];
-          const int64_t ex = base + inc - (int64_t)h;
-          if (ex <= rank && rank < ex + (int64_t)h) {
-            s_chosen = tid;
-            s_below = ex;
-          }
-        }
-        __syncthreads();
-        const int chosen = s_chosen;
-        rank -= s_below;
-        prefix |= (uint64_t)chosen << shift;
-        if (shift == 0) break;
-        if (tid == 0) s_ncand = 0;
-        __syncthreads();
-        for (int64_t e0 = 0; e0 < ncand; e0 += AT) {
-          const int64_t e = e0 + tid;
-          const bool keep = e < ncand && (int)((src[e] >> shift) & 255ull) == chosen;
-          const uint64_t bk = ballot(keep);
-          unsigned base = 0;
-          if (lane_id() == 0 && bk) base = atomicAdd(&s_ncand, (unsigned)popc(bk));
-          base = __shfl(base, 0, kWave);
-          if (keep) dst[base + rank_below(bk, lane_id())] = src[e];
-        }
-        __syncthreads();
-        ncand = s_ncand;
-        uint64_t *tmp = src;
-        src = dst;
-        dst = tmp;
-        __syncthreads();
-      }
-    }
-    const double cut = __longlong_as_double((long long)prefix);
+
+    // -- the order statistic among the listed prices -------------------------
+    const uint64_t prefix = select_rank(cand, cand2, total_c, E - below);
+    const double cut = key_value(prefix);
     for (int i = tid; i < V; i += AT) {
-      if (on_path[i]) continue;
-      const int kept = count_prefix(ws.F[i], t.n_kept[i], ws.W[i],
+      if (nd.path[i]) continue;
+      const int kept = count_prefix(nd.F[i], nd.n_kept[i], nd.W[i],
                                     [cut](double x) { return x < cut; });
-      k_out[i] = ws.F[i] + kept;
+      k_out[i] = nd.F[i] + kept;
     }
     return;
   }
@@ -339,7 +603,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   int64_t excess = sum_F - b_off;
   if (sum_red < excess) {
     for (int i = tid; i < V; i += AT)
-      if (!on_path[i]) k_out[i] = min(p.k_min, t.n_kept[i]);
+      if (!nd.path[i]) k_out[i] = min(p.k_min, nd.n_kept[i]);
     if (tid == 0) status_warn(status, ARBOR_OVER_BUDGET);
     return;
   }
@@ -350,10 +614,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     for (int b = tid; b < 256; b += AT) hist64[b] = 0;
     __syncthreads();
     for (int i = tid; i < V; i += AT) {
-      if (on_path[i]) continue;
-      const uint64_t key = (uint64_t)__double_as_longlong(ws.w[i]);
+      if (nd.path[i]) continue;
+      const uint64_t key = (uint64_t)__double_as_longlong(nd.w[i]);
       if ((key & pmask) != prefix) continue;
-      const int red = ws.F[i] - min(p.k_min, t.n_kept[i]);
+      const int red = nd.F[i] - min(p.k_min, nd.n_kept[i]);
       if (red > 0) atomicAdd(&hist64[(key >> shift) & 255ull], (unsigned long long)red);
     }
     __syncthreads();
@@ -378,15 +642,16 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     const int i = base + tid;
     int64_t red = 0;
     uint64_t key = 0;
-    if (i < V && !on_path[i]) {
-      red = ws.F[i] - min(p.k_min, t.n_kept[i]);
-      key = (uint64_t)__double_as_longlong(ws.w[i]);
+    const bool off = i < V && !nd.path[i];
+    if (off) {
+      red = nd.F[i] - min(p.k_min, nd.n_kept[i]);
+      key = (uint64_t)__double_as_longlong(nd.w[i]);
     }
-    const bool tie = i < V && !on_path[i] && key == prefix;
+    const bool tie = off && key == prefix;
     int64_t tot;
     const int64_t ex = block_exclusive_scan<int64_t>(tie ? red : 0, sm, &tot);
-    if (i < V && !on_path[i]) {
-      int kk = ws.F[i];
+    if (off) {
+      int kk = nd.F[i];
       if (key < prefix) {
         kk -= (int)red;
       } else if (tie) {
@@ -402,7 +667,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
 }  // namespace
 
 size_t allocate_workspace(const arbor_sizes_t *sz) {
-  return (size_t)sz->num_nodes * (4 * 4 + 8 * 3 + 64) + (size_t)sz->num_tokens * 16 + 8192;
+  return (size_t)sz->num_nodes * (4 * 4 + 8 * 2 + 64) + (size_t)sz->num_tokens * 16 + 8192;
 }
 
 int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_active,
@@ -417,7 +682,6 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   ws.down = cv.take<int32_t>(t.V);
   ws.F = cv.take<int32_t>(t.V);
   ws.cnt = cv.take<int32_t>(t.V);
-  ws.cnt_off = cv.take<int64_t>(t.V);
   ws.W = cv.take<double>(t.V);
   ws.w = cv.take<double>(t.V);
   ws.buf0 = cv.take<uint64_t>((size_t)t.N);
@@ -425,9 +689,17 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   ws.buf_cap = t.N;
   if (!cv.ok) return ARBOR_EWORKSPACE;
   AllocParams p{params->alpha_max, params->gamma, params->lambda_d, params->lambda_delta,
-                params->eta, params->r_min, params->k_min, params->l_tail};
-  hipLaunchKernelGGL(allocate_kernel, dim3(1), dim3(AT), 0, stream, t, active, n_active,
-                     (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws);
+                params->eta, params->r_min, params->k_min, params->l_tail, {}, {}};
+  for (int i = 0; i < kDecay; ++i) {
+    p.dexp[i] = exp(-params->lambda_d * (double)i);
+    p.texp[i] = exp(-params->lambda_delta * (double)i);
+  }
+  const int in_lds = t.V <= kLdsNodes ? 1 : 0;
+  const size_t lds = (in_lds ? ((size_t)t.V * kNodeBytes + 15) / 16 * 16 : 0) +
+                     2 * (size_t)kCandLds * sizeof(uint64_t);
+  hipLaunchKernelGGL(allocate_kernel, dim3(1), dim3(AT), lds, stream, t, active, n_active,
+                     (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws,
+                     in_lds);
   return hip_ok(hipGetLastError());
 }
 

@@ -86,49 +86,144 @@ __device__ __forceinline__ uint32_t ordered_key(float x) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-// ---- block-wide scans (blockDim.x a multiple of 64, at most 1024) ----------
+// ---- cross-lane steps on the VALU ----------------------------------------
+// DPP moves within 16-lane rows and lane swaps across rows: no round trip
+// through the LDS permute unit.  Values of 4 or 8 bytes; 8-byte values move
+// as two 32-bit halves.
+namespace dpp {
+constexpr int kQuadXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141;  // lane i <- 7 - i within each 8
+constexpr int kRowMirror = 0x140;      // lane i <- 15 - i within each row
+constexpr int kRowShr = 0x110;         // + n: lane i <- i - n within the row
+constexpr int kRowBcast15 = 0x142;     // lane 15 of each row -> the next row
+constexpr int kRowBcast31 = 0x143;     // lane 31 -> rows 2 and 3
+}  // namespace dpp
+
 template <class T>
-__device__ __forceinline__ T wave_inclusive_scan(T v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    T o = __shfl_up(v, d, kWave);
-    if (lane >= d) v += o;
+__device__ __forceinline__ uint64_t bits64(T v) {
+  if constexpr (sizeof(T) == 4)
+    return (uint64_t)__builtin_bit_cast(uint32_t, v);
+  else
+    return __builtin_bit_cast(uint64_t, v);
+}
+template <class T>
+__device__ __forceinline__ T from_bits64(uint64_t b) {
+  if constexpr (sizeof(T) == 4)
+    return __builtin_bit_cast(T, (uint32_t)b);
+  else
+    return __builtin_bit_cast(T, b);
+}
+
+// v moved by a DPP control; lanes without a source (or outside row_mask) get 0
+template <int CTRL, int ROW_MASK = 0xF, class T>
+__device__ __forceinline__ T dpp_move(T v) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8, "4- or 8-byte lanes");
+  const uint64_t b = bits64(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROW_MASK,
+                                                            0xF, true);
+  if constexpr (sizeof(T) == 4) {
+    return from_bits64<T>(lo);
+  } else {
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL,
+                                                              ROW_MASK, 0xF, true);
+    return from_bits64<T>((uint64_t)lo | ((uint64_t)hi << 32));
   }
-  return v;
+}
+
+// the pair (own value, value of lane ^ 16) or (.., lane ^ 32), in either order
+template <bool X32, class T>
+__device__ __forceinline__ void row_swap(T v, T &a, T &b) {
+  const uint64_t u = bits64(v);
+  const uint32_t lo = (uint32_t)u;
+  auto rl = X32 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  if constexpr (sizeof(T) == 4) {
+    a = from_bits64<T>(rl[0]);
+    b = from_bits64<T>(rl[1]);
+  } else {
+    const uint32_t hi = (uint32_t)(u >> 32);
+    auto rh = X32 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                  : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    a = from_bits64<T>((uint64_t)rl[0] | ((uint64_t)rh[0] << 32));
+    b = from_bits64<T>((uint64_t)rl[1] | ((uint64_t)rh[1] << 32));
+  }
+}
+
+// op over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the same position in each
+// 16-lane row), result in every lane
+template <class T, class Op>
+__device__ __forceinline__ T across_rows(T v, Op op) {
+  T a, b;
+  row_swap<false>(v, a, b);
+  v = op(a, b);
+  row_swap<true>(v, a, b);
+  return op(a, b);
+}
+
+// op over all 64 lanes (op commutative and associative), result in every lane
+template <class T, class Op>
+__device__ __forceinline__ T wave_allreduce(T v, Op op) {
+  v = op(v, dpp_move<dpp::kQuadXor1>(v));
+  v = op(v, dpp_move<dpp::kQuadXor2>(v));
+  v = op(v, dpp_move<dpp::kRowHalfMirror>(v));
+  v = op(v, dpp_move<dpp::kRowMirror>(v));
+  T a, b;
+  row_swap<false>(v, a, b);
+  v = op(a, b);
+  row_swap<true>(v, a, b);
+  return op(a, b);
 }
 
 template <class T>
 __device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
+  return wave_allreduce(v, [](T x, T y) { return x + y; });
+}
+
+// value of lane `l` (wave-uniform l) in every lane
+template <class T>
+__device__ __forceinline__ T lane_value(T v, int l) {
+  const uint64_t u = bits64(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+  if constexpr (sizeof(T) == 4) {
+    return from_bits64<T>(lo);
+  } else {
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+    return from_bits64<T>((uint64_t)lo | ((uint64_t)hi << 32));
+  }
+}
+
+// ---- block-wide scans (blockDim.x a multiple of 64, at most 1024) ----------
+// Inclusive prefix sum over the wave in lane order: shifts by 1, 2, 4, 8
+// within each row, then the row totals carried by two row broadcasts.
+template <class T>
+__device__ __forceinline__ T wave_inclusive_scan(T v) {
+  v = v + dpp_move<dpp::kRowShr + 1>(v);
+  v = v + dpp_move<dpp::kRowShr + 2>(v);
+  v = v + dpp_move<dpp::kRowShr + 4>(v);
+  v = v + dpp_move<dpp::kRowShr + 8>(v);
+  v = v + dpp_move<dpp::kRowBcast15, 0xA>(v);
+  v = v + dpp_move<dpp::kRowBcast31, 0xC>(v);
   return v;
 }
 
 // Exclusive prefix of v over the block in thread order; *total gets the sum.
-// `smem` holds at least 17 elements.  Contains __syncthreads.
+// `smem` holds at least 17 elements.  Contains __syncthreads.  Every wave
+// scans the (at most 16) wave totals itself, so no thread walks them serially.
 template <class T>
 __device__ T block_exclusive_scan(T v, T *smem, T *total) {
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
-  T inc = wave_inclusive_scan(v);
+  const T inc = wave_inclusive_scan(v);
   if (lane == kWave - 1) smem[w] = inc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    T run = 0;
-    for (int j = 0; j < nw; ++j) {
-      T x = smem[j];
-      smem[j] = run;
-      run += x;
-    }
-    smem[16] = run;
-  }
+  const T t = lane < nw ? smem[lane] : T(0);
+  const T tinc = wave_inclusive_scan(t);
+  const T base = lane_value(tinc, w) - lane_value(t, w);
+  *total = lane_value(tinc, nw - 1);
   __syncthreads();
-  T ex = smem[w] + inc - v;
-  *total = smem[16];
-  __syncthreads();
-  return ex;
+  return base + inc - v;
 }
 
 template <class T>

@@ -285,8 +285,7 @@ __device__ __forceinline__ void attend(const KVFrag<T, D, GSP> &f,
   }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 16, kWave));
-    gmax[nb] = fmaxf(gmax[nb], __shfl_xor(gmax[nb], 32, kWave));
+    gmax[nb] = across_rows(gmax[nb], [](float x, float y) { return fmaxf(x, y); });
     const float mn = fmaxf(m_run[nb], gmax[nb]);
     const float alpha = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
     m_run[nb] = mn;
@@ -412,9 +411,7 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   float *outp = a.part + (slab + a.item_rowbase[item]) * stride;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    float l = l_run[nb];
-    l += __shfl_xor(l, 16, kWave);
-    l += __shfl_xor(l, 32, kWave);
+    const float l = across_rows(l_run[nb], [](float x, float y) { return x + y; });
     const int row = rbase + nb * 16 + rr;
     if (g4 == 0 && row < R) {
       outp[row * stride] = m_run[nb];
@@ -484,8 +481,7 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
       const float m = k < np ? base[(int64_t)lp[k] * stride] : -__builtin_inff();
       M = fmaxf(M, m);
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+    M = wave_allreduce(M, [](float x, float y) { return fmaxf(x, y); });
     float L = 0.f, ov[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) ov[e] = 0.f;
@@ -507,8 +503,8 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 #pragma unroll
           for (int u = 0; u < U; ++u) {
             const int j = min(j0 + u, nk - 1);
-            const int64_t oj = __shfl(off, j, kWave);
-            fj[u] = j0 + u < nk ? __shfl(f, j, kWave) : 0.f;
+            const int64_t oj = lane_value(off, j);
+            fj[u] = j0 + u < nk ? lane_value(f, j) : 0.f;
 #pragma unroll
             for (int e = 0; e < EPL; ++e) xv[u][e] = base[oj + 2 + 64 * e + lane];
           }

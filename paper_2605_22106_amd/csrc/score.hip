@@ -182,14 +182,9 @@ __device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
 }
 
 // sum over the four 16-lane groups of the wave (lanes l, l ^ 16, l ^ 32,
-// l ^ 48), in every lane: two lane swaps across rows instead of LDS permutes
+// l ^ 48), in every lane
 __device__ __forceinline__ float group_sum(float x) {
-  const unsigned u = __float_as_uint(x);
-  const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const unsigned w = __float_as_uint(y);
-  const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  return across_rows(x, [](float a, float b) { return a + b; });
 }
 
 template <int N>

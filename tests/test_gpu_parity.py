@@ -80,6 +80,49 @@ def test_allocate_bit_exact(seed):
         assert np.array_equal(onp.cpu().numpy(), on_o)
 
 
+@pytest.mark.parametrize("V,max_n,seed", [(300, 400, 0), (300, 400, 1), (1500, 100, 2)])
+def test_allocate_large_bracketed(V, max_n, seed):
+    """Tens of thousands of prices, so the order statistic is bracketed by the
+    rounded counts before the prices in the bracket are listed.  Node sizes come
+    from a small set and weights are rounded to 1/8, so whole runs of prices tie
+    exactly; alpha_max both open and binding.  V = 300 keeps the per-node state
+    in LDS, V = 1500 in the workspace."""
+    parent, _ = synth.random_tree(V, max_n, seed)
+    rng = np.random.default_rng(seed)
+    sizes = np.array([max_n // 4, max_n // 2, max_n])
+    n_full = [int(x) for x in rng.choice(sizes, size=V)]
+    leaves = [i for i in range(V) if i not in set(parent)]
+    active = sorted(rng.choice(leaves, size=4, replace=False).tolist())
+    st = synth.build_state(parent, n_full, layers=1, kv_heads=1, q_per_kv=1, head_dim=64,
+                           dtype="f32", seed=seed, active=active)
+    kv = to_gpu(st)
+    n_full = st["n_full"].numpy()
+    n_kept = np.array([int(rng.integers(n // 2, n + 1)) if rng.random() < 0.3 else n
+                       for n in n_full])
+    kv.n_kept.copy_(torch.tensor(n_kept, dtype=torch.int32))
+    s = (np.round(rng.random(V) * 8) / 8).astype(np.float32)
+    ws = workspace(kv)
+    act = torch.tensor(active, dtype=torch.int32, device="cuda")
+    total = int(n_kept.sum())
+    for amax in (math.inf, 0.5):
+        p = dict(PARAMS, alpha_max=amax)
+        for rho in (0.05, 0.2, 0.5, 0.9):
+            budget = int(rho * total)
+            k_o, d_o, on_o, st_o = O.allocate(st["parent"].numpy(), n_full, n_kept, active,
+                                              budget, s, p)
+            k = torch.empty(V, dtype=torch.int32, device="cuda")
+            dl = torch.empty_like(k)
+            onp = torch.empty(V, dtype=torch.uint8, device="cuda")
+            stt = status()
+            check_rc(L.arbor_allocate(kv, act, budget, torch.tensor(s, device="cuda"), p, k, dl,
+                                      onp, stt, ws))
+            torch.cuda.synchronize()
+            assert int(stt) == st_o, (amax, rho)
+            assert np.array_equal(k.cpu().numpy(), k_o), (amax, rho)
+            assert np.array_equal(dl.cpu().numpy(), d_o)
+            assert np.array_equal(onp.cpu().numpy(), on_o)
+
+
 def test_allocate_tiny_config_over_budget():
     st = synth.build_config("tiny")
     kv = to_gpu(st)
