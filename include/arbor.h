@@ -261,6 +261,31 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
                            int32_t *status, void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/*
+ * arbor_set_kernel_events -- timing support for callers that measure one
+ * kernel of the path on its own (a roofline of that kernel rather than of the
+ * whole entry point).  After the call, every launch of `kernel` by later entry
+ * point calls is bracketed by hipEventRecord(start, s) and
+ * hipEventRecord(stop, s) on the launch stream s, so hipEventElapsedTime(start,
+ * stop) after the stream has synchronised gives the duration of the most recent
+ * launch (for ARBOR_KERNEL_DECODE_ATTN: of the up to three attention launches
+ * of one call, which run back to back).  The events belong to the caller, who
+ * creates them with timing enabled on the device the calls run on and keeps
+ * them alive while they are set.  start = stop = NULL stops the recording.
+ * The setting is process-wide and is not synchronised with entry point calls
+ * running on other host threads.
+ * Errors: EINVAL for an unknown kernel id or only one of start, stop NULL.
+ */
+typedef enum {
+  ARBOR_KERNEL_SCORE_ATTN = 0,    /* the two-pass score kernel of arbor_score      */
+  ARBOR_KERNEL_SELECT = 1,        /* the selection kernel of arbor_select          */
+  ARBOR_KERNEL_COMPACT_MOVE = 2,  /* the row-move kernel of arbor_compact          */
+  ARBOR_KERNEL_DECODE_ATTN = 3,   /* the attention kernels of arbor_tree_decode_attn */
+  ARBOR_KERNEL_COUNT = 4
+} arbor_kernel_t;
+
+int arbor_set_kernel_events(int32_t kernel, hipEvent_t start, hipEvent_t stop);
+
 #ifdef __cplusplus
 }
 #endif

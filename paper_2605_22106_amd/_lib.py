@@ -22,6 +22,8 @@ LIB_PATH = os.path.join(_HERE, "libarbor.so")
 OK, OVER_BUDGET = 0, 1
 EINVAL, ENOPAGES, EHIP, EUNSUPPORTED, ENONFINITE, EWORKSPACE, ECORRUPT = -1, -2, -3, -4, -5, -6, -7
 BF16, F32 = 0, 1
+# kernels whose launches arbor_set_kernel_events can bracket with events
+KERNEL_SCORE_ATTN, KERNEL_SELECT, KERNEL_COMPACT_MOVE, KERNEL_DECODE_ATTN = 0, 1, 2, 3
 SELECT_TAIL_HEAVY, SELECT_TAIL_ONLY = 0, 1
 MAX_DEPTH = 63
 
@@ -86,6 +88,7 @@ def load() -> ctypes.CDLL:
             "arbor_rehydrate": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_tree_decode_attn": (ctypes.c_int, [G, T, Pl, vp, i32, i32, i32, vp, vp, i32,
                                                       vp, ctypes.c_float, vp, vp, sz, vp]),
+            "arbor_set_kernel_events": (ctypes.c_int, [i32, vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(lib, name)
@@ -97,7 +100,8 @@ def load() -> ctypes.CDLL:
 
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
-            "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn"]
+            "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn",
+            "arbor_set_kernel_events"]
 
 
 def _dev(t: torch.Tensor | None, name: str):
@@ -277,3 +281,11 @@ def arbor_tree_decode_attn(kv: KVState, leaves, layer_begin, layer_end, q, out, 
                                          float(softmax_scale), _dev(status, "status"),
                                          _dev(workspace, "workspace"), int(workspace.numel()),
                                          _stream(stream))
+
+
+def arbor_set_kernel_events(kernel: int, start=None, stop=None) -> int:
+    """Bracket later launches of `kernel` with two timing events (torch.cuda.Event
+    objects, already recorded once so that they exist), or stop with None, None."""
+    def handle(e):
+        return None if e is None else ctypes.c_void_p(e.cuda_event)
+    return load().arbor_set_kernel_events(int(kernel), handle(start), handle(stop))

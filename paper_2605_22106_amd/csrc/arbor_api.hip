@@ -26,6 +26,7 @@ size_t allocate_workspace(const arbor_sizes_t *);
 size_t compact_workspace(const arbor_sizes_t *);
 size_t rehydrate_workspace(const arbor_sizes_t *);
 size_t decode_workspace(const arbor_geom_t *, const arbor_sizes_t *);
+KernelEvents g_kernel_events[ARBOR_KERNEL_COUNT];
 }  // namespace arbor
 
 using namespace arbor;
@@ -180,3 +181,11 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
 }
 
 }  // extern "C"
+
+int arbor_set_kernel_events(int32_t kernel, hipEvent_t start, hipEvent_t stop) {
+  if (kernel < 0 || kernel >= ARBOR_KERNEL_COUNT) return ARBOR_EINVAL;
+  if ((start == nullptr) != (stop == nullptr)) return ARBOR_EINVAL;
+  g_kernel_events[kernel].start = start;
+  g_kernel_events[kernel].stop = stop;
+  return ARBOR_OK;
+}

@@ -258,4 +258,17 @@ struct Carve {
 
 static inline int hip_ok(hipError_t e) { return e == hipSuccess ? ARBOR_OK : ARBOR_EHIP; }
 
+// Events a caller asked to have recorded around one kernel's launches
+// (arbor_set_kernel_events); defined in the API translation unit.
+struct KernelEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern KernelEvents g_kernel_events[ARBOR_KERNEL_COUNT];
+inline void timing_begin(int kernel, hipStream_t s) {
+  if (g_kernel_events[kernel].start) (void)hipEventRecord(g_kernel_events[kernel].start, s);
+}
+inline void timing_end(int kernel, hipStream_t s) {
+  if (g_kernel_events[kernel].stop) (void)hipEventRecord(g_kernel_events[kernel].stop, s);
+}
+
 }  // namespace arbor

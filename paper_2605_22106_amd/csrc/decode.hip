@@ -539,11 +539,13 @@ void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *ls
   // rows of a work unit are at most n_leaves * G: only the row classes that
   // can occur are launched
   const int max_rows = a.n_leaves * a.pl.G;
+  timing_begin(ARBOR_KERNEL_DECODE_ATTN, stream);
   hipLaunchKernelGGL((decode_attn<T, D, 1>), dim3(grid), dim3(256), 0, stream, a, 0);
   if (max_rows > 16)
     hipLaunchKernelGGL((decode_attn<T, D, 2>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
   if (max_rows > 32)
     hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
+  timing_end(ARBOR_KERNEL_DECODE_ATTN, stream);
   const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv * a.pl.G;
   const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
   hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,

@@ -892,7 +892,9 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
     hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
+    timing_begin(ARBOR_KERNEL_SCORE_ATTN, stream);
     launch_attn(geom->dtype, geom->head_dim, NBW, grid, stream, a);
+    timing_end(ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, part, fbase);
     hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, part, fbase, A,
                        rows_seen);

@@ -49,3 +49,12 @@ def test_product_path_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError):
         L._dev(torch.zeros(3), "x")
+
+
+def test_kernel_events_setter_validates_on_the_host():
+    lib = L.load()
+    assert lib.arbor_set_kernel_events(L.KERNEL_SCORE_ATTN, None, None) == L.OK
+    assert lib.arbor_set_kernel_events(4, None, None) == L.EINVAL
+    assert lib.arbor_set_kernel_events(-1, None, None) == L.EINVAL
+    # one of the two events missing
+    assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_ATTN, ctypes.c_void_p(1), None) == L.EINVAL
