@@ -170,18 +170,20 @@ __device__ void block_min_sum3(int64_t (&v)[3], int64_t *sm) {
   __syncthreads();
 }
 
-// The rank-th smallest (0-based) of the keys src[0, n), 0 <= rank < n: an
-// MSB-first radix select over 8-bit digits until at most 64 candidates are
-// left, which one wave then ranks directly.  src and dst (room for n keys) may
-// be LDS or global memory; both are overwritten.  Called by the whole block;
-// contains __syncthreads.
-__device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t rank) {
+// The rank-th smallest (0-based) of the keys src[0, n), 0 <= rank < n.  Keys
+// are taken relative to the smallest one, and each pass splits the remaining
+// range [lo, lo + span] into 256 equal power-of-two buckets: the listed prices
+// are spread fairly evenly over their small range, so one pass usually leaves
+// at most 64 candidates, which one wave then ranks directly.  src and dst
+// (room for n keys) may be LDS or global memory; both are overwritten.
+// Called by the whole block; contains __syncthreads.
+__device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t rank,
+                                int64_t *sm) {
   __shared__ unsigned hist4[4 * 256];
   __shared__ int64_t s_wtot[4];
   __shared__ int s_chosen;
   __shared__ int64_t s_below;
   __shared__ unsigned s_ncand;
-  __shared__ uint64_t s_mm[17];
   __shared__ uint64_t s_key;
   const int tid = threadIdx.x, lane = lane_id();
   uint64_t cmin = ~0ull, cmax = 0ull;
@@ -190,21 +192,28 @@ __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t
     cmin = key < cmin ? key : cmin;
     cmax = key > cmax ? key : cmax;
   }
-  cmin = block_min_u64(cmin, s_mm);
-  cmax = block_max_u64(cmax, s_mm);
+  {
+    // both extremes in one exchange (keys of finite positive doubles < 2^63)
+    int64_t v3[3] = {0, cmin == ~0ull ? INT64_MAX : (int64_t)cmin, INT64_MAX - (int64_t)cmax};
+    block_min_sum3(v3, sm);
+    cmin = (uint64_t)v3[1];
+    cmax = (uint64_t)(INT64_MAX - v3[2]);
+  }
   if (cmin == cmax) return cmin;
   int64_t ncand = n;
-  const int top = 63 - __builtin_clzll(cmin ^ cmax);
-  int shift = (top / 8) * 8;
-  uint64_t prefix = cmin & ~((shift + 8 >= 64) ? ~0ull : ((1ull << (shift + 8)) - 1ull));
-  for (; ncand > kWave; shift -= 8) {
+  uint64_t lo = cmin, span = cmax - cmin;
+  while (ncand > kWave) {
+    if (span == 0) return lo;   // every candidate left is lo
+    // buckets of 2^shift keys: span >> shift < 256
+    const int bits = 64 - __builtin_clzll(span);
+    const int shift = bits > 8 ? bits - 8 : 0;
     for (int bn = tid; bn < 4 * 256; bn += blockDim.x) hist4[bn] = 0;
     __syncthreads();
     unsigned *myh = hist4 + 256 * ((tid >> 6) & 3);
     for (int64_t e = tid; e < ncand; e += blockDim.x)
-      atomicAdd(&myh[(src[e] >> shift) & 255ull], 1u);
+      atomicAdd(&myh[(src[e] - lo) >> shift], 1u);
     __syncthreads();
-    // bin holding the element of rank `rank` (first 256 threads, 4 waves)
+    // bucket holding the element of rank `rank` (first 256 threads, 4 waves)
     const unsigned h =
         tid < 256 ? hist4[tid] + hist4[256 + tid] + hist4[512 + tid] + hist4[768 + tid] : 0u;
     const int64_t inc = wave_inclusive_scan<int64_t>((int64_t)h);
@@ -220,15 +229,15 @@ __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t
       }
     }
     __syncthreads();
-    const int chosen = s_chosen;
+    const uint64_t chosen = (uint64_t)s_chosen;
     rank -= s_below;
-    prefix |= (uint64_t)chosen << shift;
-    if (shift == 0) return prefix;
+    const uint64_t blo = chosen << shift;
+    if (shift == 0) return lo + blo;
     if (tid == 0) s_ncand = 0;
     __syncthreads();
     for (int64_t e0 = 0; e0 < ncand; e0 += blockDim.x) {
       const int64_t e = e0 + tid;
-      const bool keep = e < ncand && (int)((src[e] >> shift) & 255ull) == chosen;
+      const bool keep = e < ncand && ((src[e] - lo) >> shift) == chosen;
       const uint64_t bk = ballot(keep);
       unsigned base = 0;
       if (lane == 0 && bk) base = atomicAdd(&s_ncand, (unsigned)popc(bk));
@@ -237,6 +246,9 @@ __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t
     }
     __syncthreads();
     ncand = s_ncand;
+    const uint64_t rest = span - blo;
+    lo += blo;
+    span = rest < (1ull << shift) - 1ull ? rest : (1ull << shift) - 1ull;
     uint64_t *tmp = src;
     src = dst;
     dst = tmp;
@@ -247,9 +259,7 @@ __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t
     const uint64_t k = lane < ncand ? src[lane] : ~0ull;
     int less = 0, leq = 0;
     for (int j = 0; j < (int)ncand; ++j) {
-      const uint64_t kj =
-          (uint64_t)(unsigned)__builtin_amdgcn_readlane((int)(unsigned)k, j) |
-          ((uint64_t)(unsigned)__builtin_amdgcn_readlane((int)(unsigned)(k >> 32), j) << 32);
+      const uint64_t kj = lane_value(k, j);
       less += kj < k ? 1 : 0;
       leq += kj <= k ? 1 : 0;
     }
@@ -282,6 +292,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   __shared__ int s_err;
   __shared__ unsigned long long hist64[256];
   __shared__ double s_cnt[2][2 * kSearchWaves];
+  __shared__ uint64_t s_x[2][2 * kSearchWaves];
   if (status_failed(status)) return;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = lane_id();
@@ -496,15 +507,17 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
         }
         c = wave_sum(c);
       }
-      if (lane == 0) s_cnt[round & 1][wave] = c;
+      if (lane == 0) {
+        s_cnt[round & 1][wave] = c;
+        s_x[round & 1][wave] = x;
+      }
       __syncthreads();
       // every thread narrows both brackets from the same counts, in the same order
       if (!a_done) {
-        const uint64_t span_a = a_hi - a_lo;
         uint64_t nlo = a_lo, nhi = a_hi;
         double nca = ca;
         for (int qq = 0; qq < kSearchWaves; ++qq) {
-          const uint64_t xq = split_point<kSearchWaves>(a_lo, span_a, qq);
+          const uint64_t xq = s_x[round & 1][qq];
           const double cq = s_cnt[round & 1][qq];
           if (cq <= t_lo) {
             nlo = xq;
@@ -519,11 +532,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
         if (a_hi - a_lo <= 1) a_done = true;
       }
       if (!b_done) {
-        const uint64_t span_b = b_hi - b_lo;
         uint64_t nlo = b_lo, nhi = b_hi;
         double ncb = cb;
         for (int qq = kSearchWaves - 1; qq >= 0; --qq) {
-          const uint64_t xq = split_point<kSearchWaves>(b_lo, span_b, qq);
+          const uint64_t xq = s_x[round & 1][kSearchWaves + qq];
           const double cq = s_cnt[round & 1][kSearchWaves + qq];
           if (cq >= t_hi) {
             nhi = xq;
@@ -588,7 +600,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     __syncthreads();
 
     // -- the order statistic among the listed prices -------------------------
-    const uint64_t prefix = select_rank(cand, cand2, total_c, E - below);
+    const uint64_t prefix = select_rank(cand, cand2, total_c, E - below, sm);
     const double cut = key_value(prefix);
     for (int i = tid; i < V; i += AT) {
       if (nd.path[i]) continue;

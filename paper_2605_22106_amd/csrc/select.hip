@@ -1,8 +1,8 @@
 // arbor_select: per-block retained set, tail + heavy hitters (Sec. 4 Execution,
 // Alg. 1 Evict).  One wavefront per node; the m-th largest accumulated
-// attention key is found by an MSB-first radix select over 4-bit digits whose
-// bins are counted with wavefront ballots and popcounts, then the kept
-// positions are emitted in slot (= position) order with a ballot prefix sum.
+// attention key is found by an MSB-first radix select over 8-bit digits whose
+// bins are counted in a per-wave LDS histogram, then the kept positions are
+// emitted in slot (= position) order with a ballot prefix sum.
 #include "arbor_internal.h"
 
 namespace arbor {
@@ -22,35 +22,52 @@ struct NodeView {
 
 constexpr int kCached = 8;   // resident slots per lane held in registers
 
-// Count, per 4-bit digit, the matching keys of one 64-wide chunk (ballots).
-__device__ __forceinline__ void digit_counts(bool match, uint32_t dig, int (&cnt)[16]) {
-  const uint64_t bm = ballot(match);
-  const uint64_t b0 = ballot(match && (dig & 1u));
-  const uint64_t b1 = ballot(match && (dig & 2u));
-  const uint64_t b2 = ballot(match && (dig & 4u));
-  const uint64_t b3 = ballot(match && (dig & 8u));
+// One wave's 256-bin histogram of the current 8-bit digit, in LDS.  LDS
+// operations of one wave execute in order, so no barrier is needed between
+// clearing, counting and reading it.
+struct Hist {
+  unsigned *h;
+  __device__ __forceinline__ void clear(int lane) const {
 #pragma unroll
-  for (int b = 0; b < 16; ++b) {
-    const uint64_t mm = bm & ((b & 1) ? b0 : ~b0) & ((b & 2) ? b1 : ~b1) &
-                        ((b & 4) ? b2 : ~b2) & ((b & 8) ? b3 : ~b3);
-    cnt[b] += popc(mm);
+    for (int b = 0; b < 256 / kWave; ++b) h[b * kWave + lane] = 0u;
   }
-}
-
-// Pick the digit holding the `remaining`-th largest key; updates remaining.
-__device__ __forceinline__ int pick_digit(const int (&cnt)[16], int &remaining) {
-  for (int b = 15; b >= 0; --b) {
-    if (cnt[b] >= remaining) return b;
-    remaining -= cnt[b];
+  __device__ __forceinline__ void add(bool match, uint32_t key, int shift) const {
+    if (match) atomicAdd(&h[(key >> shift) & 255u], 1u);
   }
-  return 0;
-}
+  // Digit holding the `remaining`-th largest counted key; updates remaining
+  // to its rank within that digit.  Lane l holds bins 255 - 4l - 3 .. 255 - 4l,
+  // so a lane-order prefix sum runs from the largest digit down.
+  __device__ __forceinline__ int pick(int &remaining, int lane) const {
+    const int top = 255 - 4 * lane;
+    const int c0 = (int)h[top], c1 = (int)h[top - 1], c2 = (int)h[top - 2], c3 = (int)h[top - 3];
+    const int mine = c0 + c1 + c2 + c3;
+    const int inc = wave_inclusive_scan(mine);
+    const uint64_t hit = ballot(inc >= remaining);
+    const int l = (int)__builtin_ctzll(hit);            // the key is counted, so hit != 0
+    int before = lane_value(inc - mine, l);
+    const int b0 = lane_value(c0, l), b1 = lane_value(c1, l), b2 = lane_value(c2, l);
+    int d = 255 - 4 * l;
+    if (before + b0 >= remaining) {
+    } else if (before + b0 + b1 >= remaining) {
+      before += b0;
+      d -= 1;
+    } else if (before + b0 + b1 + b2 >= remaining) {
+      before += b0 + b1;
+      d -= 2;
+    } else {
+      before += b0 + b1 + b2;
+      d -= 3;
+    }
+    remaining -= before;
+    return d;
+  }
+};
 
 // Nodes with at most 64 * kCached resident slots: keys and positions stay in
 // registers for every radix pass.
 __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, int c, int ki,
                               int thr, int mode, int32_t *__restrict__ out, int32_t *status,
-                              int lane) {
+                              int lane, const Hist &hist) {
   uint32_t key[kCached];
   int pos[kCached];
   bool nan = false;
@@ -82,19 +99,16 @@ __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, i
   const int m = ki - n_tail;
   uint32_t prefix = 0, pmask = 0;
   int remaining = m;
-  for (int shift = 28; shift >= 0; shift -= 4) {
-    int cnt[16];
-#pragma unroll
-    for (int b = 0; b < 16; ++b) cnt[b] = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    hist.clear(lane);
 #pragma unroll
     for (int r = 0; r < kCached; ++r) {
       if (r * kWave >= n_head) break;
       const int s = r * kWave + lane;
-      const bool match = s < n_head && ((key[r] & pmask) == prefix);
-      digit_counts(match, (key[r] >> shift) & 15u, cnt);
+      hist.add(s < n_head && ((key[r] & pmask) == prefix), key[r], shift);
     }
-    prefix |= (uint32_t)pick_digit(cnt, remaining) << shift;
-    pmask |= 15u << shift;
+    prefix |= (uint32_t)hist.pick(remaining, lane) << shift;
+    pmask |= 255u << shift;
   }
   int written = 0, ties = 0;
 #pragma unroll
@@ -119,7 +133,7 @@ __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, i
 // Larger nodes: every pass streams the keys again (L2-resident).
 __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A, int c, int ki,
                                 int thr, int mode, int32_t *__restrict__ out, int32_t *status,
-                                int lane) {
+                                int lane, const Hist &hist) {
   int n_head = 0;
   bool nan = false;
   for (int base = 0; base < c; base += kWave) {
@@ -142,18 +156,16 @@ __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A,
   const int m = ki - n_tail;
   uint32_t prefix = 0, pmask = 0;
   int remaining = m;
-  for (int shift = 28; shift >= 0; shift -= 4) {
-    int cnt[16];
-#pragma unroll
-    for (int b = 0; b < 16; ++b) cnt[b] = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    hist.clear(lane);
     for (int base = 0; base < n_head; base += kWave) {
       const int s = base + lane;
       const bool v = s < n_head;
       const uint32_t key = v ? ordered_key(A[nv.pos(s)]) : 0u;
-      digit_counts(v && ((key & pmask) == prefix), (key >> shift) & 15u, cnt);
+      hist.add(v && ((key & pmask) == prefix), key, shift);
     }
-    prefix |= (uint32_t)pick_digit(cnt, remaining) << shift;
-    pmask |= 15u << shift;
+    prefix |= (uint32_t)hist.pick(remaining, lane) << shift;
+    pmask |= 255u << shift;
   }
   int written = 0, ties = 0;
   for (int base = 0; base < n_head; base += kWave) {
@@ -179,9 +191,11 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
                                                      const int32_t *__restrict__ k, int l_tail,
                                                      int mode, int32_t *__restrict__ sel_pos,
                                                      int32_t *status) {
+  __shared__ unsigned s_hist[4][256];
   if (status_failed(status)) return;
   const int lane = lane_id();
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const Hist hist{s_hist[threadIdx.x >> 6]};
   if (i >= t.V) return;
   const int c = t.n_kept[i];
   const int ki = k[i];
@@ -194,8 +208,10 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
   const int64_t tb = t.tok_off[i];
   const NodeView nv{t.page_table, pl.slot_pos, t.page_off[i], pl.P};
   int32_t *out = sel_pos + tb;
-  if (c <= kWave * kCached) select_cached(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane);
-  else select_streamed(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane);
+  if (c <= kWave * kCached)
+    select_cached(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane, hist);
+  else
+    select_streamed(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane, hist);
 }
 
 }  // namespace
