@@ -8,9 +8,10 @@
 // credited to tokens of proper ancestors (u > b_i).
 //
 // Launches on one stream:
-//   plan    (one workgroup) validate the tree, per-observer chain lengths,
-//           partial / table offsets;
-//   tables  one workgroup per observer: its chain's 16-slot sub-pages;
+//   setup   one workgroup per observer: every workgroup walks all observer
+//           chains for the partial / table offsets (a prefix over observers),
+//           writes its own observer's chain data and 16-slot sub-page table;
+//           workgroup 0 also validates the tree;
 //   attn    per (observer, slice layer, kv head, row group), two passes over
 //           the same (row, key) pairs as MFMA tiles of 16 keys x 16 rows:
 //           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
@@ -44,7 +45,6 @@ struct ScoreArgs {
   int n_rg;
   float sl2;        // softmax scale * log2(e)
   int self_window;
-  float *lse;       // [n_obs][S][Hkv][n_rg][16*NB]
   float *part;      // partial column sums
   const int64_t *pbase;   // [n_obs]
   const int64_t *tbase;   // [n_obs]: float offset (in part) of the observer's sub-page table
@@ -563,113 +563,142 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
       [&](const Red &RD, int st, int n) __attribute__((always_inline)) { finish(RD, st, n); });
 }
 
-// Observer chains, partial offsets and validation (one workgroup).
-__global__ __launch_bounds__(1024) void score_plan(Tree t, const int32_t *__restrict__ obs, int n_obs,
-                                                   int S, int Hkv, int n_rg, int64_t part_cap,
+// Chain length and sub-page count of observer j, with the same checks as the
+// validation (a malformed chain gives ok = false and no sub-pages).
+struct ObsChain {
+  int64_t len, subs;
+  int depth;
+  bool ok;
+};
+__device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
+  ObsChain r{0, 0, 0, true};
+  int chainv[MAXD];
+  int d = 0;
+  for (int x = j; x >= 0; x = t.parent[x]) {
+    if (d >= MAXD || (x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) ||
+        (x == 0 && t.parent[x] != -1)) {
+      r.ok = false;
+      break;
+    }
+    const int c = t.n_kept[x];
+    if (c < 0 || c > t.n_full[x]) {
+      r.ok = false;
+      break;
+    }
+    chainv[d++] = x;
+    r.len += c;
+    r.subs += (c + 15) / 16;
+  }
+  if (!r.ok) {
+    r.subs = 0;
+    d = 1;
+    chainv[0] = j;
+  }
+  r.depth = d - 1;
+  if (anc_out)
+    for (int e = 0; e < d; ++e) anc_out[e] = chainv[d - 1 - e];
+  return r;
+}
+
+// One workgroup per observer.  Offsets of the partials and sub-page tables are
+// prefixes over observers, so every workgroup walks every observer chain (in
+// parallel, one per thread) and keeps its own observer's offsets; it then
+// writes that observer's chain data and sub-page table, root first, as
+// 16-byte entries (plane row, slot, context offset, valid slots | own << 8)
+// that the streaming kernel reads with scalar loads.  Workgroup 0 validates
+// the whole tree.
+__global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap,
                                                    int64_t *__restrict__ pbase,
                                                    int64_t *__restrict__ fbase,
                                                    int64_t *__restrict__ tbase,
-                                                   int32_t *__restrict__ nsp, int self_window,
+                                                   int32_t *__restrict__ nsp,
                                                    int32_t *__restrict__ ctxlen,
                                                    int32_t *__restrict__ odepth,
-                                                   int32_t *__restrict__ anc, int32_t *status) {
+                                                   int32_t *__restrict__ anc) {
   __shared__ int64_t sm[17];
   __shared__ int s_err;
-  if (status_failed(status)) return;
-  if (threadIdx.x == 0) s_err = 0;
+  __shared__ int64_t s_mine[4];
+  __shared__ ChainLds ch;
+  if (status_failed(a.status)) return;
+  const Tree &t = a.t;
+  const int me = blockIdx.x;
+  const int tid = threadIdx.x;
+  if (tid == 0) s_err = 0;
   __syncthreads();
-  for (int i = threadIdx.x; i < t.V; i += blockDim.x) {
-    const int par = t.parent[i];
-    const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
-    const int c = t.n_kept[i];
-    if (!ok || c < 0 || c > t.n_full[i]) atomicOr(&s_err, 1);
+  if (me == 0) {
+    for (int i = tid; i < t.V; i += blockDim.x) {
+      const int par = t.parent[i];
+      const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
+      const int c = t.n_kept[i];
+      if (!ok || c < 0 || c > t.n_full[i]) atomicOr(&s_err, 1);
+    }
   }
-  __syncthreads();
+  const int slabs = a.S * a.pl.Hkv * a.n_rg;
   int64_t run = 0, frun = 0, trun = 0;
-  for (int base = 0; base < n_obs; base += blockDim.x) {
-    const int o = base + threadIdx.x;
+  for (int base = 0; base < a.n_obs; base += blockDim.x) {
+    const int o = base + tid;
     int64_t len = 0, subs = 0;
-    if (o < n_obs) {
-      const int j = obs[o];
+    if (o < a.n_obs) {
+      const int j = a.obs[o];
       if (j < 0 || j >= t.V) {
         atomicOr(&s_err, 1);
       } else {
-        int chainv[MAXD];
-        int d = 0;
-        bool ok = true;
-        for (int x = j; x >= 0; x = t.parent[x]) {
-          if (d >= MAXD || (x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) ||
-              (x == 0 && t.parent[x] != -1)) {
-            ok = false;
-            break;
-          }
-          chainv[d++] = x;
-          len += t.n_kept[x];
-          subs += (t.n_kept[x] + 15) / 16;
+        const ObsChain r = walk_chain(t, j, o == me ? anc + (int64_t)o * MAXD : nullptr);
+        if (!r.ok) atomicOr(&s_err, 2);
+        len = r.len;
+        subs = r.subs;
+        if (o == me) {
+          odepth[o] = r.depth;
+          const int own = r.ok ? (t.n_kept[j] + 15) / 16 : 0;
+          nsp[2 * o] = (int32_t)subs;
+          nsp[2 * o + 1] = r.ok ? (int32_t)(a.self_window ? subs : subs - own) : 0;
+          ctxlen[o] = (int32_t)len;
+          s_mine[2] = subs;
         }
-        if (!ok) {
-          atomicOr(&s_err, 2);
-          d = 1;
-        }
-        odepth[o] = d - 1;
-        for (int e = 0; e < d; ++e) anc[(int64_t)o * MAXD + e] = chainv[d - 1 - e];
-        const int own = ok ? (t.n_kept[j] + 15) / 16 : 0;
-        nsp[2 * o] = ok ? (int32_t)subs : 0;
-        nsp[2 * o + 1] = ok ? (int32_t)(self_window ? subs : subs - own) : 0;
       }
-      ctxlen[o] = (int32_t)len;
     }
     int64_t tot, ftot, ttot;
-    const int64_t ex = block_exclusive_scan<int64_t>(len * S * Hkv * n_rg, sm, &tot);
+    const int64_t ex = block_exclusive_scan<int64_t>(len * slabs, sm, &tot);
     const int64_t fx = block_exclusive_scan<int64_t>(len, sm, &ftot);
     const int64_t tx = block_exclusive_scan<int64_t>(subs, sm, &ttot);
-    if (o < n_obs) {
-      pbase[o] = run + ex;
-      fbase[o] = frun + fx;
-      tbase[o] = 4 * (trun + tx);
+    if (o == me) {
+      s_mine[0] = run + ex;
+      s_mine[1] = trun + tx;
+      s_mine[3] = frun + fx;
     }
     run += tot;
     frun += ftot;
     trun += ttot;
   }
   __syncthreads();
-  // the folded sums live after the partials in the same buffer, then the
-  // sub-page tables (16-byte entries, 16-byte aligned)
+  // the folded sums follow the partials, then the sub-page tables (16-byte
+  // entries, 16-byte aligned)
   const int64_t tab0 = (run + frun + 3) & ~(int64_t)3;
-  for (int o = threadIdx.x; o < n_obs; o += blockDim.x) {
-    fbase[o] += run;
-    tbase[o] += tab0;
+  const bool fits = tab0 + 4 * trun <= part_cap;
+  if (tid == 0) {
+    pbase[me] = s_mine[0];
+    fbase[me] = run + s_mine[3];
+    tbase[me] = tab0 + 4 * s_mine[1];
+    if (me == 0) {
+      if (s_err & 1) status_error(a.status, ARBOR_EINVAL);
+      else if (s_err & 2) status_error(a.status, ARBOR_EUNSUPPORTED);
+      else if (!fits) status_error(a.status, ARBOR_EWORKSPACE);
+    }
   }
-  if (threadIdx.x == 0) {
-    if (s_err & 1) status_error(status, ARBOR_EINVAL);
-    else if (s_err & 2) status_error(status, ARBOR_EUNSUPPORTED);
-    else if (tab0 + 4 * trun > part_cap) status_error(status, ARBOR_EWORKSPACE);
-  }
-}
-
-// One workgroup per observer: its chain's 16-slot sub-pages, root first, as
-// 16-byte entries (plane row, slot, context offset, valid slots | own << 8),
-// so the streaming kernel reads them with scalar loads.
-__global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
-  __shared__ ChainLds ch;
-  __shared__ int s_bad;
-  if (threadIdx.x == 0) s_bad = status_failed(a.status);
-  __syncthreads();
-  if (s_bad) return;
-  const int o = blockIdx.x;
-  build_chain(a.t, a.pl, a.obs[o], ch);
-  const int n = a.nsp[2 * o];
-  int4 *tab = reinterpret_cast<int4 *>(a.part + a.tbase[o]);
-  for (int sp = threadIdx.x; sp < n; sp += blockDim.x) {
-    const SubPage e = sub_page(a.t, a.pl, ch, sp);
+  const int j = a.obs[me];
+  if (s_err || !fits || j < 0 || j >= t.V) return;   // uniform: s_err settled at the sync
+  build_chain(t, a.pl, j, ch);
+  const int n = (int)s_mine[2];
+  int4 *tab = reinterpret_cast<int4 *>(a.part + tab0 + 4 * s_mine[1]);
+  for (int sp = tid; sp < n; sp += blockDim.x) {
+    const SubPage e = sub_page(t, a.pl, ch, sp);
     tab[sp] = make_int4(e.row, e.slot, e.ctx, e.nvalid | ((e.d == ch.depth ? 1 : 0) << 8));
   }
 }
 
 // Fold the (slice layer, kv head, row group) slabs of every observer: one
 // column sum per (observer, credited context key), summed in slab order.
-__global__ __launch_bounds__(256) void score_fold(ScoreArgs a, float *__restrict__ fold,
-                                                  const int64_t *__restrict__ fbase) {
+__global__ __launch_bounds__(256) void score_fold(ScoreArgs a, const int64_t *__restrict__ fbase) {
   if (status_failed(a.status)) return;
   const int o = blockIdx.x;
   const int len = a.ctxlen[o];
@@ -677,7 +706,7 @@ __global__ __launch_bounds__(256) void score_fold(ScoreArgs a, float *__restrict
   const int credited = a.self_window ? len : len - own_c;
   const int nslab = a.S * a.pl.Hkv * a.n_rg;
   const float *src = a.part + a.pbase[o];
-  float *dst = fold + fbase[o];
+  float *dst = a.part + fbase[o];
   for (int x = blockIdx.y * blockDim.x + threadIdx.x; x < credited; x += gridDim.y * blockDim.x) {
     float acc = 0.f;
     for (int sl = 0; sl < nslab; ++sl) acc += src[(int64_t)sl * len + x];
@@ -685,11 +714,38 @@ __global__ __launch_bounds__(256) void score_fold(ScoreArgs a, float *__restrict
   }
 }
 
+// a_i and s_i of block i from its A (one wave).
+__device__ void block_final(const Tree &t, int i, const float *__restrict__ A,
+                            const int64_t *__restrict__ rows_seen, const float *__restrict__ v_in,
+                            const float *__restrict__ u_in, float th0, float th1, float th2,
+                            float *__restrict__ a_out, float *__restrict__ s_out) {
+  const int lane = lane_id();
+  const int64_t tb = t.tok_off[i];
+  const int n = t.n_full[i];
+  double sum = 0.0;
+  for (int p = lane; p < n; p += kWave) sum += (double)A[tb + p];
+  sum = wave_sum<double>(sum);
+  if (lane == 0) {
+    const int64_t rs = rows_seen[i];
+    const double av = rs > 0 ? sum / (double)rs : 0.0;
+    const double x = (double)th0 * (double)v_in[i] + (double)th1 * (double)u_in[i] + (double)th2 * av;
+    double sv = 1.0 / (1.0 + exp(-x));
+    sv = fmin(1.0, fmax(0.0, sv));
+    a_out[i] = (float)av;
+    s_out[i] = (float)sv;
+  }
+}
+
+struct FinalArgs {
+  const float *v_in, *u_in;
+  float th0, th1, th2;
+  float *a_out, *s_out;
+};
+
 // A += folded sums of every observer below block i (observer order, fp64);
 // rows_seen_i grows.  The four waves of a workgroup split the observers of a
 // 64-slot chunk and are combined in wave order.
-__global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const float *__restrict__ fold,
-                                                    const int64_t *__restrict__ fbase,
+__global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *__restrict__ fbase,
                                                     float *__restrict__ A,
                                                     int64_t *__restrict__ rows_seen) {
   __shared__ int64_t hbase[256];
@@ -702,6 +758,7 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const float *__
   const int c = t.n_kept[i];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
+  const float *fold = a.part;
   int di = 0, ctxoff = 0;
   for (int x = t.parent[i]; x >= 0 && di < MAXD; x = t.parent[x]) {
     ++di;
@@ -768,28 +825,11 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const float *__
 // a_i and s_i from the updated A (one wave per block).
 __global__ __launch_bounds__(256) void score_final(Tree t, const float *__restrict__ A,
                                                    const int64_t *__restrict__ rows_seen,
-                                                   const float *__restrict__ v_in,
-                                                   const float *__restrict__ u_in, float th0,
-                                                   float th1, float th2, float *__restrict__ a_out,
-                                                   float *__restrict__ s_out, int32_t *status) {
+                                                   FinalArgs fa, int32_t *status) {
   if (status_failed(status)) return;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= t.V) return;
-  const int lane = lane_id();
-  const int64_t tb = t.tok_off[i];
-  const int n = t.n_full[i];
-  double sum = 0.0;
-  for (int p = lane; p < n; p += kWave) sum += (double)A[tb + p];
-  sum = wave_sum<double>(sum);
-  if (lane == 0) {
-    const int64_t rs = rows_seen[i];
-    const double av = rs > 0 ? sum / (double)rs : 0.0;
-    const double x = (double)th0 * (double)v_in[i] + (double)th1 * (double)u_in[i] + (double)th2 * av;
-    double sv = 1.0 / (1.0 + exp(-x));
-    sv = fmin(1.0, fmax(0.0, sv));
-    a_out[i] = (float)av;
-    s_out[i] = (float)sv;
-  }
+  block_final(t, i, A, rows_seen, fa.v_in, fa.u_in, fa.th0, fa.th1, fa.th2, fa.a_out, fa.s_out);
 }
 
 template <class T, int D>
@@ -827,8 +867,9 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
-  b += nobs * 8 * 3 + nobs * 4 * 4 + nobs * MAXD * 4 + 5 * 256;
-  b += nobs * slabs * 16 * NB * 4 + 256;
+  // offsets, counts, chains (each carve rounds up to 256 B)
+  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + 8 * 256;
+  // partials and their folded sums
   b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
   // sub-page tables: at most one ragged sub-page per chain node
   b += nobs * ((size_t)sz->max_context / 16 + MAXD + 1) * 16 + 256;
@@ -872,12 +913,9 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   int32_t *ctxlen = cv.take<int32_t>(nobs);
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
-  const size_t slabs = (size_t)n_slice * pl.Hkv * a.n_rg;
-  float *lse = cv.take<float>(nobs * slabs * 16 * NB);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   float *part = reinterpret_cast<float *>(cv.rest());
   const int64_t part_cap = (int64_t)(cv.remaining() / 4);
-  a.lse = lse;
   a.part = part;
   a.pbase = pbase;
   a.tbase = tbase;
@@ -885,23 +923,20 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.ctxlen = ctxlen;
   a.odepth = odepth;
   a.anc = anc;
+  const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
-    hipLaunchKernelGGL(score_plan, dim3(1), dim3(1024), 0, stream, t, observers, n_obs, n_slice,
-                       pl.Hkv, a.n_rg, part_cap, pbase, fbase, tbase, nsp, a.self_window, ctxlen,
-                       odepth, anc, status);
-    hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(score_setup, dim3(n_obs), dim3(256), 0, stream, a, part_cap, pbase, fbase,
+                       tbase, nsp, ctxlen, odepth, anc);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     timing_begin(ARBOR_KERNEL_SCORE_ATTN, stream);
     launch_attn(geom->dtype, geom->head_dim, NBW, grid, stream, a);
     timing_end(ARBOR_KERNEL_SCORE_ATTN, stream);
-    hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, part, fbase);
-    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, part, fbase, A,
-                       rows_seen);
+    hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
+    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen);
   }
-  hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen,
-                     v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out,
-                     s_out, status);
+  hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen, fa,
+                     status);
   return hip_ok(hipGetLastError());
 }
 
