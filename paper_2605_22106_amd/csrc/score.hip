@@ -12,8 +12,9 @@
 //           chains for the partial / table offsets (a prefix over observers),
 //           writes its own observer's chain data and 16-slot sub-page table;
 //           workgroup 0 also validates the tree;
-//   attn    per (observer, slice layer, kv head, row group), two passes over
-//           the same (row, key) pairs as MFMA tiles of 16 keys x 16 rows:
+//   attn    per (observer, slice layer, kv head, group of up to 64 rows),
+//           two passes over the same (row, key) pairs as MFMA tiles of 16
+//           keys x 16 rows, the four waves taking alternate 16-key sub-pages:
 //           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
 //           sums of exp2(z - lse) -> one partial per credited context key;
 //   fold    per observer: sum its (slice layer, kv head, row group) partials;
@@ -135,35 +136,45 @@ __device__ __forceinline__ SubPage sub_page(const Tree &t, const Pool &pl, const
   return r;
 }
 
-// Layout of one 16-key sub-page of K in LDS: unit u = blk * 64 + lane is 16
-// bytes: key (lane % 16), quarter (lane / 16), bytes [16 blk, 16 blk + 16) of
-// that quarter row, so the MFMA operand of a k-step is one conflict-free
-// 16-byte read per lane.
+// ---------------------------------------------------------------------------
+// Streaming kernel.  One workgroup of four waves per (observer, slice layer,
+// kv head, group of up to 128 query rows).  The waves split the chain's 16-key
+// sub-pages round-robin (wave w takes sub-pages w, w + 4, ...), and every wave
+// holds the Q of all the group's rows in registers.  So each key tile is read
+// from LDS by one wave only, and a key's sum over the rows never leaves its
+// wave.
+//   pass 0  C = K Q^T: each lane keeps a running max / sum of one row over its
+//           keys; lanes, then waves, are merged into the row's log2-sum-exp;
+//   pass 1  C = Q K^T: per key, the sum over all rows of exp2(z - lse), stored
+//           as the row group's partial for that key.
+// Keys reach the wave's own ring of LDS buffers by direct global->LDS loads in
+// which each 16-lane group reads one whole 256-byte key row (coalesced).  The
+// 16-byte pieces of key r are stored XOR-permuted by r, so the sixteen lanes of
+// an MFMA operand read (keys 0..15, one piece each) hit distinct banks.  A wave
+// waits only for its own loads; neither pass has a barrier.
 template <class T, int D>
-struct Stage {
-  static constexpr int QB = D / 4 * (int)sizeof(T);  // bytes of a quarter row
-  static constexpr int NBLK = QB / 16;                // 16-byte units per lane
-  static constexpr int UNITS = NBLK * kWave;          // units per sub-page
-  static constexpr int BYTES = UNITS * 16;
+struct KTile {
+  static constexpr int R = D * (int)sizeof(T) / 16;   // 16-byte pieces of a key row
+  static constexpr int RQ = R / 4;                     // pieces of one lane group
+  static constexpr int XM = (R < 16 ? R : 16) - 1;     // piece swizzle mask
+  static constexpr int BYTES = 16 * R * 16;            // one 16-key sub-page
+  static constexpr int NDMA = BYTES / 1024;            // 1 KB direct loads per sub-page
+  static constexpr int ND = NDMA + 1;                  // + the positions
+  static constexpr int KS = D / 4 / Op<T>::kPerStep;   // MFMA k-steps over head_dim
+  static constexpr int SPP = KS / RQ;                   // k-steps per 16-byte piece
 };
 
-// ---------------------------------------------------------------------------
-// Fused two-pass kernel.  Keys stream through a ring of RING stages of GS
-// sub-pages in LDS, filled by direct global->LDS loads; each wave owns 16 NBW
-// query rows and keeps their Q in registers for both passes:
-//   pass 0  C = K Q^T: running max / sum of each row over the chain -> lse;
-//   pass 1  C = Q K^T: per key, sum over the wave's rows of exp2(z - lse);
-//           the four waves' sums are added in wave order and stored as the
-//           row group's partial for that key.
-// One barrier per stage: a wave waits for its own loads of the stage, then the
-// barrier makes every wave's loads visible and frees the slot the next load
-// refills.  Ring slots are distinct LDS arrays (the loop is unrolled by RING),
-// so the compiler can tell a slot being filled from the one being read.
-constexpr int kGS = 4;         // sub-pages per stage
-constexpr int kRing = 3;       // stages in the ring
-constexpr int kXcds = 8;       // accelerator dies of the device; workgroups go round-robin
+template <class T, int D>
+struct KBuf {
+  __attribute__((aligned(16))) char k[KTile<T, D>::BYTES];
+  __attribute__((aligned(16))) int pos[kWave];   // positions of the 16 slots (repeated)
+};
 template <int N>
 using Ic = std::integral_constant<int, N>;
+constexpr int kNBuf = 4;     // ring depth per wave: three sub-pages in flight
+constexpr int kXcds = 8;     // accelerator dies of the device; workgroups go round-robin
+constexpr int kMask0 = 1 << 9;    // table flag: pass 0 must mask keys of this sub-page
+constexpr int kMask1 = 1 << 10;   // table flag: pass 1 must mask keys of this sub-page
 
 // v_max3 without the quieting the IEEE maxnum lowering adds to each operand:
 // the operands are MFMA results or -inf, never signalling NaNs.
@@ -179,6 +190,15 @@ __device__ __forceinline__ void load_to_lds16(const void *g, void *lds) {
 }
 __device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
   __builtin_amdgcn_global_load_lds(g, lds, 4, 0, 0);
+}
+
+// Wait until at most n vector-memory operations of this wave are in flight
+// (gfx9 encoding: vmcnt bits 3:0 and 15:14; expcnt and lgkmcnt not waited).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+  asm volatile("" ::: "memory");
 }
 
 // sum over the four 16-lane groups of the wave (lanes l, l ^ 16, l ^ 32,
@@ -200,50 +220,41 @@ __device__ __forceinline__ float tree_sum(const float (&v)[N]) {
   return w[0];
 }
 
-// max of v[] and m, three operands per instruction
-template <int N>
-__device__ __forceinline__ float tree_max(const float (&v)[N], float m) {
-  static_assert(N == 16, "one stage of a row block");
-  const float x0 = max3f(v[0], v[1], v[2]), x1 = max3f(v[3], v[4], v[5]);
-  const float x2 = max3f(v[6], v[7], v[8]), x3 = max3f(v[9], v[10], v[11]);
-  const float x4 = max3f(v[12], v[13], v[14]);
-  return max3f(max3f(x0, x1, x2), max3f(x3, x4, v[15]), m);
+// MFMA operand of k-step c within a 16-byte piece
+template <class T>
+__device__ __forceinline__ typename Op<T>::reg piece_op(const uint4 &p, int c);
+template <>
+__device__ __forceinline__ bf16x8 piece_op<__bf16>(const uint4 &p, int) {
+  return __builtin_bit_cast(bf16x8, p);
+}
+template <>
+__device__ __forceinline__ float piece_op<float>(const uint4 &p, int c) {
+  return __uint_as_float(c == 0 ? p.x : (c == 1 ? p.y : (c == 2 ? p.z : p.w)));
 }
 
-template <class T, int D>
-struct Ring {
-  typedef Stage<T, D> SG;
-  __attribute__((aligned(16))) char k[kGS][SG::BYTES];
-  __attribute__((aligned(16))) int pos[kGS][16];
-};
-// per-stage column sums of the four waves (not a load target, so reading it
-// never has to wait for loads in flight)
-struct Red {
-  float v[kGS][4][16];
-};
-
-template <class T, int D, int NBW>
-__global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
+template <class T, int D, int NRB>
+__global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
   using O = Op<T>;
-  using SG = Stage<T, D>;
-  constexpr int KS = D / 4 / O::kPerStep;   // MFMA k-steps over head_dim
-  constexpr int RW = 64 * NBW;              // rows of the workgroup
-  constexpr int DPW = kGS * SG::NBLK / 4;   // K loads per wave per stage
-  constexpr int VM = DPW + 1;               // vector-memory ops per wave per stage
-  static_assert(kGS == 4, "one position load per wave per stage");
-  static_assert((kRing - 2) * VM <= 15, "vmcnt immediate");
+  using KT = KTile<T, D>;
+  using Buf = KBuf<T, D>;
+  constexpr int R = KT::R, RQ = KT::RQ, KS = KT::KS, SPP = KT::SPP, ND = KT::ND;
+  constexpr int ROWS = 16 * NRB;            // rows of the workgroup
   constexpr float kFloor = -1e30f;
-  __shared__ Ring<T, D> r0, r1, r2;
-  __shared__ Red d0, d1, d2;
+  // one ring slot per object, so the compiler can tell a buffer being filled
+  // from the one being read
+  __shared__ Buf b0[4], b1[4], b2[4], b3[4];
+  __shared__ float2 s_ml[4][ROWS];
+  __shared__ __attribute__((aligned(16))) float s_lse[ROWS];
   __shared__ int s_bad;
   // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
   // (slice layer, kv head, row group) planes p = x, x + 8, ... and, within a
-  // plane, the observers in id order -- siblings, which share their whole
-  // ancestor chain, run together and read those keys from the XCD's L2
+  // plane, the observers from the deepest (longest chain) down -- siblings,
+  // which share their whole ancestor chain, run together and read those keys
+  // from the XCD's L2
   const int n_planes = a.S * a.pl.Hkv * a.n_rg;
   const int xcd = (int)blockIdx.x % kXcds;
   const int idx = (int)blockIdx.x / kXcds;
-  const int o = idx % a.n_obs;
+  const int o = a.n_obs - 1 - idx % a.n_obs;
   const int plane = (idx / a.n_obs) * kXcds + xcd;
   if (plane >= n_planes) return;
   if (threadIdx.x == 0) s_bad = status_failed(a.status);
@@ -257,287 +268,264 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
   const int g = slg % pl.Hkv;
   const int layer = a.slice[si];
   const int j = a.obs[o];
-  // the chain's sub-page table, read with scalar loads (constant address space)
-  // entry sp: [4 sp] plane row, [4 sp + 1] slot, [4 sp + 2] context offset,
-  // [4 sp + 3] valid slots | own << 8
-  typedef const __attribute__((address_space(4))) int *TabPtr;
-  const TabPtr tab = (TabPtr)(a.part + a.tbase[o]);
+  // the chain's sub-page table: entry sp = (plane row, slot, context offset,
+  // valid slots | own << 8 | mask flags)
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  // (& 3: four waves; lets the compiler resolve each load's sub-page statically)
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;
-  const int rr = lane & 15;
-  const int g4 = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15;
+  const int q = lane >> 4;
   const int G = pl.G;
   const int nj = t.n_full[j];
   const int wj = min(a.W, nj);
   const int rows_total = G * a.W;
-  const int row0 = rg * RW + wave * 16 * NBW;   // first row of this wave
+  const int row0 = rg * ROWS;
   const float sl2 = a.sl2;
-  auto row_u = [&](int r) __attribute__((always_inline)) -> int {
-    if (r >= rows_total) return -1;
-    const int tt = r % a.W;
+  // position of window row `row` of the group, -1 if none
+  auto urow = [&](int row) __attribute__((always_inline)) -> int {
+    row += row0;
+    if (row >= rows_total) return -1;
+    const int tt = row % a.W;
     return tt < wj ? nj - wj + tt : -1;
   };
 
-  typename O::reg q[NBW][KS];
+  // Q of every row of the group: lane (r, q) holds the q-th quarter of row
+  // 16 rb + r, as RQ 16-byte pieces
+  uint4 qp[NRB][RQ];
   const T *qbase = static_cast<const T *>(a.q_win) +
                    ((((int64_t)o * a.S + si) * (pl.Hkv * G) + (int64_t)g * G) * a.W) * D;
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    const int r = row0 + nb * 16 + rr;
-    const bool rv = r < rows_total;
-    const T *rp = qbase + (int64_t)(rv ? r : 0) * D + g4 * (D / 4);
+  for (int rb = 0; rb < NRB; ++rb) {
+    const int row = row0 + rb * 16 + r;
+    const bool rv = row < rows_total;
+    const uint4 *rp = reinterpret_cast<const uint4 *>(qbase + (int64_t)(rv ? row : 0) * D) + q * RQ;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) q[nb][ks] = rv ? O::load(rp + ks * O::kPerStep) : O::zero();
+    for (int jp = 0; jp < RQ; ++jp) qp[rb][jp] = rv ? rp[jp] : make_uint4(0, 0, 0, 0);
   }
   const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
   const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
-  // this lane's 16-byte unit of a key tile: key rr, quarter g4
-  const int64_t lane_off = (int64_t)rr * (D * (int)sizeof(T)) + g4 * SG::QB;
+  // byte offset, within a sub-page, of the piece lane L fetches for direct load c
+  int src_off[KT::NDMA];
+#pragma unroll
+  for (int c = 0; c < KT::NDMA; ++c) {
+    const int sig = 64 * c + lane;           // LDS slot: key sig / R, stored piece sig % R
+    const int kr = sig / R;
+    src_off[c] = 16 * (R * kr + ((sig % R) ^ (kr & KT::XM)));
+  }
+  // LDS byte offset of piece jp of this lane's quarter of key r
+  const int lbase = 16 * (R * r + ((q * RQ) ^ (r & KT::XM)));
 
-  // direct loads of stage st (sub-pages st*GS .. st*GS+GS-1, clamped) into R;
-  // all addresses are formed before the first load is issued
-  auto issue = [&](Ring<T, D> &R, int st, int n_sp) __attribute__((always_inline)) {
-    int rows[kGS], slots[kGS];
+  // the chain's sub-page table as 16-byte vectors (read into registers)
+  const int4 *tabv = reinterpret_cast<const int4 *>(a.part + a.tbase[o]);
+  auto issue = [&](Buf &B, int row, int slot) __attribute__((always_inline)) {
+    const char *src = kplane + (int64_t)row * (D * (int)sizeof(T));
 #pragma unroll
-    for (int k = 0; k < kGS; ++k) {
-      const int sp = min(st * kGS + k, n_sp - 1);
-      rows[k] = tab[4 * sp];
-      slots[k] = tab[4 * sp + 1];
-    }
-    // lane L: position (L & 15) of sub-page L >> 4
-    int lane_slot = slots[0];
-#pragma unroll
-    for (int k = 1; k < kGS; ++k) lane_slot = g4 == k ? slots[k] : lane_slot;
-#pragma unroll
-    for (int i = 0; i < DPW; ++i) {
-      const int u = wave + 4 * i;          // unit (sub-page k, 16-byte block blk)
-      const int k = u / SG::NBLK, blk = u % SG::NBLK;
-      int row = rows[0];
-#pragma unroll
-      for (int kk = 1; kk < kGS; ++kk) row = k == kk ? rows[kk] : row;
-      const char *src = kplane + (int64_t)row * (D * (int)sizeof(T)) + lane_off + blk * 16;
-      load_to_lds16(src, &R.k[k][blk * kWave * 16]);
-    }
-    // the key positions of all four sub-pages, loaded by every wave (the
-    // waves write the same values).  An unmasked load: a load under a lane
-    // mask gives the compiler paths with different numbers of loads in
-    // flight, and it then waits for all of them before each read of the ring.
-    load_to_lds4(pl.slot_pos + lane_slot + rr, &R.pos[0][0]);
+    for (int c = 0; c < KT::NDMA; ++c) load_to_lds16(src + src_off[c], &B.k[1024 * c]);
+    // an unmasked load: every lane fetches position (lane & 15)
+    load_to_lds4(pl.slot_pos + slot + r, &B.pos[0]);
   };
-  // my loads of the stage about to be computed are done; everyone's are visible
-  // (s_waitcnt immediate: vmcnt in bits 3:0, expcnt 6:4, lgkmcnt 11:8.)  The
-  // LDS writes of this wave are complete too (lgkmcnt 0), so no release fence
-  // is needed -- one would also wait for the loads still filling later slots.
-  // (`later`: how many stages' loads may stay in flight, a compile-time count)
-  auto stage_sync = [&](auto later) __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(0x070 | (decltype(later)::value * VM));
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  };
-  auto operand = [&](const Ring<T, D> &R, int k, typename O::reg (&kr)[KS]) __attribute__((always_inline)) {
-    const char *base = &R.k[k][0] + lane * 16;
+  auto read_k = [&](const Buf &B, uint4 (&kp)[RQ]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int byte = ks * O::kPerStep * (int)sizeof(T);   // within the quarter row
-      kr[ks] = O::load(reinterpret_cast<const T *>(base + (byte / 16) * (kWave * 16) + byte % 16));
+    for (int jp = 0; jp < RQ; ++jp)
+      kp[jp] = *reinterpret_cast<const uint4 *>(&B.k[lbase ^ (16 * jp)]);
+  };
+
+  // One pass over this wave's sub-pages sp = wave + 4 i (i < cnt) of the
+  // first n_sp of the chain, software-pipelined.  Step i
+  //   fix(prev)  rare, branchy corrections of sub-page i - 1 (key masks);
+  //   refills the ring slot freed in the previous step;
+  //   mm(kp)     the MFMAs of sub-page i, interleaved in one straight-line
+  //   hot(prev)  block with the VALU work of sub-page i - 1, so the matrix
+  //              core and the VALU work side by side within the wave;
+  //   post(prev) rare corrections after the fact, and stores;
+  //   then waits for sub-page i + 1 and reads its operands into registers.
+  // The table entries of a window of up to 64 steps sit in registers (lane L
+  // holds step L) and are read with readlane, so the loop has no scalar loads.
+  struct StepState {
+    f32x4 acc[NRB];
+    int meta, ctx;
+    int4 kpos;
+  };
+  auto run = [&](auto pass, int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post)
+                 __attribute__((always_inline)) {
+    const int cnt = n_sp > wave ? (n_sp - wave + 3) / 4 : 0;
+    for (int base = 0; base < cnt; base += 64) {
+      const int wc = min(64, cnt - base);
+      int4 e = make_int4(0, 0, 0, 0);
+      if (lane < wc) e = tabv[wave + 4 * (base + lane)];
+      // a field of window step i (clamped to the last step)
+      auto ent = [&](int i, int v) __attribute__((always_inline)) -> int {
+        return __builtin_amdgcn_readlane(v, min(i, wc - 1));
+      };
+      auto issue_i = [&](Buf &B, int i) __attribute__((always_inline)) {
+        issue(B, ent(i, e.x), ent(i, e.y));
+      };
+      uint4 kp[RQ];
+      int4 kposv;
+      // key positions: pass 0 holds keys 4 q + e of a sub-page, pass 1 key r
+      auto read_i = [&](const Buf &B) __attribute__((always_inline)) {
+        read_k(B, kp);
+        if constexpr (decltype(pass)::value == 0)
+          kposv = *reinterpret_cast<const int4 *>(&B.pos[4 * q]);
+        else
+          kposv = make_int4(B.pos[r], 0, 0, 0);
+      };
+      issue_i(b0[wave], 0);
+      issue_i(b1[wave], 1);
+      issue_i(b2[wave], 2);
+      wait_vm<2 * ND>();
+      read_i(b0[wave]);
+      StepState prev = mm(kp, kposv, ent(0, e.w), ent(0, e.z));
+      issue_i(b3[wave], 3);
+      wait_vm<2 * ND>();
+      read_i(b1[wave]);
+      auto body = [&](int i) __attribute__((always_inline)) {
+        fix(prev);
+        const StepState cur = mm(kp, kposv, ent(i, e.w), ent(i, e.z));
+        hot(prev);
+#pragma unroll
+        for (int k = 0; k < KS * NRB; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        }
+        post(prev);
+        prev = cur;
+      };
+      // whole rounds of four steps in a loop with one exit, so every path
+      // into a step has the same loads in flight
+      int i = 1;
+      for (; i + 4 <= wc; i += 4) {
+        issue_i(b0[wave], i + 3);
+        body(i);
+        wait_vm<2 * ND>();
+        read_i(b2[wave]);
+        issue_i(b1[wave], i + 4);
+        body(i + 1);
+        wait_vm<2 * ND>();
+        read_i(b3[wave]);
+        issue_i(b2[wave], i + 5);
+        body(i + 2);
+        wait_vm<2 * ND>();
+        read_i(b0[wave]);
+        issue_i(b3[wave], i + 6);
+        body(i + 3);
+        wait_vm<2 * ND>();
+        read_i(b1[wave]);
+      }
+      // the last one to three sub-pages: their loads are already in flight
+      // (sub-page i in slot 1, i + 1 in slot 2, i + 2 in slot 3)
+      if (i < wc) {
+        body(i);
+        if (i + 1 < wc) {
+          wait_vm<ND>();
+          read_i(b2[wave]);
+          body(i + 1);
+          if (i + 2 < wc) {
+            wait_vm<0>();
+            read_i(b3[wave]);
+            body(i + 2);
+          }
+        }
+      }
+      fix(prev);
+      hot(prev);
+      post(prev);
+      // drain (the clamped reloads past the end) before the ring is reused
+      wait_vm<0>();
     }
   };
 
   // ---- pass 0: row log2-sum-exp ----
-  float m[NBW], l[NBW];
+  float m[NRB], l[NRB];
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    m[nb] = kFloor;
-    l[nb] = 0.f;
+  for (int rb = 0; rb < NRB; ++rb) {
+    m[rb] = kFloor;
+    l[rb] = 0.f;
   }
-  auto lse_stage = [&](const Ring<T, D> &R, int st, int n_sp, auto &&between)
-                       __attribute__((always_inline)) {
-    f32x4 acc[kGS][NBW];
-    int meta[kGS];
-    typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
+  // The running sum of a row is kept relative to a reference m that moves
+  // only when a logit exceeds it by more than kSlack / sl2 (terms stay below
+  // 2^kSlack).  The terms of a sub-page are computed against the current
+  // reference first; if any row's max moved past it, the wave rescales every
+  // row to its new max and recomputes that sub-page's terms.
+  constexpr float kSlack = 8.f;
+  const float slack = kSlack / sl2;
+  float nm[NRB], lt[NRB], mx[NRB];
+  bool grow = false;
 #pragma unroll
-    for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
-    between();
+  for (int rb = 0; rb < NRB; ++rb) nm[rb] = -m[rb] * sl2;
+  run(Ic<0>{}, a.nsp[2 * o],
+      [&](const uint4 (&kp)[RQ], int4 kposv, int meta, int ctx) __attribute__((always_inline)) {
+        StepState st;
+        st.meta = meta;
+        st.ctx = ctx;
+        st.kpos = kposv;
 #pragma unroll
-    for (int k = 0; k < kGS; ++k) {
-      const int sp = st * kGS + k;
-      meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
-    }
+        for (int rb = 0; rb < NRB; ++rb) st.acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = 0; k < kGS; ++k)
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) {
-        acc[k][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int rb = 0; rb < NRB; ++rb)
+            st.acc[rb] = O::mma(piece_op<T>(kp[ks / SPP], ks % SPP),
+                                piece_op<T>(qp[rb][ks / SPP], ks % SPP), st.acc[rb]);
+        return st;
+      },
+      [&](StepState &st) __attribute__((always_inline)) {
+        if (st.meta & kMask0) {
+          // a ragged sub-page, or own keys some rows may not see (position > row)
+          const int nvalid = st.meta & 255;
+          const bool own = ((st.meta >> 8) & 1) != 0;
+          const int kpos[4] = {st.kpos.x, st.kpos.y, st.kpos.z, st.kpos.w};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc[k][nb] = O::mma(kr[k][ks], q[nb][ks], acc[k][nb]);
-      }
-    // meta == 16: a full sub-page of ancestor keys, nothing to mask
-    const bool any_mask = ((meta[0] ^ 16) | (meta[1] ^ 16) | (meta[2] ^ 16) | (meta[3] ^ 16)) != 0;
+          for (int rb = 0; rb < NRB; ++rb) {
+            const int ur = urow(rb * 16 + r);
 #pragma unroll
-    for (int k = 0; k < kGS; ++k) {
-      const int nvalid = meta[k] & 255;
-      const bool own = (meta[k] >> 8) != 0;
-      if (any_mask && (own || nvalid < 16)) {
-        int kpos[4] = {0, 0, 0, 0};
-        if (own) {
-          const int4 pv = *reinterpret_cast<const int4 *>(&R.pos[k][4 * g4]);
-          kpos[0] = pv.x;
-          kpos[1] = pv.y;
-          kpos[2] = pv.z;
-          kpos[3] = pv.w;
-        }
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb) {
-          const int ur = row_u(row0 + nb * 16 + rr);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool ok = 4 * g4 + e < nvalid && (!own || kpos[e] <= ur);
-            acc[k][nb][e] = ok ? acc[k][nb][e] : -__builtin_inff();
+            for (int e = 0; e < 4; ++e) {
+              const bool ok = 4 * q + e < nvalid && (!own || kpos[e] <= ur);
+              st.acc[rb][e] = ok ? st.acc[rb][e] : -__builtin_inff();
+            }
           }
         }
-      }
-    }
+      },
+      [&](const StepState &st) __attribute__((always_inline)) {
+        grow = false;
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb) {
-      // reductions as trees: short dependency chains keep the VALU busy
-      float v[4 * kGS];
-#pragma unroll
-      for (int k = 0; k < kGS; ++k)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[4 * k + e] = acc[k][nb][e];
-      const float mx = tree_max(v, m[nb]);
-      const float nm = -mx * sl2;
-#pragma unroll
-      for (int i = 0; i < 4 * kGS; ++i) v[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(v[i], sl2, nm));
-      // (m - mx) is exactly 0 while the max is unchanged
-      l[nb] = __builtin_fmaf(l[nb], __builtin_amdgcn_exp2f((m[nb] - mx) * sl2), tree_sum(v));
-      m[nb] = mx;
-    }
-  };
-
-  // ---- pass 1: credited column sums ----
-  float nlse[NBW][4];
-  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
-  auto col_stage = [&](Ring<T, D> &R, Red &RD, int st, int n_sp, auto &&between)
-                       __attribute__((always_inline)) {
-    typename O::reg kr[kGS][KS];   // all operands of the stage first: one LDS wait
-#pragma unroll
-    for (int k = 0; k < kGS; ++k) operand(R, k, kr[k]);
-    between();
-    int meta[kGS];
-#pragma unroll
-    for (int k = 0; k < kGS; ++k) {
-      const int sp = st * kGS + k;
-      meta[k] = sp < n_sp ? tab[4 * sp + 3] : 0;
-    }
-    const bool any_own = ((meta[0] | meta[1] | meta[2] | meta[3]) >> 8) != 0;
-#pragma unroll
-    for (int k = 0; k < kGS; ++k) {
-      const bool own = any_own && (meta[k] >> 8) != 0;
-      f32x4 acc[NBW];
-#pragma unroll
-      for (int nb = 0; nb < NBW; ++nb) {
-        acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc[nb] = O::mma(q[nb][ks], kr[k][ks], acc[nb]);
-      }
-      float pz[4 * NBW];
-#pragma unroll
-      for (int nb = 0; nb < NBW; ++nb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          pz[4 * nb + e] = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[nb][e], sl2, nlse[nb][e]));
-      if (own) {
-        // own tokens are credited only by later rows of the window
-        const int kp = R.pos[k][rr];
-#pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
+        for (int rb = 0; rb < NRB; ++rb) {
+          mx[rb] = max3f(max3f(st.acc[rb][0], st.acc[rb][1], st.acc[rb][2]), st.acc[rb][3], m[rb]);
+          grow |= mx[rb] > m[rb] + slack;
+          float e4[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            pz[4 * nb + e] = kp < row_u(row0 + nb * 16 + 4 * g4 + e) ? pz[4 * nb + e] : 0.f;
-      }
-      const float colsum = group_sum(tree_sum(pz));
-      if (lane < 16) RD.v[k][wave][lane] = colsum;
-    }
-  };
-  // the previous stage's sums of all four waves, in wave order
-  auto finish = [&](const Red &RD, int st, int n_sp) __attribute__((always_inline)) {
-    if (wave == 0) {
-      // table entries by scalar loads (a per-lane load would wait behind the
-      // direct loads in flight)
-#pragma unroll
-      for (int k = 0; k < kGS; ++k) {
-        const int sp = st * kGS + k;
-        if (sp >= 0 && sp < n_sp) {
-          const int ctx = tab[4 * sp + 2], nvalid = tab[4 * sp + 3] & 255;
-          if ((lane >> 4) == k && rr < nvalid)
-            pout[ctx + rr] = ((RD.v[k][0][rr] + RD.v[k][1][rr]) + RD.v[k][2][rr]) + RD.v[k][3][rr];
+            e4[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st.acc[rb][e], sl2, nm[rb]));
+          lt[rb] = tree_sum(e4);
+          // computed here, inside the block shared with the MFMAs (the
+          // compiler would otherwise sink it into the branch that uses it)
+          asm volatile("" : "+v"(lt[rb]));
         }
-      }
-    }
-  };
-
-  // one pass over the chain's sub-pages with the ring; `work` computes a
-  // stage from a slot, `after` runs (for the previous stage) right after the
-  // stage barrier
-  auto run = [&](int n_sp, auto &&work, auto &&after) __attribute__((always_inline)) {
-    if (n_sp <= 0) return;
-    const int n_st = (n_sp + kGS - 1) / kGS;
-    issue(r0, 0, n_sp);
-    issue(r1, 1, n_sp);
-    // A stage reads its operands from the slot first and only then issues the
-    // loads that refill the previous slot.  `after` of the previous stage runs
-    // once the current stage is computed: its data became visible at this
-    // stage's barrier.  Whole rounds of three stages run in a loop with one
-    // exit, so every path into a stage has the same loads in flight and the
-    // compiler keeps the partial waits.
-    int st = 0;
-    for (; st + 3 <= n_st; st += 3) {
-      stage_sync(Ic<kRing - 2>{});
-      work(r0, d0, st, n_sp, [&]() __attribute__((always_inline)) { issue(r2, st + 2, n_sp); });
-      after(d2, st - 1, n_sp);   // nothing to finish before the first stage (st - 1 < 0)
-      stage_sync(Ic<kRing - 2>{});
-      work(r1, d1, st + 1, n_sp, [&]() __attribute__((always_inline)) { issue(r0, st + 3, n_sp); });
-      after(d0, st, n_sp);
-      stage_sync(Ic<kRing - 2>{});
-      work(r2, d2, st + 2, n_sp, [&]() __attribute__((always_inline)) { issue(r1, st + 4, n_sp); });
-      after(d1, st + 1, n_sp);
-    }
-    // the last one or two stages: their loads are already in flight
-    auto none = []() __attribute__((always_inline)) {};
-    if (st < n_st) {
-      stage_sync(Ic<1>{});
-      work(r0, d0, st, n_sp, none);
-      after(d2, st - 1, n_sp);
-      if (st + 1 < n_st) {
-        stage_sync(Ic<0>{});
-        work(r1, d1, st + 1, n_sp, none);
-        after(d0, st, n_sp);
-      }
-    }
-    // drain: every load has landed and the last stage's results are visible
-    __builtin_amdgcn_s_waitcnt(0x070);
-    __syncthreads();
-    const int last = n_st - 1;
-    after(last % 3 == 0 ? d0 : (last % 3 == 1 ? d1 : d2), last, n_sp);
-    __syncthreads();
-  };
-  auto nothing = [](const Red &, int, int) __attribute__((always_inline)) {};
-
-  const int n_sp0 = a.nsp[2 * o];
-  run(n_sp0,
-      [&](Ring<T, D> &R, Red &, int st, int n, auto &&between) __attribute__((always_inline)) {
-        lse_stage(R, st, n, between);
       },
-      nothing);
-  // rows: lane groups merged (log2 units), then each lane takes the lse of
-  // the rows it holds in the pass-1 layout (rows 4 g4 + e of each block)
+      [&](const StepState &st) __attribute__((always_inline)) {
+        if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    float mm = m[nb] > kFloor ? m[nb] * sl2 : -__builtin_inff();
-    float ll = l[nb];
+          for (int rb = 0; rb < NRB; ++rb) {
+            // (m - mx) is exactly 0 for a row whose max is unchanged
+            const float sc = __builtin_amdgcn_exp2f((m[rb] - mx[rb]) * sl2);
+            m[rb] = mx[rb];
+            nm[rb] = -mx[rb] * sl2;
+            float e4[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              e4[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st.acc[rb][e], sl2, nm[rb]));
+            l[rb] = __builtin_fmaf(l[rb], sc, tree_sum(e4));
+          }
+        } else {
+#pragma unroll
+          for (int rb = 0; rb < NRB; ++rb) l[rb] += lt[rb];
+        }
+      });
+  // merge the four lane groups (log2 units), then the four waves, in order
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    float mm = m[rb] > kFloor ? m[rb] * sl2 : -__builtin_inff();
+    float ll = l[rb];
 #pragma unroll
     for (int off = 16; off <= 32; off <<= 1) {
       const float mo = __shfl_xor(mm, off, kWave);
@@ -550,17 +538,81 @@ __global__ __launch_bounds__(256) void score_attn(ScoreArgs a) {
       mm = mn;
       ll = ln;
     }
-    const bool valid = row_u(row0 + nb * 16 + rr) >= 0 && ll > 0.f;
-    const float lse = valid ? mm + __log2f(ll) : __builtin_inff();
-#pragma unroll
-    for (int e = 0; e < 4; ++e) nlse[nb][e] = -__shfl(lse, 4 * g4 + e, kWave);
+    if (lane < 16) s_ml[wave][rb * 16 + lane] = make_float2(mm, ll);
   }
-  const int n_sp1 = a.nsp[2 * o + 1];
-  run(n_sp1,
-      [&](Ring<T, D> &R, Red &RD, int st, int n, auto &&between) __attribute__((always_inline)) {
-        col_stage(R, RD, st, n, between);
+  __syncthreads();
+  for (int row = tid; row < ROWS; row += blockDim.x) {
+    float mm = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mm = fmaxf(mm, s_ml[w][row].x);
+    float ll = 0.f;
+    if (mm > -__builtin_inff()) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float2 v = s_ml[w][row];
+        ll += v.x > -__builtin_inff() ? v.y * __builtin_amdgcn_exp2f(v.x - mm) : 0.f;
+      }
+    }
+    const bool valid = urow(row) >= 0 && ll > 0.f;
+    s_lse[row] = valid ? mm + __log2f(ll) : __builtin_inff();
+  }
+  __syncthreads();
+  // pass-1 layout: this lane holds rows 16 rb + 4 q + e of its key
+  float nlse[NRB][4];
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    const float4 v = *reinterpret_cast<const float4 *>(&s_lse[rb * 16 + 4 * q]);
+    nlse[rb][0] = -v.x;
+    nlse[rb][1] = -v.y;
+    nlse[rb][2] = -v.z;
+    nlse[rb][3] = -v.w;
+  }
+
+  // ---- pass 1: credited column sums ----
+  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
+  float colsum = 0.f;
+  run(Ic<1>{}, a.nsp[2 * o + 1],
+      [&](const uint4 (&kp)[RQ], int4 kposv, int meta, int ctx) __attribute__((always_inline)) {
+        StepState st;
+        st.meta = meta;
+        st.ctx = ctx;
+        st.kpos = kposv;
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) st.acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int rb = 0; rb < NRB; ++rb)
+            st.acc[rb] = O::mma(piece_op<T>(qp[rb][ks / SPP], ks % SPP),
+                                piece_op<T>(kp[ks / SPP], ks % SPP), st.acc[rb]);
+        return st;
       },
-      [&](const Red &RD, int st, int n) __attribute__((always_inline)) { finish(RD, st, n); });
+      [&](StepState &st) __attribute__((always_inline)) {
+        if (st.meta & kMask1) {
+          // own tokens are credited only by later rows of the window: this
+          // lane's key r has position kpos[r % 4] of the four it read, so
+          // take it from the lane of the same row group holding key r
+          const int kpos = st.kpos.x;
+#pragma unroll
+          for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              st.acc[rb][e] = kpos < urow(rb * 16 + 4 * q + e) ? st.acc[rb][e] : -__builtin_inff();
+        }
+      },
+      [&](const StepState &st) __attribute__((always_inline)) {
+        float pz[4 * NRB];
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            pz[4 * rb + e] = __builtin_amdgcn_exp2f(__builtin_fmaf(st.acc[rb][e], sl2, nlse[rb][e]));
+        colsum = group_sum(tree_sum(pz));
+        asm volatile("" : "+v"(colsum));
+      },
+      [&](const StepState &st) __attribute__((always_inline)) {
+        if (lane < (st.meta & 255)) pout[st.ctx + lane] = colsum;
+      });
 }
 
 // Chain length and sub-page count of observer j, with the same checks as the
@@ -690,9 +742,18 @@ __global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap
   build_chain(t, a.pl, j, ch);
   const int n = (int)s_mine[2];
   int4 *tab = reinterpret_cast<int4 *>(a.part + tab0 + 4 * s_mine[1]);
+  // the window rows see own positions up to u >= u_min: an own sub-page whose
+  // last position is above u_min needs per-key masking in pass 0; in the
+  // self-window mode, one whose last position reaches u_min needs it in pass 1
+  const int u_min = t.n_full[j] - min(a.W, t.n_full[j]);
   for (int sp = tid; sp < n; sp += blockDim.x) {
     const SubPage e = sub_page(t, a.pl, ch, sp);
-    tab[sp] = make_int4(e.row, e.slot, e.ctx, e.nvalid | ((e.d == ch.depth ? 1 : 0) << 8));
+    const bool own = e.d == ch.depth;
+    const int last = own ? a.pl.slot_pos[e.slot + e.nvalid - 1] : 0;
+    const bool m0 = e.nvalid < 16 || (own && last > u_min);
+    const bool m1 = a.self_window && own && last >= u_min;
+    tab[sp] = make_int4(e.row, e.slot, e.ctx,
+                        e.nvalid | (own ? 1 << 8 : 0) | (m0 ? kMask0 : 0) | (m1 ? kMask1 : 0));
   }
 }
 
@@ -833,37 +894,44 @@ __global__ __launch_bounds__(256) void score_final(Tree t, const float *__restri
 }
 
 template <class T, int D>
-void launch_attn_nb(int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
-  switch (NBW) {
+void launch_attn_nb(int NRB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  switch (NRB) {
     case 1: hipLaunchKernelGGL((score_attn<T, D, 1>), grid, dim3(256), 0, stream, a); break;
     case 2: hipLaunchKernelGGL((score_attn<T, D, 2>), grid, dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL((score_attn<T, D, 4>), grid, dim3(256), 0, stream, a); break;
+    default:
+      if constexpr (sizeof(T) == 2)
+        hipLaunchKernelGGL((score_attn<T, D, 4>), grid, dim3(256), 0, stream, a);
+      break;
   }
 }
 
-void launch_attn(int dtype, int D, int NBW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+void launch_attn(int dtype, int D, int NRB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
   if (dtype == ARBOR_BF16) {
-    if (D == 128) launch_attn_nb<__bf16, 128>(NBW, grid, stream, a);
-    else launch_attn_nb<__bf16, 64>(NBW, grid, stream, a);
+    if (D == 128) launch_attn_nb<__bf16, 128>(NRB, grid, stream, a);
+    else launch_attn_nb<__bf16, 64>(NRB, grid, stream, a);
   } else {
-    if (D == 128) launch_attn_nb<float, 128>(NBW, grid, stream, a);
-    else launch_attn_nb<float, 64>(NBW, grid, stream, a);
+    if (D == 128) launch_attn_nb<float, 128>(NRB, grid, stream, a);
+    else launch_attn_nb<float, 64>(NRB, grid, stream, a);
   }
 }
 
-// Row blocks per wave: the workgroup (4 waves) covers 64 * NBW query rows.
-int blocks_per_wave(int rows_total) {
-  if (rows_total <= 64) return 1;
-  if (rows_total <= 128) return 2;
-  return 4;
+// 16-row blocks of a workgroup: enough for all the rows up to 64 (32 for fp32,
+// whose operands take four times the registers), a power of two.  Every wave
+// holds the Q of all the group's rows; 64 rows keep it within the registers
+// of two waves per SIMD.
+int row_blocks(int rows_total, int dtype) {
+  const int cap = dtype == ARBOR_BF16 ? 4 : 2;
+  int nrb = 1;
+  while (nrb < cap && 16 * nrb < rows_total) nrb *= 2;
+  return nrb;
 }
 
 }  // namespace
 
 size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const int rows_total = g->q_per_kv * sz->window;
-  const int NB = 4 * blocks_per_wave(rows_total);
-  const int n_rg = (rows_total + 16 * NB - 1) / (16 * NB);
+  const int NRB = row_blocks(rows_total, g->dtype);
+  const int n_rg = (rows_total + 16 * NRB - 1) / (16 * NRB);
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
@@ -896,9 +964,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.S = n_slice;
   for (int e = 0; e < 8; ++e) a.slice[e] = e < n_slice ? slice_layers[e] : 0;
   const int rows_total = pl.G * window;
-  const int NBW = blocks_per_wave(rows_total);
-  const int NB = 4 * NBW;
-  a.n_rg = (rows_total + 16 * NB - 1) / (16 * NB);
+  const int NRB = row_blocks(rows_total, geom->dtype);
+  a.n_rg = (rows_total + 16 * NRB - 1) / (16 * NRB);
   const float scale = params->softmax_scale > 0.f ? params->softmax_scale
                                                   : 1.0f / sqrtf((float)geom->head_dim);
   a.sl2 = scale * kLog2e;
@@ -930,7 +997,7 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     timing_begin(ARBOR_KERNEL_SCORE_ATTN, stream);
-    launch_attn(geom->dtype, geom->head_dim, NBW, grid, stream, a);
+    launch_attn(geom->dtype, geom->head_dim, NRB, grid, stream, a);
     timing_end(ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
     hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen);
