@@ -159,19 +159,33 @@ struct KTile {
   static constexpr int XM = (R < 16 ? R : 16) - 1;     // piece swizzle mask
   static constexpr int BYTES = 16 * R * 16;            // one 16-key sub-page
   static constexpr int NDMA = BYTES / 1024;            // 1 KB direct loads per sub-page
-  static constexpr int ND = NDMA + 1;                  // + the positions
+  static constexpr int ND = NDMA;
   static constexpr int KS = D / 4 / Op<T>::kPerStep;   // MFMA k-steps over head_dim
   static constexpr int SPP = KS / RQ;                   // k-steps per 16-byte piece
 };
 
+typedef __attribute__((address_space(3))) void *LdsPtr;
+// NDMA direct loads (global -> LDS) of one BYTES-long tile at src: lane L's 16
+// bytes of load c land at lds + 1024 c + 16 L.  A buffer resource over the
+// tile (scalar registers) leaves each lane a 32-bit offset, and bounds every
+// access to the tile.
+// (host-device so the kernel's host-device lambdas can call it; the host
+// pass of the compiler never runs it)
+template <int NDMA, int BYTES>
+__host__ __device__ __forceinline__ void dma_tile(const char *src, char *lds,
+                                                  const int (&off)[NDMA]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(src), 0, BYTES, 0x00020000);
+#pragma unroll
+  for (int c = 0; c < NDMA; ++c)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LdsPtr)(lds + 1024 * c), 16, off[c], 0, 0, 0);
+#endif
+}
 template <class T, int D>
 struct KBuf {
   __attribute__((aligned(16))) char k[KTile<T, D>::BYTES];
-  __attribute__((aligned(16))) int pos[kWave];   // positions of the 16 slots (repeated)
 };
-template <int N>
-using Ic = std::integral_constant<int, N>;
-constexpr int kNBuf = 4;     // ring depth per wave: three sub-pages in flight
 constexpr int kXcds = 8;     // accelerator dies of the device; workgroups go round-robin
 constexpr int kMask0 = 1 << 9;    // table flag: pass 0 must mask keys of this sub-page
 constexpr int kMask1 = 1 << 10;   // table flag: pass 1 must mask keys of this sub-page
@@ -182,14 +196,6 @@ __device__ __forceinline__ float max3f(float a, float b, float c) {
   float r;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
   return r;
-}
-
-// Direct global -> LDS loads: lane L's `size` bytes land at lds + size * L.
-__device__ __forceinline__ void load_to_lds16(const void *g, void *lds) {
-  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
-}
-__device__ __forceinline__ void load_to_lds4(const void *g, void *lds) {
-  __builtin_amdgcn_global_load_lds(g, lds, 4, 0, 0);
 }
 
 // Wait until at most n vector-memory operations of this wave are in flight
@@ -233,7 +239,7 @@ __device__ __forceinline__ float piece_op<float>(const uint4 &p, int c) {
 }
 
 template <class T, int D, int NRB>
-__global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
+__global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   using O = Op<T>;
   using KT = KTile<T, D>;
   using Buf = KBuf<T, D>;
@@ -242,7 +248,7 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
   constexpr float kFloor = -1e30f;
   // one ring slot per object, so the compiler can tell a buffer being filled
   // from the one being read
-  __shared__ Buf b0[4], b1[4], b2[4], b3[4];
+  __shared__ Buf b0[4], b1[4], b2[4];
   __shared__ float2 s_ml[4][ROWS];
   __shared__ __attribute__((aligned(16))) float s_lse[ROWS];
   __shared__ int s_bad;
@@ -317,12 +323,10 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
 
   // the chain's sub-page table as 16-byte vectors (read into registers)
   const int4 *tabv = reinterpret_cast<const int4 *>(a.part + a.tbase[o]);
-  auto issue = [&](Buf &B, int row, int slot) __attribute__((always_inline)) {
-    const char *src = kplane + (int64_t)row * (D * (int)sizeof(T));
-#pragma unroll
-    for (int c = 0; c < KT::NDMA; ++c) load_to_lds16(src + src_off[c], &B.k[1024 * c]);
-    // an unmasked load: every lane fetches position (lane & 15)
-    load_to_lds4(pl.slot_pos + slot + r, &B.pos[0]);
+  // one sub-page: a buffer resource over its BYTES (set up in scalar
+  // registers), so each lane supplies only a 32-bit offset
+  auto issue = [&](Buf &B, int row) __attribute__((always_inline)) {
+    dma_tile<KT::NDMA, KT::BYTES>(kplane + (int64_t)row * (D * (int)sizeof(T)), B.k, src_off);
   };
   auto read_k = [&](const Buf &B, uint4 (&kp)[RQ]) __attribute__((always_inline)) {
 #pragma unroll
@@ -331,22 +335,22 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
   };
 
   // One pass over this wave's sub-pages sp = wave + 4 i (i < cnt) of the
-  // first n_sp of the chain, software-pipelined.  Step i
+  // first n_sp of the chain, software-pipelined over a ring of three LDS
+  // slots.  Step i waits for its own sub-page (the next one may stay in
+  // flight), refills the slot of sub-page i - 1 with sub-page i + 2, reads its
+  // operands, then runs
   //   fix(prev)  rare, branchy corrections of sub-page i - 1 (key masks);
-  //   refills the ring slot freed in the previous step;
   //   mm(kp)     the MFMAs of sub-page i, interleaved in one straight-line
   //   hot(prev)  block with the VALU work of sub-page i - 1, so the matrix
   //              core and the VALU work side by side within the wave;
-  //   post(prev) rare corrections after the fact, and stores;
-  //   then waits for sub-page i + 1 and reads its operands into registers.
+  //   post(prev) rare corrections after the fact, and stores.
   // The table entries of a window of up to 64 steps sit in registers (lane L
   // holds step L) and are read with readlane, so the loop has no scalar loads.
   struct StepState {
     f32x4 acc[NRB];
-    int meta, ctx;
-    int4 kpos;
+    int meta, ctx, slot;
   };
-  auto run = [&](auto pass, int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post)
+  auto run = [&](int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post)
                  __attribute__((always_inline)) {
     const int cnt = n_sp > wave ? (n_sp - wave + 3) / 4 : 0;
     for (int base = 0; base < cnt; base += 64) {
@@ -358,30 +362,23 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
         return __builtin_amdgcn_readlane(v, min(i, wc - 1));
       };
       auto issue_i = [&](Buf &B, int i) __attribute__((always_inline)) {
-        issue(B, ent(i, e.x), ent(i, e.y));
-      };
-      uint4 kp[RQ];
-      int4 kposv;
-      // key positions: pass 0 holds keys 4 q + e of a sub-page, pass 1 key r
-      auto read_i = [&](const Buf &B) __attribute__((always_inline)) {
-        read_k(B, kp);
-        if constexpr (decltype(pass)::value == 0)
-          kposv = *reinterpret_cast<const int4 *>(&B.pos[4 * q]);
-        else
-          kposv = make_int4(B.pos[r], 0, 0, 0);
+        issue(B, ent(i, e.x));
       };
       issue_i(b0[wave], 0);
       issue_i(b1[wave], 1);
-      issue_i(b2[wave], 2);
-      wait_vm<2 * ND>();
-      read_i(b0[wave]);
-      StepState prev = mm(kp, kposv, ent(0, e.w), ent(0, e.z));
-      issue_i(b3[wave], 3);
-      wait_vm<2 * ND>();
-      read_i(b1[wave]);
-      auto body = [&](int i) __attribute__((always_inline)) {
+      StepState prev;
+      {
+        wait_vm<ND>();
+        uint4 kp[RQ];
+        read_k(b0[wave], kp);
+        issue_i(b2[wave], 2);
+        prev = mm(kp, ent(0, e.y), ent(0, e.w), ent(0, e.z));
+      }
+      auto body = [&](const Buf &B, int i) __attribute__((always_inline)) {
+        uint4 kp[RQ];
+        read_k(B, kp);
         fix(prev);
-        const StepState cur = mm(kp, kposv, ent(i, e.w), ent(i, e.z));
+        const StepState cur = mm(kp, ent(i, e.y), ent(i, e.w), ent(i, e.z));
         hot(prev);
 #pragma unroll
         for (int k = 0; k < KS * NRB; ++k) {
@@ -391,40 +388,25 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
         post(prev);
         prev = cur;
       };
-      // whole rounds of four steps in a loop with one exit, so every path
-      // into a step has the same loads in flight
       int i = 1;
-      for (; i + 4 <= wc; i += 4) {
-        issue_i(b0[wave], i + 3);
-        body(i);
-        wait_vm<2 * ND>();
-        read_i(b2[wave]);
-        issue_i(b1[wave], i + 4);
-        body(i + 1);
-        wait_vm<2 * ND>();
-        read_i(b3[wave]);
-        issue_i(b2[wave], i + 5);
-        body(i + 2);
-        wait_vm<2 * ND>();
-        read_i(b0[wave]);
-        issue_i(b3[wave], i + 6);
-        body(i + 3);
-        wait_vm<2 * ND>();
-        read_i(b1[wave]);
+      for (; i + 3 <= wc; i += 3) {
+        wait_vm<ND>();
+        issue_i(b0[wave], i + 2);
+        body(b1[wave], i);
+        wait_vm<ND>();
+        issue_i(b1[wave], i + 3);
+        body(b2[wave], i + 1);
+        wait_vm<ND>();
+        issue_i(b2[wave], i + 4);
+        body(b0[wave], i + 2);
       }
-      // the last one to three sub-pages: their loads are already in flight
-      // (sub-page i in slot 1, i + 1 in slot 2, i + 2 in slot 3)
+      // the last one or two sub-pages (i in slot 1, i + 1 in slot 2)
       if (i < wc) {
-        body(i);
+        wait_vm<ND>();
+        body(b1[wave], i);
         if (i + 1 < wc) {
-          wait_vm<ND>();
-          read_i(b2[wave]);
-          body(i + 1);
-          if (i + 2 < wc) {
-            wait_vm<0>();
-            read_i(b3[wave]);
-            body(i + 2);
-          }
+          wait_vm<0>();
+          body(b2[wave], i + 1);
         }
       }
       fix(prev);
@@ -453,12 +435,12 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
   bool grow = false;
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) nm[rb] = -m[rb] * sl2;
-  run(Ic<0>{}, a.nsp[2 * o],
-      [&](const uint4 (&kp)[RQ], int4 kposv, int meta, int ctx) __attribute__((always_inline)) {
+  run(a.nsp[2 * o],
+      [&](const uint4 (&kp)[RQ], int slot, int meta, int ctx) __attribute__((always_inline)) {
         StepState st;
         st.meta = meta;
         st.ctx = ctx;
-        st.kpos = kposv;
+        st.slot = slot;
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb) st.acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -474,7 +456,14 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
           // a ragged sub-page, or own keys some rows may not see (position > row)
           const int nvalid = st.meta & 255;
           const bool own = ((st.meta >> 8) & 1) != 0;
-          const int kpos[4] = {st.kpos.x, st.kpos.y, st.kpos.z, st.kpos.w};
+          int kpos[4] = {0, 0, 0, 0};
+          if (own) {
+            const int4 pv = *reinterpret_cast<const int4 *>(pl.slot_pos + st.slot + 4 * q);
+            kpos[0] = pv.x;
+            kpos[1] = pv.y;
+            kpos[2] = pv.z;
+            kpos[3] = pv.w;
+          }
 #pragma unroll
           for (int rb = 0; rb < NRB; ++rb) {
             const int ur = urow(rb * 16 + r);
@@ -571,12 +560,12 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
   // ---- pass 1: credited column sums ----
   float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
   float colsum = 0.f;
-  run(Ic<1>{}, a.nsp[2 * o + 1],
-      [&](const uint4 (&kp)[RQ], int4 kposv, int meta, int ctx) __attribute__((always_inline)) {
+  run(a.nsp[2 * o + 1],
+      [&](const uint4 (&kp)[RQ], int slot, int meta, int ctx) __attribute__((always_inline)) {
         StepState st;
         st.meta = meta;
         st.ctx = ctx;
-        st.kpos = kposv;
+        st.slot = slot;
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb) st.acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -589,10 +578,10 @@ __global__ __launch_bounds__(256, 2) void score_attn(ScoreArgs a) {
       },
       [&](StepState &st) __attribute__((always_inline)) {
         if (st.meta & kMask1) {
-          // own tokens are credited only by later rows of the window: this
-          // lane's key r has position kpos[r % 4] of the four it read, so
-          // take it from the lane of the same row group holding key r
-          const int kpos = st.kpos.x;
+          // own tokens are credited only by later rows of the window (this
+          // lane's key is slot r of the sub-page; a rare step, so the
+          // position comes by a plain load)
+          const int kpos = pl.slot_pos[st.slot + r];
 #pragma unroll
           for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
