@@ -326,8 +326,10 @@ def algorithmic_work(st, kv, k_after, n_kept_before, active):
                 union_tokens=union_tok)
 
 
-def cpu_baseline(st, kv_cpu_state, sel_budget_active, work):
-    """Time the oracle on a bounded sample and scale to one full step."""
+def cpu_baseline(st, kv_cpu_state, sel_budget_active, work, reps=2):
+    """Time the oracle on the host cores: `reps` whole steps of the same event (every
+    observer window scored, allocate, select, compact, decode of every active leaf over all
+    layers), on the same input bytes; the value is the mean over the reps."""
     from oracle import arbor_oracle as O
 
     def np_float(t):
@@ -346,54 +348,37 @@ def cpu_baseline(st, kv_cpu_state, sel_budget_active, work):
     t_conv = time.perf_counter() - t0
     parent = st["parent"].numpy()
     V = len(parent)
-    obs_all = st["observers"].tolist()
-    # sample: every 8th observer for the score
-    sample = obs_all[::8]
-    idx = [obs_all.index(j) for j in sample]
-    q = np_float(st["q_win"])[idx]
-    t0 = time.perf_counter()
-    O.score(ost, sample, q, st["window"], st["slice_layers"], st["q_per_kv"],
-            st["v_sig"].numpy(), st["u_sig"].numpy(), np.zeros(st["num_tokens"], np.float32),
-            np.zeros(V, np.int64), theta=st["params"]["theta"])
-    t_score_s = time.perf_counter() - t0
-    W, S, Hq = st["window"], len(st["slice_layers"]), st["kv_heads"] * st["q_per_kv"]
-    n_full = st["n_full"].tolist()
-    samp_pairs = 0
-    for j in sample:
-        ch = _chain(parent.tolist(), j)
-        anc = sum(n_full[a] for a in ch[1:])
-        wj = min(W, n_full[j])
-        samp_pairs += (anc * wj + sum(n_full[j] - wj + t + 1 for t in range(wj))) * S * Hq
-    t_score = t_score_s * work["score_pairs"] / samp_pairs
-    # full-size allocate / select / compact
-    s = np.random.default_rng(0).random(V).astype(np.float32)
+    obs = st["observers"].tolist()
+    q = np_float(st["q_win"])
+    qd = np_float(st["q_dec"])
     active, budget, params = sel_budget_active
-    t0 = time.perf_counter()
-    k, _, _, _ = O.allocate(parent, ost["n_full"], ost["n_kept"], active, budget, s, params)
-    t_alloc = time.perf_counter() - t0
-    A = np.random.default_rng(1).random(st["num_tokens"]).astype(np.float32)
-    t0 = time.perf_counter()
-    sel, _ = O.select(ost, A, k, params["l_tail"])
-    t_select = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    new = O.compact(ost, k, sel)
-    t_compact = time.perf_counter() - t0
-    # decode: all active leaves, 2 of the layers, scaled to all layers
     Lyr = st["layers"]
-    qd = np_float(st["q_dec"])[:, :2]
-    t0 = time.perf_counter()
-    O.tree_decode_attn(new, active, 0, 2, qd, st["q_per_kv"])
-    t_dec = (time.perf_counter() - t0) * Lyr / 2
-    total = t_score + t_alloc + t_select + t_compact + t_dec
+    stage = {"score": 0.0, "allocate": 0.0, "select": 0.0, "compact": 0.0, "decode": 0.0}
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        A, _, _, s = O.score(ost, obs, q, st["window"], st["slice_layers"], st["q_per_kv"],
+                             st["v_sig"].numpy(), st["u_sig"].numpy(),
+                             np.zeros(st["num_tokens"], np.float32), np.zeros(V, np.int64),
+                             theta=st["params"]["theta"])
+        t1 = time.perf_counter()
+        k, _, _, _ = O.allocate(parent, ost["n_full"], ost["n_kept"], active, budget, s, params)
+        t2 = time.perf_counter()
+        sel, _ = O.select(ost, A, k, params["l_tail"])
+        t3 = time.perf_counter()
+        new = O.compact(ost, k, sel)
+        t4 = time.perf_counter()
+        O.tree_decode_attn(new, active, 0, Lyr, qd, st["q_per_kv"])
+        t5 = time.perf_counter()
+        for name, dt in zip(stage, (t1 - t0, t2 - t1, t3 - t2, t4 - t3, t5 - t4)):
+            stage[name] += dt / reps
+    total = sum(stage.values())
     cores = len(os.sched_getaffinity(0))
     return {"value": st["num_tokens"] / total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": (f"oracle score on {len(sample)} of {len(obs_all)} observers "
-                       f"({t_score_s:.1f} s, scaled by scored pairs), full allocate/select/"
-                       f"compact ({t_alloc + t_select + t_compact:.1f} s), decode of all "
-                       f"{len(active)} leaves on 2 of {Lyr} layers ({t_dec * 2 / Lyr:.1f} s, "
-                       f"scaled); estimated {total:.1f} s per step"),
-            "stage_s": {"score": t_score, "allocate": t_alloc, "select": t_select,
-                        "compact": t_compact, "decode": t_dec, "state_to_numpy": t_conv}}
+            "sample": (f"{reps} whole steps of the same event on the same inputs (all "
+                       f"{len(obs)} observer windows scored, allocate, select, compact, decode of "
+                       f"the {len(active)} active leaves over all {Lyr} layers), "
+                       f"{total:.1f} s per step, {reps * total:.1f} s in all"),
+            "stage_s": dict(stage, state_to_numpy=t_conv)}
 
 
 def main():
