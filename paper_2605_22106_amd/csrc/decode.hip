@@ -222,43 +222,53 @@ struct KVFrag {
   static constexpr int NC = D / 16;
   typename Op<T>::reg k[GSP][KS];
   VT v[GSP][4][NC];
-  int nval[GSP];  // valid slots of each sub-page (0: padding, never counted)
+  int nval[GSP];  // valid slots of each sub-page (0: padding, never counted); wave-uniform
+};
+
+// Where a unit's rows live: the (layer, kv head) plane of K and V at page 0,
+// the bytes between pages, and this lane's offsets within a 16-row sub-page.
+struct UnitAddr {
+  const char *k, *v;
+  int64_t page_bytes;
+  int row_bytes;
+  uint32_t koff, voff;
 };
 
 template <class T, int D, int GSP>
-__device__ __forceinline__ KVFrag<T, D, GSP> fetch_kv(const Pool &pl, int pg, int layer, int g,
-                                                      int s_begin, int s_end, int n_sub, int sub0,
-                                                      int rr, int g4) {
+__device__ __forceinline__ KVFrag<T, D, GSP> fetch_kv(const UnitAddr &ua, int pg, int s_begin,
+                                                      int s_end, int n_sub, int sub0, int P) {
   typedef KVFrag<T, D, GSP> F;
   F f;
-  const char *kb = static_cast<const char *>(pl.k);
-  const char *vb = static_cast<const char *>(pl.v);
 #pragma unroll
   for (int sp = 0; sp < GSP; ++sp) {
     // clamped to a valid sub-page so that every load is unconditional
     const int sub = min(sub0 + sp, n_sub - 1);
     const int q0 = s_begin + sub * 16;
     f.nval[sp] = sub0 + sp < n_sub ? min(16, s_end - q0) : 0;
-    const int page = __shfl(pg, sub, kWave);  // lane j holds sub-page j's page
-    const int r0 = q0 % pl.P;
-    const T *kp = reinterpret_cast<const T *>(kb + row_byte_offset(pl, layer, page, g, r0 + rr));
+    // lane j holds sub-page j's page; the page base is wave-uniform
+    const int page = __builtin_amdgcn_readlane(pg, sub);
+    const int64_t base = (int64_t)page * ua.page_bytes + (int64_t)(q0 % P) * ua.row_bytes;
+    const char *kp = ua.k + base + ua.koff;
+    const char *vp = ua.v + base + ua.voff;
 #pragma unroll
-    for (int ks = 0; ks < F::KS; ++ks) f.k[sp][ks] = Op<T>::load(kp + frag_col<T>(ks, g4));
+    for (int ks = 0; ks < F::KS; ++ks)
+      f.k[sp][ks] = Op<T>::load(reinterpret_cast<const T *>(kp + frag_col<T>(ks, 0) * (int)sizeof(T)));
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const typename F::VT *vp = reinterpret_cast<const typename F::VT *>(
-                                     vb + row_byte_offset(pl, layer, page, g, r0 + 4 * g4 + e)) +
-                                 F::NC * rr;
+      const typename F::VT *vr = reinterpret_cast<const typename F::VT *>(vp + e * ua.row_bytes);
 #pragma unroll
-      for (int cc = 0; cc < F::NC; ++cc) f.v[sp][e][cc] = vp[cc];
+      for (int cc = 0; cc < F::NC; ++cc) f.v[sp][e][cc] = vr[cc];
     }
   }
   return f;
 }
 
-// Online-softmax update of one wave's rows with one fragment.
+// Online-softmax update of one wave's rows with one fragment.  Slots past a
+// sub-page's resident count may hold anything: only a ragged sub-page (the
+// last of a node) masks its logits and zeroes its value rows.  The output is
+// rescaled only when some row's running max moved.
 template <class T, int D, int NB, int GSP>
-__device__ __forceinline__ void attend(const KVFrag<T, D, GSP> &f,
+__device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
                                        const typename Op<T>::reg (&q)[NB][KVFrag<T, D, GSP>::KS],
                                        float sl2, int g4, float (&m_run)[NB], float (&l_run)[NB],
                                        f32x4 (&o)[NB][D / 16]) {
@@ -276,25 +286,45 @@ __device__ __forceinline__ void attend(const KVFrag<T, D, GSP> &f,
 #pragma unroll
       for (int ks = 0; ks < F::KS; ++ks) acc = Op<T>::mma(f.k[sp][ks], q[nb][ks], acc);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float z = (4 * g4 + e < f.nval[sp]) ? acc[e] * sl2 : -__builtin_inff();
-        sv[sp][nb][e] = z;
-        gmax[nb] = fmaxf(gmax[nb], z);
-      }
+      for (int e = 0; e < 4; ++e) sv[sp][nb][e] = acc[e] * sl2;
     }
+    if (f.nval[sp] < 16) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          sv[sp][nb][e] = 4 * g4 + e < f.nval[sp] ? sv[sp][nb][e] : -__builtin_inff();
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc)
+          f.v[sp][e][cc] = 4 * g4 + e < f.nval[sp] ? f.v[sp][e][cc] : (typename F::VT)0.f;
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      gmax[nb] = fmaxf(gmax[nb], fmaxf(fmaxf(sv[sp][nb][0], sv[sp][nb][1]),
+                                       fmaxf(sv[sp][nb][2], sv[sp][nb][3])));
   }
+  bool moved = false;
+  float alpha[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     gmax[nb] = across_rows(gmax[nb], [](float x, float y) { return fmaxf(x, y); });
     const float mn = fmaxf(m_run[nb], gmax[nb]);
-    const float alpha = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
+    moved |= mn != m_run[nb];
+    alpha[nb] = (m_run[nb] > -__builtin_inff()) ? __builtin_amdgcn_exp2f(m_run[nb] - mn) : 0.f;
     m_run[nb] = mn;
-    l_run[nb] *= alpha;
+  }
+  if (__builtin_amdgcn_ballot_w64(moved) != 0) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float fe = __shfl(alpha, 4 * g4 + e, kWave);
+    for (int nb = 0; nb < NB; ++nb) {
+      l_run[nb] *= alpha[nb];
 #pragma unroll
-      for (int cc = 0; cc < NC; ++cc) o[nb][cc][e] *= fe;
+      for (int e = 0; e < 4; ++e) {
+        const float fe = __shfl(alpha[nb], 4 * g4 + e, kWave);
+#pragma unroll
+        for (int cc = 0; cc < NC; ++cc) o[nb][cc][e] *= fe;
+      }
     }
   }
 #pragma unroll
@@ -309,13 +339,10 @@ __device__ __forceinline__ void attend(const KVFrag<T, D, GSP> &f,
         l_run[nb] += p[e];
       }
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        // a slot past the resident count may hold anything: its row is zeroed
-        const bool kv = 4 * g4 + ks < f.nval[sp];
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int cc = 0; cc < NC; ++cc)
-          o[nb][cc] = mma_f32(p[ks], kv ? (float)f.v[sp][ks][cc] : 0.f, o[nb][cc]);
-      }
+          o[nb][cc] = mma_f32(p[ks], (float)f.v[sp][ks][cc], o[nb][cc]);
     }
   }
 }
@@ -376,7 +403,18 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
       for (int ks = 0; ks < KS; ++ks) q[nb][ks] = O::zero();
     }
   }
-  F cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, 0, rr, g4);
+  UnitAddr ua;
+  {
+    const int esz = (int)sizeof(T);
+    ua.row_bytes = D * esz;
+    ua.page_bytes = (int64_t)pl.Hkv * pl.P * D * esz;
+    const int64_t plane = ((int64_t)layer * pl.num_pages * pl.Hkv + g) * pl.P * D * esz;
+    ua.k = static_cast<const char *>(pl.k) + plane;
+    ua.v = static_cast<const char *>(pl.v) + plane;
+    ua.koff = (uint32_t)(rr * D * esz + frag_col<T>(0, g4) * esz);
+    ua.voff = (uint32_t)(4 * g4 * D * esz + F::NC * rr * esz);
+  }
+  F cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, 0, pl.P);
   float m_run[NB], l_run[NB];
   f32x4 o[NB][NC];
 #pragma unroll
@@ -390,18 +428,18 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
     // two fragments alternate; the last prefetch of an odd count is a clamped
     // re-read of the final sub-pages with no valid slots
     for (int gi = 0; gi < n_grp; gi += 2) {
-      F nxt = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, (gi + 1) * GSP, rr, g4);
+      F nxt = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 1) * GSP, pl.P);
       // keep the prefetch ahead of the work on the current fragment
       __builtin_amdgcn_sched_barrier(0);
       attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
       if (gi + 1 >= n_grp) break;
-      cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, (gi + 2) * GSP, rr, g4);
+      cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 2) * GSP, pl.P);
       __builtin_amdgcn_sched_barrier(0);
       attend<T, D, NB, GSP>(nxt, q, a.sl2, g4, m_run, l_run, o);
     }
   } else {
     for (int gi = 0; gi < n_grp; ++gi) {
-      if (gi > 0) cur = fetch_kv<T, D, GSP>(pl, pg, layer, g, s_begin, s_end, n_sub, gi * GSP, rr, g4);
+      if (gi > 0) cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
       attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
     }
   }
