@@ -55,6 +55,7 @@ ENTRY_KERNELS = {
     "arbor_compact": ("compact_", "compact.hip"),
     "arbor_tree_decode_attn": ("decode_", "decode.hip"),
     "arbor_rehydrate": ("rehyd_", "rehydrate.hip"),
+    "arbor_uncertainty": ("uncert_", "uncertainty.hip"),
 }
 
 
@@ -187,6 +188,7 @@ def parse():
     ap.add_argument("--config", default="llama8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rehydrate-leg", action="store_true")
+    ap.add_argument("--no-uncertainty-leg", action="store_true")
     ap.add_argument("--summarize-trace", metavar="DB",
                     help="write a per-kernel summary of a rocprofv3 kernel-trace database and exit")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -560,6 +562,38 @@ def main():
                                "nodes": int(np.sum(onp & (n_kept_before < nf))),
                                "status": int(ev.status),
                                "note": "pinned host -> HBM, PCIe-inclusive; not part of value"}
+
+    # Eq. 1 uncertainty at the block boundaries: one logit row per block
+    if not args.no_uncertainty_leg:
+        vocab = 128256
+        z = synth.boundary_logits(kv.num_nodes, vocab, seed=11, dtype="bf16", device="cuda")
+        u = torch.empty(kv.num_nodes, device="cuda")
+        st_u = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ws_u = torch.empty(L.arbor_uncertainty_workspace_size(kv.num_nodes, vocab, L.BF16),
+                           dtype=torch.uint8, device="cuda")
+        leg = {}
+        for top_k in (0, 40):
+            ts = []
+            for rep in range(args.warmup + args.steps):
+                flush.sum()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                ev.check(L.arbor_uncertainty(z, top_k, u, st_u, ws_u))
+                e1.record()
+                torch.cuda.synchronize()
+                if rep >= args.warmup:
+                    ts.append(e0.elapsed_time(e1))
+            t = float(np.mean(ts))
+            # algorithmic bytes: the logits once (the top-K variant reads them
+            # five times: stats, three radix passes, sums)
+            nbytes = z.numel() * 2
+            gbs = nbytes / (t * 1e-3) / 1e9
+            leg["full" if top_k == 0 else f"top{top_k}"] = {
+                "ms": t, "rows": kv.num_nodes, "vocab": vocab, "bytes": nbytes,
+                "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS}
+        leg["status"] = int(st_u)
+        leg["note"] = "arbor_uncertainty over one bf16 logit row per block; not part of value"
+        result["uncertainty"] = leg
 
     if not args.no_cpu_baseline:
         cpu_state = {k: (v.cpu() if isinstance(v, torch.Tensor) else v) for k, v in st.items()

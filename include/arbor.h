@@ -15,6 +15,9 @@
  *   arbor_tree_decode_attn  decode attention of each active leaf over its
  *                           ancestor chain (Sec. 1 and Sec. 3: the next step
  *                           depends only on the chain).
+ *   arbor_uncertainty       normalised next-token entropy u_i at block
+ *                           boundaries (Sec. 4 MSVE, Eq. 1), the input u_in of
+ *                           arbor_score.
  *
  * Conventions
  *  - Every pointer is a DEVICE pointer unless marked (host) or (pinned host).
@@ -60,7 +63,7 @@ typedef enum {
   ARBOR_ENOPAGES = -2,      /* rehydration needs more pages than are free          */
   ARBOR_EHIP = -3,          /* a HIP launch failed                                 */
   ARBOR_EUNSUPPORTED = -4,  /* shape outside what the kernels implement            */
-  ARBOR_ENONFINITE = -5,    /* NaN in A or s                                       */
+  ARBOR_ENONFINITE = -5,    /* NaN in A or s; NaN or infinite logit                */
   ARBOR_EWORKSPACE = -6,    /* workspace too small for this tree                   */
   ARBOR_ECORRUPT = -7       /* pool bookkeeping inconsistent (free stack overflow) */
 } arbor_status_t;
@@ -260,6 +263,33 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
                            int32_t out_dtype, float *lse_out, float softmax_scale,
                            int32_t *status, void *workspace, size_t workspace_bytes,
                            hipStream_t stream);
+
+/*
+ * arbor_uncertainty -- the uncertainty signal of MSVE (Sec. 4, Eq. 1).  Row r of
+ * logits ([n_rows][vocab], dtype ARBOR_BF16 or ARBOR_F32, rows contiguous) is
+ * the next-token logit vector after closing a block; with p = softmax(row):
+ *   top_k = 0 or >= vocab:  H = -sum_w p(w) ln p(w) over the whole vocabulary;
+ *   0 < top_k < vocab:      H = -sum_{top} p ln p - p_o ln p_o over the top_k
+ *                           largest probabilities and one "other" outcome with
+ *                           the remaining mass p_o (omitted when p_o = 0);
+ *   u_out[dst[r]] = 1 - H / ln(vocab)    (dst NULL: u_out[r]).
+ * u_out is fp32 [n_out]; dst int32 [n_rows] (nullable), each in [0, n_out)
+ * (typically the block ids whose u_in arbor_score reads).  The whole-vocabulary
+ * form splits each row over several workgroups and needs `workspace` of at least
+ * arbor_uncertainty_workspace_size(n_rows, vocab, dtype) bytes (the top-K form
+ * needs none).  fp32 arithmetic with a fixed reduction order: bitwise
+ * reproducible.  vocab must be a multiple of 8 (bf16) or 4 (fp32) and logits
+ * 16-byte aligned (EUNSUPPORTED otherwise).
+ * Errors: EINVAL (arguments, a dst entry out of range), ENONFINITE (a NaN or
+ * infinite logit in a row; that row's u is not written), EWORKSPACE.
+ */
+int arbor_uncertainty(const void *logits, int32_t dtype, int32_t n_rows, int64_t vocab,
+                      int32_t top_k, const int32_t *dst, float *u_out, int32_t n_out,
+                      int32_t *status, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream);
+
+/* Bytes of workspace arbor_uncertainty needs for n_rows rows of `vocab` logits. */
+size_t arbor_uncertainty_workspace_size(int32_t n_rows, int64_t vocab, int32_t dtype);
 
 /*
  * arbor_set_kernel_events -- timing support for callers that measure one

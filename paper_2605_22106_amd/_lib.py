@@ -88,6 +88,9 @@ def load() -> ctypes.CDLL:
             "arbor_rehydrate": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_tree_decode_attn": (ctypes.c_int, [G, T, Pl, vp, i32, i32, i32, vp, vp, i32,
                                                       vp, ctypes.c_float, vp, vp, sz, vp]),
+            "arbor_uncertainty": (ctypes.c_int, [vp, i32, i32, i64, i32, vp, vp, i32, vp, vp, sz,
+                                                 vp]),
+            "arbor_uncertainty_workspace_size": (sz, [i32, i64, i32]),
             "arbor_set_kernel_events": (ctypes.c_int, [i32, vp, vp]),
         }
         for name, (res, args) in sig.items():
@@ -101,7 +104,7 @@ def load() -> ctypes.CDLL:
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
             "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn",
-            "arbor_set_kernel_events"]
+            "arbor_uncertainty", "arbor_uncertainty_workspace_size", "arbor_set_kernel_events"]
 
 
 def _dev(t: torch.Tensor | None, name: str):
@@ -281,6 +284,26 @@ def arbor_tree_decode_attn(kv: KVState, leaves, layer_begin, layer_end, q, out, 
                                          float(softmax_scale), _dev(status, "status"),
                                          _dev(workspace, "workspace"), int(workspace.numel()),
                                          _stream(stream))
+
+
+def arbor_uncertainty_workspace_size(n_rows: int, vocab: int, dtype: int) -> int:
+    return int(load().arbor_uncertainty_workspace_size(int(n_rows), int(vocab), int(dtype)))
+
+
+def arbor_uncertainty(logits, top_k, u_out, status, workspace, dst=None, stream=None) -> int:
+    """u_out[dst[r]] (or u_out[r]) = 1 - H / ln(vocab) of row r of `logits`
+    ([n_rows, vocab], bf16 or fp32), H over the whole row or its top_k plus one
+    "other" outcome."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [n_rows, vocab]")
+    if logits.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("logits must be bfloat16 or float32")
+    dtype = BF16 if logits.dtype == torch.bfloat16 else F32
+    return load().arbor_uncertainty(_dev(logits, "logits"), dtype, int(logits.shape[0]),
+                                    int(logits.shape[1]), int(top_k), _dev(dst, "dst"),
+                                    _dev(u_out, "u_out"), int(u_out.numel()),
+                                    _dev(status, "status"), _dev(workspace, "workspace"),
+                                    int(workspace.numel()), _stream(stream))
 
 
 def arbor_set_kernel_events(kernel: int, start=None, stop=None) -> int:

@@ -21,6 +21,9 @@ int launch_rehydrate(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const
 int launch_decode(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t *,
                   const int32_t *, int32_t, int32_t, int32_t, const void *, void *, int32_t,
                   float *, float, int32_t *, void *, size_t, hipStream_t);
+int launch_uncertainty(const void *, int32_t, int32_t, int64_t, int32_t, const int32_t *, float *,
+                       int32_t, int32_t *, void *, size_t, hipStream_t);
+size_t uncertainty_workspace(int32_t, int64_t, int32_t);
 size_t score_workspace(const arbor_geom_t *, const arbor_sizes_t *);
 size_t allocate_workspace(const arbor_sizes_t *);
 size_t compact_workspace(const arbor_sizes_t *);
@@ -178,6 +181,27 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
   return launch_decode(geom, tree, pool, leaves, n_leaves, layer_begin, layer_end, q, out,
                        out_dtype, lse_out, softmax_scale, status, workspace, workspace_bytes,
                        stream);
+}
+
+size_t arbor_uncertainty_workspace_size(int32_t n_rows, int64_t vocab, int32_t dtype) {
+  if (n_rows < 0 || vocab < 2) return 0;
+  return uncertainty_workspace(n_rows, vocab, dtype);
+}
+
+int arbor_uncertainty(const void *logits, int32_t dtype, int32_t n_rows, int64_t vocab,
+                      int32_t top_k, const int32_t *dst, float *u_out, int32_t n_out,
+                      int32_t *status, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream) {
+  if (!status || !u_out || n_rows < 0 || (n_rows > 0 && !logits)) return ARBOR_EINVAL;
+  if (vocab < 2 || top_k < 0 || n_out < 0 || (!dst && n_rows > n_out)) return ARBOR_EINVAL;
+  if (dtype != ARBOR_BF16 && dtype != ARBOR_F32) return ARBOR_EUNSUPPORTED;
+  // rows are read as 16-byte vectors
+  const int64_t per16 = dtype == ARBOR_BF16 ? 8 : 4;
+  if (vocab % per16 != 0 || reinterpret_cast<uintptr_t>(logits) % 16 != 0 ||
+      vocab > ((int64_t)1 << 31))
+    return ARBOR_EUNSUPPORTED;
+  return launch_uncertainty(logits, dtype, n_rows, vocab, top_k, dst, u_out, n_out, status,
+                            workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

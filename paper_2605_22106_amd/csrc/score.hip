@@ -19,12 +19,9 @@
 //           sums of exp2(z - lse) -> one partial per credited context key;
 //   fold    per observer: sum its (slice layer, kv head, row group) partials;
 //   reduce  per block i and 64-slot chunk: sum the folded partials of every
-//           observer below i in observer order (fp64) into A, rows_seen; the
-//           last workgroup of block i then computes a_i = sum_p A_i(p) /
-//           rows_seen_i and s_i = clip(sigmoid(theta.phi)) (with no observers,
-//           a small kernel computes them from A alone).
-// No atomics in any sum (one counter only picks the last workgroup), so A is
-// bitwise reproducible.  The reduction dimension
+//           observer below i in observer order (fp64) into A, rows_seen;
+//   final   a_i = sum_p A_i(p) / rows_seen_i, s_i = clip(sigmoid(theta.phi)).
+// No atomics anywhere, so A is bitwise reproducible.  The reduction dimension
 // (head_dim) is permuted identically in both MFMA operands so that every lane
 // reads one contiguous quarter of a K or Q row (64 B for bf16 d = 128).
 #include "arbor_internal.h"
@@ -56,7 +53,6 @@ struct ScoreArgs {
   const int32_t *ctxlen;  // [n_obs]
   const int32_t *odepth;  // [n_obs]
   const int32_t *anc;     // [n_obs][MAXD]
-  int32_t *done;          // [V]: workgroups of score_reduce finished per block
   int32_t *status;
 };
 
@@ -672,7 +668,6 @@ __global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap
   __syncthreads();
   if (me == 0) {
     for (int i = tid; i < t.V; i += blockDim.x) {
-      a.done[i] = 0;
       const int par = t.parent[i];
       const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
       const int c = t.n_kept[i];
@@ -811,7 +806,7 @@ struct FinalArgs {
 // 64-slot chunk and are combined in wave order.
 __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *__restrict__ fbase,
                                                     float *__restrict__ A,
-                                                    int64_t *__restrict__ rows_seen, FinalArgs fa) {
+                                                    int64_t *__restrict__ rows_seen) {
   __shared__ int64_t hbase[256];
   __shared__ int s_wcnt[4];
   __shared__ double s_acc[4][64];
@@ -884,22 +879,6 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
     rows_add = block_sum<int64_t>(rows_add, reinterpret_cast<int64_t *>(&s_acc[0][0]));
     if (threadIdx.x == 0) rows_seen[i] += rows_add;
   }
-  // the last of block i's workgroups to finish computes a_i and s_i (the
-  // counter orders nothing that enters a sum; it is zeroed by score_setup and
-  // again here, for the next call)
-  __shared__ int s_last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    s_last = atomicAdd(&a.done[i], 1) == (int)gridDim.y - 1;
-  }
-  __syncthreads();
-  if (s_last) {
-    __threadfence();
-    if (threadIdx.x < kWave)
-      block_final(t, i, A, rows_seen, fa.v_in, fa.u_in, fa.th0, fa.th1, fa.th2, fa.a_out, fa.s_out);
-    if (threadIdx.x == 0) a.done[i] = 0;
-  }
 }
 
 // a_i and s_i from the updated A (one wave per block).
@@ -955,7 +934,7 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
   // offsets, counts, chains (each carve rounds up to 256 B)
-  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + (size_t)sz->num_nodes * 4 + 9 * 256;
+  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + 8 * 256;
   // partials and their folded sums
   b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
   // sub-page tables: at most one ragged sub-page per chain node
@@ -999,7 +978,6 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   int32_t *ctxlen = cv.take<int32_t>(nobs);
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
-  int32_t *done = cv.take<int32_t>((size_t)t.V);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   float *part = reinterpret_cast<float *>(cv.rest());
   const int64_t part_cap = (int64_t)(cv.remaining() / 4);
@@ -1010,7 +988,6 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.ctxlen = ctxlen;
   a.odepth = odepth;
   a.anc = anc;
-  a.done = done;
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
     hipLaunchKernelGGL(score_setup, dim3(n_obs), dim3(256), 0, stream, a, part_cap, pbase, fbase,
@@ -1021,12 +998,10 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
     launch_attn(geom->dtype, geom->head_dim, NRB, grid, stream, a);
     timing_end(ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
-    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen,
-                       fa);
-  } else {
-    hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen,
-                       fa, status);
+    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen);
   }
+  hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen, fa,
+                     status);
   return hip_ok(hipGetLastError());
 }
 

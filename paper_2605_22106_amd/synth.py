@@ -282,6 +282,26 @@ def build_config(cfg: Config | str, device="cpu", **overrides):
     return st
 
 
+def boundary_logits(n_rows: int, vocab: int, seed: int, dtype="bf16", device="cpu"):
+    """Seeded next-token logit rows standing in for a model's output at block
+    boundaries: rows cycle through flat (std 0.5), spread (std 2), peaked (std 2
+    with one token raised by 12) and coarsely quantised rows (std 2 rounded to
+    multiples of 0.5, so many logits tie, also at any top-K boundary)."""
+    g = _gen(seed, 17, "cpu")
+    z = torch.randn(n_rows, vocab, generator=g, dtype=torch.float32)
+    for r in range(n_rows):
+        kind = r % 4
+        if kind == 0:
+            z[r] *= 0.5
+        else:
+            z[r] *= 2.0
+        if kind == 2:
+            z[r, int(torch.randint(vocab, (1,), generator=g))] += 12.0
+        if kind == 3:
+            z[r] = torch.round(z[r] * 2.0) / 2.0
+    return z.to(_torch_dtype(dtype)).to(device)
+
+
 def walk_targets(parent, steps: int, p_backtrack: float, seed: int, start: int):
     """Random walk over the tree: with probability p backtrack to a uniform proper
     ancestor and step into one of its children off the current path, otherwise

@@ -224,3 +224,28 @@ def test_uncertainty_eq1():
     # top-K with "other": 4 equal logits, K=2 -> outcomes (1/4, 1/4, 1/2)
     H2 = -(2 * 0.25 * math.log(0.25) + 0.5 * math.log(0.5))
     assert O.uncertainty(np.zeros(4), top_k=2) == pytest.approx(1 - H2 / math.log(4))
+
+
+def test_uncertainty_top_k_against_hand_computed_outcomes():
+    # distinct probabilities 0.5, 0.3, 0.15, 0.05 with K = 2: outcomes 0.5, 0.3, other 0.2
+    z = [math.log(0.5), math.log(0.3), math.log(0.15), math.log(0.05)]
+    H = -(0.5 * math.log(0.5) + 0.3 * math.log(0.3) + 0.2 * math.log(0.2))
+    assert O.uncertainty(z, top_k=2) == pytest.approx(1 - H / math.log(4), abs=1e-12)
+    # a tie at the K-th value: [e, 1, 1, 1] / S with K = 2 keeps e and one of the 1s
+    z = [1.0, 0.0, 0.0, 0.0]
+    S = math.e + 3
+    p1, p0 = math.e / S, 1 / S
+    H = -(p1 * math.log(p1) + p0 * math.log(p0) + 2 * p0 * math.log(2 * p0))
+    assert O.uncertainty(z, top_k=2) == pytest.approx(1 - H / math.log(4), abs=1e-12)
+
+
+def test_uncertainty_top_k_is_a_coarsening():
+    # merging outcomes into "other" can only lower the entropy, and K >= |V| is the full sum
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        z = rng.normal(0, rng.uniform(0.2, 4.0), size=int(rng.integers(2, 300)))
+        full = O.uncertainty(z)
+        assert 0.0 <= full <= 1.0 + 1e-12
+        for k in (1, 3, len(z) - 1):
+            assert O.uncertainty(z, top_k=k) >= full - 1e-12
+        assert O.uncertainty(z, top_k=len(z)) == pytest.approx(full, abs=1e-12)
