@@ -125,6 +125,10 @@ typedef struct {
   int32_t select_mode;       /* arbor_select_mode_t                                 */
   int32_t score_self_window; /* 0: credit proper ancestors only (u > b_i);
                                 1: also an observer's own earlier tokens            */
+  int32_t lazy_rehydration;  /* 1: Path* blocks are restored to full retention
+                                (arbor_rehydrate) and count n_i; 0: evicted tokens
+                                stay lost for the episode, Path* blocks keep (and
+                                count) their resident c_i                           */
 } arbor_params_t;
 
 /* (host) Upper bounds used to size the workspace. */
@@ -181,7 +185,8 @@ int arbor_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_
  * Path* = union of the root-to-leaf chains of active[0 .. n_active) (device
  * int32).  delta_out[i] = tree distance from i to the nearest active leaf,
  * on_path_out[i] = 1 on Path* (uint8).  Path* nodes get k = n_i (invariant
- * (i)).  Every other node i gets Eq. 3 at its Eq. 2 ratio
+ * (i)), or k = c_i when params->lazy_rehydration = 0 (no restoring).  Every
+ * other node i gets Eq. 3 at its Eq. 2 ratio
  * r_i = clip(alpha w_i, r_min, 1), w_i = eta s_i^gamma e^{-lambda_d d_i}
  * e^{-lambda_delta Delta_i}, capped at its resident count c_i (off-path blocks
  * are only ever lowered), where alpha is the largest value <= alpha_max whose

@@ -247,7 +247,9 @@ def floor_count(n, c, p):
 def allocate(parent, n_full, n_kept, active, budget, s, p):
     """Keep-counts k_i under the global token budget B.
 
-    Path* nodes are pinned at k_i = n_i (invariant (i), full protection).  For
+    Path* nodes are pinned at k_i = n_i (invariant (i), full protection), or at
+    their resident count c_i when p["lazy_rehydration"] is 0 (evicted tokens are
+    never restored: the "w/o lazy rehydration" setting of Table 4).  For
     every other node, Eq. 2 gives r_i(alpha) = clip(alpha w_i, r_min, 1) and
     Eq. 3 gives k_i(alpha); an off-path node never re-grows beyond its resident
     count c_i (Alg. 2 only lowers k off the path).  alpha is the one global
@@ -264,10 +266,11 @@ def allocate(parent, n_full, n_kept, active, budget, s, p):
     d, on_path, delta = geometry(parent, active)
     k = np.zeros(V, dtype=np.int64)
     path_total = 0
+    rehyd = int(p.get("lazy_rehydration", 1)) != 0
     for i in range(V):
         if on_path[i]:
-            k[i] = int(n_full[i])
-            path_total += int(n_full[i])
+            k[i] = int(n_full[i]) if rehyd else int(n_kept[i])
+            path_total += int(k[i])
     b_off = int(budget) - path_total
     off = [i for i in range(V) if not on_path[i]]
     F = {i: floor_count(n_full[i], n_kept[i], p) for i in off}

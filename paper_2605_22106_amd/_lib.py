@@ -53,7 +53,8 @@ class Params(ctypes.Structure):
                 ("eta", ctypes.c_double), ("r_min", ctypes.c_double),
                 ("k_min", ctypes.c_int32), ("l_tail", ctypes.c_int32),
                 ("theta", ctypes.c_float * 3), ("softmax_scale", ctypes.c_float),
-                ("select_mode", ctypes.c_int32), ("score_self_window", ctypes.c_int32)]
+                ("select_mode", ctypes.c_int32), ("score_self_window", ctypes.c_int32),
+                ("lazy_rehydration", ctypes.c_int32)]
 
 
 class Sizes(ctypes.Structure):
@@ -129,7 +130,7 @@ def params_struct(p: dict, softmax_scale: float = 0.0) -> Params:
                   float(p["lambda_delta"]), float(p["eta"]), float(p["r_min"]), int(p["k_min"]),
                   int(p["l_tail"]), (ctypes.c_float * 3)(*[float(x) for x in th]),
                   float(p.get("softmax_scale", softmax_scale)), int(p.get("select_mode", 0)),
-                  int(p.get("score_self_window", 0)))
+                  int(p.get("score_self_window", 0)), int(p.get("lazy_rehydration", 1)))
 
 
 @dataclass

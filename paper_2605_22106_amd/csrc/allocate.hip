@@ -46,6 +46,7 @@ constexpr int kDecay = 128;                    // tabulated depths and distances
 struct AllocParams {
   double alpha_max, gamma, lambda_d, lambda_delta, eta, r_min;
   int k_min, l_tail;
+  int rehydrate;   // Path* blocks count n_i (restored) or their resident c_i
   double dexp[kDecay], texp[kDecay];
 };
 
@@ -393,8 +394,11 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     const int c = nd.n_kept[i];
     if (in_lds) on_path[i] = nd.path[i];
     if (nd.path[i]) {
-      k_out[i] = n;
-      path_tok += n;
+      // pinned (invariant (i)): restored to n_i, or kept at c_i when evicted
+      // tokens stay lost
+      const int kp = p.rehydrate ? n : c;
+      k_out[i] = kp;
+      path_tok += kp;
       nd.F[i] = 0;
       nd.W[i] = 0.0;
       nd.w[i] = 0.0;
@@ -701,7 +705,8 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   ws.buf_cap = t.N;
   if (!cv.ok) return ARBOR_EWORKSPACE;
   AllocParams p{params->alpha_max, params->gamma, params->lambda_d, params->lambda_delta,
-                params->eta, params->r_min, params->k_min, params->l_tail, {}, {}};
+                params->eta, params->r_min, params->k_min, params->l_tail,
+                params->lazy_rehydration, {}, {}};
   for (int i = 0; i < kDecay; ++i) {
     p.dexp[i] = exp(-params->lambda_d * (double)i);
     p.texp[i] = exp(-params->lambda_delta * (double)i);

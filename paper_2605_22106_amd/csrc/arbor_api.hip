@@ -124,7 +124,8 @@ int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_ac
   if (!(params->eta > 0.0 && params->eta <= 1.0) || params->k_min < 0 || params->l_tail < 0 ||
       !(params->r_min >= 0.0 && params->r_min <= 1.0) || isnan(params->gamma) ||
       isnan(params->lambda_d) || isnan(params->lambda_delta) || isnan(params->alpha_max) ||
-      !(params->alpha_max > 0.0))
+      !(params->alpha_max > 0.0) ||
+      (params->lazy_rehydration != 0 && params->lazy_rehydration != 1))
     return ARBOR_EINVAL;
   return launch_allocate(tree, active, n_active, budget_tokens, s, params, k_out, delta_out,
                          on_path_out, status, workspace, workspace_bytes, stream);

@@ -31,7 +31,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(L.Geom) == 32
     assert ctypes.sizeof(L.TreeS) == 64
     assert ctypes.sizeof(L.PoolS) == 40
-    assert ctypes.sizeof(L.Params) == 80
+    assert ctypes.sizeof(L.Params) == 88
     assert ctypes.sizeof(L.Sizes) == 48
 
 

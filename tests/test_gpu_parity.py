@@ -48,6 +48,15 @@ def rand_A(N, seed, ties=True):
 # --------------------------------------------------------------------------- allocate
 @pytest.mark.parametrize("seed", range(10))
 def test_allocate_bit_exact(seed):
+    run_allocate_bit_exact(seed, dict(PARAMS))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_allocate_bit_exact_without_rehydration(seed):
+    run_allocate_bit_exact(seed + 50, dict(PARAMS, lazy_rehydration=0))
+
+
+def run_allocate_bit_exact(seed, base):
     st = rand_tree_state(seed, V=60, max_n=50)
     kv = to_gpu(st)
     rng = np.random.default_rng(seed)
@@ -58,7 +67,7 @@ def test_allocate_bit_exact(seed):
     s = rng.random(V).astype(np.float32)
     s[rng.random(V) < 0.1] = 0.0
     s[:5] = s[5]                                  # exact weight ties
-    p = dict(PARAMS)
+    p = dict(base)
     if seed % 3 == 1:
         p["alpha_max"] = 0.9
     ws = workspace(kv)

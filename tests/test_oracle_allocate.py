@@ -32,7 +32,9 @@ def brute_force(parent, n_full, n_kept, active, budget, s, p):
     V = len(parent)
     d, on_path, delta = O.geometry(parent, active)     # geometry is pinned separately
     off = [i for i in range(V) if not on_path[i]]
-    b_off = budget - sum(n_full[i] for i in range(V) if on_path[i])
+    # Path* blocks are pinned: restored to n_i, or kept at c_i without rehydration
+    pinned = n_full if p.get("lazy_rehydration", 1) else n_kept
+    b_off = budget - sum(pinned[i] for i in range(V) if on_path[i])
     W = {i: Fraction(weight(s[i], d[i], delta[i], p)) for i in off}
     rmin = Fraction(p["r_min"])
 
@@ -55,7 +57,7 @@ def brute_force(parent, n_full, n_kept, active, budget, s, p):
             best = a
     k = np.zeros(V, dtype=np.int64)
     for i in range(V):
-        k[i] = n_full[i] if on_path[i] else 0
+        k[i] = pinned[i] if on_path[i] else 0
     if best is not None:
         for i in off:
             k[i] = keep(i, best)
@@ -179,3 +181,25 @@ def test_tiny_config_is_over_budget():
     assert on_path.tolist() == [1, 1, 0, 1, 0, 0, 0]
     assert k.tolist() == [64, 32, 2, 32, 2, 2, 2]
     assert delta.tolist() == [2, 1, 3, 0, 2, 4, 4]
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_allocate_without_rehydration(seed):
+    # evicted Path* tokens stay lost (Table 4's ablation): the path keeps c_i and
+    # counts c_i, and the tokens it no longer holds go to the off-path blocks
+    parent, n_full, n_kept, active, s = random_case(seed + 300)
+    p = dict(BASE, lazy_rehydration=0)
+    V = len(parent)
+    for rho in (0.2, 0.45, 0.7, 1.0):
+        budget = int(rho * sum(n_full))
+        k, _, on_path, status = O.allocate(parent, n_full, n_kept, active, budget, s, p)
+        kb, sb = brute_force(parent, n_full, n_kept, active, budget, s, p)
+        assert status == sb and k.tolist() == kb.tolist()
+        for i in range(V):
+            if on_path[i]:
+                assert k[i] == n_kept[i]
+        if status == O.OK:
+            assert int(np.sum(k)) <= budget
+        k1, *_ = O.allocate(parent, n_full, n_kept, active, budget, s, dict(BASE))
+        off = [i for i in range(V) if not on_path[i]]
+        assert sum(int(k[i]) for i in off) >= sum(int(k1[i]) for i in off)
