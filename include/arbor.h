@@ -168,8 +168,12 @@ const char *arbor_strerror(int code);
  *   s_out[i] = clip(sigmoid(theta[0] v_in[i] + theta[1] u_in[i] + theta[2] a_out[i]), 0, 1).
  * A is fp32 [N] (in/out), rows_seen int64 [V] (in/out), v_in/u_in/a_out/s_out
  * fp32 [V].  slice_layers is a (host) array of n_slice (<= 8) layer ids.
- * Results are bitwise reproducible run to run (no atomics in any sum).
- * Errors: EINVAL (bad ids), EWORKSPACE, EUNSUPPORTED (page_size/head_dim).
+ * Results are bitwise reproducible run to run (no atomics in any sum).  With
+ * n_obs = 0 (observers and q_win may be NULL) A and rows_seen are unchanged
+ * and only a_out, s_out are computed.  On an error status A, rows_seen, a_out
+ * and s_out are left unchanged.
+ * Errors: EINVAL (bad ids), EWORKSPACE, EUNSUPPORTED (page_size/head_dim, an
+ * observer deeper than ARBOR_MAX_DEPTH).
  */
 int arbor_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,
                 const int32_t *observers, int32_t n_obs, const void *q_win, int32_t window,
@@ -259,8 +263,12 @@ int arbor_rehydrate(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *
  * query's own position), q layout [n_leaves][Lr][Hq][head_dim] (dtype), out in
  * out_dtype, lse_out [n_leaves][Lr][Hq] fp32 natural-log LSE (nullable).
  * Each chain node is read once for all active leaves below it; partial results
- * are merged per leaf root to leaf, so results are bitwise reproducible.
- * Errors: EINVAL, EWORKSPACE, EUNSUPPORTED.
+ * are merged per leaf root to leaf, so results are bitwise reproducible.  A
+ * leaf whose chain holds no resident token gets out = 0 and lse = -inf.
+ * n_leaves = 0 (or layer_end = layer_begin) does nothing; leaves, q and out
+ * may then be NULL.
+ * Errors: EINVAL, EWORKSPACE, EUNSUPPORTED (a leaf deeper than
+ * ARBOR_MAX_DEPTH).
  */
 int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
                            const arbor_pool_t *pool, const int32_t *leaves, int32_t n_leaves,

@@ -175,7 +175,7 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
   ARBOR_TRY(check_geom(geom));
   ARBOR_TRY(check_tree(tree));
   ARBOR_TRY(check_pool(pool));
-  if (!status || !leaves || !q || !out || n_leaves < 0) return ARBOR_EINVAL;
+  if (!status || n_leaves < 0 || (n_leaves > 0 && (!leaves || !q || !out))) return ARBOR_EINVAL;
   if (layer_begin < 0 || layer_end > geom->num_layers || layer_end < layer_begin)
     return ARBOR_EINVAL;
   if (out_dtype != ARBOR_BF16 && out_dtype != ARBOR_F32) return ARBOR_EINVAL;
