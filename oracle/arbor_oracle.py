@@ -26,6 +26,9 @@ of the paper it follows:
   tree_decode_attn  Sec. 1/3 (decoding depends only on the active leaf's
                     ancestor chain): softmax attention over the retained keys
                     of the chain
+  decode_credit     Sec. 4 Execution (iii): A_i(t) grown from the attention
+                    weights of the decoding step itself (thin slice of layers,
+                    all heads), credited to proper ancestors of the query's leaf
 
 Readings of points the paper leaves open are listed next to the code that
 takes them.  Parity status: every function here is pinned by the tests in
@@ -500,3 +503,62 @@ def tree_decode_attn(st, leaves, layer_begin, layer_end, q, q_per_kv, softmax_sc
                 o[li, lr, h] = (e @ Vc) / e.sum()
                 lse[li, lr, h] = m + math.log(e.sum())
     return o, lse
+
+
+# ----------------------------------------------------------------------------
+# O8  decode-time credit of accumulated attention  (Sec. 4 Execution (iii))
+# ----------------------------------------------------------------------------
+def decode_credit(st, leaves, layer_begin, q, q_per_kv, slice_layers, A, rows_seen,
+                  self_window=0, softmax_scale=None):
+    """A_i(t) grown from the weights a decoding step already computes.
+
+    The query of leaf l (one per layer of the call and query head, q laid out
+    [leaf][layer - layer_begin][head][d]) sits at the leaf's newest position,
+    after the end b_i of every proper ancestor i, so each of its attention
+    weights on a token of a proper ancestor is a term of A_i(t) (the sum over
+    u > b_i, over the slice layers and all heads).  The weights are the
+    decode softmax over the whole retained chain, the leaf's own tokens
+    included.  rows_seen_i grows by one per (leaf below i, slice layer, head).
+    With self_window = 1 the leaf's own tokens before its newest position
+    (p < n_l - 1) are credited too and the leaf counts its own rows.
+    Returns (A_out fp32, rows_seen_out).
+    """
+    K = st["k"]
+    L, _, Hkv, P, dh = K.shape
+    G = int(q_per_kv)
+    Hq = Hkv * G
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(dh)
+    contrib = np.zeros(len(A), dtype=np.float64)
+    rows_seen = np.asarray(rows_seen, dtype=np.int64).copy()
+    for li, leaf in enumerate(leaves):
+        leaf = int(leaf)
+        ch = chain(st["parent"], leaf)
+        n_leaf = int(st["n_full"][leaf])
+        toks, pages, rs, credit = [], [], [], []
+        for a in ch:
+            for (_, page, r, pos) in retained(st, a):
+                toks.append(int(st["tok_off"][a]) + pos)
+                pages.append(page)
+                rs.append(r)
+                credit.append(a != leaf or (self_window and pos < n_leaf - 1))
+        for a in ch[:-1]:
+            rows_seen[a] += len(slice_layers) * Hq
+        if self_window:
+            rows_seen[leaf] += len(slice_layers) * Hq
+        if not toks:
+            continue
+        toks = np.array(toks)
+        pages = np.array(pages)
+        rs = np.array(rs)
+        credit = np.array(credit, dtype=bool)
+        for l in slice_layers:
+            for h in range(Hq):
+                g = h // G
+                Kc = K[l, pages, g, rs, :].astype(np.float64)
+                z = softmax_scale * (Kc @ q[li, l - layer_begin, h].astype(np.float64))
+                e = np.exp(z - z.max())
+                p = e / e.sum()
+                np.add.at(contrib, toks[credit], p[credit])
+    A_out = (np.asarray(A, dtype=np.float64) + contrib).astype(np.float32)
+    return A_out, rows_seen
