@@ -278,6 +278,46 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
                            hipStream_t stream);
 
 /*
+ * arbor_tree_decode_attn_scored -- arbor_tree_decode_attn that also grows the
+ * accumulated attention A_i(t) from the weights of this decoding step (Sec. 4
+ * Execution (iii): A is kept up to date from attention weights the decoding
+ * already materialises, over a thin slice of layers and all heads).
+ *
+ * Outputs out / lse_out exactly as arbor_tree_decode_attn (bitwise the same
+ * values).  In addition, for every leaf b, slice layer l = slice_layers[s]
+ * (each in [layer_begin, layer_end)) and query head h, the decode softmax
+ * weight of every resident key of a proper ancestor i of the leaf is added to
+ * A[tok_off[i] + position] (the query sits at the leaf's newest position,
+ * after every ancestor's end), and rows_seen[i] grows by n_slice * Hq per leaf
+ * below i.  With self_window = 1 the leaf's own keys at positions below its
+ * newest one (p < n_leaf - 1) are credited too and rows_seen[leaf] grows by
+ * n_slice * Hq.  For leaves with at least one token this equals arbor_score
+ * with the leaves as observers, window 1 and q_win taken from q's slice
+ * layers.  The sums are formed in a fixed order per token (no atomics on A):
+ * bitwise reproducible.  A is fp32 [N] and rows_seen int64 [V], both in/out;
+ * nothing else of the tree or pool changes.
+ */
+typedef struct {
+  const int32_t *slice_layers;  /* (host) n_slice layer ids in [layer_begin, layer_end) */
+  int32_t n_slice;              /* 1..8                                              */
+  int32_t self_window;          /* 0 or 1, as arbor_params_t.score_self_window        */
+  float *A;                     /* device, fp32 [N], in/out                          */
+  int64_t *rows_seen;           /* device, int64 [V], in/out                         */
+} arbor_decode_credit_t;
+
+/* Errors: those of arbor_tree_decode_attn; EINVAL for a slice layer outside
+ * [layer_begin, layer_end), n_slice outside 1..8, self_window not 0 or 1, or A /
+ * rows_seen NULL with n_leaves > 0.  Needs the same workspace as
+ * arbor_tree_decode_attn. */
+int arbor_tree_decode_attn_scored(const arbor_geom_t *geom, const arbor_tree_t *tree,
+                                  const arbor_pool_t *pool, const int32_t *leaves,
+                                  int32_t n_leaves, int32_t layer_begin, int32_t layer_end,
+                                  const void *q, void *out, int32_t out_dtype, float *lse_out,
+                                  float softmax_scale, const arbor_decode_credit_t *credit,
+                                  int32_t *status, void *workspace, size_t workspace_bytes,
+                                  hipStream_t stream);
+
+/*
  * arbor_uncertainty -- the uncertainty signal of MSVE (Sec. 4, Eq. 1).  Row r of
  * logits ([n_rows][vocab], dtype ARBOR_BF16 or ARBOR_F32, rows contiguous) is
  * the next-token logit vector after closing a block; with p = softmax(row):
@@ -324,7 +364,8 @@ typedef enum {
   ARBOR_KERNEL_SELECT = 1,        /* the selection kernel of arbor_select          */
   ARBOR_KERNEL_COMPACT_MOVE = 2,  /* the row-move kernel of arbor_compact          */
   ARBOR_KERNEL_DECODE_ATTN = 3,   /* the attention kernels of arbor_tree_decode_attn */
-  ARBOR_KERNEL_COUNT = 4
+  ARBOR_KERNEL_DECODE_CREDIT = 4, /* the credit kernel of arbor_tree_decode_attn_scored */
+  ARBOR_KERNEL_COUNT = 5
 } arbor_kernel_t;
 
 int arbor_set_kernel_events(int32_t kernel, hipEvent_t start, hipEvent_t stop);

@@ -24,6 +24,7 @@ EINVAL, ENOPAGES, EHIP, EUNSUPPORTED, ENONFINITE, EWORKSPACE, ECORRUPT = -1, -2,
 BF16, F32 = 0, 1
 # kernels whose launches arbor_set_kernel_events can bracket with events
 KERNEL_SCORE_ATTN, KERNEL_SELECT, KERNEL_COMPACT_MOVE, KERNEL_DECODE_ATTN = 0, 1, 2, 3
+KERNEL_DECODE_CREDIT = 4
 SELECT_TAIL_HEAVY, SELECT_TAIL_ONLY = 0, 1
 MAX_DEPTH = 63
 
@@ -55,6 +56,12 @@ class Params(ctypes.Structure):
                 ("theta", ctypes.c_float * 3), ("softmax_scale", ctypes.c_float),
                 ("select_mode", ctypes.c_int32), ("score_self_window", ctypes.c_int32),
                 ("lazy_rehydration", ctypes.c_int32)]
+
+
+class DecodeCredit(ctypes.Structure):
+    _fields_ = [("slice_layers", ctypes.POINTER(ctypes.c_int32)), ("n_slice", ctypes.c_int32),
+                ("self_window", ctypes.c_int32), ("A", ctypes.c_void_p),
+                ("rows_seen", ctypes.c_void_p)]
 
 
 class Sizes(ctypes.Structure):
@@ -89,6 +96,10 @@ def load() -> ctypes.CDLL:
             "arbor_rehydrate": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_tree_decode_attn": (ctypes.c_int, [G, T, Pl, vp, i32, i32, i32, vp, vp, i32,
                                                       vp, ctypes.c_float, vp, vp, sz, vp]),
+            "arbor_tree_decode_attn_scored": (ctypes.c_int,
+                                              [G, T, Pl, vp, i32, i32, i32, vp, vp, i32, vp,
+                                               ctypes.c_float, ctypes.POINTER(DecodeCredit), vp,
+                                               vp, sz, vp]),
             "arbor_uncertainty": (ctypes.c_int, [vp, i32, i32, i64, i32, vp, vp, i32, vp, vp, sz,
                                                  vp]),
             "arbor_uncertainty_workspace_size": (sz, [i32, i64, i32]),
@@ -105,7 +116,7 @@ def load() -> ctypes.CDLL:
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
             "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn",
-            "arbor_uncertainty", "arbor_uncertainty_workspace_size", "arbor_set_kernel_events"]
+            "arbor_tree_decode_attn_scored", "arbor_uncertainty", "arbor_uncertainty_workspace_size", "arbor_set_kernel_events"]
 
 
 def _dev(t: torch.Tensor | None, name: str):
@@ -285,6 +296,28 @@ def arbor_tree_decode_attn(kv: KVState, leaves, layer_begin, layer_end, q, out, 
                                          float(softmax_scale), _dev(status, "status"),
                                          _dev(workspace, "workspace"), int(workspace.numel()),
                                          _stream(stream))
+
+
+def arbor_tree_decode_attn_scored(kv: KVState, leaves, layer_begin, layer_end, q, out, lse_out,
+                                  softmax_scale, slice_layers, self_window, A, rows_seen, status,
+                                  workspace, stream=None) -> int:
+    """arbor_tree_decode_attn plus the decode-time credit of this step's
+    attention weights on the slice layers into A (fp32 [N]) and rows_seen
+    (int64 [V])."""
+    g, t, p = kv.geom(), kv.tree(), kv.pool()
+    out_dtype = BF16 if out.dtype == torch.bfloat16 else F32
+    sl = (ctypes.c_int32 * max(1, len(slice_layers)))(*[int(x) for x in slice_layers])
+    cr = DecodeCredit(sl, len(slice_layers), int(self_window), _dev(A, "A"),
+                      _dev(rows_seen, "rows_seen"))
+    return load().arbor_tree_decode_attn_scored(ctypes.byref(g), ctypes.byref(t),
+                                                ctypes.byref(p), _dev(leaves, "leaves"),
+                                                int(leaves.numel()), int(layer_begin),
+                                                int(layer_end), _dev(q, "q"), _dev(out, "out"),
+                                                out_dtype, _dev(lse_out, "lse_out"),
+                                                float(softmax_scale), ctypes.byref(cr),
+                                                _dev(status, "status"),
+                                                _dev(workspace, "workspace"),
+                                                int(workspace.numel()), _stream(stream))
 
 
 def arbor_uncertainty_workspace_size(n_rows: int, vocab: int, dtype: int) -> int:

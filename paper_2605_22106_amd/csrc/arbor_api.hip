@@ -20,7 +20,8 @@ int launch_rehydrate(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const
                      const void *, const void *, int32_t *, void *, size_t, hipStream_t);
 int launch_decode(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t *,
                   const int32_t *, int32_t, int32_t, int32_t, const void *, void *, int32_t,
-                  float *, float, int32_t *, void *, size_t, hipStream_t);
+                  float *, float, const arbor_decode_credit_t *, int32_t *, void *, size_t,
+                  hipStream_t);
 int launch_uncertainty(const void *, int32_t, int32_t, int64_t, int32_t, const int32_t *, float *,
                        int32_t, int32_t *, void *, size_t, hipStream_t);
 size_t uncertainty_workspace(int32_t, int64_t, int32_t);
@@ -180,8 +181,34 @@ int arbor_tree_decode_attn(const arbor_geom_t *geom, const arbor_tree_t *tree,
     return ARBOR_EINVAL;
   if (out_dtype != ARBOR_BF16 && out_dtype != ARBOR_F32) return ARBOR_EINVAL;
   return launch_decode(geom, tree, pool, leaves, n_leaves, layer_begin, layer_end, q, out,
-                       out_dtype, lse_out, softmax_scale, status, workspace, workspace_bytes,
-                       stream);
+                       out_dtype, lse_out, softmax_scale, nullptr, status, workspace,
+                       workspace_bytes, stream);
+}
+
+int arbor_tree_decode_attn_scored(const arbor_geom_t *geom, const arbor_tree_t *tree,
+                                  const arbor_pool_t *pool, const int32_t *leaves,
+                                  int32_t n_leaves, int32_t layer_begin, int32_t layer_end,
+                                  const void *q, void *out, int32_t out_dtype, float *lse_out,
+                                  float softmax_scale, const arbor_decode_credit_t *credit,
+                                  int32_t *status, void *workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+  ARBOR_TRY(check_geom(geom));
+  ARBOR_TRY(check_tree(tree));
+  ARBOR_TRY(check_pool(pool));
+  if (!status || !credit || n_leaves < 0 || (n_leaves > 0 && (!leaves || !q || !out)))
+    return ARBOR_EINVAL;
+  if (layer_begin < 0 || layer_end > geom->num_layers || layer_end < layer_begin)
+    return ARBOR_EINVAL;
+  if (out_dtype != ARBOR_BF16 && out_dtype != ARBOR_F32) return ARBOR_EINVAL;
+  if (credit->n_slice < 1 || credit->n_slice > 8 || !credit->slice_layers) return ARBOR_EINVAL;
+  for (int e = 0; e < credit->n_slice; ++e)
+    if (credit->slice_layers[e] < layer_begin || credit->slice_layers[e] >= layer_end)
+      return ARBOR_EINVAL;
+  if (credit->self_window != 0 && credit->self_window != 1) return ARBOR_EINVAL;
+  if (n_leaves > 0 && (!credit->A || !credit->rows_seen)) return ARBOR_EINVAL;
+  return launch_decode(geom, tree, pool, leaves, n_leaves, layer_begin, layer_end, q, out,
+                       out_dtype, lse_out, softmax_scale, credit, status, workspace,
+                       workspace_bytes, stream);
 }
 
 size_t arbor_uncertainty_workspace_size(int32_t n_rows, int64_t vocab, int32_t dtype) {

@@ -54,7 +54,18 @@ struct DecArgs {
   int max_parts;
   float *part;
   int64_t part_cap;
+  float *lse2;                // [n_leaves][Lr][Hq] log2-domain LSE (credit calls only)
   int32_t *status;
+};
+
+// The decode-time credit of accumulated attention: slice layers relative to
+// the call's first layer, the crediting mode and the caller's A / rows_seen.
+struct CreditArgs {
+  int S;
+  int slice[8];
+  int self_window;
+  float *A;
+  int64_t *rows_seen;
 };
 
 __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, int32_t *cls_items,
@@ -564,15 +575,123 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 #pragma unroll
       for (int e = 0; e < EPL; ++e) op[64 * e + lane] = ov[e] * inv;
     }
-    if (lse_out && lane == 0)
-      lse_out[((int64_t)b * a.Lr + lr) * Hq + h] =
-          L > 0.f ? (M + __log2f(L)) * kLn2 : -__builtin_inff();
+    if (lane == 0) {
+      const float l2 = L > 0.f ? M + __log2f(L) : -__builtin_inff();
+      const int64_t li = ((int64_t)b * a.Lr + lr) * Hq + h;
+      if (lse_out) lse_out[li] = L > 0.f ? l2 * kLn2 : -__builtin_inff();
+      if (a.lse2) a.lse2[li] = l2;
+    }
+  }
+}
+
+// Decode-time credit (Sec. 4 Execution (iii)): the softmax weight exp2(z -
+// lse2) of every decode query row on every key of a unit, summed over the
+// rows whose leaf lies strictly below the unit's node (and, in the
+// self-window mode, the leaf's own rows on keys before its newest position),
+// over the slice layers and kv heads, and added to A at the key's token.
+// One workgroup per 16-slot sub-page of a unit; its four waves take the
+// (slice layer, kv head) pairs in turn, so each token's sum has one owner and
+// a fixed order.  S = Q K^T puts query rows along M and keys along N: lane
+// (rr, g4) receives rows 4 g4 + e of key rr, so a key's sum over 16 rows is an
+// in-lane sum of four values and one across-rows reduction.  Workgroup 0 also
+// adds the row counts to rows_seen (integer atomics: order-free).
+template <class T, int D>
+__global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
+  using O = Op<T>;
+  constexpr int KS = D / 4 / O::kPerStep;
+  constexpr int SUBS = CHUNK / 16;
+  __shared__ float s_red[4][16];
+  if (status_failed(a.status)) return;
+  const Tree &t = a.t;
+  const Pool &pl = a.pl;
+  const int G = pl.G;
+  const int Hq = pl.Hkv * G;
+  if (blockIdx.x == 0) {
+    const unsigned long long per = (unsigned long long)cr.S * Hq;
+    for (int e = threadIdx.x; e < a.n_leaves * MAXD; e += blockDim.x) {
+      const int b = e / MAXD, d = e % MAXD;
+      const int dl = a.ldepth[b];
+      if (d < dl || (d == dl && cr.self_window))
+        atomicAdd(reinterpret_cast<unsigned long long *>(cr.rows_seen) +
+                      a.lanc[(int64_t)b * MAXD + d],
+                  per);
+    }
+  }
+  const int n_items = a.meta[0] + a.meta[1] + a.meta[2];
+  const int item = blockIdx.x / SUBS;
+  if (item >= n_items) return;
+  const int node = a.item_node[item];
+  const int c = t.n_kept[node];
+  const int s0 = a.item_chunk[item] * CHUNK + (blockIdx.x % SUBS) * 16;
+  if (s0 >= c) return;                        // uniform over the workgroup
+  const int nval = min(16, c - s0);
+  const int lane = lane_id();
+  const int rr = lane & 15;
+  const int g4 = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int R = a.node_nl[node] * G;
+  const int loff = a.node_leaf_off[node];
+  const int page = t.page_table[t.page_off[node] + s0 / pl.P];
+  const int64_t slot = (int64_t)page * pl.P + s0 % pl.P + rr;
+  const int pos = rr < nval ? pl.slot_pos[slot] : 0;
+  // own rows (the node is the row's leaf) are credited only on earlier keys
+  // in the self-window mode
+  const bool own_ok = cr.self_window && rr < nval && pos < t.n_full[node] - 1;
+  const bool key_ok = rr < nval;
+  float sum = 0.f;
+  for (int pr = wave; pr < cr.S * pl.Hkv; pr += 4) {
+    const int lr = cr.slice[pr / pl.Hkv];
+    const int g = pr % pl.Hkv;
+    const int64_t plane = ((int64_t)(a.l0 + lr) * pl.num_pages * pl.Hkv + g) * pl.P * D;
+    const T *kp = static_cast<const T *>(pl.k) + plane +
+                  ((int64_t)page * pl.Hkv * pl.P + s0 % pl.P + rr) * D;
+    typename O::reg kf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) kf[ks] = O::load(kp + frag_col<T>(ks, g4));
+    for (int rb = 0; rb < R; rb += 16) {
+      // operand rows: row rb + rr of this kv head
+      const int qr = rb + rr;
+      typename O::reg qf[KS];
+      if (qr < R) {
+        const int b = a.leaf_list[loff + qr / G];
+        const T *qp = static_cast<const T *>(a.q) +
+                      (((int64_t)b * a.Lr + lr) * Hq + g * G + qr % G) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[ks] = O::load(qp + frag_col<T>(ks, g4));
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[ks] = O::zero();
+      }
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) acc = O::mma(qf[ks], kf[ks], acc);
+      float part = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = rb + 4 * g4 + e;
+        if (row < R && key_ok) {
+          const int b = a.leaf_list[loff + row / G];
+          const bool own = a.leaves[b] == node;
+          if (!own || own_ok) {
+            const float l2 = a.lse2[((int64_t)b * a.Lr + lr) * Hq + g * G + row % G];
+            part += __builtin_amdgcn_exp2f(acc[e] * a.sl2 - l2);
+          }
+        }
+      }
+      sum += across_rows(part, [](float x, float y) { return x + y; });
+    }
+  }
+  if (g4 == 0) s_red[wave][rr] = sum;
+  __syncthreads();
+  if (threadIdx.x < 16 && key_ok) {
+    const float tot = ((s_red[0][rr] + s_red[1][rr]) + s_red[2][rr]) + s_red[3][rr];
+    cr.A[t.tok_off[node] + pos] += tot;
   }
 }
 
 template <class T, int D>
 void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *lse_out,
-                           hipStream_t stream) {
+                           const CreditArgs *cr, hipStream_t stream) {
   const int grid = 2048;
   // rows of a work unit are at most n_leaves * G: only the row classes that
   // can occur are launched
@@ -588,6 +707,14 @@ void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *ls
   const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
   hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
                      lse_out);
+  if (cr) {
+    // one workgroup per possible sub-page of a unit; those past the plan's
+    // units or past a unit's resident slots return at once
+    timing_begin(ARBOR_KERNEL_DECODE_CREDIT, stream);
+    hipLaunchKernelGGL((decode_credit<T, D>), dim3((unsigned)a.max_items * (CHUNK / 16)),
+                       dim3(256), 0, stream, a, *cr);
+    timing_end(ARBOR_KERNEL_DECODE_CREDIT, stream);
+  }
 }
 
 }  // namespace
@@ -607,8 +734,9 @@ size_t decode_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t items = decode_max_items(sz);
   const size_t per_leaf = (size_t)(sz->max_context / CHUNK) + MAXD + 1;
   const size_t rows = nl * per_leaf * g->q_per_kv;
-  size_t b = 18 * 256;
+  size_t b = 19 * 256;
   b += 3 * items * 4 + 3 * items * 4 + V * 4 * 4 + nl * MAXD * 4 * 3 + nl * 4 + nl * MAXD * 4;
+  b += nl * (size_t)sz->max_layers * g->num_kv_heads * g->q_per_kv * 4;   // log2 LSE
   b += nl * 4 + nl * decode_max_parts(sz) * 4;
   b += rows * (size_t)sz->max_layers * g->num_kv_heads * (g->head_dim + 2) * 4;
   return b;
@@ -617,7 +745,8 @@ size_t decode_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
 int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,
                   const int32_t *leaves, int32_t n_leaves, int32_t layer_begin, int32_t layer_end,
                   const void *q, void *out, int32_t out_dtype, float *lse_out, float softmax_scale,
-                  int32_t *status, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+                  const arbor_decode_credit_t *credit, int32_t *status, void *workspace,
+                  size_t workspace_bytes, hipStream_t stream) {
   Tree t = make_tree(tree);
   Pool pl = make_pool(geom, pool);
   if (t.V <= 0 || n_leaves <= 0 || layer_end <= layer_begin) return ARBOR_OK;
@@ -656,7 +785,17 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   const int max_parts = (int)decode_max_parts(&sz);
   int32_t *leaf_np = cv.take<int32_t>(n_leaves);
   int32_t *leaf_part = cv.take<int32_t>((size_t)n_leaves * max_parts);
+  float *lse2 = cv.take<float>((size_t)n_leaves * a.Lr * pl.Hkv * pl.G);
   if (!cv.ok) return ARBOR_EWORKSPACE;
+  CreditArgs cr{};
+  if (credit) {
+    cr.S = credit->n_slice;
+    for (int e = 0; e < 8; ++e) cr.slice[e] = e < credit->n_slice ? credit->slice_layers[e] - layer_begin : 0;
+    cr.self_window = credit->self_window;
+    cr.A = credit->A;
+    cr.rows_seen = credit->rows_seen;
+  }
+  a.lse2 = credit ? lse2 : nullptr;
   a.meta = meta;
   a.cls_items = cls_items;
   a.item_node = item_node;
@@ -679,11 +818,11 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
                      item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list, node_item0,
                      node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part);
   if (geom->dtype == ARBOR_BF16) {
-    if (geom->head_dim == 128) launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, stream);
-    else launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, stream);
+    if (geom->head_dim == 128) launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
+    else launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
   } else {
-    if (geom->head_dim == 128) launch_decode_kernels<float, 128>(a, out, out_dtype, lse_out, stream);
-    else launch_decode_kernels<float, 64>(a, out, out_dtype, lse_out, stream);
+    if (geom->head_dim == 128) launch_decode_kernels<float, 128>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
+    else launch_decode_kernels<float, 64>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
   }
   return hip_ok(hipGetLastError());
 }

@@ -27,12 +27,36 @@ def test_library_exports_every_symbol():
         assert hasattr(lib, name), name
 
 
-def test_struct_layouts():
-    assert ctypes.sizeof(L.Geom) == 32
-    assert ctypes.sizeof(L.TreeS) == 64
-    assert ctypes.sizeof(L.PoolS) == 40
-    assert ctypes.sizeof(L.Params) == 88
-    assert ctypes.sizeof(L.Sizes) == 48
+STRUCTS = {"Geom": "arbor_geom_t", "TreeS": "arbor_tree_t", "PoolS": "arbor_pool_t",
+           "Params": "arbor_params_t", "Sizes": "arbor_sizes_t",
+           "DecodeCredit": "arbor_decode_credit_t"}
+
+
+def test_struct_layouts(tmp_path):
+    """Every binding struct has the C compiler's size and field offsets for
+    the header's struct (a host C program built with gcc prints them)."""
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "arbor.h"', "int main(void) {"]
+    for py, c in STRUCTS.items():
+        lines.append(f'  printf("{py} size %zu\\n", sizeof({c}));')
+        for name, _ in getattr(L, py)._fields_:
+            lines.append(f'  printf("{py} {name} %zu\\n", offsetof({c}, {name}));')
+    lines.append("  return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", "/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True,
+                               text=True).stdout.splitlines():
+        py, name, val = line.split()
+        got[(py, name)] = int(val)
+    for py in STRUCTS:
+        cls = getattr(L, py)
+        assert got[(py, "size")] == ctypes.sizeof(cls), py
+        for name, _ in cls._fields_:
+            assert got[(py, name)] == getattr(cls, name).offset, (py, name)
 
 
 def test_strerror_and_workspace_size_are_host_only():
@@ -54,7 +78,8 @@ def test_product_path_refuses_cpu_tensors():
 def test_kernel_events_setter_validates_on_the_host():
     lib = L.load()
     assert lib.arbor_set_kernel_events(L.KERNEL_SCORE_ATTN, None, None) == L.OK
-    assert lib.arbor_set_kernel_events(4, None, None) == L.EINVAL
+    assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, None, None) == L.OK
+    assert lib.arbor_set_kernel_events(5, None, None) == L.EINVAL
     assert lib.arbor_set_kernel_events(-1, None, None) == L.EINVAL
     # one of the two events missing
     assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_ATTN, ctypes.c_void_p(1), None) == L.EINVAL

@@ -202,6 +202,24 @@ def test_llama8b_event_stage_by_stage(llama8b):
         err = np.abs(out_np[b, layer, h] - o_ref).max()
         assert err <= 2e-3, (b, layer, h, err)
 
+    # decode with the decode-time credit: the same outputs bitwise, and A /
+    # rows_seen against the oracle on the slice layers (the only K it reads)
+    sl = st["slice_layers"]
+    A_in = A.clone()
+    rows_in = rows.clone()
+    out2 = torch.empty_like(out)
+    check_rc(L.arbor_tree_decode_attn_scored(kv, active, 0, kv.layers, q, out2, None, 0.0, sl,
+                                             0, A, rows, stt, ws))
+    torch.cuda.synchronize()
+    assert int(stt) == L.OK
+    assert torch.equal(out2.view(torch.int32), out.view(torch.int32))
+    ost_sl = _meta(kv, k=kv.k[sl].float().cpu().numpy())
+    Ao2, ro2 = O.decode_credit(ost_sl, st["active"].tolist(), 0, np_float(q[:, sl]),
+                               kv.q_per_kv, list(range(len(sl))), A_in.cpu().numpy(),
+                               rows_in.cpu().numpy())
+    _close(A.cpu().numpy(), Ao2)
+    assert np.array_equal(rows.cpu().numpy(), ro2)
+
     # rehydrate: move the frontier to other leaves; restored rows are pristine
     leaves = [i for i in range(V) if i not in parent]
     a0 = set(st["active"].tolist())
