@@ -189,6 +189,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rehydrate-leg", action="store_true")
     ap.add_argument("--no-uncertainty-leg", action="store_true")
+    ap.add_argument("--no-credit-leg", action="store_true",
+                    help="skip timing arbor_tree_decode_attn_scored (decode + A credit)")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch the timed steps eagerly instead of replaying a captured HIP graph")
     ap.add_argument("--summarize-trace", metavar="DB",
@@ -324,10 +326,18 @@ def algorithmic_work(st, kv, k_after, n_kept_before, active):
     qo = 2 * len(active) * Lyr * Hkv * G * d * 2
     decode_bytes = union_tok * row_all_layers + qo
     decode_naive = naive_tok * row_all_layers + qo
+    # decode-time credit: K of the slice layers and A (read + write) for every
+    # key of a proper ancestor of an active leaf, + the slice-layer queries
+    anc = set()
+    for l in active:
+        anc.update(_chain(parent, l)[1:])
+    anc_tok = sum(k_after[a] for a in anc)
+    credit_bytes = (anc_tok * S * Hkv * d * esz + 8 * anc_tok
+                    + len(active) * S * Hkv * G * d * esz)
     return dict(score_flops=score_flops, score_bytes=score_bytes, score_pairs=pairs,
                 compact_bytes=compact_bytes, moved_rows=moved, select_bytes=select_bytes,
                 decode_bytes=decode_bytes, decode_naive_bytes=decode_naive,
-                union_tokens=union_tok)
+                union_tokens=union_tok, credit_bytes=credit_bytes)
 
 
 def cpu_baseline(st, kv_cpu_state, sel_budget_active, work, reps=2):
@@ -563,6 +573,49 @@ def main():
         "eager_ms_per_step": eager_ms,
         "status": status,
     }
+
+    # decode that also credits its slice-layer attention weights to A, on the
+    # state the step leaves behind, beside the plain decode timed the same way
+    if not args.no_credit_leg:
+        restore()
+        ev.run(active)
+        torch.cuda.synchronize()
+        ce = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        for e in ce:
+            e.record()          # torch refuses elapsed_time on events it never recorded
+        ev.check(L.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, *ce))
+        t_sc, t_pl, t_k = [], [], []
+        for rep in range(args.warmup + args.steps):
+            for scored in (True, False):
+                flush.sum()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                if scored:
+                    ev.check(L.arbor_tree_decode_attn_scored(
+                        kv, active, 0, kv.layers, ev.q_dec, ev.out, ev.lse, 0.0,
+                        st["slice_layers"], 0, ev.A, ev.rows, ev.status, ev.ws))
+                else:
+                    ev.check(L.arbor_tree_decode_attn(kv, active, 0, kv.layers, ev.q_dec, ev.out,
+                                                      ev.lse, 0.0, ev.status, ev.ws))
+                e1.record()
+                torch.cuda.synchronize()
+                if rep >= args.warmup:
+                    (t_sc if scored else t_pl).append(e0.elapsed_time(e1))
+                    if scored:
+                        t_k.append(ce[0].elapsed_time(ce[1]))
+        ev.check(L.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, None, None))
+        if int(ev.status) < 0:
+            raise RuntimeError(f"device status {int(ev.status)}")
+        tk = float(np.mean(t_k))
+        cb = work["credit_bytes"]
+        result["decode_scored"] = {
+            "ms": float(np.mean(t_sc)), "plain_decode_ms": float(np.mean(t_pl)),
+            "credit_kernel_ms": tk, "credit_bytes": cb,
+            "credit_achieved": cb / (tk * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "credit_frac": cb / (tk * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "slice_layers": list(st["slice_layers"]),
+            "note": "arbor_tree_decode_attn_scored (decode + decode-time credit of A); "
+                    "not part of value"}
 
     # backtracking transition with lazy rehydration from pinned host memory
     if not args.no_rehydrate_leg:

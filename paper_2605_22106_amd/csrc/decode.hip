@@ -589,23 +589,118 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 // rows whose leaf lies strictly below the unit's node (and, in the
 // self-window mode, the leaf's own rows on keys before its newest position),
 // over the slice layers and kv heads, and added to A at the key's token.
-// One workgroup per 16-slot sub-page of a unit; its four waves take the
-// (slice layer, kv head) pairs in turn, so each token's sum has one owner and
-// a fixed order.  S = Q K^T puts query rows along M and keys along N: lane
-// (rr, g4) receives rows 4 g4 + e of key rr, so a key's sum over 16 rows is an
-// in-lane sum of four values and one across-rows reduction.  Workgroup 0 also
-// adds the row counts to rows_seen (integer atomics: order-free).
+// Workgroups stride over the 16-slot sub-pages of the units; the four waves
+// of a workgroup take the (slice layer, kv head) pairs of a sub-page in turn,
+// so each token's sum has one owner and a fixed order.  S = Q K^T puts query
+// rows along M and keys along N: lane (rr, g4) receives rows 4 g4 + e of key
+// rr, so a key's sum over 16 rows is an in-lane sum of four values and one
+// across-rows reduction.  Workgroup 0 also adds the row counts to rows_seen
+// (integer atomics: order-free).
+//
+// The credit of one sub-page (item, sub) of a unit.  Every return is uniform
+// over the workgroup.
 template <class T, int D>
-__global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
+__device__ __forceinline__ void credit_subpage(const DecArgs &a, const CreditArgs &cr, int item,
+                                               int sub, float (&s_red)[4][16]) {
   using O = Op<T>;
   constexpr int KS = D / 4 / O::kPerStep;
-  constexpr int SUBS = CHUNK / 16;
-  __shared__ float s_red[4][16];
-  if (status_failed(a.status)) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
   const int G = pl.G;
   const int Hq = pl.Hkv * G;
+  const int node = a.item_node[item];
+  const int c = t.n_kept[node];
+  const int s0 = a.item_chunk[item] * CHUNK + sub * 16;
+  if (s0 >= c) return;                        // uniform over the workgroup
+  const int R = a.node_nl[node] * G;
+  const int loff = a.node_leaf_off[node];
+  const int nval = min(16, c - s0);
+  const int lane = lane_id();
+  const int rr = lane & 15;
+  const int g4 = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int page = t.page_table[t.page_off[node] + s0 / pl.P];
+  const int64_t slot = (int64_t)page * pl.P + s0 % pl.P + rr;
+  const bool key_ok = rr < nval;
+  const int pos = key_ok ? pl.slot_pos[slot] : 0;
+  const int64_t tok = t.tok_off[node] + pos;
+  const float a_old = key_ok ? cr.A[tok] : 0.f;   // fetched early, added last
+  // own rows (the node is the row's leaf) are credited only on earlier keys
+  // in the self-window mode
+  const bool own_ok = cr.self_window && key_ok && pos < t.n_full[node] - 1;
+  const int npairs = cr.S * pl.Hkv;
+  // pairs per wave per pass: the K and Q fragments of all of them are loaded
+  // before the first is used, so one memory round trip covers the pass
+  constexpr int PPW = KS >= 16 ? 1 : 16 / KS;
+  float sum = 0.f;
+  for (int rb = 0; rb < R; rb += 16) {
+    // the query row this lane supplies, and the four output rows it receives
+    const int qr = rb + rr;
+    const int qb = qr < R ? a.leaf_list[loff + qr / G] : -1;
+    int ob[4];
+    bool ocr[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = rb + 4 * g4 + e;
+      ob[e] = row < R ? a.leaf_list[loff + row / G] : -1;
+      ocr[e] = ob[e] >= 0 && key_ok && (a.leaves[ob[e]] != node || own_ok);
+    }
+    for (int p0 = wave * PPW; p0 < npairs; p0 += 4 * PPW) {
+      typename O::reg kf[PPW][KS], qf[PPW][KS];
+      float l2[PPW][4];
+#pragma unroll
+      for (int j = 0; j < PPW; ++j) {
+        const int pr = min(p0 + j, npairs - 1);   // clamped: every load stays in bounds
+        const int lr = cr.slice[pr / pl.Hkv];
+        const int g = pr % pl.Hkv;
+        const T *kp = static_cast<const T *>(pl.k) +
+                      (((int64_t)(a.l0 + lr) * pl.num_pages + page) * pl.Hkv + g) * pl.P * D +
+                      (int64_t)(s0 % pl.P + rr) * D;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) kf[j][ks] = O::load(kp + frag_col<T>(ks, g4));
+        if (qb >= 0) {
+          const T *qp = static_cast<const T *>(a.q) +
+                        (((int64_t)qb * a.Lr + lr) * Hq + g * G + qr % G) * D;
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) qf[j][ks] = O::load(qp + frag_col<T>(ks, g4));
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) qf[j][ks] = O::zero();
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = rb + 4 * g4 + e;
+          l2[j][e] = ocr[e] ? a.lse2[((int64_t)ob[e] * a.Lr + lr) * Hq + g * G + row % G] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < PPW; ++j) {
+        if (p0 + j >= npairs) break;             // wave-uniform
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) acc = O::mma(qf[j][ks], kf[j][ks], acc);
+        float part = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          part += ocr[e] ? __builtin_amdgcn_exp2f(acc[e] * a.sl2 - l2[j][e]) : 0.f;
+        sum += across_rows(part, [](float x, float y) { return x + y; });
+      }
+    }
+  }
+  if (g4 == 0) s_red[wave][rr] = sum;
+  __syncthreads();
+  if (threadIdx.x < 16 && key_ok) {
+    const float tot = ((s_red[0][rr] + s_red[1][rr]) + s_red[2][rr]) + s_red[3][rr];
+    cr.A[tok] = a_old + tot;
+  }
+}
+
+template <class T, int D>
+__global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
+  constexpr int SUBS = CHUNK / 16;
+  __shared__ float s_red[4][16];
+  if (status_failed(a.status)) return;
+  const int Hq = a.pl.Hkv * a.pl.G;
   if (blockIdx.x == 0) {
     const unsigned long long per = (unsigned long long)cr.S * Hq;
     for (int e = threadIdx.x; e < a.n_leaves * MAXD; e += blockDim.x) {
@@ -618,74 +713,9 @@ __global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
     }
   }
   const int n_items = a.meta[0] + a.meta[1] + a.meta[2];
-  const int item = blockIdx.x / SUBS;
-  if (item >= n_items) return;
-  const int node = a.item_node[item];
-  const int c = t.n_kept[node];
-  const int s0 = a.item_chunk[item] * CHUNK + (blockIdx.x % SUBS) * 16;
-  if (s0 >= c) return;                        // uniform over the workgroup
-  const int nval = min(16, c - s0);
-  const int lane = lane_id();
-  const int rr = lane & 15;
-  const int g4 = lane >> 4;
-  const int wave = threadIdx.x >> 6;
-  const int R = a.node_nl[node] * G;
-  const int loff = a.node_leaf_off[node];
-  const int page = t.page_table[t.page_off[node] + s0 / pl.P];
-  const int64_t slot = (int64_t)page * pl.P + s0 % pl.P + rr;
-  const int pos = rr < nval ? pl.slot_pos[slot] : 0;
-  // own rows (the node is the row's leaf) are credited only on earlier keys
-  // in the self-window mode
-  const bool own_ok = cr.self_window && rr < nval && pos < t.n_full[node] - 1;
-  const bool key_ok = rr < nval;
-  float sum = 0.f;
-  for (int pr = wave; pr < cr.S * pl.Hkv; pr += 4) {
-    const int lr = cr.slice[pr / pl.Hkv];
-    const int g = pr % pl.Hkv;
-    const int64_t plane = ((int64_t)(a.l0 + lr) * pl.num_pages * pl.Hkv + g) * pl.P * D;
-    const T *kp = static_cast<const T *>(pl.k) + plane +
-                  ((int64_t)page * pl.Hkv * pl.P + s0 % pl.P + rr) * D;
-    typename O::reg kf[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kf[ks] = O::load(kp + frag_col<T>(ks, g4));
-    for (int rb = 0; rb < R; rb += 16) {
-      // operand rows: row rb + rr of this kv head
-      const int qr = rb + rr;
-      typename O::reg qf[KS];
-      if (qr < R) {
-        const int b = a.leaf_list[loff + qr / G];
-        const T *qp = static_cast<const T *>(a.q) +
-                      (((int64_t)b * a.Lr + lr) * Hq + g * G + qr % G) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[ks] = O::load(qp + frag_col<T>(ks, g4));
-      } else {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[ks] = O::zero();
-      }
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) acc = O::mma(qf[ks], kf[ks], acc);
-      float part = 0.f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int row = rb + 4 * g4 + e;
-        if (row < R && key_ok) {
-          const int b = a.leaf_list[loff + row / G];
-          const bool own = a.leaves[b] == node;
-          if (!own || own_ok) {
-            const float l2 = a.lse2[((int64_t)b * a.Lr + lr) * Hq + g * G + row % G];
-            part += __builtin_amdgcn_exp2f(acc[e] * a.sl2 - l2);
-          }
-        }
-      }
-      sum += across_rows(part, [](float x, float y) { return x + y; });
-    }
-  }
-  if (g4 == 0) s_red[wave][rr] = sum;
-  __syncthreads();
-  if (threadIdx.x < 16 && key_ok) {
-    const float tot = ((s_red[0][rr] + s_red[1][rr]) + s_red[2][rr]) + s_red[3][rr];
-    cr.A[t.tok_off[node] + pos] += tot;
+  for (int w = blockIdx.x; w < n_items * SUBS; w += gridDim.x) {
+    credit_subpage<T, D>(a, cr, w / SUBS, w % SUBS, s_red);
+    __syncthreads();                        // s_red is reused by the next sub-page
   }
 }
 
@@ -708,11 +738,10 @@ void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *ls
   hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
                      lse_out);
   if (cr) {
-    // one workgroup per possible sub-page of a unit; those past the plan's
-    // units or past a unit's resident slots return at once
+    // workgroups stride over the sub-pages of the plan's units
     timing_begin(ARBOR_KERNEL_DECODE_CREDIT, stream);
-    hipLaunchKernelGGL((decode_credit<T, D>), dim3((unsigned)a.max_items * (CHUNK / 16)),
-                       dim3(256), 0, stream, a, *cr);
+    const int cgrid = std::min(a.max_items * (CHUNK / 16), 1024);
+    hipLaunchKernelGGL((decode_credit<T, D>), dim3(cgrid), dim3(256), 0, stream, a, *cr);
     timing_end(ARBOR_KERNEL_DECODE_CREDIT, stream);
   }
 }
