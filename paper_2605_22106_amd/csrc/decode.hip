@@ -95,25 +95,27 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
       ldepth[b] = -1;
       continue;
     }
-    int tmp[MAXD];
-    int d = 0;
-    bool ok = true;
+    // validate and measure the chain, then write it root first (two walks up
+    // the parent links keep the chain out of per-lane scratch memory)
+    int d = 0, bad = 0;
     for (int x = l; x >= 0; x = t.parent[x]) {
-      if (d >= MAXD || (x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) ||
-          (x == 0 && t.parent[x] != -1)) {
-        ok = false;
+      if ((x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) || (x == 0 && t.parent[x] != -1)) {
+        bad = 1;
         break;
       }
-      tmp[d++] = x;
+      if (++d > MAXD) {
+        bad = 2;
+        break;
+      }
     }
-    if (!ok) {
-      atomicOr(&s_err, 2);
+    if (bad) {
+      atomicOr(&s_err, bad);
       ldepth[b] = -1;
       continue;
     }
     ldepth[b] = d - 1;
-    for (int e = 0; e < d; ++e) {
-      const int x = tmp[d - 1 - e];
+    int e = d - 1;
+    for (int x = l; x >= 0; x = t.parent[x], --e) {
       lanc[(int64_t)b * MAXD + e] = x;
       atomicAdd(&node_nl[x], 1);
     }
@@ -338,22 +340,62 @@ __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
       }
     }
   }
-#pragma unroll
-  for (int sp = 0; sp < GSP; ++sp) {
+  if constexpr (sizeof(T) == 2) {
+    // bf16 values: O += P V as one bf16 MFMA (16x16x32) per 16 output columns
+    // over the fragment's keys, element t = 4 sp + e of a lane's k-slice being
+    // key 4 g4 + e of sub-page sp (zero past GSP sub-pages).  P is split into
+    // a bf16 high part and a bf16 remainder, p = hi + lo to about 2^-17
+    // relative, and both are multiplied by the exact bf16 V, so the product
+    // keeps fp32-level accuracy at a quarter of the fp32 MFMA's issue time.
+    bf16x8 ph[NB], pl[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      float p[4];
       const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
-        l_run[nb] += p[e];
+      for (int t = 0; t < 8; ++t) {
+        const int sp = t / 4, e = t % 4;
+        if (sp < GSP) {
+          const float p = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
+          l_run[nb] += p;
+          const __bf16 hi = (__bf16)p;
+          ph[nb][t] = hi;
+          pl[nb][t] = (__bf16)(p - (float)hi);
+        } else {
+          ph[nb][t] = (__bf16)0.f;
+          pl[nb][t] = (__bf16)0.f;
+        }
       }
+    }
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
+    for (int cc = 0; cc < NC; ++cc) {
+      bf16x8 vv;
 #pragma unroll
-        for (int cc = 0; cc < NC; ++cc)
-          o[nb][cc] = mma_f32(p[ks], (float)f.v[sp][ks][cc], o[nb][cc]);
+      for (int t = 0; t < 8; ++t)
+        vv[t] = t / 4 < GSP ? (__bf16)f.v[t / 4 < GSP ? t / 4 : 0][t % 4][cc] : (__bf16)0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        o[nb][cc] = Op<__bf16>::mma(ph[nb], vv, o[nb][cc]);
+        o[nb][cc] = Op<__bf16>::mma(pl[nb], vv, o[nb][cc]);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int sp = 0; sp < GSP; ++sp) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        float p[4];
+        const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
+          l_run[nb] += p[e];
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int cc = 0; cc < NC; ++cc)
+            o[nb][cc] = mma_f32(p[ks], (float)f.v[sp][ks][cc], o[nb][cc]);
+      }
     }
   }
 }

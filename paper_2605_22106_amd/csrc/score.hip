@@ -613,7 +613,6 @@ struct ObsChain {
 };
 __device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
   ObsChain r{0, 0, 0, true};
-  int chainv[MAXD];
   int d = 0;
   for (int x = j; x >= 0; x = t.parent[x]) {
     if (d >= MAXD || (x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) ||
@@ -626,18 +625,23 @@ __device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
       r.ok = false;
       break;
     }
-    chainv[d++] = x;
+    ++d;
     r.len += c;
     r.subs += (c + 15) / 16;
   }
   if (!r.ok) {
     r.subs = 0;
-    d = 1;
-    chainv[0] = j;
+    r.depth = 0;
+    if (anc_out) anc_out[0] = j;
+    return r;
   }
   r.depth = d - 1;
-  if (anc_out)
-    for (int e = 0; e < d; ++e) anc_out[e] = chainv[d - 1 - e];
+  // the chain root first, by a second walk up the parent links (no per-lane
+  // copy of the chain)
+  if (anc_out) {
+    int e = d - 1;
+    for (int x = j; x >= 0; x = t.parent[x], --e) anc_out[e] = x;
+  }
   return r;
 }
 
