@@ -328,10 +328,15 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   auto issue = [&](Buf &B, int row) __attribute__((always_inline)) {
     dma_tile<KT::NDMA, KT::BYTES>(kplane + (int64_t)row * (D * (int)sizeof(T)), B.k, src_off);
   };
-  auto read_k = [&](const Buf &B, uint4 (&kp)[RQ]) __attribute__((always_inline)) {
+  // offsets of this lane's pieces from the start of a ring (slot `wave`
+  // included), so a read addresses the ring's fixed LDS base plus a register
+  int roff[RQ];
+#pragma unroll
+  for (int jp = 0; jp < RQ; ++jp) roff[jp] = wave * (int)sizeof(Buf) + (lbase ^ (16 * jp));
+  auto read_k = [&](const Buf (&ring)[4], uint4 (&kp)[RQ]) __attribute__((always_inline)) {
 #pragma unroll
     for (int jp = 0; jp < RQ; ++jp)
-      kp[jp] = *reinterpret_cast<const uint4 *>(&B.k[lbase ^ (16 * jp)]);
+      kp[jp] = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(ring) + roff[jp]);
   };
 
   // One pass over this wave's sub-pages sp = wave + 4 i (i < cnt) of the
@@ -370,13 +375,13 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       {
         wait_vm<ND>();
         uint4 kp[RQ];
-        read_k(b0[wave], kp);
+        read_k(b0, kp);
         issue_i(b2[wave], 2);
         prev = mm(kp, ent(0, e.y), ent(0, e.w), ent(0, e.z));
       }
-      auto body = [&](const Buf &B, int i) __attribute__((always_inline)) {
+      auto body = [&](const Buf (&ring)[4], int i) __attribute__((always_inline)) {
         uint4 kp[RQ];
-        read_k(B, kp);
+        read_k(ring, kp);
         fix(prev);
         const StepState cur = mm(kp, ent(i, e.y), ent(i, e.w), ent(i, e.z));
         hot(prev);
@@ -392,21 +397,21 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       for (; i + 3 <= wc; i += 3) {
         wait_vm<ND>();
         issue_i(b0[wave], i + 2);
-        body(b1[wave], i);
+        body(b1, i);
         wait_vm<ND>();
         issue_i(b1[wave], i + 3);
-        body(b2[wave], i + 1);
+        body(b2, i + 1);
         wait_vm<ND>();
         issue_i(b2[wave], i + 4);
-        body(b0[wave], i + 2);
+        body(b0, i + 2);
       }
       // the last one or two sub-pages (i in slot 1, i + 1 in slot 2)
       if (i < wc) {
         wait_vm<ND>();
-        body(b1[wave], i);
+        body(b1, i);
         if (i + 1 < wc) {
           wait_vm<0>();
-          body(b2[wave], i + 1);
+          body(b2, i + 1);
         }
       }
       fix(prev);
@@ -418,23 +423,22 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   };
 
   // ---- pass 0: row log2-sum-exp ----
-  float m[NRB], l[NRB];
-#pragma unroll
-  for (int rb = 0; rb < NRB; ++rb) {
-    m[rb] = kFloor;
-    l[rb] = 0.f;
-  }
-  // The running sum of a row is kept relative to a reference m that moves
-  // only when a logit exceeds it by more than kSlack / sl2 (terms stay below
-  // 2^kSlack).  The terms of a sub-page are computed against the current
-  // reference first; if any row's max moved past it, the wave rescales every
-  // row to its new max and recomputes that sub-page's terms.
-  constexpr float kSlack = 8.f;
-  const float slack = kSlack / sl2;
-  float nm[NRB], lt[NRB], mx[NRB];
+  // The running sum l of a row is kept relative to a reference max m, held as
+  // nm = -m sl2 (log2 units; nm0 while the row has no reference).  m moves
+  // only when the terms of a sub-page grow large: the terms are computed
+  // against the current reference first, and if the four terms of any lane of
+  // any row add up to more than 2^kSlack (or overflow), the wave moves every
+  // row's reference to its max, rescales the sum and recomputes that
+  // sub-page's terms.  The common step thus needs no max at all.
+  constexpr float kGrow = 256.f;   // 2^kSlack, kSlack = 8
+  const float nm0 = -kFloor * sl2;
+  float nm[NRB], l[NRB], lt[NRB];
   bool grow = false;
 #pragma unroll
-  for (int rb = 0; rb < NRB; ++rb) nm[rb] = -m[rb] * sl2;
+  for (int rb = 0; rb < NRB; ++rb) {
+    nm[rb] = nm0;
+    l[rb] = 0.f;
+  }
   run(a.nsp[2 * o],
       [&](const uint4 (&kp)[RQ], int slot, int meta, int ctx) __attribute__((always_inline)) {
         StepState st;
@@ -479,8 +483,6 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
         grow = false;
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb) {
-          mx[rb] = max3f(max3f(st.acc[rb][0], st.acc[rb][1], st.acc[rb][2]), st.acc[rb][3], m[rb]);
-          grow |= mx[rb] > m[rb] + slack;
           float e4[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
@@ -489,16 +491,21 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
           // computed here, inside the block shared with the MFMAs (the
           // compiler would otherwise sink it into the branch that uses it)
           asm volatile("" : "+v"(lt[rb]));
+          grow |= !(lt[rb] <= kGrow);          // also true for +inf
         }
       },
       [&](const StepState &st) __attribute__((always_inline)) {
         if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
           for (int rb = 0; rb < NRB; ++rb) {
-            // (m - mx) is exactly 0 for a row whose max is unchanged
-            const float sc = __builtin_amdgcn_exp2f((m[rb] - mx[rb]) * sl2);
-            m[rb] = mx[rb];
-            nm[rb] = -mx[rb] * sl2;
+            // the new reference in log2 units, and the factor that moves the
+            // sum onto it (exactly 1 for a row whose max is unchanged)
+            const float mxs = fmaxf(
+                max3f(max3f(st.acc[rb][0], st.acc[rb][1], st.acc[rb][2]), st.acc[rb][3],
+                      st.acc[rb][3]) * sl2,
+                -nm[rb]);
+            const float sc = __builtin_amdgcn_exp2f(-mxs - nm[rb]);
+            nm[rb] = -mxs;
             float e4[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -513,7 +520,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   // merge the four lane groups (log2 units), then the four waves, in order
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
-    float mm = m[rb] > kFloor ? m[rb] * sl2 : -__builtin_inff();
+    float mm = nm[rb] < nm0 ? -nm[rb] : -__builtin_inff();
     float ll = l[rb];
 #pragma unroll
     for (int off = 16; off <= 32; off <<= 1) {
@@ -600,7 +607,9 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
         asm volatile("" : "+v"(colsum));
       },
       [&](const StepState &st) __attribute__((always_inline)) {
-        if (lane < (st.meta & 255)) pout[st.ctx + lane] = colsum;
+        // wave-uniform base (scalar registers) plus the lane's offset
+        float *const dst = pout + st.ctx;
+        if (lane < (st.meta & 255)) dst[lane] = colsum;
       });
 }
 
