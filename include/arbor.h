@@ -328,10 +328,11 @@ int arbor_tree_decode_attn_scored(const arbor_geom_t *geom, const arbor_tree_t *
  *   u_out[dst[r]] = 1 - H / ln(vocab)    (dst NULL: u_out[r]).
  * u_out is fp32 [n_out]; dst int32 [n_rows] (nullable), each in [0, n_out)
  * (typically the block ids whose u_in arbor_score reads).  The whole-vocabulary
- * form splits each row over several workgroups and needs `workspace` of at least
- * arbor_uncertainty_workspace_size(n_rows, vocab, dtype) bytes (the top-K form
- * needs none).  fp32 arithmetic with a fixed reduction order: bitwise
- * reproducible.  vocab must be a multiple of 8 (bf16) or 4 (fp32) and logits
+ * form and the top-K form with top_k <= 256 split each row over several
+ * workgroups and need `workspace` of at least
+ * arbor_uncertainty_workspace_size(n_rows, vocab, dtype) bytes (a larger top_k
+ * uses one workgroup per row and no workspace).  fp32 arithmetic with a fixed
+ * reduction order: bitwise reproducible.  vocab must be a multiple of 8 (bf16) or 4 (fp32) and logits
  * 16-byte aligned (EUNSUPPORTED otherwise).
  * Errors: EINVAL (arguments, a dst entry out of range), ENONFINITE (a NaN or
  * infinite logit in a row; that row's u is not written), EWORKSPACE.

@@ -52,6 +52,25 @@ def test_uncertainty_rows(vocab, dtype, top_k):
     assert np.max(np.abs(u - ref)) <= TOL, np.max(np.abs(u - ref))
 
 
+@pytest.mark.parametrize("top_k", [1, 40, 255, 256, 257])
+def test_uncertainty_top_k_chunked_edges(top_k):
+    # rows split over several chunks (64 rows of 65536): K at and around the
+    # chunked path's limit; constant rows (every value ties with the bound, so
+    # the chunks fall back to a select over all their values), a row whose
+    # top K all sit in one chunk, and the synthetic mix
+    rows, vocab = 64, 65536
+    z = synth.boundary_logits(rows, vocab, seed=top_k, dtype="bf16", device="cuda")
+    z[0] = 0.25
+    z[1, :300] = 9.0
+    z[2] = torch.arange(vocab, device="cuda").float().remainder(7).to(torch.bfloat16)
+    u, s = run(z, top_k)
+    assert s == L.OK
+    ref = oracle_u(z, top_k)
+    assert np.max(np.abs(u - ref)) <= TOL, np.max(np.abs(u - ref))
+    u2, _ = run(z, top_k)
+    assert np.array_equal(u.view(np.uint32), u2.view(np.uint32))
+
+
 def test_uncertainty_closed_forms():
     # uniform row -> 0; a near one-hot row -> 1; two equal logits among -inf-like ones
     z = torch.zeros(3, 1024, device="cuda")
