@@ -226,6 +226,31 @@ __device__ T block_exclusive_scan(T v, T *smem, T *total) {
   return base + inc - v;
 }
 
+// N exclusive scans over the block in one exchange (two barriers in all);
+// smem holds N * 16 values.
+template <int N>
+__device__ void block_exclusive_scan_n(const int64_t (&v)[N], int64_t (&ex)[N],
+                                       int64_t (&total)[N], int64_t *smem) {
+  const int lane = lane_id();
+  const int w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  int64_t inc[N];
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    inc[k] = wave_inclusive_scan(v[k]);
+    if (lane == kWave - 1) smem[k * 16 + w] = inc[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    const int64_t t = lane < nw ? smem[k * 16 + lane] : 0;
+    const int64_t tinc = wave_inclusive_scan(t);
+    ex[k] = lane_value(tinc, w) - lane_value(t, w) + inc[k] - v[k];
+    total[k] = lane_value(tinc, nw - 1);
+  }
+  __syncthreads();
+}
+
 template <class T>
 __device__ T block_sum(T v, T *smem) {
   T tot;

@@ -23,6 +23,7 @@ namespace {
 constexpr int MAXD = ARBOR_MAX_DEPTH + 1;
 static_assert(MAXD == kWave, "one wave covers a chain");
 constexpr int CHUNK = 256;        // slots per work unit
+constexpr int kPlanLds = 4096;    // trees up to this many nodes are planned from LDS
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -76,8 +77,11 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
                                                     int32_t *lanc, int32_t *ldepth,
                                                     int32_t *lrank, int32_t *leaf_np,
                                                     int32_t *leaf_part) {
-  __shared__ int64_t sm[17];
+  __shared__ int64_t sm[6 * 16];
   __shared__ int s_err;
+  // parent links and leaf counts in LDS for trees of up to kPlanLds nodes, so
+  // the chain walks and the counting do not wait on global memory
+  __shared__ int32_t s_par[kPlanLds], s_nl[kPlanLds];
   if (status_failed(a.status)) {
     if (threadIdx.x == 0) meta[0] = meta[1] = meta[2] = 0;
     return;
@@ -85,8 +89,14 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   const Tree &t = a.t;
   const int V = t.V;
   const int G = a.pl.G;
+  const bool small = V <= kPlanLds;
+  const int32_t *par = small ? s_par : t.parent;
+  int32_t *nlp = small ? s_nl : node_nl;
   if (threadIdx.x == 0) s_err = 0;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) node_nl[i] = 0;
+  for (int i = threadIdx.x; i < V; i += blockDim.x) {
+    nlp[i] = 0;
+    if (small) s_par[i] = t.parent[i];
+  }
   __syncthreads();
   for (int b = threadIdx.x; b < a.n_leaves; b += blockDim.x) {
     const int l = a.leaves[b];
@@ -98,8 +108,8 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     // validate and measure the chain, then write it root first (two walks up
     // the parent links keep the chain out of per-lane scratch memory)
     int d = 0, bad = 0;
-    for (int x = l; x >= 0; x = t.parent[x]) {
-      if ((x > 0 && (t.parent[x] < 0 || t.parent[x] >= x)) || (x == 0 && t.parent[x] != -1)) {
+    for (int x = l; x >= 0; x = par[x]) {
+      if ((x > 0 && (par[x] < 0 || par[x] >= x)) || (x == 0 && par[x] != -1)) {
         bad = 1;
         break;
       }
@@ -115,9 +125,9 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     }
     ldepth[b] = d - 1;
     int e = d - 1;
-    for (int x = l; x >= 0; x = t.parent[x], --e) {
+    for (int x = l; x >= 0; x = par[x], --e) {
       lanc[(int64_t)b * MAXD + e] = x;
-      atomicAdd(&node_nl[x], 1);
+      atomicAdd(&nlp[x], 1);
     }
   }
   __syncthreads();
@@ -142,19 +152,20 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   int64_t run_leaf = 0, run_item = 0, run_rows = 0, run_cls[3] = {0, 0, 0};
   for (int base = 0; base < V; base += blockDim.x) {
     const int i = base + threadIdx.x;
-    const int nl = i < V ? node_nl[i] : 0;
+    const int nl = i < V ? nlp[i] : 0;
+    if (small && i < V) node_nl[i] = nl;
     const int c = (i < V && nl > 0) ? t.n_kept[i] : 0;
     const int chunks = (c + CHUNK - 1) / CHUNK;
     const int rows = nl * G;
     const int nbr = (rows + 15) / 16;
     const int cls = nbr <= 1 ? 0 : (nbr <= 2 ? 1 : 2);
-    int64_t tl, ti, tr, tc0, tc1, tc2;
-    const int64_t el = block_exclusive_scan<int64_t>(nl, sm, &tl);
-    const int64_t ei = block_exclusive_scan<int64_t>(chunks, sm, &ti);
-    const int64_t er = block_exclusive_scan<int64_t>((int64_t)chunks * rows, sm, &tr);
-    const int64_t e0 = block_exclusive_scan<int64_t>(cls == 0 ? chunks : 0, sm, &tc0);
-    const int64_t e1 = block_exclusive_scan<int64_t>(cls == 1 ? chunks : 0, sm, &tc1);
-    const int64_t e2 = block_exclusive_scan<int64_t>(cls == 2 ? chunks : 0, sm, &tc2);
+    const int64_t sv[6] = {nl, chunks, (int64_t)chunks * rows, cls == 0 ? chunks : 0,
+                           cls == 1 ? chunks : 0, cls == 2 ? chunks : 0};
+    int64_t sx[6], stot[6];
+    block_exclusive_scan_n<6>(sv, sx, stot, sm);
+    const int64_t el = sx[0], ei = sx[1], er = sx[2], e0 = sx[3], e1 = sx[4], e2 = sx[5];
+    const int64_t tl = stot[0], ti = stot[1], tr = stot[2], tc0 = stot[3], tc1 = stot[4],
+                  tc2 = stot[5];
     if (i < V) {
       node_leaf_off[i] = (int32_t)(run_leaf + el);
       node_item0[i] = (int32_t)(run_item + ei);
