@@ -59,6 +59,7 @@ struct ScoreArgs {
 // Chain of observer j in LDS, root first, with a table of its 16-slot
 // sub-pages so the key loop needs no dependent page-table load.
 constexpr int SPCAP = 512;
+constexpr int kSetupLds = 2048;   // trees up to this many nodes are walked from LDS
 struct ChainLds {
   int node[MAXD];
   int c[MAXD];
@@ -673,11 +674,24 @@ __global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap
   __shared__ int s_err;
   __shared__ int64_t s_mine[4];
   __shared__ ChainLds ch;
+  // parent links and block sizes in LDS for trees of up to kSetupLds nodes, so
+  // the chain walks do not wait on global memory at every step
+  __shared__ int32_t s_par[kSetupLds], s_full[kSetupLds], s_kept[kSetupLds];
   if (status_failed(a.status)) return;
-  const Tree &t = a.t;
+  Tree t = a.t;
   const int me = blockIdx.x;
   const int tid = threadIdx.x;
   if (tid == 0) s_err = 0;
+  if (t.V <= kSetupLds) {
+    for (int i = tid; i < t.V; i += blockDim.x) {
+      s_par[i] = t.parent[i];
+      s_full[i] = t.n_full[i];
+      s_kept[i] = t.n_kept[i];
+    }
+    t.parent = s_par;
+    t.n_full = s_full;
+    t.n_kept = s_kept;
+  }
   __syncthreads();
   if (me == 0) {
     for (int i = tid; i < t.V; i += blockDim.x) {
