@@ -19,6 +19,8 @@ namespace arbor {
 
 namespace {
 
+constexpr int kPlanPos = 1024;   // per-wave LDS positions in the compaction plan
+
 __device__ __forceinline__ int pos_at(const Tree &t, const Pool &pl, int64_t po, int s) {
   const int page = t.page_table[po + s / pl.P];
   return pl.slot_pos[(int64_t)page * pl.P + (s % pl.P)];
@@ -37,6 +39,9 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
                                                     int32_t *__restrict__ mv_dst,
                                                     int32_t *__restrict__ first_moved,
                                                     int32_t *__restrict__ freed, int32_t *status) {
+  // each wave's node positions, slot order, when the node holds at most
+  // kPlanPos resident tokens: the binary searches then run in LDS
+  __shared__ int s_pos[4][kPlanPos];
   if (status_failed(status)) return;
   const int lane = lane_id();
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -51,6 +56,14 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
   const int64_t tb = t.tok_off[i];
   const int64_t po = t.page_off[i];
   bool bad = ki < 0;
+  int *lp = s_pos[threadIdx.x >> 6];
+  const bool in_lds = c <= kPlanPos;
+  if (in_lds) {
+    for (int s = lane; s < c; s += kWave) lp[s] = pos_at(t, pl, po, s);
+    // LDS operations of one wave complete in order: the reads below see these
+    // writes once the compiler keeps them in program order
+    __builtin_amdgcn_wave_barrier();
+  }
   for (int s = lane; s < ki; s += kWave) {
     const int p = sel_pos[tb + s];
     bad |= p < 0 || p >= n || (s > 0 && sel_pos[tb + s - 1] >= p);
@@ -59,7 +72,7 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
     int lo = s, hi = c - 1, found = -1;
     while (!bad && lo <= hi) {
       const int mid = (lo + hi) >> 1;
-      const int pm = pos_at(t, pl, po, mid);
+      const int pm = in_lds ? lp[mid] : pos_at(t, pl, po, mid);
       if (pm == p) {
         found = mid;
         break;
