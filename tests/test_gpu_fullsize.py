@@ -415,3 +415,20 @@ def test_dpts_wide_frontier():
         w = np.exp(z - z.max())
         err = np.abs(out_np[b, layer, h] - (w / w.sum()) @ Vv).max()
         assert err <= 2e-3, (b, layer, h, err)
+    # the same decode with the decode-time credit on the slice layers: bitwise
+    # the same outputs, and A / rows_seen against the oracle on those layers
+    # (16 leaves: more than 16 query rows per kv head on the shared ancestors)
+    sl = st["slice_layers"]
+    A0 = torch.zeros(N, device="cuda")
+    r0 = torch.zeros(V, dtype=torch.int64, device="cuda")
+    out2 = torch.empty_like(out)
+    check_rc(L.arbor_tree_decode_attn_scored(kv, active, 0, kv.layers, q, out2, None, 0.0, sl, 0,
+                                             A0, r0, stt, ws))
+    torch.cuda.synchronize()
+    assert int(stt) == L.OK
+    assert torch.equal(out2.view(torch.int32), out.view(torch.int32))
+    ost_sl = _meta(kv, k=kv.k[sl].float().cpu().numpy())
+    Ao, ro = O.decode_credit(ost_sl, st["active"].tolist(), 0, np_float(q[:, sl]), kv.q_per_kv,
+                             list(range(len(sl))), np.zeros(N, np.float32), np.zeros(V, np.int64))
+    _close(A0.cpu().numpy(), Ao)
+    assert np.array_equal(r0.cpu().numpy(), ro)
