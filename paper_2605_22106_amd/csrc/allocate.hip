@@ -35,7 +35,9 @@ constexpr int AT = 1024;
 constexpr int kLdsNodes = 512;    // per-node state in LDS up to this many nodes
 constexpr int kCandLds = 1536;    // listed prices selected in LDS up to this many
 constexpr int kNodeBytes = 2 * 8 + 7 * 4 + 1;
-constexpr int kSearchWaves = AT / kWave / 2;   // test points per bracket end
+constexpr int kSearchWaves = AT / kWave / 2;   // waves per bracket end
+constexpr int kPtsPerWave = 4;                  // test points of each wave
+constexpr int kSearchPts = kSearchWaves * kPtsPerWave;   // test points per end
 constexpr int kDecay = 128;                    // tabulated depths and distances
 
 // The decay factors exp(-lambda_d d) and exp(-lambda_Delta Delta) for small
@@ -292,8 +294,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   __shared__ int64_t sm[3 * 16];
   __shared__ int s_err;
   __shared__ unsigned long long hist64[256];
-  __shared__ double s_cnt[2][2 * kSearchWaves];
-  __shared__ uint64_t s_x[2][2 * kSearchWaves];
+  __shared__ double s_cnt[2][2 * kSearchPts];
+  __shared__ uint64_t s_x[2][2 * kSearchPts];
   if (status_failed(status)) return;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = lane_id();
@@ -482,8 +484,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     //   approx(a) <= E - 2 n_elig - 1  ->  exact(a) <= E - 1, and
     //   approx(b) >= E + 2 n_elig + 1  ->  exact(b) >= E + 1:
     // the order statistic lies in (a, b].  Each end has its own bracket
-    // [lo, hi] around the crossing of its threshold; waves 0..7 test eight
-    // points inside the bracket of a, waves 8..15 inside that of b.
+    // [lo, hi] around the crossing of its threshold; waves 0..7 test 32
+    // points (four each) inside the bracket of a, waves 8..15 inside that of b.
     const double t_lo = (double)(E - 2 * n_elig - 1);
     const double t_hi = (double)(E + 2 * n_elig + 1);
     // a: approx(a_lo) <= t_lo < approx(a_hi); b: approx(b_lo) < t_hi, and
@@ -497,60 +499,79 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     // stop once the bracket holds few prices: listing them costs less than
     // another round
     const double enough = 256.0 + 4.0 * (double)n_elig;
+    static_assert(2 * kSearchPts == kWave, "one lane per test point in the narrowing");
     for (int round = 0; !(a_done && b_done) && cb - ca > enough; ++round) {
       const bool end_b = wave >= kSearchWaves;
-      const int q = wave % kSearchWaves;
+      const int q0 = (wave % kSearchWaves) * kPtsPerWave;
       const uint64_t lo = end_b ? b_lo : a_lo;
-      const uint64_t x = split_point<kSearchWaves>(lo, (end_b ? b_hi : a_hi) - lo, q);
-      double c = 0.0;
+      const uint64_t span = (end_b ? b_hi : a_hi) - lo;
+      uint64_t x[kPtsPerWave];
+      double xv[kPtsPerWave], c[kPtsPerWave];
+#pragma unroll
+      for (int p = 0; p < kPtsPerWave; ++p) {
+        x[p] = split_point<kSearchPts>(lo, span, q0 + p);
+        xv[p] = key_value(x[p]);
+        c[p] = 0.0;
+      }
       if (!(end_b ? b_done : a_done)) {
-        const double xv = key_value(x);
         for (int i = lane; i < V; i += kWave) {
           const int cnt = nd.cnt[i];
-          if (cnt > 0) c += approx_le(xv, nd.F[i], cnt, nd.W[i]);
-        }
-        c = wave_sum(c);
-      }
-      if (lane == 0) {
-        s_cnt[round & 1][wave] = c;
-        s_x[round & 1][wave] = x;
-      }
-      __syncthreads();
-      // every thread narrows both brackets from the same counts, in the same order
-      if (!a_done) {
-        uint64_t nlo = a_lo, nhi = a_hi;
-        double nca = ca;
-        for (int qq = 0; qq < kSearchWaves; ++qq) {
-          const uint64_t xq = s_x[round & 1][qq];
-          const double cq = s_cnt[round & 1][qq];
-          if (cq <= t_lo) {
-            nlo = xq;
-            nca = cq;
-          } else if (xq < nhi) {
-            nhi = xq;
+          if (cnt > 0) {
+            const int F = nd.F[i];
+            const double W = nd.W[i];
+#pragma unroll
+            for (int p = 0; p < kPtsPerWave; ++p) c[p] += approx_le(xv[p], F, cnt, W);
           }
         }
-        a_lo = nlo;
-        a_hi = nhi;
-        ca = nca;
+#pragma unroll
+        for (int p = 0; p < kPtsPerWave; ++p) c[p] = wave_sum(c[p]);
+      }
+      if (lane < kPtsPerWave) {
+        const int slot = (end_b ? kSearchPts : 0) + q0 + lane;
+        double cl = c[0];
+        uint64_t xl = x[0];
+#pragma unroll
+        for (int p = 1; p < kPtsPerWave; ++p) {
+          cl = lane == p ? c[p] : cl;
+          xl = lane == p ? x[p] : xl;
+        }
+        s_cnt[round & 1][slot] = cl;
+        s_x[round & 1][slot] = xl;
+      }
+      __syncthreads();
+      // every wave narrows both brackets from the same counts: lane l holds
+      // point l of end a (l < 32) or point l - 32 of end b.  The points ascend
+      // and the counts with them, so the points at or below a threshold form
+      // a prefix: one ballot finds its last point and the first point after it.
+      const uint64_t xq = s_x[round & 1][lane];
+      const double cq = s_cnt[round & 1][lane];
+      const uint64_t m_a = ballot(lane < kSearchPts && cq <= t_lo);
+      const uint64_t m_b = ballot(lane >= kSearchPts && cq < t_hi) >> kSearchPts;
+      constexpr uint64_t kAll = (1ull << kSearchPts) - 1;
+      if (!a_done) {
+        if (m_a) {
+          const int ql = 63 - __builtin_clzll(m_a);
+          a_lo = lane_value(xq, ql);
+          ca = lane_value(cq, ql);
+        }
+        const uint64_t above = ~m_a & kAll;
+        if (above) {
+          const uint64_t xh = lane_value(xq, __builtin_ctzll(above));
+          a_hi = xh < a_hi ? xh : a_hi;
+        }
         if (a_hi - a_lo <= 1) a_done = true;
       }
       if (!b_done) {
-        uint64_t nlo = b_lo, nhi = b_hi;
-        double ncb = cb;
-        for (int qq = kSearchWaves - 1; qq >= 0; --qq) {
-          const uint64_t xq = s_x[round & 1][kSearchWaves + qq];
-          const double cq = s_cnt[round & 1][kSearchWaves + qq];
-          if (cq >= t_hi) {
-            nhi = xq;
-            ncb = cq;
-          } else if (xq > nlo) {
-            nlo = xq;
-          }
+        if (m_b) {
+          const uint64_t xl = lane_value(xq, kSearchPts + 63 - __builtin_clzll(m_b));
+          b_lo = xl > b_lo ? xl : b_lo;
         }
-        b_lo = nlo;
-        b_hi = nhi;
-        cb = ncb;
+        const uint64_t reach = ~m_b & kAll;
+        if (reach) {
+          const int qh = kSearchPts + __builtin_ctzll(reach);
+          b_hi = lane_value(xq, qh);
+          cb = lane_value(cq, qh);
+        }
         if (b_hi - b_lo <= 1) b_done = true;
       }
     }
