@@ -254,15 +254,17 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   __shared__ __attribute__((aligned(16))) float s_lse[ROWS];
   __shared__ int s_bad;
   // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
-  // (slice layer, kv head, row group) planes p = x, x + 8, ... and, within a
-  // plane, the observers from the deepest (longest chain) down -- siblings,
-  // which share their whole ancestor chain, run together and read those keys
-  // from the XCD's L2
+  // (slice layer, kv head, row group) planes p = x, x + 8, ...; it runs the
+  // observers from the deepest (longest chain) down, each over all its
+  // planes in turn -- the longest work starts first, so the grid ends on the
+  // shortest, and siblings, which share their whole ancestor chain, run
+  // together and read those keys from the XCD's L2
   const int n_planes = a.S * a.pl.Hkv * a.n_rg;
   const int xcd = (int)blockIdx.x % kXcds;
   const int idx = (int)blockIdx.x / kXcds;
-  const int o = a.n_obs - 1 - idx % a.n_obs;
-  const int plane = (idx / a.n_obs) * kXcds + xcd;
+  const int ppx = (n_planes + kXcds - 1) / kXcds;   // planes per XCD
+  const int o = a.n_obs - 1 - idx / ppx;
+  const int plane = (idx % ppx) * kXcds + xcd;
   if (plane >= n_planes) return;
   if (threadIdx.x == 0) s_bad = status_failed(a.status);
   __syncthreads();
