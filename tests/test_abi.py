@@ -83,3 +83,28 @@ def test_kernel_events_setter_validates_on_the_host():
     assert lib.arbor_set_kernel_events(-1, None, None) == L.EINVAL
     # one of the two events missing
     assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_ATTN, ctypes.c_void_p(1), None) == L.EINVAL
+
+
+def test_uncertainty_workspace_sizes_on_the_host():
+    # the chunked forms need per-chunk partials and, for top-K, K <= 256
+    # candidates per chunk: the size grows with the rows and covers them
+    small = L.arbor_uncertainty_workspace_size(8, 128256, L.BF16)
+    large = L.arbor_uncertainty_workspace_size(85, 128256, L.BF16)
+    assert 0 < small < large
+    assert large >= 85 * (16 + 4 * 256 + 4)
+    assert L.arbor_uncertainty_workspace_size(0, 128256, L.BF16) > 0
+    with pytest.raises(ValueError):
+        import torch
+        L.arbor_uncertainty(torch.zeros(4), 0, None, None, None)
+
+
+def test_decode_workspace_covers_the_credit_lse():
+    # the scored decode keeps a log2 LSE per (leaf, layer, query head) in the
+    # shared workspace: more leaves or layers need more bytes
+    lib = L.load()
+    g = L.Geom(32, 8, 4, 128, 16, L.BF16, 1408)
+    a = L.Sizes(85, 22528, 1792, 1, 32, 2, 4, 32)
+    b = L.Sizes(85, 22528, 1792, 1, 32, 2, 64, 32)
+    na = lib.arbor_workspace_size(ctypes.byref(g), ctypes.byref(a))
+    nb = lib.arbor_workspace_size(ctypes.byref(g), ctypes.byref(b))
+    assert nb - na >= (64 - 4) * 32 * 32 * 4
