@@ -80,12 +80,21 @@ __device__ __forceinline__ void build_chain(const Tree &t, const Pool &pl, int j
     ch.depth = d;
     int e = d;
     for (int x = j; x >= 0 && e >= 0; x = t.parent[x]) ch.node[e--] = x;
+  }
+  __syncthreads();
+  // one thread per chain node fetches its size and page-table offset (the
+  // loads run side by side), then one thread forms the prefix sums
+  if ((int)threadIdx.x <= ch.depth) {
+    const int x = ch.node[threadIdx.x];
+    ch.c[threadIdx.x] = t.n_kept[x];
+    ch.po[threadIdx.x] = t.page_off[x];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int d = ch.depth;
     int ctx = 0, sp = 0;
-    for (e = 0; e <= d; ++e) {
-      const int x = ch.node[e];
-      const int c = t.n_kept[x];
-      ch.c[e] = c;
-      ch.po[e] = t.page_off[x];
+    for (int e = 0; e <= d; ++e) {
+      const int c = ch.c[e];
       ch.ctx[e] = ctx;
       ch.sp_off[e] = sp;
       ctx += c;
