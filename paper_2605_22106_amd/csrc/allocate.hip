@@ -113,31 +113,6 @@ __device__ __forceinline__ double approx_le(double x, int F, int cnt, double W) 
   return y < 0.0 ? 0.0 : (y > (double)cnt ? (double)cnt : y);
 }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-  return wave_allreduce(v, [](uint64_t a, uint64_t b) { return a < b ? a : b; });
-}
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-  return wave_allreduce(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
-}
-
-// block-wide min / max: wave partials in sm, then every wave combines them
-__device__ uint64_t block_min_u64(uint64_t v, uint64_t *sm) {
-  v = wave_min_u64(v);
-  if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
-  __syncthreads();
-  const uint64_t r = wave_min_u64(lane_id() < (int)(blockDim.x >> 6) ? sm[lane_id()] : ~0ull);
-  __syncthreads();
-  return r;
-}
-__device__ uint64_t block_max_u64(uint64_t v, uint64_t *sm) {
-  v = wave_max_u64(v);
-  if (lane_id() == 0) sm[threadIdx.x >> 6] = v;
-  __syncthreads();
-  const uint64_t r = wave_max_u64(lane_id() < (int)(blockDim.x >> 6) ? sm[lane_id()] : 0ull);
-  __syncthreads();
-  return r;
-}
-
 // three block-wide sums in one exchange; sm holds 48 values
 __device__ void block_sum3(int64_t (&v)[3], int64_t *sm) {
   const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
