@@ -120,3 +120,42 @@ def test_scored_decode_rejects_bad_slices():
         rc = L.arbor_tree_decode_attn_scored(kv, lt.cuda(), 1, 3, q, out, None, 0.0, sl, sw, A,
                                              rows, status(), ws)
         assert rc == L.EINVAL, (sl, sw)
+
+
+def test_incremental_scores_drive_an_eviction():
+    """A kept up to date by three scored decode steps (new queries each step)
+    matches the oracle's running credit, and an eviction driven by it selects
+    the same tokens on both sides (the GPU's A handed to both)."""
+    st = rand_tree_state(21, V=20, max_n=120, min_n=20, G=4, L_=2)
+    kv = to_gpu(st)
+    ost = oracle_state(st)
+    N, V = st["num_tokens"], kv.num_nodes
+    Hq = kv.kv_heads * kv.q_per_kv
+    leaves = st["active"].tolist()
+    lt = st["active"].cuda()
+    A_o = np.zeros(N, np.float32)
+    r_o = np.zeros(V, np.int64)
+    A_g = torch.zeros(N, device="cuda")
+    r_g = torch.zeros(V, dtype=torch.int64, device="cuda")
+    ws = workspace(kv, max_leaves=len(leaves), max_layers=2)
+    gen = torch.Generator().manual_seed(21)
+    for step in range(3):
+        q = torch.randn((len(leaves), 2, Hq, kv.head_dim), generator=gen).to(torch.bfloat16)
+        out = torch.empty((len(leaves), 2, Hq, kv.head_dim), device="cuda")
+        stt = status()
+        check_rc(L.arbor_tree_decode_attn_scored(kv, lt, 0, 2, q.cuda().contiguous(), out, None,
+                                                 0.0, [1], 0, A_g, r_g, stt, ws))
+        torch.cuda.synchronize()
+        assert int(stt) == L.OK
+        A_o, r_o = O.decode_credit(ost, leaves, 0, np_float(q), kv.q_per_kv, [1], A_o, r_o)
+    _close(A_g.cpu().numpy(), A_o)
+    assert np.array_equal(r_g.cpu().numpy(), r_o)
+    A = A_g.cpu().numpy()
+    rng = np.random.default_rng(21)
+    k = np.array([int(rng.integers(1, c + 1)) for c in ost["n_kept"]], np.int32)
+    sel_o, _ = O.select(ost, A, k, PARAMS["l_tail"])
+    sel, sg = _event(st, kv, A, k, PARAMS)
+    assert sg == L.OK
+    for i, keep in sel_o.items():
+        b = int(ost["tok_off"][i])
+        assert np.array_equal(sel[b:b + len(keep)], np.array(keep, np.int32)), i
