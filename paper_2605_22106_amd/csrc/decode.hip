@@ -872,7 +872,8 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   CreditArgs cr{};
   if (credit) {
     cr.S = credit->n_slice;
-    for (int e = 0; e < 8; ++e) cr.slice[e] = e < credit->n_slice ? credit->slice_layers[e] - layer_begin : 0;
+    for (int e = 0; e < 8; ++e)
+      cr.slice[e] = e < credit->n_slice ? credit->slice_layers[e] - layer_begin : 0;
     cr.self_window = credit->self_window;
     cr.A = credit->A;
     cr.rows_seen = credit->rows_seen;
@@ -899,12 +900,17 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   hipLaunchKernelGGL(decode_plan, dim3(1), dim3(1024), 0, stream, a, meta, cls_items, item_node,
                      item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list, node_item0,
                      node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part);
+  const CreditArgs *crp = credit ? &cr : nullptr;
   if (geom->dtype == ARBOR_BF16) {
-    if (geom->head_dim == 128) launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
-    else launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
+    if (geom->head_dim == 128)
+      launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, crp, stream);
+    else
+      launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, crp, stream);
   } else {
-    if (geom->head_dim == 128) launch_decode_kernels<float, 128>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
-    else launch_decode_kernels<float, 64>(a, out, out_dtype, lse_out, credit ? &cr : nullptr, stream);
+    if (geom->head_dim == 128)
+      launch_decode_kernels<float, 128>(a, out, out_dtype, lse_out, crp, stream);
+    else
+      launch_decode_kernels<float, 64>(a, out, out_dtype, lse_out, crp, stream);
   }
   return hip_ok(hipGetLastError());
 }
