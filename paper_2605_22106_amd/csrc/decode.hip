@@ -576,9 +576,18 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
     const float *base = a.part + (((int64_t)lr * pl.Hkv + g) * a.meta[3] + hl) * stride;
     const int32_t *lp = a.leaf_part + (int64_t)b * a.max_parts;
     const int np = a.leaf_np[b];
-    // global max over the chain's partials
-    float M = -__builtin_inff();
-    for (int k0 = 0; k0 < np; k0 += kWave) {
+    // global max over the chain's partials; the first kWave partials'
+    // offsets, maxima and sums stay in registers for the second pass (longer
+    // chains reload the rest there)
+    int64_t off0 = 0;
+    float m0 = -__builtin_inff(), l0 = 0.f;
+    if (lane < np) {
+      off0 = (int64_t)lp[lane] * stride;
+      m0 = base[off0];
+      l0 = base[off0 + 1];
+    }
+    float M = m0;
+    for (int k0 = kWave; k0 < np; k0 += kWave) {
       const int k = k0 + lane;
       const float m = k < np ? base[(int64_t)lp[k] * stride] : -__builtin_inff();
       M = fmaxf(M, m);
@@ -593,9 +602,14 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
         int64_t off = 0;
         float f = 0.f, lk = 0.f;
         if (k < np) {
-          off = (int64_t)lp[k] * stride;
-          const float m = base[off];
-          lk = base[off + 1];
+          float m = m0;
+          off = off0;
+          lk = l0;
+          if (k0 > 0) {
+            off = (int64_t)lp[k] * stride;
+            m = base[off];
+            lk = base[off + 1];
+          }
           f = m > -__builtin_inff() ? __builtin_amdgcn_exp2f(m - M) : 0.f;
         }
         L += wave_sum(lk * f);
