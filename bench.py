@@ -158,7 +158,7 @@ def summarize_traffic(fetch_csv: str, write_csv: str, title: str, command: str,
 
 
 # the kernel of each rated stage whose launches are timed on their own
-# (arbor_set_kernel_events) and rated against its roofline
+# (a per-call timing request, arbor_timing_t) and rated against its roofline
 STAGE_KERNEL = {"score": (L.KERNEL_SCORE_ATTN, "score_attn", "score.hip"),
                 "select": (L.KERNEL_SELECT, "select_kernel", "select.hip"),
                 "compact": (L.KERNEL_COMPACT_MOVE, "compact_move", "compact.hip"),
@@ -249,8 +249,11 @@ class Event:
         self.rows.zero_()
         self.status.zero_()
 
-    def run(self, active, marks=None):
-        """score -> allocate -> select -> compact -> decode; `marks` records events."""
+    def run(self, active, marks=None, timings=None):
+        """score -> allocate -> select -> compact -> decode; `marks` records events
+        between the entry points, `timings` ({stage: L.Timing}) asks each call to
+        time its rated kernel."""
+        tm = timings or {}
         kv, st = self.kv, self.st
         ev = (lambda: marks.append(torch.cuda.Event(enable_timing=True))) if marks is not None else None
 
@@ -262,17 +265,20 @@ class Event:
         mark()
         self.check(L.arbor_score(kv, self.observers, self.q_win, st["window"], st["slice_layers"],
                                  self.v_sig, self.u_sig, self.A, self.rows, self.a, self.s,
-                                 self.params, self.status, self.ws))
+                                 self.params, self.status, self.ws, timing=tm.get("score")))
         mark()
         self.check(L.arbor_allocate(kv, active, st["budget"], self.s, self.params, self.k,
                                     self.delta, self.on_path, self.status, self.ws))
         mark()
-        self.check(L.arbor_select(kv, self.A, self.k, self.params, self.sel, self.status))
+        self.check(L.arbor_select(kv, self.A, self.k, self.params, self.sel, self.status,
+                                  timing=tm.get("select")))
         mark()
-        self.check(L.arbor_compact(kv, self.k, self.sel, self.status, self.ws))
+        self.check(L.arbor_compact(kv, self.k, self.sel, self.status, self.ws,
+                                   timing=tm.get("compact")))
         mark()
         self.check(L.arbor_tree_decode_attn(kv, active, 0, kv.layers, self.q_dec, self.out,
-                                            self.lse, 0.0, self.status, self.ws))
+                                            self.lse, 0.0, self.status, self.ws,
+                                            timing=tm.get("decode")))
         mark()
 
 
@@ -428,13 +434,14 @@ def main():
         flush.sum()  # reads only: leaves the last-level cache clean
     stages = ["score", "allocate", "select", "compact", "decode"]
     # events around the rated kernels' own launches, recorded by the library
-    # during the breakdown pass only
+    # during the breakdown pass only (one timing request per call)
     kevents = {}
     for name in STAGE_KERNEL:
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         e1.record()
         kevents[name] = (e0, e1)
+    ktiming = {name: L.timing(STAGE_KERNEL[name][0], *kevents[name]) for name in STAGE_KERNEL}
 
     # warmup
     for _ in range(args.warmup):
@@ -492,22 +499,18 @@ def main():
     # breakdown pass (as many steps again): events between the entry points and
     # around the rated kernels' launches.  Kept apart from the timed steps
     # because every recorded event also costs the stream a little time.
-    for name, (kid, _, _) in STAGE_KERNEL.items():
-        ev.check(L.arbor_set_kernel_events(kid, *kevents[name]))
     per_stage = {s: [] for s in stages}
     per_kernel = {s: [] for s in STAGE_KERNEL}
     for _ in range(args.steps):
         restore()
         torch.cuda.synchronize()
         marks = []
-        ev.run(active, marks)
+        ev.run(active, marks, ktiming)
         torch.cuda.synchronize()
         for si, s in enumerate(stages):
             per_stage[s].append(marks[si].elapsed_time(marks[si + 1]))
         for s, (e0, e1) in kevents.items():
             per_kernel[s].append(e0.elapsed_time(e1))
-    for kid, _, _ in STAGE_KERNEL.values():
-        ev.check(L.arbor_set_kernel_events(kid, None, None))
     status = int(ev.status)
     if status < 0:
         raise RuntimeError(f"device status {status}: {L.arbor_strerror(status)}")
@@ -583,7 +586,7 @@ def main():
         ce = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
         for e in ce:
             e.record()          # torch refuses elapsed_time on events it never recorded
-        ev.check(L.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, *ce))
+        ctm = L.timing(L.KERNEL_DECODE_CREDIT, *ce)
         t_sc, t_pl, t_k = [], [], []
         for rep in range(args.warmup + args.steps):
             for scored in (True, False):
@@ -593,7 +596,7 @@ def main():
                 if scored:
                     ev.check(L.arbor_tree_decode_attn_scored(
                         kv, active, 0, kv.layers, ev.q_dec, ev.out, ev.lse, 0.0,
-                        st["slice_layers"], 0, ev.A, ev.rows, ev.status, ev.ws))
+                        st["slice_layers"], 0, ev.A, ev.rows, ev.status, ev.ws, timing=ctm))
                 else:
                     ev.check(L.arbor_tree_decode_attn(kv, active, 0, kv.layers, ev.q_dec, ev.out,
                                                       ev.lse, 0.0, ev.status, ev.ws))
@@ -603,7 +606,6 @@ def main():
                     (t_sc if scored else t_pl).append(e0.elapsed_time(e1))
                     if scored:
                         t_k.append(ce[0].elapsed_time(ce[1]))
-        ev.check(L.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, None, None))
         if int(ev.status) < 0:
             raise RuntimeError(f"device status {int(ev.status)}")
         tk = float(np.mean(t_k))

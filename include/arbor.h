@@ -72,9 +72,34 @@ typedef enum { ARBOR_BF16 = 0, ARBOR_F32 = 1 } arbor_dtype_t;
 
 typedef enum { ARBOR_SELECT_TAIL_HEAVY = 0, ARBOR_SELECT_TAIL_ONLY = 1 } arbor_select_mode_t;
 
+/* Kernels of the path that a caller can time on their own (arbor_timing_t). */
+typedef enum {
+  ARBOR_KERNEL_SCORE_ATTN = 0,    /* the two-pass score kernel of arbor_score      */
+  ARBOR_KERNEL_SELECT = 1,        /* the selection kernel of arbor_select          */
+  ARBOR_KERNEL_COMPACT_MOVE = 2,  /* the row-move kernel of arbor_compact          */
+  ARBOR_KERNEL_DECODE_ATTN = 3,   /* the attention kernels of arbor_tree_decode_attn */
+  ARBOR_KERNEL_DECODE_CREDIT = 4, /* the credit kernel of arbor_tree_decode_attn_scored */
+  ARBOR_KERNEL_COUNT = 5
+} arbor_kernel_t;
+
+/* (host) A timing request that belongs to one call: when a call launches
+ * `kernel`, it records `start` on the launch stream right before that launch
+ * and `stop` right after it (for ARBOR_KERNEL_DECODE_ATTN around the up to
+ * three attention launches of the call, which run back to back), so
+ * hipEventElapsedTime(start, stop) after the stream has synchronised is the
+ * kernel's own duration.  The caller owns the events (created with timing on
+ * the device of the call) and the struct; the library keeps no reference
+ * after the call returns.  Calls that do not launch `kernel` record nothing. */
+typedef struct {
+  int32_t kernel;           /* arbor_kernel_t                                     */
+  hipEvent_t start;
+  hipEvent_t stop;
+} arbor_timing_t;
+
 /* (host) Shape of the KV pool.  head_dim in {64, 128}; page_size a multiple of
  * 16 and at most 256; q_per_kv = G query heads share one KV head (query head h
- * reads KV head h / G). */
+ * reads KV head h / G).  `timing` is an optional per-call timing request
+ * (NULL: none); it is read during the call only. */
 typedef struct {
   int32_t num_layers;
   int32_t num_kv_heads;
@@ -83,6 +108,7 @@ typedef struct {
   int32_t page_size;
   int32_t dtype;            /* arbor_dtype_t of K, V, q_win and decode q */
   int64_t num_pages;
+  const arbor_timing_t *timing;   /* (host, nullable) */
 } arbor_geom_t;
 
 /* (host struct of device pointers) The thought tree T = (V, E) of Sec. 3. */
@@ -345,31 +371,6 @@ int arbor_uncertainty(const void *logits, int32_t dtype, int32_t n_rows, int64_t
 /* Bytes of workspace arbor_uncertainty needs for n_rows rows of `vocab` logits. */
 size_t arbor_uncertainty_workspace_size(int32_t n_rows, int64_t vocab, int32_t dtype);
 
-/*
- * arbor_set_kernel_events -- timing support for callers that measure one
- * kernel of the path on its own (a roofline of that kernel rather than of the
- * whole entry point).  After the call, every launch of `kernel` by later entry
- * point calls is bracketed by hipEventRecord(start, s) and
- * hipEventRecord(stop, s) on the launch stream s, so hipEventElapsedTime(start,
- * stop) after the stream has synchronised gives the duration of the most recent
- * launch (for ARBOR_KERNEL_DECODE_ATTN: of the up to three attention launches
- * of one call, which run back to back).  The events belong to the caller, who
- * creates them with timing enabled on the device the calls run on and keeps
- * them alive while they are set.  start = stop = NULL stops the recording.
- * The setting is process-wide and is not synchronised with entry point calls
- * running on other host threads.
- * Errors: EINVAL for an unknown kernel id or only one of start, stop NULL.
- */
-typedef enum {
-  ARBOR_KERNEL_SCORE_ATTN = 0,    /* the two-pass score kernel of arbor_score      */
-  ARBOR_KERNEL_SELECT = 1,        /* the selection kernel of arbor_select          */
-  ARBOR_KERNEL_COMPACT_MOVE = 2,  /* the row-move kernel of arbor_compact          */
-  ARBOR_KERNEL_DECODE_ATTN = 3,   /* the attention kernels of arbor_tree_decode_attn */
-  ARBOR_KERNEL_DECODE_CREDIT = 4, /* the credit kernel of arbor_tree_decode_attn_scored */
-  ARBOR_KERNEL_COUNT = 5
-} arbor_kernel_t;
-
-int arbor_set_kernel_events(int32_t kernel, hipEvent_t start, hipEvent_t stop);
 
 #ifdef __cplusplus
 }

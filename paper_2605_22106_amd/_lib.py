@@ -22,18 +22,22 @@ LIB_PATH = os.path.join(_HERE, "libarbor.so")
 OK, OVER_BUDGET = 0, 1
 EINVAL, ENOPAGES, EHIP, EUNSUPPORTED, ENONFINITE, EWORKSPACE, ECORRUPT = -1, -2, -3, -4, -5, -6, -7
 BF16, F32 = 0, 1
-# kernels whose launches arbor_set_kernel_events can bracket with events
+# kernels a call can time on their own (arbor_timing_t)
 KERNEL_SCORE_ATTN, KERNEL_SELECT, KERNEL_COMPACT_MOVE, KERNEL_DECODE_ATTN = 0, 1, 2, 3
-KERNEL_DECODE_CREDIT = 4
+KERNEL_DECODE_CREDIT, KERNEL_COUNT = 4, 5
 SELECT_TAIL_HEAVY, SELECT_TAIL_ONLY = 0, 1
 MAX_DEPTH = 63
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("start", ctypes.c_void_p), ("stop", ctypes.c_void_p)]
 
 
 class Geom(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("q_per_kv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("num_pages", ctypes.c_int64)]
+                ("num_pages", ctypes.c_int64), ("timing", ctypes.POINTER(Timing))]
 
 
 class TreeS(ctypes.Structure):
@@ -103,7 +107,6 @@ def load() -> ctypes.CDLL:
             "arbor_uncertainty": (ctypes.c_int, [vp, i32, i32, i64, i32, vp, vp, i32, vp, vp, sz,
                                                  vp]),
             "arbor_uncertainty_workspace_size": (sz, [i32, i64, i32]),
-            "arbor_set_kernel_events": (ctypes.c_int, [i32, vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(lib, name)
@@ -116,7 +119,8 @@ def load() -> ctypes.CDLL:
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
             "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn",
-            "arbor_tree_decode_attn_scored", "arbor_uncertainty", "arbor_uncertainty_workspace_size", "arbor_set_kernel_events"]
+            "arbor_tree_decode_attn_scored", "arbor_uncertainty",
+            "arbor_uncertainty_workspace_size"]
 
 
 def _dev(t: torch.Tensor | None, name: str):
@@ -174,9 +178,12 @@ class KVState:
     def num_pages(self) -> int:
         return int(self.k.shape[1])
 
-    def geom(self) -> Geom:
-        return Geom(self.layers, self.kv_heads, self.q_per_kv, self.head_dim, self.page_size,
-                    self.dtype, self.num_pages)
+    def geom(self, timing: "Timing | None" = None) -> Geom:
+        g = Geom(self.layers, self.kv_heads, self.q_per_kv, self.head_dim, self.page_size,
+                 self.dtype, self.num_pages)
+        if timing is not None:
+            g.timing = ctypes.pointer(timing)
+        return g
 
     def tree(self) -> TreeS:
         return TreeS(self.num_nodes, self.num_tokens, _dev(self.parent, "parent"),
@@ -225,9 +232,15 @@ def arbor_strerror(code: int) -> str:
     return load().arbor_strerror(int(code)).decode()
 
 
+def timing(kernel: int, start, stop) -> Timing:
+    """A per-call timing request: `start` / `stop` (torch.cuda.Event with timing
+    enabled) are recorded around the call's launches of `kernel`."""
+    return Timing(int(kernel), ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event))
+
+
 def arbor_score(kv: KVState, observers, q_win, window, slice_layers, v_in, u_in, A, rows_seen,
-                a_out, s_out, params: dict, status, workspace, stream=None) -> int:
-    g, t, p = kv.geom(), kv.tree(), kv.pool()
+                a_out, s_out, params: dict, status, workspace, stream=None, timing=None) -> int:
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
     pa = params_struct(params)
     sl = (ctypes.c_int32 * len(slice_layers))(*[int(x) for x in slice_layers])
     return load().arbor_score(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p),
@@ -252,16 +265,17 @@ def arbor_allocate(kv: KVState, active, budget, s, params: dict, k_out, delta_ou
                                  _stream(stream))
 
 
-def arbor_select(kv: KVState, A, k, params: dict, sel_pos, status, stream=None) -> int:
-    g, t, p = kv.geom(), kv.tree(), kv.pool()
+def arbor_select(kv: KVState, A, k, params: dict, sel_pos, status, stream=None,
+                 timing=None) -> int:
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
     pa = params_struct(params)
     return load().arbor_select(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p), _dev(A, "A"),
                                _dev(k, "k"), ctypes.byref(pa), _dev(sel_pos, "sel_pos"),
                                _dev(status, "status"), _stream(stream))
 
 
-def arbor_compact(kv: KVState, k, sel_pos, status, workspace, stream=None) -> int:
-    g, t, p = kv.geom(), kv.tree(), kv.pool()
+def arbor_compact(kv: KVState, k, sel_pos, status, workspace, stream=None, timing=None) -> int:
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
     return load().arbor_compact(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p), _dev(k, "k"),
                                 _dev(sel_pos, "sel_pos"), _dev(status, "status"),
                                 _dev(workspace, "workspace"), int(workspace.numel()),
@@ -286,8 +300,8 @@ def arbor_rehydrate(kv: KVState, on_path, host_k, host_v, status, workspace, str
 
 
 def arbor_tree_decode_attn(kv: KVState, leaves, layer_begin, layer_end, q, out, lse_out,
-                           softmax_scale, status, workspace, stream=None) -> int:
-    g, t, p = kv.geom(), kv.tree(), kv.pool()
+                           softmax_scale, status, workspace, stream=None, timing=None) -> int:
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
     out_dtype = BF16 if out.dtype == torch.bfloat16 else F32
     return load().arbor_tree_decode_attn(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p),
                                          _dev(leaves, "leaves"), int(leaves.numel()),
@@ -300,11 +314,11 @@ def arbor_tree_decode_attn(kv: KVState, leaves, layer_begin, layer_end, q, out, 
 
 def arbor_tree_decode_attn_scored(kv: KVState, leaves, layer_begin, layer_end, q, out, lse_out,
                                   softmax_scale, slice_layers, self_window, A, rows_seen, status,
-                                  workspace, stream=None) -> int:
+                                  workspace, stream=None, timing=None) -> int:
     """arbor_tree_decode_attn plus the decode-time credit of this step's
     attention weights on the slice layers into A (fp32 [N]) and rows_seen
     (int64 [V])."""
-    g, t, p = kv.geom(), kv.tree(), kv.pool()
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
     out_dtype = BF16 if out.dtype == torch.bfloat16 else F32
     sl = (ctypes.c_int32 * max(1, len(slice_layers)))(*[int(x) for x in slice_layers])
     cr = DecodeCredit(sl, len(slice_layers), int(self_window), _dev(A, "A"),
@@ -338,11 +352,3 @@ def arbor_uncertainty(logits, top_k, u_out, status, workspace, dst=None, stream=
                                     _dev(u_out, "u_out"), int(u_out.numel()),
                                     _dev(status, "status"), _dev(workspace, "workspace"),
                                     int(workspace.numel()), _stream(stream))
-
-
-def arbor_set_kernel_events(kernel: int, start=None, stop=None) -> int:
-    """Bracket later launches of `kernel` with two timing events (torch.cuda.Event
-    objects, already recorded once so that they exist), or stop with None, None."""
-    def handle(e):
-        return None if e is None else ctypes.c_void_p(e.cuda_event)
-    return load().arbor_set_kernel_events(int(kernel), handle(start), handle(stop))

@@ -30,7 +30,6 @@ size_t allocate_workspace(const arbor_sizes_t *);
 size_t compact_workspace(const arbor_sizes_t *);
 size_t rehydrate_workspace(const arbor_sizes_t *);
 size_t decode_workspace(const arbor_geom_t *, const arbor_sizes_t *);
-KernelEvents g_kernel_events[ARBOR_KERNEL_COUNT];
 }  // namespace arbor
 
 using namespace arbor;
@@ -43,6 +42,11 @@ static int check_geom(const arbor_geom_t *g) {
   if (g->head_dim != 64 && g->head_dim != 128) return ARBOR_EUNSUPPORTED;
   if (g->page_size <= 0 || g->page_size % 16 != 0 || g->page_size > 256) return ARBOR_EUNSUPPORTED;
   if (g->num_pages > INT32_MAX) return ARBOR_EUNSUPPORTED;
+  if (g->timing) {
+    const arbor_timing_t *tm = g->timing;
+    if (tm->kernel < 0 || tm->kernel >= ARBOR_KERNEL_COUNT || !tm->start || !tm->stop)
+      return ARBOR_EINVAL;
+  }
   return ARBOR_OK;
 }
 
@@ -233,11 +237,3 @@ int arbor_uncertainty(const void *logits, int32_t dtype, int32_t n_rows, int64_t
 }
 
 }  // extern "C"
-
-int arbor_set_kernel_events(int32_t kernel, hipEvent_t start, hipEvent_t stop) {
-  if (kernel < 0 || kernel >= ARBOR_KERNEL_COUNT) return ARBOR_EINVAL;
-  if ((start == nullptr) != (stop == nullptr)) return ARBOR_EINVAL;
-  g_kernel_events[kernel].start = start;
-  g_kernel_events[kernel].stop = stop;
-  return ARBOR_OK;
-}

@@ -283,17 +283,15 @@ struct Carve {
 
 static inline int hip_ok(hipError_t e) { return e == hipSuccess ? ARBOR_OK : ARBOR_EHIP; }
 
-// Events a caller asked to have recorded around one kernel's launches
-// (arbor_set_kernel_events); defined in the API translation unit.
-struct KernelEvents {
-  hipEvent_t start = nullptr, stop = nullptr;
-};
-extern KernelEvents g_kernel_events[ARBOR_KERNEL_COUNT];
-inline void timing_begin(int kernel, hipStream_t s) {
-  if (g_kernel_events[kernel].start) (void)hipEventRecord(g_kernel_events[kernel].start, s);
+// The call's own timing request (arbor_geom_t.timing): events recorded on the
+// launch stream around the launches of one named kernel.
+inline void timing_begin(const arbor_geom_t *g, int kernel, hipStream_t s) {
+  const arbor_timing_t *tm = g->timing;
+  if (tm && tm->kernel == kernel && tm->start) (void)hipEventRecord(tm->start, s);
 }
-inline void timing_end(int kernel, hipStream_t s) {
-  if (g_kernel_events[kernel].stop) (void)hipEventRecord(g_kernel_events[kernel].stop, s);
+inline void timing_end(const arbor_geom_t *g, int kernel, hipStream_t s) {
+  const arbor_timing_t *tm = g->timing;
+  if (tm && tm->kernel == kernel && tm->stop) (void)hipEventRecord(tm->stop, s);
 }
 
 }  // namespace arbor

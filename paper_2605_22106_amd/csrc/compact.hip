@@ -295,11 +295,11 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
   const int fin_blocks = (t.V + 3) / 4;
-  timing_begin(ARBOR_KERNEL_COMPACT_MOVE, stream);
+  timing_begin(geom, ARBOR_KERNEL_COMPACT_MOVE, stream);
   hipLaunchKernelGGL(compact_move, dim3(move_blocks + fin_blocks), dim3(256), 0, stream, t, pl, k,
                      mv_src, mv_dst, first_moved, sel_pos, push_base, changed, meta, move_blocks,
                      status);
-  timing_end(ARBOR_KERNEL_COMPACT_MOVE, stream);
+  timing_end(geom, ARBOR_KERNEL_COMPACT_MOVE, stream);
   return hip_ok(hipGetLastError());
 }
 

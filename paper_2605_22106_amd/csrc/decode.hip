@@ -6,8 +6,10 @@
 // kv head).  Its rows are the G query heads of every active leaf below a, so a
 // shared ancestor is streamed from HBM once for all leaves that need it.  A
 // wave computes S = K Q^T with bf16 MFMA (keys along M, so each lane owns one
-// query row), an online softmax at 64-key granularity, and O += P V with fp32
-// MFMA (16x16x4) so P is never rounded to bf16; the key order inside each MFMA
+// query row), an online softmax at 64-key granularity, and O += P V.  For
+// bf16 pools P is split into a bf16 high part and a bf16 remainder, both
+// multiplied with the exact bf16 V by bf16 MFMAs (fp32-level accuracy of P);
+// fp32 pools use the fp32 MFMA (16x16x4).  The key order inside each MFMA
 // step is permuted so P needs no cross-lane movement.  Each unit writes an
 // unnormalised partial (max, sum, o); the merge kernel combines the partials of
 // a leaf in root-to-leaf order, so results are bitwise reproducible.
@@ -787,29 +789,29 @@ __global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
 }
 
 template <class T, int D>
-void launch_decode_kernels(const DecArgs &a, void *out, int out_dtype, float *lse_out,
-                           const CreditArgs *cr, hipStream_t stream) {
+void launch_decode_kernels(const arbor_geom_t *geom, const DecArgs &a, void *out, int out_dtype,
+                           float *lse_out, const CreditArgs *cr, hipStream_t stream) {
   const int grid = 2048;
   // rows of a work unit are at most n_leaves * G: only the row classes that
   // can occur are launched
   const int max_rows = a.n_leaves * a.pl.G;
-  timing_begin(ARBOR_KERNEL_DECODE_ATTN, stream);
+  timing_begin(geom, ARBOR_KERNEL_DECODE_ATTN, stream);
   hipLaunchKernelGGL((decode_attn<T, D, 1>), dim3(grid), dim3(256), 0, stream, a, 0);
   if (max_rows > 16)
     hipLaunchKernelGGL((decode_attn<T, D, 2>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
   if (max_rows > 32)
     hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
-  timing_end(ARBOR_KERNEL_DECODE_ATTN, stream);
+  timing_end(geom, ARBOR_KERNEL_DECODE_ATTN, stream);
   const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv * a.pl.G;
   const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
   hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
                      lse_out);
   if (cr) {
     // workgroups stride over the sub-pages of the plan's units
-    timing_begin(ARBOR_KERNEL_DECODE_CREDIT, stream);
+    timing_begin(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
     const int cgrid = std::min(a.max_items * (CHUNK / 16), 1024);
     hipLaunchKernelGGL((decode_credit<T, D>), dim3(cgrid), dim3(256), 0, stream, a, *cr);
-    timing_end(ARBOR_KERNEL_DECODE_CREDIT, stream);
+    timing_end(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
   }
 }
 
@@ -917,14 +919,14 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   const CreditArgs *crp = credit ? &cr : nullptr;
   if (geom->dtype == ARBOR_BF16) {
     if (geom->head_dim == 128)
-      launch_decode_kernels<__bf16, 128>(a, out, out_dtype, lse_out, crp, stream);
+      launch_decode_kernels<__bf16, 128>(geom, a, out, out_dtype, lse_out, crp, stream);
     else
-      launch_decode_kernels<__bf16, 64>(a, out, out_dtype, lse_out, crp, stream);
+      launch_decode_kernels<__bf16, 64>(geom, a, out, out_dtype, lse_out, crp, stream);
   } else {
     if (geom->head_dim == 128)
-      launch_decode_kernels<float, 128>(a, out, out_dtype, lse_out, crp, stream);
+      launch_decode_kernels<float, 128>(geom, a, out, out_dtype, lse_out, crp, stream);
     else
-      launch_decode_kernels<float, 64>(a, out, out_dtype, lse_out, crp, stream);
+      launch_decode_kernels<float, 64>(geom, a, out, out_dtype, lse_out, crp, stream);
   }
   return hip_ok(hipGetLastError());
 }

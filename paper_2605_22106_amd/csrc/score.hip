@@ -1032,9 +1032,9 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
                        tbase, nsp, ctxlen, odepth, anc);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
-    timing_begin(ARBOR_KERNEL_SCORE_ATTN, stream);
+    timing_begin(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     launch_attn(geom->dtype, geom->head_dim, NRB, grid, stream, a);
-    timing_end(ARBOR_KERNEL_SCORE_ATTN, stream);
+    timing_end(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
     hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen);
   }

@@ -223,10 +223,10 @@ int launch_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   Pool pl = make_pool(geom, pool);
   if (t.V <= 0) return ARBOR_OK;
   dim3 grid((t.V + 3) / 4);
-  timing_begin(ARBOR_KERNEL_SELECT, stream);
+  timing_begin(geom, ARBOR_KERNEL_SELECT, stream);
   hipLaunchKernelGGL(select_kernel, grid, dim3(256), 0, stream, t, pl, A, k, params->l_tail,
                      params->select_mode, sel_pos, status);
-  timing_end(ARBOR_KERNEL_SELECT, stream);
+  timing_end(geom, ARBOR_KERNEL_SELECT, stream);
   return hip_ok(hipGetLastError());
 }
 

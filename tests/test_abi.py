@@ -29,7 +29,7 @@ def test_library_exports_every_symbol():
 
 STRUCTS = {"Geom": "arbor_geom_t", "TreeS": "arbor_tree_t", "PoolS": "arbor_pool_t",
            "Params": "arbor_params_t", "Sizes": "arbor_sizes_t",
-           "DecodeCredit": "arbor_decode_credit_t"}
+           "DecodeCredit": "arbor_decode_credit_t", "Timing": "arbor_timing_t"}
 
 
 def test_struct_layouts(tmp_path):
@@ -75,14 +75,26 @@ def test_product_path_refuses_cpu_tensors():
         L._dev(torch.zeros(3), "x")
 
 
-def test_kernel_events_setter_validates_on_the_host():
+def test_timing_request_is_validated_on_the_host():
+    """A per-call timing request names a known kernel and both events; a bad
+    one is refused before anything is enqueued (the geometry is checked
+    first, so no tree or pool is needed)."""
     lib = L.load()
-    assert lib.arbor_set_kernel_events(L.KERNEL_SCORE_ATTN, None, None) == L.OK
-    assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_CREDIT, None, None) == L.OK
-    assert lib.arbor_set_kernel_events(5, None, None) == L.EINVAL
-    assert lib.arbor_set_kernel_events(-1, None, None) == L.EINVAL
-    # one of the two events missing
-    assert lib.arbor_set_kernel_events(L.KERNEL_DECODE_ATTN, ctypes.c_void_p(1), None) == L.EINVAL
+    e = ctypes.c_void_p(1)
+    for bad in (L.Timing(L.KERNEL_COUNT, e, e),
+                L.Timing(-1, e, e), L.Timing(L.KERNEL_SELECT, e, None),
+                L.Timing(L.KERNEL_SELECT, None, e)):
+        g = L.Geom(32, 8, 4, 128, 16, L.BF16, 1408)
+        g.timing = ctypes.pointer(bad)
+        assert lib.arbor_select(ctypes.byref(g), None, None, None, None, None, None, None,
+                                None) == L.EINVAL
+
+
+def test_library_keeps_no_timing_state():
+    """No entry point other than those of the header is exported: in
+    particular no process-wide setter of timing events."""
+    lib = L.load()
+    assert not hasattr(lib, "arbor_set_kernel_events")
 
 
 def test_uncertainty_workspace_sizes_on_the_host():
