@@ -232,12 +232,25 @@ def score(st, observers, q_win, window, slice_layers, q_per_kv, v_sig, u_sig, A,
 # ----------------------------------------------------------------------------
 # O3  allocate  (Eq. 2, Eq. 3, KKT view; Alg. 2 Transition / Pressure)
 # ----------------------------------------------------------------------------
+def power(s, gamma):
+    """s^gamma of Eq. 2.  For an integer exponent up to 4 the plain product:
+    s is an fp32 value, so s * s is exact in fp64 and one more product rounds
+    once, which is the correctly rounded power; other exponents use math.pow."""
+    s = float(s)
+    if gamma in (1.0, 2.0, 3.0, 4.0):
+        g = int(gamma)
+        return s if g == 1 else (s * s if g == 2 else (s * s * s if g == 3 else (s * s) * (s * s)))
+    return math.pow(s, gamma)
+
+
 def value_geometry_weight(s, d, delta, p):
     """w_i = eta * s_i^gamma * exp(-lambda_d d_i) * exp(-lambda_Delta Delta_i):
     the off-path weight of Eq. 2 without alpha (the KKT weight with the eta
-    discount that applies to every node outside Path*)."""
-    return (p["eta"] * math.pow(float(s), p["gamma"])) * math.exp(-p["lambda_d"] * float(d)) \
+    discount that applies to every node outside Path*).  -0 is returned as +0
+    (s = -0 with an odd gamma), the same weight as s = +0."""
+    w = (p["eta"] * power(s, p["gamma"])) * math.exp(-p["lambda_d"] * float(d)) \
         * math.exp(-p["lambda_delta"] * float(delta))
+    return 0.0 if w == 0.0 else w
 
 
 def floor_count(n, c, p):
@@ -276,6 +289,12 @@ def allocate(parent, n_full, n_kept, active, budget, s, p):
             path_total += int(k[i])
     b_off = int(budget) - path_total
     off = [i for i in range(V) if not on_path[i]]
+    # s_i = clip(sigmoid(theta^T phi_i), 0, 1) (Sec. 4 MSVE) lies in [0, 1]
+    s_off = [float(s[i]) for i in off]
+    if any(math.isnan(x) for x in s_off):
+        return k.astype(np.int32), delta.astype(np.int32), on_path, ENONFINITE
+    if any(not (0.0 <= x <= 1.0) for x in s_off):
+        return k.astype(np.int32), delta.astype(np.int32), on_path, EINVAL
     F = {i: floor_count(n_full[i], n_kept[i], p) for i in off}
     w = {i: value_geometry_weight(s[i], d[i], delta[i], p) for i in off}
     status = OK

@@ -23,8 +23,16 @@ BASE = dict(alpha_max=math.inf, gamma=2.0, lambda_d=0.1, lambda_delta=0.5, eta=0
             r_min=0.05, k_min=2, l_tail=3)
 
 
+def power(s, gamma):
+    """s^gamma: the exact rational power rounded once for integer exponents
+    (float(Fraction) rounds to nearest), numpy's power otherwise."""
+    if float(gamma).is_integer() and gamma >= 1:
+        return float(Fraction(float(s)) ** int(gamma))
+    return float(np.power(np.float64(s), gamma))
+
+
 def weight(s, d, delta, p):
-    return float(np.float64(p["eta"]) * np.power(np.float64(s), p["gamma"])
+    return float(np.float64(p["eta"]) * np.float64(power(s, p["gamma"]))
                  * np.exp(-p["lambda_d"] * d) * np.exp(-p["lambda_delta"] * delta))
 
 
@@ -94,6 +102,8 @@ def test_allocate_matches_brute_force(seed):
         p["alpha_max"] = 0.7
     if seed % 4 == 2:
         p.update(gamma=1.0, lambda_d=-0.2)
+    if seed % 4 == 3:
+        p.update(gamma=3.0)
     total = sum(n_full)
     for rho in (0.2, 0.45, 0.7, 1.0):
         budget = int(rho * total)
@@ -203,3 +213,48 @@ def test_allocate_without_rehydration(seed):
         k1, *_ = O.allocate(parent, n_full, n_kept, active, budget, s, dict(BASE))
         off = [i for i in range(V) if not on_path[i]]
         assert sum(int(k[i]) for i in off) >= sum(int(k1[i]) for i in off)
+
+
+def test_integer_powers_are_correctly_rounded():
+    """s^gamma of Eq. 2 for gamma = 1..4 equals the exact power of the fp32
+    score rounded once to fp64."""
+    rng = np.random.default_rng(5)
+    for x in rng.random(2000).astype(np.float32):
+        for g in (1, 2, 3, 4):
+            assert O.power(x, float(g)) == float(Fraction(float(x)) ** g)
+
+
+@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("gamma", [1.0, 3.0])
+def test_negative_zero_score_is_zero(seed, gamma):
+    """s = -0 gives w = -0 for an odd gamma; it ranks exactly as s = +0, also in
+    the Pressure drain (ties to the lower id), against the brute force."""
+    parent, n_full, n_kept, active, s = random_case(seed + 500)
+    rng = np.random.default_rng(seed)
+    zeros = rng.choice(len(parent), size=4, replace=False)
+    s_neg, s_pos = s.copy(), s.copy()
+    s_neg[zeros] = np.float32(-0.0)
+    s_pos[zeros] = np.float32(0.0)
+    p = dict(BASE, gamma=gamma)
+    for rho in (0.1, 0.2, 0.45, 1.0):
+        budget = int(rho * sum(n_full))
+        k, _, _, st = O.allocate(parent, n_full, n_kept, active, budget, s_neg, p)
+        k0, _, _, st0 = O.allocate(parent, n_full, n_kept, active, budget, s_pos, p)
+        kb, sb = brute_force(parent, n_full, n_kept, active, budget, s_pos, p)
+        assert st == st0 == sb
+        assert k.tolist() == k0.tolist() == kb.tolist()
+
+
+def test_scores_outside_the_unit_interval_are_rejected():
+    """s_i = clip(sigmoid(.), 0, 1): an off-path score outside [0, 1] is an
+    invalid argument, a NaN one is non-finite; Path* scores are never read."""
+    parent, n_full = synth.complete_tree(2, 2, 20, 10)
+    s = np.full(len(parent), 0.5, np.float32)
+    p = dict(BASE)
+    for bad, code in ((1.5, O.EINVAL), (-0.25, O.EINVAL), (np.nan, O.ENONFINITE)):
+        x = s.copy()
+        x[2] = bad                                  # off the path of leaf 3
+        assert O.allocate(parent, n_full, n_full, [3], 40, x, p)[3] == code
+        x = s.copy()
+        x[1] = bad                                  # on the path of leaf 3
+        assert O.allocate(parent, n_full, n_full, [3], 40, x, p)[3] in (O.OK, O.OVER_BUDGET)
