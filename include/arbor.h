@@ -225,8 +225,11 @@ int arbor_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_
  * the Eq. 3 floors already exceed the budget (Pressure) blocks are lowered
  * towards min(K_min, c_i) in ascending w_i (ties: lower id); if that is not
  * enough *status gets ARBOR_OVER_BUDGET and k_out holds the lowered counts.
- * s is fp32 [V] in [0, 1]; k_out int32 [V].  fp64 arithmetic, no contraction.
- * Errors: EINVAL (malformed tree, bad leaf ids, n_active < 1), ENONFINITE (NaN s).
+ * s is fp32 [V] in [0, 1] (the clipped MSVE score; -0 counts as +0); k_out
+ * int32 [V].  fp64 arithmetic, no contraction; s^gamma is correctly rounded
+ * for gamma in {1, 2, 3, 4} and the device pow otherwise.
+ * Errors: EINVAL (malformed tree, bad leaf ids, n_active < 1, an off-path s
+ * outside [0, 1]), ENONFINITE (NaN s off the path).
  */
 int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_active,
                    int64_t budget_tokens, const float *s, const arbor_params_t *params,

@@ -52,11 +52,13 @@ struct AllocParams {
   double dexp[kDecay], texp[kDecay];
 };
 
-// s^gamma; exact for the common gamma = 2 (s is an fp32 value, its square is
-// a double) and gamma = 1
+// s^gamma, correctly rounded for the integer exponents 1..4: s is an fp32
+// value, so s * s is exact in fp64 and one more product rounds once
 __device__ __forceinline__ double pow_gamma(double s, double gamma) {
-  if (gamma == 2.0) return s * s;
   if (gamma == 1.0) return s;
+  if (gamma == 2.0) return s * s;
+  if (gamma == 3.0) return (s * s) * s;
+  if (gamma == 4.0) return (s * s) * (s * s);
   return pow(s, gamma);
 }
 
@@ -381,8 +383,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       nd.w[i] = 0.0;
       continue;
     }
+    // s_i = clip(sigmoid(.), 0, 1) lies in [0, 1]
     const float sf = s_in[i];
     if (!(sf == sf)) atomicOr(&s_err, 2);
+    else if (!(sf >= 0.f && sf <= 1.f)) atomicOr(&s_err, 4);
     const double s = (double)sf;
     // Eq. 3 at the ratio floor r_min, capped at the resident count
     int f = max(p.k_min, min(p.l_tail, n));
@@ -394,6 +398,9 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     double w = p.eta * pow_gamma(s, p.gamma);
     w = w * (di < kDecay ? p.dexp[di] : exp(-p.lambda_d * (double)di));
     w = w * (best < kDecay ? p.texp[best] : exp(-p.lambda_delta * (double)best));
+    // -0 (s = -0 with an odd gamma) as +0: the Pressure order compares bit
+    // patterns, in which -0 would rank above every positive weight
+    w = w == 0.0 ? 0.0 : w;
     nd.w[i] = w;
     nd.W[i] = w * (double)n;
     sum_F += f;
@@ -407,7 +414,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     sum_red = v3[2];
   }
   if (s_err) {
-    if (tid == 0) status_error(status, ARBOR_ENONFINITE);
+    if (tid == 0) status_error(status, (s_err & 2) ? ARBOR_ENONFINITE : ARBOR_EINVAL);
     return;
   }
   const int64_t b_off = budget - path_tok;
