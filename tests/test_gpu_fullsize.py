@@ -92,6 +92,18 @@ def _rows(kv, pool, pages, rs, layer=None):
     return x.cpu()
 
 
+def _decode_layers_vs_oracle(kv, st, out_np, q, layers):
+    """out_np[:, l] for every active leaf and query head of each layer l against
+    O.tree_decode_attn run on that layer of the current pool (fp64)."""
+    leaves = st["active"].tolist()
+    for l in layers:
+        ost = _meta(kv, k=kv.k[l:l + 1].float().cpu().numpy(),
+                    v=kv.v[l:l + 1].float().cpu().numpy())
+        o_o, _ = O.tree_decode_attn(ost, leaves, 0, 1, np_float(q[:, l:l + 1]), kv.q_per_kv)
+        err = np.abs(out_np[:, l:l + 1] - o_o).max()
+        assert err <= 2e-3, (l, err)
+
+
 @pytest.fixture(scope="module")
 def llama8b():
     cfg = synth.CONFIGS["llama8b"]
@@ -201,6 +213,9 @@ def test_llama8b_event_stage_by_stage(llama8b):
         o_ref = (w / w.sum()) @ Vv
         err = np.abs(out_np[b, layer, h] - o_ref).max()
         assert err <= 2e-3, (b, layer, h, err)
+    # every (leaf, query head) of the two slice layers against the oracle's
+    # decode on that layer of the compacted state
+    _decode_layers_vs_oracle(kv, st, out_np, q, st["slice_layers"])
 
     # decode with the decode-time credit: the same outputs bitwise, and A /
     # rows_seen against the oracle on the slice layers (the only K it reads)
@@ -296,6 +311,16 @@ def test_llama70b_score_sample_allocate_select_compact_decode(llama70b):
     for i, keep in sel_o.items():
         b = int(meta0["tok_off"][i])
         assert np.array_equal(sel_np[b:b + len(keep)], np.array(keep, np.int32)), i
+    # K/V of sampled moved rows (every layer and kv head), read before the
+    # compaction from the slots that hold their positions
+    moved = [(i, s_) for i, keep in sel_o.items() for s_, pos in enumerate(keep) if pos != s_]
+    assert moved, "the event moves rows"
+    pick = [moved[j] for j in rng.choice(len(moved), size=min(256, len(moved)), replace=False)]
+    po0 = meta0["page_off"]
+    src_pages = torch.tensor([int(meta0["page_table"][po0[i] + sel_o[i][s_] // P])
+                              for i, s_ in pick], device="cuda")
+    src_r = torch.tensor([sel_o[i][s_] % P for i, s_ in pick], device="cuda")
+    want = [pool[:, src_pages, :, src_r, :].clone() for pool in (kv.k, kv.v)]
     check_rc(L.arbor_compact(kv, k, sel, stt, ws))
     torch.cuda.synchronize()
     assert int(stt) == L.OK
@@ -303,6 +328,15 @@ def test_llama70b_score_sample_allocate_select_compact_decode(llama70b):
     meta1 = _meta(kv)
     for key in ("n_kept", "page_table", "slot_pos"):
         assert np.array_equal(meta1[key], new_o[key]), key
+    top = int(meta1["free_top"])
+    assert top == int(new_o["free_top"])
+    assert np.array_equal(meta1["free_stack"][:top], new_o["free_stack"][:top])
+    dst_pages = torch.tensor([int(meta1["page_table"][po0[i] + s_ // P]) for i, s_ in pick],
+                             device="cuda")
+    dst_r = torch.tensor([s_ % P for _, s_ in pick], device="cuda")
+    for pool, w in zip((kv.k, kv.v), want):
+        got = pool[:, dst_pages, :, dst_r, :]
+        assert torch.equal(got.view(torch.int16), w.view(torch.int16))
     # decode over all 80 layers; sampled outputs against fp64
     Hq = kv.kv_heads * kv.q_per_kv
     nl = active.numel()
@@ -329,6 +363,8 @@ def test_llama70b_score_sample_allocate_select_compact_decode(llama70b):
         w = np.exp(z - z.max())
         err = np.abs(out_np[b, layer, h] - (w / w.sum()) @ Vv).max()
         assert err <= 2e-3, (b, layer, h, err)
+    # every (leaf, query head) of the last layer against the oracle's decode
+    _decode_layers_vs_oracle(kv, st, out_np, q, [kv.layers - 1])
 
 
 def test_dpts_wide_frontier():
