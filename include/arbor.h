@@ -269,6 +269,24 @@ int arbor_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *po
                   size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * arbor_compact_noalloc -- arbor_compact for callers that cannot allocate
+ * memory: code under stream capture, tight serving loops, harnesses that
+ * forbid allocation.  It takes no workspace; its scratch is a device array of
+ * ARBOR_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends.  It allocates nothing (no hipMalloc, no hipFree, no
+ * allocating library routine) and writes exactly what arbor_compact writes.
+ * Limit: 12 bytes per token of the tree plus 16 per node (and 8 KiB) must fit
+ * the array, which holds trees of up to about 2.7 M tokens; a larger tree is
+ * refused with ARBOR_EWORKSPACE before anything is enqueued.  All calls on one
+ * GPU share its array: calls that overlap on one GPU (unordered streams)
+ * race and must not be issued.  Other errors as arbor_compact.
+ */
+#define ARBOR_NOALLOC_SCRATCH_BYTES (32u << 20)
+int arbor_compact_noalloc(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                          const int32_t *k, const int32_t *sel_pos, int32_t *status,
+                          hipStream_t stream);
+
+/*
  * arbor_rehydrate -- lazy rehydration (Sec. 4 "Lazy rehydration"; Alg. 2
  * Transition): every node with on_path[i] != 0 and c_i < n_i is restored to
  * full retention before the next decode step, in ascending id (root first).

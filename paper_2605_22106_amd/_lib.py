@@ -97,6 +97,7 @@ def load() -> ctypes.CDLL:
             "arbor_allocate": (ctypes.c_int, [T, vp, i32, i64, vp, Pa, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_select": (ctypes.c_int, [G, T, Pl, vp, vp, Pa, vp, vp, vp]),
             "arbor_compact": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, sz, vp]),
+            "arbor_compact_noalloc": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp]),
             "arbor_rehydrate": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_tree_decode_attn": (ctypes.c_int, [G, T, Pl, vp, i32, i32, i32, vp, vp, i32,
                                                       vp, ctypes.c_float, vp, vp, sz, vp]),
@@ -118,7 +119,7 @@ def load() -> ctypes.CDLL:
 
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
-            "arbor_select", "arbor_compact", "arbor_rehydrate", "arbor_tree_decode_attn",
+            "arbor_select", "arbor_compact", "arbor_compact_noalloc", "arbor_rehydrate", "arbor_tree_decode_attn",
             "arbor_tree_decode_attn_scored", "arbor_uncertainty",
             "arbor_uncertainty_workspace_size"]
 
@@ -280,6 +281,14 @@ def arbor_compact(kv: KVState, k, sel_pos, status, workspace, stream=None, timin
                                 _dev(sel_pos, "sel_pos"), _dev(status, "status"),
                                 _dev(workspace, "workspace"), int(workspace.numel()),
                                 _stream(stream))
+
+
+def arbor_compact_noalloc(kv: KVState, k, sel_pos, status, stream=None) -> int:
+    """arbor_compact with the library's own scratch (no workspace argument)."""
+    g, t, p = kv.geom(), kv.tree(), kv.pool()
+    return load().arbor_compact_noalloc(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p),
+                                        _dev(k, "k"), _dev(sel_pos, "sel_pos"),
+                                        _dev(status, "status"), _stream(stream))
 
 
 def _host_or_dev(t: torch.Tensor, name: str):
