@@ -58,6 +58,7 @@ ENONFINITE = -5
 
 TAIL_HEAVY = 0
 TAIL_ONLY = 1
+SINKS_TAIL = 2
 
 
 # ----------------------------------------------------------------------------
@@ -243,12 +244,14 @@ def power(s, gamma):
     return math.pow(s, gamma)
 
 
-def value_geometry_weight(s, d, delta, p):
-    """w_i = eta * s_i^gamma * exp(-lambda_d d_i) * exp(-lambda_Delta Delta_i):
-    the off-path weight of Eq. 2 without alpha (the KKT weight with the eta
-    discount that applies to every node outside Path*).  -0 is returned as +0
-    (s = -0 with an odd gamma), the same weight as s = +0."""
-    w = (p["eta"] * power(s, p["gamma"])) * math.exp(-p["lambda_d"] * float(d)) \
+def value_geometry_weight(s, d, delta, p, on_path=False):
+    """w_i = eta^[i not in Path*] * s_i^gamma * exp(-lambda_d d_i) * exp(-lambda_Delta Delta_i):
+    the weight of Eq. 2 without alpha (the KKT weight).  The off-path discount
+    eta applies to every block outside Path*; a Path* block only reaches Eq. 2
+    under floor protection.  -0 is returned as +0 (s = -0 with an odd gamma),
+    the same weight as s = +0."""
+    eta = 1.0 if on_path else p["eta"]
+    w = (eta * power(s, p["gamma"])) * math.exp(-p["lambda_d"] * float(d)) \
         * math.exp(-p["lambda_delta"] * float(delta))
     return 0.0 if w == 0.0 else w
 
@@ -263,47 +266,63 @@ def floor_count(n, c, p):
 def allocate(parent, n_full, n_kept, active, budget, s, p):
     """Keep-counts k_i under the global token budget B.
 
-    Path* nodes are pinned at k_i = n_i (invariant (i), full protection), or at
-    their resident count c_i when p["lazy_rehydration"] is 0 (evicted tokens are
-    never restored: the "w/o lazy rehydration" setting of Table 4).  For
-    every other node, Eq. 2 gives r_i(alpha) = clip(alpha w_i, r_min, 1) and
-    Eq. 3 gives k_i(alpha); an off-path node never re-grows beyond its resident
-    count c_i (Alg. 2 only lowers k off the path).  alpha is the one global
-    scale of the KKT view, chosen as the largest alpha (<= alpha_max) whose
-    total fits B.  Eq. 3 keeps the j-th token of block i exactly when
-    floor(alpha w_i n_i) >= j, i.e. when alpha >= j / (w_i n_i): that quotient
-    is the price of token j.  Equal prices enter together, because alpha is a
-    single scalar.  If even the floors do not fit (Pressure), nodes are lowered
-    towards min(K_min, c_i) in ascending priority w_i (ties: lower id) until
-    the total fits; if it still does not, the status is OVER_BUDGET.
+    Invariant (i), active-path protection, comes in two forms.  Full
+    protection (p["k_protect"] = 0, the default) pins every Path* node at
+    k_i = n_i, or at its resident count c_i when p["lazy_rehydration"] is 0
+    (evicted tokens are never restored: the "w/o lazy rehydration" setting of
+    Table 4).  Floor protection (k_protect > 0) lets Path* nodes take part in
+    Eq. 2 and Eq. 3 like every other node, without the off-path discount eta,
+    with a floor of k_protect tokens, up to n_i (up to c_i without
+    rehydration).
+
+    Every node that is not pinned gets r_i(alpha) = clip(alpha w_i, r_min, 1)
+    from Eq. 2 and k_i(alpha) from Eq. 3; a node off the path never re-grows
+    beyond its resident count c_i (Alg. 2 only lowers k off the path).  alpha
+    is the one global scale of the KKT view, chosen as the largest alpha
+    (<= alpha_max) whose total fits B.  Eq. 3 keeps the j-th token of block i
+    exactly when floor(alpha w_i n_i) >= j, i.e. when alpha >= j / (w_i n_i):
+    that quotient is the price of token j.  Equal prices enter together,
+    because alpha is a single scalar.  If even the floors do not fit
+    (Pressure), nodes off the path are lowered towards min(K_min, c_i) in
+    ascending priority w_i (ties: lower id) until the total fits; if it still
+    does not, the status is OVER_BUDGET.  Path* nodes keep their floors.
     Returns (k, delta, on_path, status).
     """
     V = len(parent)
     d, on_path, delta = geometry(parent, active)
     k = np.zeros(V, dtype=np.int64)
-    path_total = 0
     rehyd = int(p.get("lazy_rehydration", 1)) != 0
-    for i in range(V):
-        if on_path[i]:
-            k[i] = int(n_full[i]) if rehyd else int(n_kept[i])
-            path_total += int(k[i])
+    k_protect = int(p.get("k_protect", 0))
+    pinned = [i for i in range(V) if on_path[i] and k_protect == 0]
+    free = [i for i in range(V) if not (on_path[i] and k_protect == 0)]
+    path_total = 0
+    for i in pinned:
+        k[i] = int(n_full[i]) if rehyd else int(n_kept[i])
+        path_total += int(k[i])
     b_off = int(budget) - path_total
-    off = [i for i in range(V) if not on_path[i]]
     # s_i = clip(sigmoid(theta^T phi_i), 0, 1) (Sec. 4 MSVE) lies in [0, 1]
-    s_off = [float(s[i]) for i in off]
-    if any(math.isnan(x) for x in s_off):
+    s_free = [float(s[i]) for i in free]
+    if any(math.isnan(x) for x in s_free):
         return k.astype(np.int32), delta.astype(np.int32), on_path, ENONFINITE
-    if any(not (0.0 <= x <= 1.0) for x in s_off):
+    if any(not (0.0 <= x <= 1.0) for x in s_free):
         return k.astype(np.int32), delta.astype(np.int32), on_path, EINVAL
-    F = {i: floor_count(n_full[i], n_kept[i], p) for i in off}
-    w = {i: value_geometry_weight(s[i], d[i], delta[i], p) for i in off}
+    # upper end of each node's count: resident tokens, or the whole span for
+    # a Path* node that rehydration restores
+    cap = {i: int(n_full[i]) if (on_path[i] and rehyd) else int(n_kept[i]) for i in free}
+    F = {}
+    for i in free:
+        f = floor_count(n_full[i], cap[i], p)
+        if on_path[i]:
+            f = max(f, min(cap[i], k_protect))
+        F[i] = f
+    w = {i: value_geometry_weight(s[i], d[i], delta[i], p, bool(on_path[i])) for i in free}
     status = OK
     if sum(F.values()) <= b_off:
         extra = b_off - sum(F.values())
         prices = []
-        for i in off:
+        for i in free:
             W = w[i] * float(n_full[i])
-            for j in range(F[i] + 1, int(n_kept[i]) + 1):
+            for j in range(F[i] + 1, cap[i] + 1):
                 price = float(j) / W if W > 0 else math.inf
                 if math.isfinite(price) and price <= p["alpha_max"]:
                     prices.append((price, i))
@@ -313,14 +332,15 @@ def allocate(parent, n_full, n_kept, active, budget, s, p):
         else:
             cut = prices[extra][0]        # the first price that no longer fits
             kept = [t for t in prices if t[0] < cut]
-        for i in off:
+        for i in free:
             k[i] = F[i]
         for (_, i) in kept:
             k[i] += 1
     else:
-        for i in off:
+        for i in free:
             k[i] = F[i]
         excess = sum(F.values()) - b_off
+        off = [i for i in free if not on_path[i]]
         for i in sorted(off, key=lambda i: (w[i], i)):
             if excess <= 0:
                 break
@@ -337,7 +357,7 @@ def allocate(parent, n_full, n_kept, active, budget, s, p):
 # ----------------------------------------------------------------------------
 # O4  select  (Sec. 4 Execution; Alg. 1 Evict)
 # ----------------------------------------------------------------------------
-def select(st, A, k, l_tail, select_mode=TAIL_HEAVY):
+def select(st, A, k, l_tail, select_mode=TAIL_HEAVY, n_sinks=0):
     """Retained set R'_i for every node whose count drops (k_i < c_i).
 
     The mandatory tail is the retained tokens among the last L_tail positions
@@ -345,7 +365,15 @@ def select(st, A, k, l_tail, select_mode=TAIL_HEAVY):
     k_i most recent retained tokens are kept; otherwise the tail plus the
     m_i = k_i - |tail| non-tail tokens with the largest accumulated attention
     A_i(t), ties to the lower position.  Selection is nested: it picks from the
-    current resident set only.  Returns ({node: sorted positions}, status).
+    current resident set only.
+
+    Global sinks S (Sec. 4 Execution (i)) are the first n_sinks positions of
+    the initial prompt, the root block 0.  When the root is cut, its resident
+    sinks are kept before anything else (the k_i lowest of them if k_i is
+    smaller), then the tail, then heavy hitters, all within k_i.  Modes, after
+    Table 7: TAIL_HEAVY (sinks + tail + heavy hitters), TAIL_ONLY (the most
+    recent k_i, no sinks), SINKS_TAIL (sinks, then the most recent of the
+    rest).  Returns ({node: sorted positions}, status).
     """
     out = {}
     for i in range(len(st["parent"])):
@@ -359,14 +387,24 @@ def select(st, A, k, l_tail, select_mode=TAIL_HEAVY):
         vals = [float(np.float32(A[base + p_])) for p_ in R]
         if any(math.isnan(x) for x in vals):
             return {}, ENONFINITE
-        tail = [p_ for p_ in R if p_ >= n - int(l_tail)]
-        if select_mode == TAIL_ONLY or ki <= len(tail):
-            keep = R[c - ki:] if ki > 0 else []
+        n_s = int(n_sinks) if (i == 0 and select_mode != TAIL_ONLY) else 0
+        sinks = [p_ for p_ in R if p_ < n_s]
+        rest = [p_ for p_ in R if p_ >= n_s]
+        if ki <= len(sinks):
+            keep = sinks[:ki]
+        elif select_mode in (TAIL_ONLY, SINKS_TAIL):
+            m = ki - len(sinks)
+            keep = sinks + rest[len(rest) - m:]
         else:
-            m = ki - len(tail)
-            cand = [p_ for p_ in R if p_ < n - int(l_tail)]
-            cand.sort(key=lambda p_: (-float(np.float32(A[base + p_])) + 0.0, p_))
-            keep = sorted(cand[:m] + tail)
+            m = ki - len(sinks)
+            tail = [p_ for p_ in rest if p_ >= n - int(l_tail)]
+            if m <= len(tail):
+                keep = sinks + tail[len(tail) - m:]
+            else:
+                h = m - len(tail)
+                cand = [p_ for p_ in rest if p_ < n - int(l_tail)]
+                cand.sort(key=lambda p_: (-float(np.float32(A[base + p_])) + 0.0, p_))
+                keep = sorted(sinks + cand[:h] + tail)
         out[i] = keep
     return out, OK
 

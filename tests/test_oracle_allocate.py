@@ -31,28 +31,37 @@ def power(s, gamma):
     return float(np.power(np.float64(s), gamma))
 
 
-def weight(s, d, delta, p):
-    return float(np.float64(p["eta"]) * np.float64(power(s, p["gamma"]))
+def weight(s, d, delta, p, on_path=False):
+    eta = 1.0 if on_path else p["eta"]
+    return float(np.float64(eta) * np.float64(power(s, p["gamma"]))
                  * np.exp(-p["lambda_d"] * d) * np.exp(-p["lambda_delta"] * delta))
 
 
 def brute_force(parent, n_full, n_kept, active, budget, s, p):
     V = len(parent)
     d, on_path, delta = O.geometry(parent, active)     # geometry is pinned separately
+    rehyd = p.get("lazy_rehydration", 1)
+    kp = p.get("k_protect", 0)
+    # full protection pins Path* blocks (restored to n_i, or kept at c_i without
+    # rehydration); floor protection puts them through Eq. 2-3 with eta^0 and
+    # a floor of k_protect, up to n_i (c_i without rehydration)
+    pinned = n_full if rehyd else n_kept
+    free = [i for i in range(V) if not on_path[i] or kp > 0]
     off = [i for i in range(V) if not on_path[i]]
-    # Path* blocks are pinned: restored to n_i, or kept at c_i without rehydration
-    pinned = n_full if p.get("lazy_rehydration", 1) else n_kept
-    b_off = budget - sum(pinned[i] for i in range(V) if on_path[i])
-    W = {i: Fraction(weight(s[i], d[i], delta[i], p)) for i in off}
+    b_off = budget - sum(pinned[i] for i in range(V) if on_path[i] and kp == 0)
+    W = {i: Fraction(weight(s[i], d[i], delta[i], p, bool(on_path[i]))) for i in free}
     rmin = Fraction(p["r_min"])
+    cap = {i: (n_full[i] if rehyd else n_kept[i]) if on_path[i] else n_kept[i] for i in free}
 
     def keep(i, alpha):
         r = min(Fraction(1), max(rmin, alpha * W[i]))
         kk = max(p["k_min"], min(p["l_tail"], n_full[i]), math.floor(r * n_full[i]))
-        return min(n_kept[i], min(n_full[i], kk))
+        if on_path[i]:
+            kk = max(kk, kp)
+        return min(cap[i], min(n_full[i], kk))
 
     cands = [Fraction(0)]
-    for i in off:
+    for i in free:
         if W[i] > 0:
             cands += [Fraction(j) / (W[i] * n_full[i]) for j in range(1, n_full[i] + 1)]
     if math.isfinite(p["alpha_max"]):
@@ -60,21 +69,21 @@ def brute_force(parent, n_full, n_kept, active, budget, s, p):
         cands = [a for a in cands if a <= amax] + [amax]
     best = None
     for a in sorted(set(cands)):
-        tot = sum(keep(i, a) for i in off)
+        tot = sum(keep(i, a) for i in free)
         if tot <= b_off:
             best = a
     k = np.zeros(V, dtype=np.int64)
     for i in range(V):
-        k[i] = pinned[i] if on_path[i] else 0
+        k[i] = pinned[i] if (on_path[i] and kp == 0) else 0
     if best is not None:
-        for i in off:
+        for i in free:
             k[i] = keep(i, best)
         return k, O.OK
     # Pressure (Alg. 2): floors first, then lower the lowest-priority node by one
-    for i in off:
+    for i in free:
         k[i] = keep(i, Fraction(0))
     prio = {i: weight(s[i], d[i], delta[i], p) for i in off}
-    while sum(k[i] for i in off) > b_off:
+    while sum(k[i] for i in free) > b_off:
         movable = [i for i in off if k[i] > min(p["k_min"], n_kept[i])]
         if not movable:
             return k, O.OVER_BUDGET
@@ -258,3 +267,39 @@ def test_scores_outside_the_unit_interval_are_rejected():
         x = s.copy()
         x[1] = bad                                  # on the path of leaf 3
         assert O.allocate(parent, n_full, n_full, [3], 40, x, p)[3] in (O.OK, O.OVER_BUDGET)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_floor_protection_matches_brute_force(seed):
+    """Floor protection (invariant (i) with a floor k_protect): Path* blocks
+    take part in Eq. 2-3 without the eta discount, never below k_protect, up
+    to n_i (or c_i without rehydration); Pressure drains only off-path
+    blocks."""
+    parent, n_full, n_kept, active, s = random_case(seed + 700, V=14, max_n=16)
+    p = dict(BASE, k_protect=[3, 6, 9, 20][seed % 4], lazy_rehydration=1 - (seed % 5 == 4))
+    V = len(parent)
+    for rho in (0.15, 0.3, 0.5, 0.75, 1.0):
+        budget = int(rho * sum(n_full))
+        k, _, on_path, status = O.allocate(parent, n_full, n_kept, active, budget, s, p)
+        kb, sb = brute_force(parent, n_full, n_kept, active, budget, s, p)
+        assert status == sb, rho
+        assert k.tolist() == kb.tolist(), (rho, k, kb)
+        for i in range(V):
+            if on_path[i]:
+                cap = n_full[i] if p["lazy_rehydration"] else n_kept[i]
+                assert min(cap, p["k_protect"]) <= k[i] <= cap
+        if status == O.OK:
+            assert int(np.sum(k)) <= budget
+
+
+def test_floor_protection_discounts_only_off_path_blocks():
+    """Two leaves of equal size and score, one on Path*: with eta < 1 the
+    on-path one keeps at least as many tokens; with eta = 1 the same."""
+    parent, n_full = [-1, 0, 0], [10, 40, 40]
+    s = np.array([0.5, 0.7, 0.7], np.float32)
+    for eta, strict in ((0.5, True), (1.0, False)):
+        p = dict(BASE, eta=eta, k_protect=1, lambda_delta=0.0, lambda_d=0.0, k_min=0, l_tail=0,
+                 r_min=0.0)
+        k, _, on_path, st = O.allocate(parent, n_full, n_full, [1], 50, s, p)
+        assert st == O.OK and on_path.tolist() == [1, 1, 0]
+        assert (k[1] > k[2]) if strict else (abs(int(k[1]) - int(k[2])) <= 1)

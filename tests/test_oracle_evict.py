@@ -225,3 +225,54 @@ def test_decode_closed_forms():
     np.testing.assert_allclose(o[0, 0, 0], mean_v, rtol=1e-12, atol=1e-14)
     z = float(np_float(st["host_k"])[0, 0, 0].astype(np.float64) @ np_float(st["q_dec"])[0, 0, 0]) / math.sqrt(8)
     assert lse[0, 0, 0] == pytest.approx(z + math.log(len(toks)), rel=1e-12)
+
+
+def _priority_brute_force(R, n, A_of, k, l_tail, mode, n_sinks):
+    """The kept set as the first k of one priority list: sinks (lowest position
+    first), then -- tail + heavy hitters -- the tail (most recent first) and the
+    other tokens by (A desc, position asc), or -- tail-only / sinks + tail --
+    the other tokens most recent first."""
+    sink = [p for p in R if p < n_sinks]
+    rest = [p for p in R if p >= n_sinks]
+    if mode == O.TAIL_HEAVY:
+        tail = sorted([p for p in rest if p >= n - l_tail], reverse=True)
+        head = sorted([p for p in rest if p < n - l_tail], key=lambda p: (-A_of(p) + 0.0, p))
+        order = sink + tail + head
+    else:
+        order = sink + sorted(rest, reverse=True)
+    return sorted(order[:k])
+
+
+@pytest.mark.parametrize("seed", range(30))
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_sinks_and_modes_match_priority_brute_force(seed, mode):
+    """Global sinks (the root's first n_sinks positions, Sec. 4 Execution (i))
+    and the three intra-block rules of Table 7 against one priority list."""
+    rng = np.random.default_rng(seed)
+    parent = [-1, 0, 0, 1]
+    n_full = [int(x) for x in rng.integers(3, 40, size=4)]
+    st = synth.build_state(parent, n_full, layers=1, kv_heads=1, q_per_kv=1, head_dim=64,
+                           dtype="f32", seed=seed, active=[3])
+    ost = oracle_state(st)
+    # a first eviction so that resident sets are ragged (sinks may be gone)
+    A0 = rng.random(st["num_tokens"]).astype(np.float32)
+    k0 = np.array([int(rng.integers(1, n + 1)) for n in n_full])
+    sel0, _ = O.select(ost, A0, k0, 3, O.TAIL_HEAVY, n_sinks=0)
+    ost = O.compact(ost, k0, sel0)
+    A = (np.round(rng.random(st["num_tokens"]) * 6) / 6).astype(np.float32)
+    n_sinks = int(rng.integers(0, 12))
+    l_tail = int(rng.integers(0, 6))
+    k = np.array([int(rng.integers(0, int(c) + 1)) for c in ost["n_kept"]])
+    sel, status = O.select(ost, A, k, l_tail, mode, n_sinks=n_sinks)
+    assert status == O.OK
+    for i in range(4):
+        c = int(ost["n_kept"][i])
+        if k[i] >= c:
+            assert i not in sel
+            continue
+        R = [r[3] for r in O.retained(ost, i)]
+        base = int(ost["tok_off"][i])
+        ns = n_sinks if (i == 0 and mode != O.TAIL_ONLY) else 0
+        want = _priority_brute_force(R, n_full[i], lambda p: float(A[base + p]), int(k[i]),
+                                     l_tail, mode, ns)
+        assert sel[i] == want, (i, mode, n_sinks)
