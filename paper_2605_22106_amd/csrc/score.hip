@@ -439,10 +439,14 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   // nm = -m sl2 (log2 units; nm0 while the row has no reference).  m moves
   // only when the terms of a sub-page grow large: the terms are computed
   // against the current reference first, and if the four terms of any lane of
-  // any row add up to more than 2^kSlack (or overflow), the wave moves every
-  // row's reference to its max, rescales the sum and recomputes that
-  // sub-page's terms.  The common step thus needs no max at all.
-  constexpr float kGrow = 256.f;   // 2^kSlack, kSlack = 8
+  // any row add up to more than 2^64 (or overflow), the wave moves every row's
+  // reference to its max, rescales the sum and recomputes that sub-page's
+  // terms.  In practice only a wave's first sub-page sets the reference: a
+  // term stays below 2^64 unless a key's logit exceeds the reference by 64
+  // bits, and a row's sum of at most 2^20 such terms stays far below the fp32
+  // range, while terms that fall far below the reference were negligible
+  // against the sum (at least 1) anyway.  The common step needs no max.
+  constexpr float kGrow = 0x1p64f;
   const float nm0 = -kFloor * sl2;
   float nm[NRB], l[NRB], lt[NRB];
   bool grow = false;
