@@ -70,7 +70,12 @@ typedef enum {
 
 typedef enum { ARBOR_BF16 = 0, ARBOR_F32 = 1 } arbor_dtype_t;
 
-typedef enum { ARBOR_SELECT_TAIL_HEAVY = 0, ARBOR_SELECT_TAIL_ONLY = 1 } arbor_select_mode_t;
+/* Intra-block retention rules (Sec. 4 Execution; the three rows of Table 7). */
+typedef enum {
+  ARBOR_SELECT_TAIL_HEAVY = 0,  /* global sinks + block tail + heavy hitters by A        */
+  ARBOR_SELECT_TAIL_ONLY = 1,   /* the most recent resident tokens, no sinks             */
+  ARBOR_SELECT_SINKS_TAIL = 2   /* global sinks, then the most recent resident tokens    */
+} arbor_select_mode_t;
 
 /* Kernels of the path that a caller can time on their own (arbor_timing_t). */
 typedef enum {
@@ -155,6 +160,14 @@ typedef struct {
                                 (arbor_rehydrate) and count n_i; 0: evicted tokens
                                 stay lost for the episode, Path* blocks keep (and
                                 count) their resident c_i                           */
+  int32_t n_sinks;           /* |S|: the global sinks are positions [0, n_sinks) of
+                                the root block 0, the initial prompt (Sec. 4
+                                Execution (i)); 0 = none                            */
+  int32_t k_protect;         /* active-path protection (Sec. 3 invariant (i)): 0 =
+                                full (Path* blocks keep all n_i tokens); > 0 = a
+                                floor: Path* blocks take part in Eq. 2-3 without
+                                the eta discount and keep at least k_protect
+                                tokens (up to n_i, or c_i without rehydration)      */
 } arbor_params_t;
 
 /* (host) Upper bounds used to size the workspace. */
@@ -214,17 +227,21 @@ int arbor_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_
  *
  * Path* = union of the root-to-leaf chains of active[0 .. n_active) (device
  * int32).  delta_out[i] = tree distance from i to the nearest active leaf,
- * on_path_out[i] = 1 on Path* (uint8).  Path* nodes get k = n_i (invariant
- * (i)), or k = c_i when params->lazy_rehydration = 0 (no restoring).  Every
- * other node i gets Eq. 3 at its Eq. 2 ratio
- * r_i = clip(alpha w_i, r_min, 1), w_i = eta s_i^gamma e^{-lambda_d d_i}
- * e^{-lambda_delta Delta_i}, capped at its resident count c_i (off-path blocks
- * are only ever lowered), where alpha is the largest value <= alpha_max whose
- * total fits budget_tokens.  Token j of block i is kept when
+ * on_path_out[i] = 1 on Path* (uint8).  With full protection
+ * (params->k_protect = 0) Path* nodes get k = n_i (invariant (i)), or k = c_i
+ * when params->lazy_rehydration = 0 (no restoring).  Every other node i gets
+ * Eq. 3 at its Eq. 2 ratio r_i = clip(alpha w_i, r_min, 1),
+ * w_i = eta^[i not in Path*] s_i^gamma e^{-lambda_d d_i} e^{-lambda_delta Delta_i},
+ * capped at its resident count c_i (off-path blocks are only ever lowered),
+ * where alpha is the largest value <= alpha_max whose total fits
+ * budget_tokens.  With floor protection (k_protect > 0) Path* nodes are among
+ * those "other" nodes, with the floor max(Eq. 3 floor, k_protect) and the cap
+ * n_i (c_i when lazy_rehydration = 0).  Token j of block i is kept when
  * alpha >= j / (w_i n_i) (its price, fp64); equal prices enter together.  If
- * the Eq. 3 floors already exceed the budget (Pressure) blocks are lowered
- * towards min(K_min, c_i) in ascending w_i (ties: lower id); if that is not
- * enough *status gets ARBOR_OVER_BUDGET and k_out holds the lowered counts.
+ * the Eq. 3 floors already exceed the budget (Pressure) off-path blocks are
+ * lowered towards min(K_min, c_i) in ascending w_i (ties: lower id); if that
+ * is not enough *status gets ARBOR_OVER_BUDGET and k_out holds the lowered
+ * counts.
  * s is fp32 [V] in [0, 1] (the clipped MSVE score; -0 counts as +0); k_out
  * int32 [V].  fp64 arithmetic, no contraction; s^gamma is correctly rounded
  * for gamma in {1, 2, 3, 4} and the device pow otherwise.
@@ -245,8 +262,12 @@ int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_ac
  * If k[i] <= |tail| or select_mode = TAIL_ONLY, the k[i] most recent resident
  * positions are kept; otherwise the tail plus the k[i] - |tail| other resident
  * positions with the largest A (fp32 compare, -0 == +0), ties to the lower
- * position.  sel_pos[tok_off[i] + s] (s < k[i]) receives the kept positions in
- * ascending order; entries of other nodes are not written.
+ * position.  The global sinks (resident positions < n_sinks of the root block
+ * 0) come before everything else in the TAIL_HEAVY and SINKS_TAIL modes: the
+ * root keeps its k[0] lowest sinks if k[0] is smaller, else all of them plus
+ * the rule applied to its other tokens with k[0] - |sinks| (SINKS_TAIL: the
+ * most recent ones).  sel_pos[tok_off[i] + s] (s < k[i]) receives the kept
+ * positions in ascending order; entries of other nodes are not written.
  * Errors: ENONFINITE (NaN in A over a changed block), EINVAL (k < 0).
  */
 int arbor_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,

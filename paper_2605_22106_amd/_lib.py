@@ -25,7 +25,7 @@ BF16, F32 = 0, 1
 # kernels a call can time on their own (arbor_timing_t)
 KERNEL_SCORE_ATTN, KERNEL_SELECT, KERNEL_COMPACT_MOVE, KERNEL_DECODE_ATTN = 0, 1, 2, 3
 KERNEL_DECODE_CREDIT, KERNEL_COUNT = 4, 5
-SELECT_TAIL_HEAVY, SELECT_TAIL_ONLY = 0, 1
+SELECT_TAIL_HEAVY, SELECT_TAIL_ONLY, SELECT_SINKS_TAIL = 0, 1, 2
 MAX_DEPTH = 63
 
 
@@ -59,7 +59,8 @@ class Params(ctypes.Structure):
                 ("k_min", ctypes.c_int32), ("l_tail", ctypes.c_int32),
                 ("theta", ctypes.c_float * 3), ("softmax_scale", ctypes.c_float),
                 ("select_mode", ctypes.c_int32), ("score_self_window", ctypes.c_int32),
-                ("lazy_rehydration", ctypes.c_int32)]
+                ("lazy_rehydration", ctypes.c_int32), ("n_sinks", ctypes.c_int32),
+                ("k_protect", ctypes.c_int32)]
 
 
 class DecodeCredit(ctypes.Structure):
@@ -146,7 +147,8 @@ def params_struct(p: dict, softmax_scale: float = 0.0) -> Params:
                   float(p["lambda_delta"]), float(p["eta"]), float(p["r_min"]), int(p["k_min"]),
                   int(p["l_tail"]), (ctypes.c_float * 3)(*[float(x) for x in th]),
                   float(p.get("softmax_scale", softmax_scale)), int(p.get("select_mode", 0)),
-                  int(p.get("score_self_window", 0)), int(p.get("lazy_rehydration", 1)))
+                  int(p.get("score_self_window", 0)), int(p.get("lazy_rehydration", 1)),
+                  int(p.get("n_sinks", 0)), int(p.get("k_protect", 0)))
 
 
 @dataclass

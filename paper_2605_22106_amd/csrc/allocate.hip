@@ -34,7 +34,7 @@ namespace {
 constexpr int AT = 1024;
 constexpr int kLdsNodes = 512;    // per-node state in LDS up to this many nodes
 constexpr int kCandLds = 1536;    // listed prices selected in LDS up to this many
-constexpr int kNodeBytes = 2 * 8 + 7 * 4 + 1;
+constexpr int kNodeBytes = 2 * 8 + 8 * 4 + 1;
 constexpr int kSearchWaves = AT / kWave / 2;   // waves per bracket end
 constexpr int kPtsPerWave = 4;                  // test points of each wave
 constexpr int kSearchPts = kSearchWaves * kPtsPerWave;   // test points per end
@@ -49,6 +49,7 @@ struct AllocParams {
   double alpha_max, gamma, lambda_d, lambda_delta, eta, r_min;
   int k_min, l_tail;
   int rehydrate;   // Path* blocks count n_i (restored) or their resident c_i
+  int k_protect;   // 0: Path* blocks pinned; > 0: they take part with this floor
   double dexp[kDecay], texp[kDecay];
 };
 
@@ -66,13 +67,13 @@ __device__ __forceinline__ double pow_gamma(double s, double gamma) {
 // LDS copies of them; `path` is the on-path output or its LDS copy.
 struct Nodes {
   int32_t *parent, *n_full, *n_kept;
-  int32_t *depth, *down, *F, *cnt;
+  int32_t *depth, *down, *F, *cnt, *cap;
   double *W, *w;
   uint8_t *path;
 };
 
 struct AllocWs {
-  int32_t *depth, *down, *F, *cnt;
+  int32_t *depth, *down, *F, *cnt, *cap;
   double *W, *w;
   uint64_t *buf0, *buf1;
   int64_t buf_cap;
@@ -295,7 +296,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     nd.down = ip + 4 * V;
     nd.F = ip + 5 * V;
     nd.cnt = ip + 6 * V;
-    nd.path = reinterpret_cast<uint8_t *>(ip + 7 * V);
+    nd.cap = ip + 7 * V;
+    nd.path = reinterpret_cast<uint8_t *>(ip + 8 * V);
 
     for (int i = tid; i < V; i += AT) {
       nd.parent[i] = t.parent[i];
@@ -310,6 +312,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     nd.down = ws.down;
     nd.F = ws.F;
     nd.cnt = ws.cnt;
+    nd.cap = ws.cap;
     nd.W = ws.W;
     nd.w = ws.w;
     nd.path = on_path;
@@ -371,13 +374,17 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     delta_out[i] = best;
     const int n = nd.n_full[i];
     const int c = nd.n_kept[i];
+    const bool on = nd.path[i] != 0;
     if (in_lds) on_path[i] = nd.path[i];
-    if (nd.path[i]) {
-      // pinned (invariant (i)): restored to n_i, or kept at c_i when evicted
-      // tokens stay lost
-      const int kp = p.rehydrate ? n : c;
-      k_out[i] = kp;
-      path_tok += kp;
+    // the most a block can keep: a Path* block is restored to n_i by
+    // rehydration (or keeps c_i when evicted tokens stay lost), any other
+    // block only ever loses tokens
+    const int cap = on && p.rehydrate ? n : c;
+    nd.cap[i] = cap;
+    if (on && p.k_protect == 0) {
+      // pinned (invariant (i), full protection)
+      k_out[i] = cap;
+      path_tok += cap;
       nd.F[i] = 0;
       nd.W[i] = 0.0;
       nd.w[i] = 0.0;
@@ -388,14 +395,16 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     if (!(sf == sf)) atomicOr(&s_err, 2);
     else if (!(sf >= 0.f && sf <= 1.f)) atomicOr(&s_err, 4);
     const double s = (double)sf;
-    // Eq. 3 at the ratio floor r_min, capped at the resident count
+    // Eq. 3 at the ratio floor r_min, capped; a Path* block under floor
+    // protection keeps at least k_protect
     int f = max(p.k_min, min(p.l_tail, n));
     f = max(f, (int)floor(p.r_min * (double)n));
-    f = min(c, min(n, f));
+    f = min(cap, min(n, f));
+    if (on) f = max(f, min(cap, p.k_protect));
     nd.F[i] = f;
-    // the off-path Eq. 2 weight without alpha, in the same operation order as
-    // ((eta * s^gamma) * e^{-lambda_d d}) * e^{-lambda_Delta Delta}
-    double w = p.eta * pow_gamma(s, p.gamma);
+    // the Eq. 2 weight without alpha, in the same operation order as
+    // ((eta^[off path] * s^gamma) * e^{-lambda_d d}) * e^{-lambda_Delta Delta}
+    double w = (on ? 1.0 : p.eta) * pow_gamma(s, p.gamma);
     w = w * (di < kDecay ? p.dexp[di] : exp(-p.lambda_d * (double)di));
     w = w * (best < kDecay ? p.texp[best] : exp(-p.lambda_delta * (double)best));
     // -0 (s = -0 with an odd gamma) as +0: the Pressure order compares bit
@@ -404,7 +413,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     nd.w[i] = w;
     nd.W[i] = w * (double)n;
     sum_F += f;
-    sum_red += f - min(p.k_min, c);
+    // Pressure lowers only off-path blocks
+    if (!on) sum_red += f - min(p.k_min, c);
   }
   {
     int64_t v3[3] = {path_tok, sum_F, sum_red};
@@ -428,10 +438,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     uint64_t kmin = ~0ull, kmax = 0ull;
     for (int i = tid; i < V; i += AT) {
       int cnt = 0;
-      if (!nd.path[i]) {
+      if (!(nd.path[i] && p.k_protect == 0)) {
         const double W = nd.W[i];
         const int F = nd.F[i];
-        cnt = count_prefix(F, nd.n_kept[i], W,
+        cnt = count_prefix(F, nd.cap[i], W,
                            [amax](double x) { return x <= amax && x < __builtin_inf(); });
         if (cnt > 0) {
           const uint64_t lo = (uint64_t)__double_as_longlong(price(F + 1, W));
@@ -447,7 +457,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     total = block_sum<int64_t>(total, sm);
     if (total <= E) {
       for (int i = tid; i < V; i += AT)
-        if (!nd.path[i]) k_out[i] = nd.F[i] + nd.cnt[i];
+        if (!(nd.path[i] && p.k_protect == 0)) k_out[i] = nd.F[i] + nd.cnt[i];
       return;
     }
     {
@@ -610,8 +620,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     const uint64_t prefix = select_rank(cand, cand2, total_c, E - below, sm);
     const double cut = key_value(prefix);
     for (int i = tid; i < V; i += AT) {
-      if (nd.path[i]) continue;
-      const int kept = count_prefix(nd.F[i], nd.n_kept[i], nd.W[i],
+      if (nd.path[i] && p.k_protect == 0) continue;
+      const int kept = count_prefix(nd.F[i], nd.cap[i], nd.W[i],
                                     [cut](double x) { return x < cut; });
       k_out[i] = nd.F[i] + kept;
     }
@@ -621,8 +631,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   // ---- pressure: drain the lowest-priority blocks (Alg. 2) ---------------
   int64_t excess = sum_F - b_off;
   if (sum_red < excess) {
-    for (int i = tid; i < V; i += AT)
+    for (int i = tid; i < V; i += AT) {
       if (!nd.path[i]) k_out[i] = min(p.k_min, nd.n_kept[i]);
+      else if (p.k_protect > 0) k_out[i] = nd.F[i];   // Path* keeps its floor
+    }
     if (tid == 0) status_warn(status, ARBOR_OVER_BUDGET);
     return;
   }
@@ -678,6 +690,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
         if (before < need) kk -= (int)min<int64_t>(red, need - before);
       }
       k_out[i] = kk;
+    } else if (i < V && p.k_protect > 0) {
+      k_out[i] = nd.F[i];                                // Path* keeps its floor
     }
     run += tot;
   }
@@ -686,7 +700,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
 }  // namespace
 
 size_t allocate_workspace(const arbor_sizes_t *sz) {
-  return (size_t)sz->num_nodes * (4 * 4 + 8 * 2 + 64) + (size_t)sz->num_tokens * 16 + 8192;
+  return (size_t)sz->num_nodes * (5 * 4 + 8 * 2 + 64) + (size_t)sz->num_tokens * 16 + 8192;
 }
 
 int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_active,
@@ -701,6 +715,7 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   ws.down = cv.take<int32_t>(t.V);
   ws.F = cv.take<int32_t>(t.V);
   ws.cnt = cv.take<int32_t>(t.V);
+  ws.cap = cv.take<int32_t>(t.V);
   ws.W = cv.take<double>(t.V);
   ws.w = cv.take<double>(t.V);
   ws.buf0 = cv.take<uint64_t>((size_t)t.N);
@@ -709,7 +724,7 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   if (!cv.ok) return ARBOR_EWORKSPACE;
   AllocParams p{params->alpha_max, params->gamma, params->lambda_d, params->lambda_delta,
                 params->eta, params->r_min, params->k_min, params->l_tail,
-                params->lazy_rehydration, {}, {}};
+                params->lazy_rehydration, params->k_protect, {}, {}};
   for (int i = 0; i < kDecay; ++i) {
     p.dexp[i] = exp(-params->lambda_d * (double)i);
     p.texp[i] = exp(-params->lambda_delta * (double)i);

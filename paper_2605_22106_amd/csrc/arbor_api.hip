@@ -129,7 +129,7 @@ int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_ac
   if (!(params->eta > 0.0 && params->eta <= 1.0) || params->k_min < 0 || params->l_tail < 0 ||
       !(params->r_min >= 0.0 && params->r_min <= 1.0) || isnan(params->gamma) ||
       isnan(params->lambda_d) || isnan(params->lambda_delta) || isnan(params->alpha_max) ||
-      !(params->alpha_max > 0.0) ||
+      !(params->alpha_max > 0.0) || params->k_protect < 0 ||
       (params->lazy_rehydration != 0 && params->lazy_rehydration != 1))
     return ARBOR_EINVAL;
   return launch_allocate(tree, active, n_active, budget_tokens, s, params, k_out, delta_out,
@@ -143,8 +143,10 @@ int arbor_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   ARBOR_TRY(check_tree(tree));
   ARBOR_TRY(check_pool(pool));
   if (!params || !status || !A || !k || !sel_pos) return ARBOR_EINVAL;
-  if (params->l_tail < 0) return ARBOR_EINVAL;
-  if (params->select_mode != ARBOR_SELECT_TAIL_HEAVY && params->select_mode != ARBOR_SELECT_TAIL_ONLY)
+  if (params->l_tail < 0 || params->n_sinks < 0) return ARBOR_EINVAL;
+  if (params->select_mode != ARBOR_SELECT_TAIL_HEAVY &&
+      params->select_mode != ARBOR_SELECT_TAIL_ONLY &&
+      params->select_mode != ARBOR_SELECT_SINKS_TAIL)
     return ARBOR_EINVAL;
   return launch_select(geom, tree, pool, A, k, params, sel_pos, status, stream);
 }

@@ -1,5 +1,5 @@
-// arbor_select: per-block retained set, tail + heavy hitters (Sec. 4 Execution,
-// Alg. 1 Evict).  One wavefront per node; the m-th largest accumulated
+// arbor_select: per-block retained set: global sinks of the root prompt, block
+// tail and heavy hitters (Sec. 4 Execution, Alg. 1 Evict, Table 7's rules).  One wavefront per node; the m-th largest accumulated
 // attention key is found by an MSB-first radix select over 8-bit digits whose
 // bins are counted in a per-wave LDS histogram, then the kept positions are
 // emitted in slot (= position) order with a ballot prefix sum.
@@ -63,15 +63,32 @@ struct Hist {
   }
 };
 
+// Slot ranges of one node.  Resident positions ascend with the slot, so the
+// sinks (positions < sk), the heavy-hitter candidates and the tail (positions
+// >= max(n - L_tail, sk)) are consecutive slot ranges: sinks [0, lo),
+// candidates [lo, hi), tail [hi, c).  The kept set is
+//   - the first a = min(k, lo) slots and the last k - a slots, when k <= lo,
+//     in the recency modes, or when the sinks and the tail hold k already;
+//   - otherwise the sinks, the tail and the k - lo - (c - hi) candidates with
+//     the largest keys (ties to the lower slot).
+struct Ranges {
+  int lo, hi;
+};
+
+__device__ __forceinline__ bool recency_only(int mode, int ki, int c, const Ranges &rg) {
+  return ki <= rg.lo || mode != ARBOR_SELECT_TAIL_HEAVY || ki - rg.lo <= c - rg.hi;
+}
+
 // Nodes with at most 64 * kCached resident slots: keys and positions stay in
 // registers for every radix pass.
 __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, int c, int ki,
-                              int thr, int mode, int32_t *__restrict__ out, int32_t *status,
-                              int lane, const Hist &hist) {
+                              int thr, int sk, int mode, int32_t *__restrict__ out,
+                              int32_t *status, int lane, const Hist &hist) {
   uint32_t key[kCached];
   int pos[kCached];
   bool nan = false;
-  int n_head = 0;
+  Ranges rg{0, 0};
+  const int hthr = thr > sk ? thr : sk;
 #pragma unroll
   for (int r = 0; r < kCached; ++r) {
     const int s = r * kWave + lane;
@@ -81,31 +98,36 @@ __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, i
     nan |= v && (a != a);
     key[r] = ordered_key(a);
     pos[r] = p;
-    if (r * kWave < c) n_head += popc(ballot(v && p < thr));
+    if (r * kWave < c) {
+      rg.lo += popc(ballot(v && p < sk));
+      rg.hi += popc(ballot(v && p < hthr));
+    }
   }
   if (ballot(nan)) {
     if (lane == 0) status_error(status, ARBOR_ENONFINITE);
     return;
   }
-  const int n_tail = c - n_head;
-  if (mode == ARBOR_SELECT_TAIL_ONLY || ki <= n_tail) {
+  if (recency_only(mode, ki, c, rg)) {
+    const int a = ki < rg.lo ? ki : rg.lo;
+    const int b0 = c - (ki - a);   // first of the last ki - a slots
 #pragma unroll
     for (int r = 0; r < kCached; ++r) {
       const int s = r * kWave + lane;
-      if (s >= c - ki && s < c) out[s - (c - ki)] = pos[r];
+      if (s < a) out[s] = pos[r];
+      else if (s >= b0 && s < c) out[a + s - b0] = pos[r];
     }
     return;
   }
-  const int m = ki - n_tail;
+  const int m = ki - rg.lo - (c - rg.hi);   // heavy hitters among the candidates
   uint32_t prefix = 0, pmask = 0;
   int remaining = m;
   for (int shift = 24; shift >= 0; shift -= 8) {
     hist.clear(lane);
 #pragma unroll
     for (int r = 0; r < kCached; ++r) {
-      if (r * kWave >= n_head) break;
+      if (r * kWave >= rg.hi) break;
       const int s = r * kWave + lane;
-      hist.add(s < n_head && ((key[r] & pmask) == prefix), key[r], shift);
+      hist.add(s >= rg.lo && s < rg.hi && ((key[r] & pmask) == prefix), key[r], shift);
     }
     prefix |= (uint32_t)hist.pick(remaining, lane) << shift;
     pmask |= 255u << shift;
@@ -115,26 +137,28 @@ __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, i
   for (int r = 0; r < kCached; ++r) {
     if (r * kWave >= c) break;
     const int s = r * kWave + lane;
-    const bool head = s < n_head;
-    const bool gt = head && key[r] > prefix;
-    const bool eq = head && key[r] == prefix;
+    const bool cand = s >= rg.lo && s < rg.hi;
+    const bool gt = cand && key[r] > prefix;
+    const bool eq = cand && key[r] == prefix;
     const uint64_t beq = ballot(eq);
     const bool take = gt || (eq && ties + rank_below(beq, lane) < remaining);
     const uint64_t bt = ballot(take);
     const int dst = written + rank_below(bt, lane);
-    if (take && dst < m) out[dst] = pos[r];
+    if (take && dst < m) out[rg.lo + dst] = pos[r];
     written += popc(bt);
     ties += popc(beq);
-    if (s >= n_head && s < c) out[m + s - n_head] = pos[r];   // the tail, in order
+    if (s < rg.lo) out[s] = pos[r];                                     // the sinks
+    if (s >= rg.hi && s < c) out[rg.lo + m + s - rg.hi] = pos[r];       // the tail, in order
   }
   if (written != m && lane == 0) status_error(status, ARBOR_ECORRUPT);
 }
 
 // Larger nodes: every pass streams the keys again (L2-resident).
 __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A, int c, int ki,
-                                int thr, int mode, int32_t *__restrict__ out, int32_t *status,
-                                int lane, const Hist &hist) {
-  int n_head = 0;
+                                int thr, int sk, int mode, int32_t *__restrict__ out,
+                                int32_t *status, int lane, const Hist &hist) {
+  Ranges rg{0, 0};
+  const int hthr = thr > sk ? thr : sk;
   bool nan = false;
   for (int base = 0; base < c; base += kWave) {
     const int s = base + lane;
@@ -142,25 +166,26 @@ __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A,
     const int p = v ? nv.pos(s) : 0;
     const float a = v ? A[p] : 0.f;
     nan |= v && (a != a);
-    n_head += popc(ballot(v && p < thr));
+    rg.lo += popc(ballot(v && p < sk));
+    rg.hi += popc(ballot(v && p < hthr));
   }
   if (ballot(nan)) {
     if (lane == 0) status_error(status, ARBOR_ENONFINITE);
     return;
   }
-  const int n_tail = c - n_head;
-  if (mode == ARBOR_SELECT_TAIL_ONLY || ki <= n_tail) {
-    for (int s = lane; s < ki; s += kWave) out[s] = nv.pos(c - ki + s);
+  if (recency_only(mode, ki, c, rg)) {
+    const int a = ki < rg.lo ? ki : rg.lo;
+    for (int s = lane; s < ki; s += kWave) out[s] = nv.pos(s < a ? s : c - ki + s);
     return;
   }
-  const int m = ki - n_tail;
+  const int m = ki - rg.lo - (c - rg.hi);
   uint32_t prefix = 0, pmask = 0;
   int remaining = m;
   for (int shift = 24; shift >= 0; shift -= 8) {
     hist.clear(lane);
-    for (int base = 0; base < n_head; base += kWave) {
+    for (int base = rg.lo; base < rg.hi; base += kWave) {
       const int s = base + lane;
-      const bool v = s < n_head;
+      const bool v = s < rg.hi;
       const uint32_t key = v ? ordered_key(A[nv.pos(s)]) : 0u;
       hist.add(v && ((key & pmask) == prefix), key, shift);
     }
@@ -168,9 +193,9 @@ __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A,
     pmask |= 255u << shift;
   }
   int written = 0, ties = 0;
-  for (int base = 0; base < n_head; base += kWave) {
+  for (int base = rg.lo; base < rg.hi; base += kWave) {
     const int s = base + lane;
-    const bool v = s < n_head;
+    const bool v = s < rg.hi;
     const int p = v ? nv.pos(s) : 0;
     const uint32_t key = v ? ordered_key(A[p]) : 0u;
     const bool gt = v && key > prefix;
@@ -179,17 +204,19 @@ __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A,
     const bool take = gt || (eq && ties + rank_below(beq, lane) < remaining);
     const uint64_t bt = ballot(take);
     const int dst = written + rank_below(bt, lane);
-    if (take && dst < m) out[dst] = p;
+    if (take && dst < m) out[rg.lo + dst] = p;
     written += popc(bt);
     ties += popc(beq);
   }
   if (written != m && lane == 0) status_error(status, ARBOR_ECORRUPT);
-  for (int s = lane; s < n_tail; s += kWave) out[m + s] = nv.pos(n_head + s);
+  for (int s = lane; s < rg.lo; s += kWave) out[s] = nv.pos(s);
+  for (int s = lane; s < c - rg.hi; s += kWave) out[rg.lo + m + s] = nv.pos(rg.hi + s);
 }
 
 __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const float *__restrict__ A,
                                                      const int32_t *__restrict__ k, int l_tail,
-                                                     int mode, int32_t *__restrict__ sel_pos,
+                                                     int n_sinks, int mode,
+                                                     int32_t *__restrict__ sel_pos,
                                                      int32_t *status) {
   __shared__ unsigned s_hist[4][256];
   if (status_failed(status)) return;
@@ -208,10 +235,12 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
   const int64_t tb = t.tok_off[i];
   const NodeView nv{t.page_table, pl.slot_pos, t.page_off[i], pl.P};
   int32_t *out = sel_pos + tb;
+  // the global sinks are the first positions of the root block (the prompt)
+  const int sk = (i == 0 && mode != ARBOR_SELECT_TAIL_ONLY) ? n_sinks : 0;
   if (c <= kWave * kCached)
-    select_cached(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane, hist);
+    select_cached(nv, A + tb, c, ki, n - l_tail, sk, mode, out, status, lane, hist);
   else
-    select_streamed(nv, A + tb, c, ki, n - l_tail, mode, out, status, lane, hist);
+    select_streamed(nv, A + tb, c, ki, n - l_tail, sk, mode, out, status, lane, hist);
 }
 
 }  // namespace
@@ -225,7 +254,7 @@ int launch_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   dim3 grid((t.V + 3) / 4);
   timing_begin(geom, ARBOR_KERNEL_SELECT, stream);
   hipLaunchKernelGGL(select_kernel, grid, dim3(256), 0, stream, t, pl, A, k, params->l_tail,
-                     params->select_mode, sel_pos, status);
+                     params->n_sinks, params->select_mode, sel_pos, status);
   timing_end(geom, ARBOR_KERNEL_SELECT, stream);
   return hip_ok(hipGetLastError());
 }
