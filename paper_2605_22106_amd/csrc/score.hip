@@ -8,18 +8,18 @@
 // credited to tokens of proper ancestors (u > b_i).
 //
 // Launches on one stream:
-//   setup   one workgroup per observer: every workgroup walks all observer
-//           chains for the partial / table offsets (a prefix over observers),
-//           writes its own observer's chain data and 16-slot sub-page table;
-//           workgroup 0 also validates the tree;
+//   setup   one workgroup: validates the tree, walks every observer chain
+//           (one thread per observer) for the partial / table offsets (prefix
+//           sums over observers) and lists the blocks that receive credit;
+//   tables  one workgroup per observer: its 16-slot sub-page table;
 //   attn    per (observer, slice layer, kv head, group of up to 64 rows),
 //           two passes over the same (row, key) pairs as MFMA tiles of 16
 //           keys x 16 rows, the four waves taking alternate 16-key sub-pages:
 //           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
 //           sums of exp2(z - lse) -> one partial per credited context key;
 //   fold    per observer: sum its (slice layer, kv head, row group) partials;
-//   reduce  per block i and 64-slot chunk: sum the folded partials of every
-//           observer below i in observer order (fp64) into A, rows_seen;
+//   reduce  per credited block i and 64-slot chunk: sum the folded partials of
+//           every observer below i in observer order (fp64) into A, rows_seen;
 //   final   a_i = sum_p A_i(p) / rows_seen_i, s_i = clip(sigmoid(theta.phi)).
 // No atomics anywhere, so A is bitwise reproducible.  The reduction dimension
 // (head_dim) is permuted identically in both MFMA operands so that every lane
@@ -73,37 +73,10 @@ struct ChainLds {
   int sp_meta[SPCAP];  // chain depth | valid slots << 8
 };
 
-__device__ __forceinline__ void build_chain(const Tree &t, const Pool &pl, int j, ChainLds &ch) {
-  if (threadIdx.x == 0) {
-    int d = 0;
-    for (int x = t.parent[j]; x >= 0 && d < MAXD - 1; x = t.parent[x]) ++d;
-    ch.depth = d;
-    int e = d;
-    for (int x = j; x >= 0 && e >= 0; x = t.parent[x]) ch.node[e--] = x;
-  }
-  __syncthreads();
-  // one thread per chain node fetches its size and page-table offset (the
-  // loads run side by side), then one thread forms the prefix sums
-  if ((int)threadIdx.x <= ch.depth) {
-    const int x = ch.node[threadIdx.x];
-    ch.c[threadIdx.x] = t.n_kept[x];
-    ch.po[threadIdx.x] = t.page_off[x];
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int d = ch.depth;
-    int ctx = 0, sp = 0;
-    for (int e = 0; e <= d; ++e) {
-      const int c = ch.c[e];
-      ch.ctx[e] = ctx;
-      ch.sp_off[e] = sp;
-      ctx += c;
-      sp += (c + 15) / 16;
-    }
-    ch.sp_off[d + 1] = sp;
-  }
-  __syncthreads();
-  const int n_sp = min(ch.sp_off[ch.depth + 1], SPCAP);
+// The chain's in-LDS sub-page table (the first SPCAP sub-pages; longer chains
+// compute the rest on demand).
+__device__ __forceinline__ void fill_table(const Tree &t, const Pool &pl, ChainLds &ch, int n) {
+  const int n_sp = min(n, SPCAP);
   for (int sp = threadIdx.x; sp < n_sp; sp += blockDim.x) {
     int d = 0;
     while (sp >= ch.sp_off[d + 1]) ++d;
@@ -670,73 +643,84 @@ __device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
   return r;
 }
 
-// One workgroup per observer.  Offsets of the partials and sub-page tables are
-// prefixes over observers, so every workgroup walks every observer chain (in
-// parallel, one per thread) and keeps its own observer's offsets; it then
-// writes that observer's chain data and sub-page table, root first, as
-// 16-byte entries (plane row, slot, context offset, valid slots | own << 8)
-// that the streaming kernel reads with scalar loads.  Workgroup 0 validates
-// the whole tree.
-__global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap,
-                                                   int64_t *__restrict__ pbase,
-                                                   int64_t *__restrict__ fbase,
-                                                   int64_t *__restrict__ tbase,
-                                                   int32_t *__restrict__ nsp,
-                                                   int32_t *__restrict__ ctxlen,
-                                                   int32_t *__restrict__ odepth,
-                                                   int32_t *__restrict__ anc) {
+// One workgroup for the whole call, O(V + n_obs depth): validates the tree,
+// walks every observer chain (one thread per observer, root first into anc),
+// forms the offsets of the partials, folded sums and sub-page tables as
+// prefixes over observers, and lists the blocks that receive credit (proper
+// ancestors of some observer; the observers themselves in the self-window
+// mode) in ascending id, so that the reduction visits only those.
+// fbase / tbase hold the prefixes of the chain lengths and sub-page counts
+// until the totals are known.
+__global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_cap,
+                                                    int64_t *__restrict__ pbase,
+                                                    int64_t *__restrict__ fbase,
+                                                    int64_t *__restrict__ tbase,
+                                                    int32_t *__restrict__ nsp,
+                                                    int32_t *__restrict__ ctxlen,
+                                                    int32_t *__restrict__ odepth,
+                                                    int32_t *__restrict__ anc,
+                                                    int32_t *__restrict__ flag,
+                                                    int32_t *__restrict__ cred) {
   __shared__ int64_t sm[17];
   __shared__ int s_err;
-  __shared__ int64_t s_mine[4];
-  __shared__ ChainLds ch;
   // parent links and block sizes in LDS for trees of up to kSetupLds nodes, so
   // the chain walks do not wait on global memory at every step
   __shared__ int32_t s_par[kSetupLds], s_full[kSetupLds], s_kept[kSetupLds];
-  if (status_failed(a.status)) return;
+  if (status_failed(a.status)) {
+    if (threadIdx.x == 0) cred[0] = 0;
+    return;
+  }
   Tree t = a.t;
-  const int me = blockIdx.x;
   const int tid = threadIdx.x;
+  const int nt = blockDim.x;
   if (tid == 0) s_err = 0;
-  if (t.V <= kSetupLds) {
-    for (int i = tid; i < t.V; i += blockDim.x) {
-      s_par[i] = t.parent[i];
-      s_full[i] = t.n_full[i];
-      s_kept[i] = t.n_kept[i];
+  const bool in_lds = t.V <= kSetupLds;
+  for (int i = tid; i < t.V; i += nt) {
+    const int par = t.parent[i];
+    const int nf = t.n_full[i];
+    const int c = t.n_kept[i];
+    const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
+    if (!ok || c < 0 || c > nf) atomicOr(&s_err, 1);
+    if (in_lds) {
+      s_par[i] = par;
+      s_full[i] = nf;
+      s_kept[i] = c;
     }
+    flag[i] = 0;
+  }
+  if (in_lds) {
     t.parent = s_par;
     t.n_full = s_full;
     t.n_kept = s_kept;
   }
   __syncthreads();
-  if (me == 0) {
-    for (int i = tid; i < t.V; i += blockDim.x) {
-      const int par = t.parent[i];
-      const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
-      const int c = t.n_kept[i];
-      if (!ok || c < 0 || c > t.n_full[i]) atomicOr(&s_err, 1);
-    }
-  }
   const int slabs = a.S * a.pl.Hkv * a.n_rg;
   int64_t run = 0, frun = 0, trun = 0;
-  for (int base = 0; base < a.n_obs; base += blockDim.x) {
+  for (int base = 0; base < a.n_obs; base += nt) {
     const int o = base + tid;
     int64_t len = 0, subs = 0;
     if (o < a.n_obs) {
       const int j = a.obs[o];
       if (j < 0 || j >= t.V) {
         atomicOr(&s_err, 1);
+        odepth[o] = -1;
+        nsp[2 * o] = nsp[2 * o + 1] = 0;
+        ctxlen[o] = 0;
       } else {
-        const ObsChain r = walk_chain(t, j, o == me ? anc + (int64_t)o * MAXD : nullptr);
+        int32_t *ao = anc + (int64_t)o * MAXD;
+        const ObsChain r = walk_chain(t, j, ao);
         if (!r.ok) atomicOr(&s_err, 2);
         len = r.len;
         subs = r.subs;
-        if (o == me) {
-          odepth[o] = r.depth;
-          const int own = r.ok ? (t.n_kept[j] + 15) / 16 : 0;
-          nsp[2 * o] = (int32_t)subs;
-          nsp[2 * o + 1] = r.ok ? (int32_t)(a.self_window ? subs : subs - own) : 0;
-          ctxlen[o] = (int32_t)len;
-          s_mine[2] = subs;
+        odepth[o] = r.ok ? r.depth : -1;
+        const int own = r.ok ? (t.n_kept[j] + 15) / 16 : 0;
+        nsp[2 * o] = (int32_t)subs;
+        nsp[2 * o + 1] = r.ok ? (int32_t)(a.self_window ? subs : subs - own) : 0;
+        ctxlen[o] = (int32_t)len;
+        if (r.ok) {
+          // blocks this observer credits (benign races: every writer stores 1)
+          for (int e = 0; e < r.depth; ++e) flag[ao[e]] = 1;
+          if (a.self_window) flag[j] = 1;
         }
       }
     }
@@ -744,10 +728,10 @@ __global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap
     const int64_t ex = block_exclusive_scan<int64_t>(len * slabs, sm, &tot);
     const int64_t fx = block_exclusive_scan<int64_t>(len, sm, &ftot);
     const int64_t tx = block_exclusive_scan<int64_t>(subs, sm, &ttot);
-    if (o == me) {
-      s_mine[0] = run + ex;
-      s_mine[1] = trun + tx;
-      s_mine[3] = frun + fx;
+    if (o < a.n_obs) {
+      pbase[o] = run + ex;
+      fbase[o] = frun + fx;
+      tbase[o] = trun + tx;
     }
     run += tot;
     frun += ftot;
@@ -758,28 +742,70 @@ __global__ __launch_bounds__(256) void score_setup(ScoreArgs a, int64_t part_cap
   // entries, 16-byte aligned)
   const int64_t tab0 = (run + frun + 3) & ~(int64_t)3;
   const bool fits = tab0 + 4 * trun <= part_cap;
-  if (tid == 0) {
-    pbase[me] = s_mine[0];
-    fbase[me] = run + s_mine[3];
-    tbase[me] = tab0 + 4 * s_mine[1];
-    if (me == 0) {
-      if (s_err & 1) status_error(a.status, ARBOR_EINVAL);
-      else if (s_err & 2) status_error(a.status, ARBOR_EUNSUPPORTED);
-      else if (!fits) status_error(a.status, ARBOR_EWORKSPACE);
-    }
+  for (int o = tid; o < a.n_obs; o += nt) {
+    fbase[o] += run;
+    tbase[o] = tab0 + 4 * tbase[o];
   }
-  const int j = a.obs[me];
-  if (s_err || !fits || j < 0 || j >= t.V) return;   // uniform: s_err settled at the sync
-  build_chain(t, a.pl, j, ch);
-  const int n = (int)s_mine[2];
-  int4 *tab = reinterpret_cast<int4 *>(a.part + tab0 + 4 * s_mine[1]);
+  if (tid == 0) {
+    if (s_err & 1) status_error(a.status, ARBOR_EINVAL);
+    else if (s_err & 2) status_error(a.status, ARBOR_EUNSUPPORTED);
+    else if (!fits) status_error(a.status, ARBOR_EWORKSPACE);
+  }
+  // the credited blocks in ascending id
+  int64_t crun = 0;
+  for (int base = 0; base < t.V; base += nt) {
+    const int i = base + tid;
+    const int f = i < t.V ? flag[i] : 0;
+    int64_t ctot;
+    const int64_t cx = block_exclusive_scan<int64_t>(f, sm, &ctot);
+    if (f) cred[1 + crun + cx] = i;
+    crun += ctot;
+  }
+  if (tid == 0) cred[0] = (s_err || !fits) ? 0 : (int32_t)crun;
+}
+
+// One workgroup per observer: its chain (root first, from the setup's walk)
+// and its sub-page table as 16-byte entries (plane row, slot, context offset,
+// valid slots | own << 8 | mask flags) that the streaming kernel reads into
+// registers.
+__global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
+  __shared__ ChainLds ch;
+  if (status_failed(a.status)) return;   // also set by the setup on any error
+  const Tree &t = a.t;
+  const int o = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int j = a.obs[o];
+  const int depth = a.odepth[o];
+  if (tid == 0) ch.depth = depth;
+  if (tid <= depth) {
+    const int x = a.anc[(int64_t)o * MAXD + tid];
+    ch.node[tid] = x;
+    ch.c[tid] = t.n_kept[x];
+    ch.po[tid] = t.page_off[x];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int ctx = 0, sp = 0;
+    for (int e = 0; e <= depth; ++e) {
+      const int c = ch.c[e];
+      ch.ctx[e] = ctx;
+      ch.sp_off[e] = sp;
+      ctx += c;
+      sp += (c + 15) / 16;
+    }
+    ch.sp_off[depth + 1] = sp;
+  }
+  __syncthreads();
+  const int n = ch.sp_off[depth + 1];
+  fill_table(t, a.pl, ch, n);
+  int4 *tab = reinterpret_cast<int4 *>(a.part + a.tbase[o]);
   // the window rows see own positions up to u >= u_min: an own sub-page whose
   // last position is above u_min needs per-key masking in pass 0; in the
   // self-window mode, one whose last position reaches u_min needs it in pass 1
   const int u_min = t.n_full[j] - min(a.W, t.n_full[j]);
   for (int sp = tid; sp < n; sp += blockDim.x) {
     const SubPage e = sub_page(t, a.pl, ch, sp);
-    const bool own = e.d == ch.depth;
+    const bool own = e.d == depth;
     const int last = own ? a.pl.slot_pos[e.slot + e.nvalid - 1] : 0;
     const bool m0 = e.nvalid < 16 || (own && last > u_min);
     const bool m1 = a.self_window && own && last >= u_min;
@@ -844,18 +870,21 @@ struct FinalArgs {
 };
 
 // A += folded sums of every observer below block i (observer order, fp64);
-// rows_seen_i grows.  The four waves of a workgroup split the observers of a
-// 64-slot chunk and are combined in wave order.
+// rows_seen_i grows.  Workgroup x takes the x-th credited block of the setup's
+// list.  The four waves of a workgroup split the observers of a 64-slot chunk
+// and are combined in wave order.
 __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *__restrict__ fbase,
+                                                    const int32_t *__restrict__ cred,
                                                     float *__restrict__ A,
                                                     int64_t *__restrict__ rows_seen) {
   __shared__ int64_t hbase[256];
   __shared__ int s_wcnt[4];
   __shared__ double s_acc[4][64];
   if (status_failed(a.status)) return;
+  if ((int)blockIdx.x >= cred[0]) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
-  const int i = blockIdx.x;
+  const int i = cred[1 + blockIdx.x];
   const int c = t.n_kept[i];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -975,8 +1004,9 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
   const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
   size_t b = 0;
-  // offsets, counts, chains (each carve rounds up to 256 B)
-  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + 8 * 256;
+  // offsets, counts, chains, credited-block flags and list (each carve
+  // rounds up to 256 B)
+  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + (size_t)sz->num_nodes * 8 + 12 * 256;
   // partials and their folded sums
   b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
   // sub-page tables: at most one ragged sub-page per chain node
@@ -1020,6 +1050,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   int32_t *ctxlen = cv.take<int32_t>(nobs);
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
+  int32_t *flag = cv.take<int32_t>((size_t)t.V);
+  int32_t *cred = cv.take<int32_t>((size_t)t.V + 1);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   float *part = reinterpret_cast<float *>(cv.rest());
   const int64_t part_cap = (int64_t)(cv.remaining() / 4);
@@ -1032,15 +1064,19 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.anc = anc;
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
-    hipLaunchKernelGGL(score_setup, dim3(n_obs), dim3(256), 0, stream, a, part_cap, pbase, fbase,
-                       tbase, nsp, ctxlen, odepth, anc);
+    hipLaunchKernelGGL(score_setup, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase, fbase,
+                       tbase, nsp, ctxlen, odepth, anc, flag, cred);
+    hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     timing_begin(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     launch_attn(geom->dtype, geom->head_dim, NRB, grid, stream, a);
     timing_end(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
-    hipLaunchKernelGGL(score_reduce, dim3(t.V, 16), dim3(256), 0, stream, a, fbase, A, rows_seen);
+    // at most V credited blocks, and at most MAXD per observer
+    const int64_t max_cred = std::min<int64_t>(t.V, (int64_t)n_obs * MAXD);
+    hipLaunchKernelGGL(score_reduce, dim3((unsigned)max_cred, 16), dim3(256), 0, stream, a, fbase,
+                       cred, A, rows_seen);
   }
   hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen, fa,
                      status);
