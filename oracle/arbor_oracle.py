@@ -29,6 +29,9 @@ of the paper it follows:
   decode_credit     Sec. 4 Execution (iii): A_i(t) grown from the attention
                     weights of the decoding step itself (thin slice of layers,
                     all heads), credited to proper ancestors of the query's leaf
+  walk              Alg. 2 (event-driven controller): Transition events to a
+                    sequence of active leaves with lazy rehydration, and the
+                    Pressure event raised at B - delta
 
 Readings of points the paper leaves open are listed next to the code that
 takes them.  Parity status: every function here is pinned by the tests in
@@ -619,3 +622,86 @@ def decode_credit(st, leaves, layer_begin, q, q_per_kv, slice_layers, A, rows_se
                 np.add.at(contrib, toks[credit], p[credit])
     A_out = (np.asarray(A, dtype=np.float64) + contrib).astype(np.float32)
     return A_out, rows_seen
+
+
+# ----------------------------------------------------------------------------
+# O9  event-driven controller over a walk  (Alg. 2: Transition, Pressure)
+# ----------------------------------------------------------------------------
+def walk(st, targets, budget, s, A, rows_seen, p, host_k, host_v, pressure_margin=0,
+         q_win=None, window=0, slice_layers=(), q_per_kv=1, v_sig=None, u_sig=None):
+    """Alg. 2 for a sequence of Transition events, one per entry of targets.
+
+    Each event: RootToLeaf and the keep-counts of every block for the new
+    active leaf (allocate: Path* pinned or floored, every other block lowered
+    only where its count drops); Path* blocks with evicted tokens are
+    restored from the token-span record before the leaf is attended (lazy
+    rehydration); the new leaf's window queries q_win[e] attend over its chain
+    and grow A, rows_seen and s (score with that one observer; the reading
+    taken here: the window stands in for the decoding at the new leaf, which
+    follows the rehydration); the blocks whose count drops are evicted
+    (select + compact).  Then, if the resident tokens M reach B - delta
+    (RaisePressureEvent, delta = pressure_margin > 0), a Pressure event
+    recomputes the counts for the budget B - delta and evicts again.
+    Returns (state, A, rows_seen, s, stats, status) where stats has one row
+    per event: [resident tokens after it, tokens restored from the record,
+    tokens evicted, 1 if Pressure fired].  A negative status stops the walk.
+    """
+    rehyd = int(p.get("lazy_rehydration", 1)) != 0
+    mode = int(p.get("select_mode", TAIL_HEAVY))
+    n_sinks = int(p.get("n_sinks", 0))
+    A = np.asarray(A, np.float32).copy()
+    rows_seen = np.asarray(rows_seen, np.int64).copy()
+    s = np.asarray(s, np.float32).copy()
+    status = OK
+    stats = []
+
+    def note(code):
+        nonlocal status
+        if code < 0:
+            status = code
+        elif code > 0 and status == OK:
+            status = code
+
+    for e, leaf in enumerate(targets):
+        n_full = st["n_full"]
+        c = st["n_kept"]
+        k, _, on_path, code = allocate(st["parent"], n_full, c, [int(leaf)], budget, s, p)
+        note(code)
+        if status < 0:
+            break
+        restored = sum(int(n_full[i]) - int(c[i]) for i in range(len(c))
+                       if rehyd and on_path[i] and c[i] < n_full[i])
+        row = [int(np.sum(k)), restored, int(np.sum(np.maximum(0, c - k))), 0]
+        if rehyd:
+            st, code = rehydrate(st, on_path, host_k, host_v)
+            note(code)
+            if status < 0:
+                break
+        if q_win is not None:
+            A, rows_seen, _, s = score(st, [int(leaf)], q_win[e:e + 1], window, list(slice_layers),
+                                       q_per_kv, v_sig, u_sig, A, rows_seen,
+                                       theta=p.get("theta", (1.0, 1.0, 1.0)),
+                                       self_window=int(p.get("score_self_window", 0)))
+        sel, code = select(st, A, k, p["l_tail"], mode, n_sinks)
+        note(code)
+        if status < 0:
+            break
+        st = compact(st, k, sel)
+        if pressure_margin > 0:
+            bp = int(budget) - int(pressure_margin)
+            if int(np.sum(st["n_kept"])) >= bp:
+                c = st["n_kept"]
+                k, _, _, code = allocate(st["parent"], st["n_full"], c, [int(leaf)], bp, s, p)
+                note(code)
+                if status < 0:
+                    break
+                row[0] = int(np.sum(k))
+                row[2] += int(np.sum(np.maximum(0, c - k)))
+                row[3] = 1
+                sel, code = select(st, A, k, p["l_tail"], mode, n_sinks)
+                note(code)
+                if status < 0:
+                    break
+                st = compact(st, k, sel)
+        stats.append(row)
+    return st, A, rows_seen, s, np.array(stats, np.int64).reshape(-1, 4), status
