@@ -386,6 +386,62 @@ int arbor_tree_decode_attn_scored(const arbor_geom_t *geom, const arbor_tree_t *
                                   hipStream_t stream);
 
 /*
+ * arbor_walk -- the event-driven controller of Alg. 2 run on the device for a
+ * sequence of Transition events (the active leaf switches by expansion or
+ * backtracking), with no host round trip between events: the host enqueues
+ * every kernel of every step at once and never waits, each step reading its
+ * active leaf from targets[step] on the device.  Step e:
+ *   1. Transition: arbor_allocate with active = {targets[e]} and the budget
+ *      (Path* pinned -- or floored, params->k_protect -- and every other
+ *      block lowered only where its new count is smaller, Alg. 2);
+ *   2. lazy rehydration of the Path* blocks with evicted tokens from the
+ *      token-span record (arbor_rehydrate; skipped when
+ *      params->lazy_rehydration = 0);
+ *   3. scoring (when q_win is not NULL): the window queries of the new
+ *      active leaf, q_win + e * n_slice * Hq * window * head_dim, attend over
+ *      its now restored chain and grow A, rows_seen, a and s (arbor_score
+ *      with that one observer); the next step's allocation reads this s;
+ *   4. arbor_select + arbor_compact of the blocks whose count drops;
+ *   5. Pressure, when pressure_margin > 0: if the resident tokens M reach
+ *      budget - pressure_margin (RaisePressureEvent of Alg. 2, margin delta),
+ *      the allocation is redone for the budget budget - pressure_margin
+ *      (off-path blocks lowered in priority order) and steps 4 run again.
+ * stats (device int64 [n_steps][4], nullable) receives per step: the resident
+ * tokens after the step, the tokens restored from the token store, the tokens
+ * evicted, and 1 if a Pressure event fired.  k, delta, on_path (device [V])
+ * and sel_pos (device [N]) are the caller's scratch for the step outputs and
+ * hold those of the last step.  The results equal n_steps sequences of the
+ * single-event entry points issued one by one.  A negative status stops every
+ * later step on the device (the status is sticky).
+ * Errors: those of the entry points above; EINVAL for n_steps < 0 or missing
+ * buffers.
+ */
+typedef struct {
+  const int32_t *targets;      /* device [n_steps]: active leaf of each step          */
+  int32_t n_steps;
+  int64_t budget_tokens;       /* B                                                   */
+  int64_t pressure_margin;     /* delta of Alg. 2; 0: no Pressure events              */
+  const void *q_win;           /* device [n_steps][n_slice][Hq][window][head_dim] or NULL */
+  int32_t window;
+  const int32_t *slice_layers; /* (host) n_slice layer ids (scoring only)             */
+  int32_t n_slice;
+  const float *v_in, *u_in;    /* device [V] (scoring only)                           */
+  float *A;                    /* device [N], in/out                                  */
+  int64_t *rows_seen;          /* device [V], in/out (scoring only)                   */
+  float *a_out;                /* device [V] (scoring only)                           */
+  float *s;                    /* device [V], in/out: the scores the allocations read */
+  const void *host_k, *host_v; /* (pinned host) or device token store [N][L][Hkv][d]  */
+  int32_t *k, *delta;          /* device [V] scratch / last step's outputs            */
+  uint8_t *on_path;            /* device [V]                                          */
+  int32_t *sel_pos;            /* device [N]                                          */
+  int64_t *stats;              /* device [n_steps][4], nullable                       */
+} arbor_walk_t;
+
+int arbor_walk(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+               const arbor_walk_t *walk, const arbor_params_t *params, int32_t *status,
+               void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * arbor_uncertainty -- the uncertainty signal of MSVE (Sec. 4, Eq. 1).  Row r of
  * logits ([n_rows][vocab], dtype ARBOR_BF16 or ARBOR_F32, rows contiguous) is
  * the next-token logit vector after closing a block; with p = softmax(row):

@@ -69,6 +69,18 @@ class DecodeCredit(ctypes.Structure):
                 ("rows_seen", ctypes.c_void_p)]
 
 
+class Walk(ctypes.Structure):
+    _fields_ = [("targets", ctypes.c_void_p), ("n_steps", ctypes.c_int32),
+                ("budget_tokens", ctypes.c_int64), ("pressure_margin", ctypes.c_int64),
+                ("q_win", ctypes.c_void_p), ("window", ctypes.c_int32),
+                ("slice_layers", ctypes.POINTER(ctypes.c_int32)), ("n_slice", ctypes.c_int32),
+                ("v_in", ctypes.c_void_p), ("u_in", ctypes.c_void_p), ("A", ctypes.c_void_p),
+                ("rows_seen", ctypes.c_void_p), ("a_out", ctypes.c_void_p), ("s", ctypes.c_void_p),
+                ("host_k", ctypes.c_void_p), ("host_v", ctypes.c_void_p), ("k", ctypes.c_void_p),
+                ("delta", ctypes.c_void_p), ("on_path", ctypes.c_void_p),
+                ("sel_pos", ctypes.c_void_p), ("stats", ctypes.c_void_p)]
+
+
 class Sizes(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_int32), ("num_tokens", ctypes.c_int64),
                 ("max_context", ctypes.c_int64), ("max_observers", ctypes.c_int32),
@@ -109,6 +121,7 @@ def load() -> ctypes.CDLL:
             "arbor_uncertainty": (ctypes.c_int, [vp, i32, i32, i64, i32, vp, vp, i32, vp, vp, sz,
                                                  vp]),
             "arbor_uncertainty_workspace_size": (sz, [i32, i64, i32]),
+            "arbor_walk": (ctypes.c_int, [G, T, Pl, ctypes.POINTER(Walk), Pa, vp, vp, sz, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(lib, name)
@@ -122,7 +135,7 @@ def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
             "arbor_select", "arbor_compact", "arbor_compact_noalloc", "arbor_rehydrate", "arbor_tree_decode_attn",
             "arbor_tree_decode_attn_scored", "arbor_uncertainty",
-            "arbor_uncertainty_workspace_size"]
+            "arbor_uncertainty_workspace_size", "arbor_walk"]
 
 
 def _dev(t: torch.Tensor | None, name: str):
@@ -343,6 +356,27 @@ def arbor_tree_decode_attn_scored(kv: KVState, leaves, layer_begin, layer_end, q
                                                 _dev(status, "status"),
                                                 _dev(workspace, "workspace"),
                                                 int(workspace.numel()), _stream(stream))
+
+
+def arbor_walk(kv: KVState, targets, budget, params: dict, A, s, k, delta, on_path, sel_pos,
+               status, workspace, host_k=None, host_v=None, pressure_margin=0, q_win=None,
+               window=0, slice_layers=(), v_in=None, u_in=None, rows_seen=None, a_out=None,
+               stats=None, stream=None) -> int:
+    """Alg. 2's controller over the Transition events to targets[0..n) on the
+    device (see include/arbor.h)."""
+    g, t, p = kv.geom(), kv.tree(), kv.pool()
+    pa = params_struct(params)
+    sl = (ctypes.c_int32 * max(1, len(slice_layers)))(*[int(x) for x in slice_layers])
+    hk = None if host_k is None else _host_or_dev(host_k, "host_k")
+    hv = None if host_v is None else _host_or_dev(host_v, "host_v")
+    w = Walk(_dev(targets, "targets"), int(targets.numel()), int(budget), int(pressure_margin),
+             _dev(q_win, "q_win"), int(window), sl, len(slice_layers), _dev(v_in, "v_in"),
+             _dev(u_in, "u_in"), _dev(A, "A"), _dev(rows_seen, "rows_seen"),
+             _dev(a_out, "a_out"), _dev(s, "s"), hk, hv, _dev(k, "k"), _dev(delta, "delta"),
+             _dev(on_path, "on_path"), _dev(sel_pos, "sel_pos"), _dev(stats, "stats"))
+    return load().arbor_walk(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p), ctypes.byref(w),
+                             ctypes.byref(pa), _dev(status, "status"), _dev(workspace, "workspace"),
+                             int(workspace.numel()), _stream(stream))
 
 
 def arbor_uncertainty_workspace_size(n_rows: int, vocab: int, dtype: int) -> int:

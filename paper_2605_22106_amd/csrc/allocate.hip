@@ -267,7 +267,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
                                                       int32_t *__restrict__ k_out,
                                                       int32_t *__restrict__ delta_out,
                                                       uint8_t *__restrict__ on_path,
-                                                      int32_t *status, AllocWs ws, int in_lds) {
+                                                      int32_t *status, AllocWs ws, int in_lds,
+                                                      int gate) {
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
   __shared__ int64_t sm[3 * 16];
   __shared__ int s_err;
@@ -279,6 +280,17 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   const int wave = tid >> 6, lane = lane_id();
   const int V = t.V;
   if (tid == 0) s_err = 0;
+  if (gate) {
+    // a Pressure event (Alg. 2): it fires only when the resident tokens
+    // reach the budget it is given; otherwise every count stays as it is
+    int64_t m = 0;
+    for (int i = tid; i < V; i += AT) m += t.n_kept[i];
+    m = block_sum<int64_t>(m, sm);
+    if (m < budget) {
+      for (int i = tid; i < V; i += AT) k_out[i] = t.n_kept[i];
+      return;
+    }
+  }
 
   // listed prices: LDS after the node state when few enough, else workspace
   uint64_t *const cand_lds =
@@ -703,10 +715,55 @@ size_t allocate_workspace(const arbor_sizes_t *sz) {
   return (size_t)sz->num_nodes * (5 * 4 + 8 * 2 + 64) + (size_t)sz->num_tokens * 16 + 8192;
 }
 
+// Per-event statistics of the device-side controller (arbor_walk): one
+// workgroup after each allocation of a step.  transition = 1: row[0] = sum of
+// the keep-counts, row[1] = tokens the rehydration of this step restores from
+// the token store (Path* blocks with c_i < n_i), row[2] = tokens evicted
+// (sum of c_i - k_i where k_i < c_i), row[3] = 0.  transition = 0 (the gated
+// Pressure event, budget `budget`): if it fired (resident tokens >= budget),
+// row[0] = the new sum, row[2] += its evictions, row[3] = 1.
+__global__ __launch_bounds__(AT) void walk_stats(Tree t, const int32_t *__restrict__ k,
+                                                 const uint8_t *__restrict__ on_path,
+                                                 int64_t budget, int transition, int rehydrate,
+                                                 int64_t *__restrict__ row, int32_t *status) {
+  __shared__ int64_t sm[3 * 16];
+  if (status_failed(status)) return;
+  int64_t v[3] = {0, 0, 0};   // sum k, evicted, restored or resident
+  for (int i = threadIdx.x; i < t.V; i += AT) {
+    const int c = t.n_kept[i], ki = k[i], n = t.n_full[i];
+    v[0] += ki;
+    v[1] += ki < c ? c - ki : 0;
+    v[2] += transition ? (on_path[i] && rehydrate && c < n ? n - c : 0) : c;
+  }
+  block_sum3(v, sm);
+  if (threadIdx.x == 0) {
+    if (transition) {
+      row[0] = v[0];
+      row[1] = v[2];
+      row[2] = v[1];
+      row[3] = 0;
+    } else if (v[2] >= budget) {
+      row[0] = v[0];
+      row[2] += v[1];
+      row[3] = 1;
+    }
+  }
+}
+
+int launch_walk_stats(const arbor_tree_t *tree, const int32_t *k, const uint8_t *on_path,
+                      int64_t budget, int transition, int rehydrate, int64_t *row,
+                      int32_t *status, hipStream_t stream) {
+  Tree t = make_tree(tree);
+  if (t.V <= 0) return ARBOR_OK;
+  hipLaunchKernelGGL(walk_stats, dim3(1), dim3(AT), 0, stream, t, k, on_path, budget, transition,
+                     rehydrate, row, status);
+  return hip_ok(hipGetLastError());
+}
+
 int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_active,
                     int64_t budget_tokens, const float *s, const arbor_params_t *params,
                     int32_t *k_out, int32_t *delta_out, uint8_t *on_path_out, int32_t *status,
-                    void *workspace, size_t workspace_bytes, hipStream_t stream) {
+                    void *workspace, size_t workspace_bytes, hipStream_t stream, int gate) {
   Tree t = make_tree(tree);
   if (t.V <= 0) return ARBOR_OK;
   Carve cv(workspace, workspace_bytes);
@@ -734,7 +791,7 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
                      2 * (size_t)kCandLds * sizeof(uint64_t);
   hipLaunchKernelGGL(allocate_kernel, dim3(1), dim3(AT), lds, stream, t, active, n_active,
                      (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws,
-                     in_lds);
+                     in_lds, gate);
   return hip_ok(hipGetLastError());
 }
 

@@ -11,7 +11,7 @@ int launch_score(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t 
                  int32_t *, void *, size_t, hipStream_t);
 int launch_allocate(const arbor_tree_t *, const int32_t *, int32_t, int64_t, const float *,
                     const arbor_params_t *, int32_t *, int32_t *, uint8_t *, int32_t *, void *,
-                    size_t, hipStream_t);
+                    size_t, hipStream_t, int gate);
 int launch_select(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t *, const float *,
                   const int32_t *, const arbor_params_t *, int32_t *, int32_t *, hipStream_t);
 int launch_compact(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const int32_t *,
@@ -133,7 +133,7 @@ int arbor_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_ac
       (params->lazy_rehydration != 0 && params->lazy_rehydration != 1))
     return ARBOR_EINVAL;
   return launch_allocate(tree, active, n_active, budget_tokens, s, params, k_out, delta_out,
-                         on_path_out, status, workspace, workspace_bytes, stream);
+                         on_path_out, status, workspace, workspace_bytes, stream, 0);
 }
 
 int arbor_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor_pool_t *pool,

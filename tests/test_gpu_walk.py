@@ -66,11 +66,17 @@ def _rows_match_store(kv, st, meta, i):
         assert torch.equal(got.view(torch.int16), want.view(torch.int16)), i
 
 
-def test_deep_tree_walk_with_lazy_rehydration():
+@pytest.fixture(scope="module")
+def deep():
     cfg = synth.CONFIGS["deep"]
     st = synth.build_config(cfg, device="cuda", decode_queries=False, host_store="device")
     kv = L.kv_state_from(st, "cuda")
     del st["k"], st["v"]                                      # the pool lives in kv
+    return cfg, st, kv
+
+
+def test_deep_tree_walk_with_lazy_rehydration(deep):
+    cfg, st, kv = deep
     p = st["params"]
     V, N, P = kv.num_nodes, kv.num_tokens, kv.page_size
     parent = st["parent"].tolist()
@@ -134,3 +140,66 @@ def test_deep_tree_walk_with_lazy_rehydration():
             _rows_match_store(kv, st, meta2, int(i))
     print(f"walk: {len(targets)} steps, {n_rehydrated} blocks rehydrated", flush=True)
     assert n_rehydrated > 0, "the walk backtracks into evicted blocks"
+
+
+def test_deep_tree_walk_on_the_device(deep):
+    """The full 256-event walk of the deep configuration as one arbor_walk call
+    (Alg. 2 on the device: Transition, lazy rehydration, scoring of each new
+    leaf's window over its restored chain, eviction, Pressure at B - delta),
+    continuing from the state the test above leaves."""
+    cfg, st, kv = deep
+    p = dict(st["params"])
+    V, N, P = kv.num_nodes, kv.num_tokens, kv.page_size
+    parent = st["parent"].tolist()
+    start = int(st["active"][0])
+    targets = synth.walk_targets(parent, cfg.walk_steps, cfg.walk_backtrack, cfg.seed + 1, start)
+    steps = len(targets)
+    Hq = kv.kv_heads * kv.q_per_kv
+    g = torch.Generator(device="cuda").manual_seed(17)
+    q = torch.randn((steps, 2, Hq, cfg.window, kv.head_dim), generator=g,
+                    device="cuda").to(torch.bfloat16)
+    rng = np.random.default_rng(cfg.seed)
+    s = torch.tensor(rng.random(V).astype(np.float32), device="cuda")
+    A = torch.zeros(N, device="cuda")
+    rows = torch.zeros(V, dtype=torch.int64, device="cuda")
+    a = torch.empty(V, device="cuda")
+    k = torch.empty(V, dtype=torch.int32, device="cuda")
+    delta = torch.empty_like(k)
+    on_path = torch.empty(V, dtype=torch.uint8, device="cuda")
+    sel = torch.empty(N, dtype=torch.int32, device="cuda")
+    stats = torch.zeros((steps, 4), dtype=torch.int64, device="cuda")
+    ws = torch.empty(L.arbor_workspace_size(kv, max_context=1024 + 8 * 64, max_observers=1,
+                                            window=cfg.window, n_slice=2),
+                     dtype=torch.uint8, device="cuda")
+    margin = 2048
+    before = int(kv.n_kept.sum())
+    stt = status()
+    print(f"device walk: {steps} events", flush=True)
+    check_rc(L.arbor_walk(kv, torch.tensor(targets, dtype=torch.int32, device="cuda"),
+                          st["budget"], p, A, s, k, delta, on_path, sel, stt, ws,
+                          host_k=st["host_k"], host_v=st["host_v"], pressure_margin=margin,
+                          q_win=q, window=cfg.window, slice_layers=st["slice_layers"],
+                          v_in=st["v_sig"].cuda(), u_in=st["u_sig"].cuda(), rows_seen=rows,
+                          a_out=a, stats=stats))
+    torch.cuda.synchronize()
+    code = int(stt)
+    assert code >= 0
+    t = stats.cpu().numpy()
+    meta = _meta(kv)
+    after = int(meta["n_kept"].sum())
+    assert t[-1, 0] == after
+    assert after == before + int(t[:, 1].sum()) - int(t[:, 2].sum())
+    assert t[:, 1].sum() > 0 and t[:, 3].sum() > 0
+    if code == L.OK:
+        assert np.all(t[:, 0] <= st["budget"])
+        assert np.all(t[t[:, 3] == 1, 0] <= st["budget"] - margin)
+    used = sum(-(-int(c) // P) for c in meta["n_kept"])
+    assert used + int(meta["free_top"]) == kv.slot_pos.shape[0]
+    for i in O.chain(parent, targets[-1]):
+        assert int(meta["n_kept"][i]) == int(meta["n_full"][i])
+    # A grew exactly where the scored leaves' ancestors are
+    rows_np = rows.cpu().numpy()
+    credited = {a_ for leaf in targets for a_ in O.chain(parent, leaf)[:-1]}
+    assert set(np.nonzero(rows_np)[0].tolist()) == credited
+    for i in [targets[-1], targets[len(targets) // 2]] + O.chain(parent, targets[0])[:2]:
+        _rows_match_store(kv, st, meta, int(i))
