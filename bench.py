@@ -191,6 +191,9 @@ def parse():
     ap.add_argument("--no-uncertainty-leg", action="store_true")
     ap.add_argument("--no-credit-leg", action="store_true",
                     help="skip timing arbor_tree_decode_attn_scored (decode + A credit)")
+    ap.add_argument("--legs", default="dpts,llama70b,deep",
+                    help="other configurations measured after the headline one")
+    ap.add_argument("--no-legs", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch the timed steps eagerly instead of replaying a captured HIP graph")
     ap.add_argument("--summarize-trace", metavar="DB",
@@ -236,7 +239,8 @@ class Event:
         nbytes = L.arbor_workspace_size(kv, max_context=chain_max,
                                         max_observers=self.observers.numel(),
                                         window=st["window"], n_slice=len(st["slice_layers"]),
-                                        max_leaves=64, max_layers=kv.layers)
+                                        max_leaves=max(4, st["active"].numel()),
+                                        max_layers=kv.layers)
         self.ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         self.params = dict(st["params"])
 
@@ -249,10 +253,10 @@ class Event:
         self.rows.zero_()
         self.status.zero_()
 
-    def run(self, active, marks=None, timings=None):
+    def run(self, active, marks=None, timings=None, decode=True):
         """score -> allocate -> select -> compact -> decode; `marks` records events
         between the entry points, `timings` ({stage: L.Timing}) asks each call to
-        time its rated kernel."""
+        time its rated kernel; decode=False stops after the compaction."""
         tm = timings or {}
         kv, st = self.kv, self.st
         ev = (lambda: marks.append(torch.cuda.Event(enable_timing=True))) if marks is not None else None
@@ -276,6 +280,8 @@ class Event:
         self.check(L.arbor_compact(kv, self.k, self.sel, self.status, self.ws,
                                    timing=tm.get("compact")))
         mark()
+        if not decode:
+            return
         self.check(L.arbor_tree_decode_attn(kv, active, 0, kv.layers, self.q_dec, self.out,
                                             self.lse, 0.0, self.status, self.ws,
                                             timing=tm.get("decode")))
@@ -363,6 +369,16 @@ def cpu_baseline(st, kv_cpu_state, sel_budget_active, work, reps=2):
                    v=np_float(d["v"]), page_size=int(d["page_size"]))
         return out
 
+    # the oracle's numpy products run on as many BLAS threads as the process
+    # has cores
+    cores = len(os.sched_getaffinity(0))
+    blas_threads = None
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores, user_api="blas")
+        blas_threads = cores
+    except Exception:       # threadpoolctl missing: numpy's own default
+        limiter = None
     t0 = time.perf_counter()
     ost = oracle_state(kv_cpu_state)
     t_conv = time.perf_counter() - t0
@@ -391,14 +407,336 @@ def cpu_baseline(st, kv_cpu_state, sel_budget_active, work, reps=2):
         t5 = time.perf_counter()
         for name, dt in zip(stage, (t1 - t0, t2 - t1, t3 - t2, t4 - t3, t5 - t4)):
             stage[name] += dt / reps
+    if limiter is not None:
+        limiter.unregister()
     total = sum(stage.values())
-    cores = len(os.sched_getaffinity(0))
     return {"value": st["num_tokens"] / total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": cpu_model(), "blas_threads": blas_threads,
             "sample": (f"{reps} whole steps of the same event on the same inputs (all "
                        f"{len(obs)} observer windows scored, allocate, select, compact, decode of "
                        f"the {len(active)} active leaves over all {Lyr} layers), "
                        f"{total:.1f} s per step, {reps * total:.1f} s in all"),
             "stage_s": dict(stage, state_to_numpy=t_conv)}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def copy_rate_gbs(mib=1024, reps=5):
+    """Read+write GB/s of a plain device-to-device copy of `mib` MiB (a
+    reference for what a data-moving kernel can reach on this GPU)."""
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2.0 * (mib << 20) / (ms * 1e-3) / 1e9
+
+
+def config_label(cfg, kv):
+    return (f"{cfg.name}: {cfg.layers} layers, {cfg.kv_heads} KV heads, {cfg.q_heads} q heads, "
+            f"head_dim {cfg.head_dim}, {cfg.dtype}; root {cfg.root_tokens}, branching "
+            f"{cfg.branching}, depth {cfg.depth}, {cfg.node_tokens} tokens/node "
+            f"({kv.num_nodes} nodes, {kv.num_tokens} tokens); {cfg.n_active} active leaves; "
+            f"budget {cfg.rho:.0%}; window {cfg.window}")
+
+
+def measure_event(cfg, steps, warmup, use_graph=True, copy_gbs=None, rehydrate_leg=True):
+    """One eviction event on configuration `cfg` (score -> allocate -> select ->
+    compact -> tree decode of the active leaves over every layer) on inputs
+    resident in HBM: the whole step and the event without the decode, each
+    captured once as a HIP graph and replayed, then a breakdown pass with the
+    rated kernels timed on their own.  Returns (result dict, objects the
+    caller may reuse)."""
+    st = synth.build_config(cfg, device="cuda", host_store=rehydrate_leg)
+    kv = L.kv_state_from(st, "cuda")
+    del st["k"], st["v"]                            # the pool lives in kv
+    pristine = kv.clone()
+    ev = Event(kv, st, cfg)
+    active = st["active"].cuda()
+    flush = torch.ones(128 << 20, dtype=torch.int32, device="cuda")  # 512 MiB
+
+    def restore():
+        kv.copy_from(pristine)
+        ev.reset_scores()
+        flush.sum()  # reads only: leaves the last-level cache clean
+
+    def raise_on_status():
+        code = int(ev.status)
+        if code < 0:
+            raise RuntimeError(f"device status {code}: {L.arbor_strerror(code)}")
+        return code
+
+    for _ in range(warmup):
+        restore()
+        ev.run(active)
+    torch.cuda.synchronize()
+    raise_on_status()
+
+    # the step (and the event without the decode) captured once as HIP graphs:
+    # their launches replay without per-launch host work (the library only
+    # enqueues kernels: no host synchronisation, allocation or memset inside
+    # an entry point)
+    graphs = {}
+    if use_graph:
+        for name, dec in (("step", True), ("event", False)):
+            restore()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                ev.run(active, decode=dec)
+            torch.cuda.synchronize()
+            graphs[name] = g
+
+    def timed(n, name):
+        times, wall = [], 0.0
+        for _ in range(n):
+            restore()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            e0.record()
+            if name in graphs:
+                graphs[name].replay()
+            else:
+                ev.run(active, decode=name == "step")
+            e1.record()
+            torch.cuda.synchronize()
+            wall += time.perf_counter() - t0
+            times.append(e0.elapsed_time(e1))
+        return times, wall
+
+    if graphs:
+        timed(warmup, "step")
+        raise_on_status()
+    step_ms, wall = timed(steps, "step")
+    event_ms, _ = timed(steps, "event")
+    eager_ms = None
+    if graphs:
+        saved = graphs
+        graphs = {}
+        eager_ms = float(np.mean(timed(steps, "step")[0]))
+        graphs = saved
+    status = raise_on_status()
+
+    # breakdown pass: events between the entry points and around the rated
+    # kernels' launches (one timing request per call); kept apart from the
+    # timed steps because every recorded event costs the stream a little time
+    kevents = {}
+    for name in STAGE_KERNEL:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        e1.record()
+        kevents[name] = (e0, e1)
+    ktiming = {name: L.timing(STAGE_KERNEL[name][0], *kevents[name]) for name in STAGE_KERNEL}
+    stages = ["score", "allocate", "select", "compact", "decode"]
+    per_stage = {x: [] for x in stages}
+    per_kernel = {x: [] for x in STAGE_KERNEL}
+    for _ in range(steps):
+        restore()
+        torch.cuda.synchronize()
+        marks = []
+        ev.run(active, marks, ktiming)
+        torch.cuda.synchronize()
+        for si, x in enumerate(stages):
+            per_stage[x].append(marks[si].elapsed_time(marks[si + 1]))
+        for x, (e0, e1) in kevents.items():
+            per_kernel[x].append(e0.elapsed_time(e1))
+    raise_on_status()
+    ms = float(np.mean(step_ms))
+    ems = float(np.mean(event_ms))
+    N_event = int(pristine.n_kept.sum())
+    k_after = ev.k.cpu().tolist()
+    st["_sel_cpu"] = ev.sel.cpu().numpy()
+    work = algorithmic_work(st, kv, k_after, pristine.n_kept.cpu().tolist(), st["active"].tolist())
+    mean = {x: float(np.mean(v)) for x, v in per_stage.items()}
+    kmean = {x: float(np.mean(v)) for x, v in per_kernel.items()}
+    rates = {
+        "score": {"bound": "mfma", "achieved": work["score_flops"] / (kmean["score"] * 1e-3) / 1e12,
+                  "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"},
+        "compact": {"bound": "hbm",
+                    "achieved": work["compact_bytes"] / (kmean["compact"] * 1e-3) / 1e9,
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+        "decode": {"bound": "hbm", "achieved": work["decode_bytes"] / (kmean["decode"] * 1e-3) / 1e9,
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+        "select": {"bound": "hbm", "achieved": work["select_bytes"] / (kmean["select"] * 1e-3) / 1e9,
+                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
+    }
+    entry = {"score": "arbor_score", "compact": "arbor_compact",
+             "decode": "arbor_tree_decode_attn", "select": "arbor_select"}
+    for st_name, r in rates.items():
+        _, kname, ksrc = STAGE_KERNEL[st_name]
+        r["frac"] = r["achieved"] / r["peak"]
+        if copy_gbs and r["unit"] == "GB/s":
+            r["frac_of_copy"] = r["achieved"] / copy_gbs
+        r["kernel"] = kname
+        r["entry_point"] = entry[st_name]
+        r["ms_per_launch"] = kmean[st_name]
+        r["stage_ms"] = mean[st_name]
+        tr = stored_kernel_traffic(cfg.name, kname, ksrc)
+        r["traffic"] = None if tr is None else tr["read_bytes"] + tr["write_bytes"]
+        if tr is not None:
+            r["traffic_kernels"] = tr["kernels"]
+    # the entry points rated on their whole time: select + compact together
+    # (the eviction and compaction of the event), the decode entry point
+    sc_ms = mean["select"] + mean["compact"]
+    entry_rates = {
+        "select+compact": {"ms": sc_ms, "bytes": work["compact_bytes"] + work["select_bytes"],
+                           "achieved": (work["compact_bytes"] + work["select_bytes"])
+                           / (sc_ms * 1e-3) / 1e9},
+        "decode": {"ms": mean["decode"], "bytes": work["decode_bytes"],
+                   "achieved": work["decode_bytes"] / (mean["decode"] * 1e-3) / 1e9},
+    }
+    for r in entry_rates.values():
+        r.update(peak=HBM_PEAK_GBS, unit="GB/s", frac=r["achieved"] / HBM_PEAK_GBS)
+        if copy_gbs:
+            r["frac_of_copy"] = r["achieved"] / copy_gbs
+    res = {
+        "workload": config_label(cfg, kv), "tokens_per_step": N_event, "ms_per_step": ms,
+        "value": N_event / (ms * 1e-3),
+        "event_ms": ems, "event_tokens_per_s": N_event / (ems * 1e-3),
+        "stages_ms": mean, "rates": rates, "entry_rates": entry_rates,
+        "decode_union_vs_naive_bytes": [work["decode_bytes"], work["decode_naive_bytes"]],
+        "compact_moved_rows": work["moved_rows"], "wall_ms_per_step": wall / steps * 1e3,
+        "launch": "hip graph replay of the captured step" if graphs else "eager",
+        "eager_ms_per_step": eager_ms, "status": status,
+    }
+    env = dict(st=st, kv=kv, pristine=pristine, ev=ev, active=active, flush=flush,
+               restore=restore, work=work)
+    if rehydrate_leg:
+        res["rehydrate"] = rehydrate_leg_of(env)
+    return res, env
+
+
+def rehydrate_leg_of(env):
+    """A transition to other leaves after the event: lazy rehydration of the
+    new Path* from the pinned-host token store (PCIe-inclusive)."""
+    st, kv, ev, restore = env["st"], env["kv"], env["ev"], env["restore"]
+    restore()
+    ev.run(env["active"])
+    parent = st["parent"].tolist()
+    leaves = [i for i in range(kv.num_nodes) if i not in parent]
+    a0 = set(st["active"].tolist())
+    alt = [l for l in leaves if l not in a0]
+    a1 = torch.tensor([alt[(j * len(alt)) // len(a0) + 3] for j in range(len(a0))],
+                      dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    n_kept_before = kv.n_kept.cpu().numpy()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    ev.check(L.arbor_allocate(kv, a1, st["budget"], ev.s, ev.params, ev.k, ev.delta,
+                              ev.on_path, ev.status, ev.ws))
+    e[1].record()
+    ev.check(L.arbor_rehydrate(kv, ev.on_path, st["host_k"], st["host_v"], ev.status, ev.ws))
+    e[2].record()
+    torch.cuda.synchronize()
+    onp = ev.on_path.cpu().numpy().astype(bool)
+    nf = st["n_full"].numpy()
+    restored = int(np.sum((nf - n_kept_before)[onp]))
+    row_bytes = kv.layers * kv.kv_heads * kv.head_dim * 2 * 2
+    t_re = e[1].elapsed_time(e[2])
+    return {"ms": t_re, "tokens_from_host": restored,
+            "host_link_gbs": restored * row_bytes / (t_re * 1e-3) / 1e9,
+            "nodes": int(np.sum(onp & (n_kept_before < nf))), "status": int(ev.status),
+            "note": "pinned host -> HBM, PCIe-inclusive; not part of value"}
+
+
+def walk_leg(steps_cap=None):
+    """The deep backtracking tree (9,841 nodes, 82.7 GB of pool, budget 20 %):
+    a 256-event random walk with 30 % backtracking run by arbor_walk (Alg. 2 on
+    the device: Transition, lazy rehydration, scoring of each new leaf's
+    window, eviction, Pressure at B - delta).  The first event (from full
+    retention down to the budget) is timed on its own, then the other 255 in
+    one call.  The token-span record stays in device memory: the 2 x 82.7 GB
+    record exceeds the host memory the box can pin."""
+    cfg = synth.CONFIGS["deep"]
+    st = synth.build_config(cfg, device="cuda", decode_queries=False, host_store="device",
+                            observers=[0])
+    kv = L.kv_state_from(st, "cuda")
+    del st["k"], st["v"], st["q_win"]
+    V, N = kv.num_nodes, kv.num_tokens
+    parent = st["parent"].tolist()
+    n_ev = cfg.walk_steps if steps_cap is None else min(cfg.walk_steps, steps_cap)
+    targets = synth.walk_targets(parent, n_ev, cfg.walk_backtrack, cfg.seed, int(st["active"][0]))
+    Hq = kv.kv_heads * kv.q_per_kv
+    g = torch.Generator(device="cuda").manual_seed(cfg.seed)
+    q = torch.randn((len(targets), len(st["slice_layers"]), Hq, cfg.window, kv.head_dim),
+                    generator=g, device="cuda").to(torch.bfloat16)
+    rng = np.random.default_rng(cfg.seed)
+    s = torch.tensor(rng.random(V).astype(np.float32), device="cuda")
+    A = torch.zeros(N, device="cuda")
+    rows = torch.zeros(V, dtype=torch.int64, device="cuda")
+    a = torch.empty(V, device="cuda")
+    k = torch.empty(V, dtype=torch.int32, device="cuda")
+    delta = torch.empty_like(k)
+    on_path = torch.empty(V, dtype=torch.uint8, device="cuda")
+    sel = torch.empty(N, dtype=torch.int32, device="cuda")
+    stats = torch.zeros((len(targets), 4), dtype=torch.int64, device="cuda")
+    ws = torch.empty(L.arbor_workspace_size(kv, max_context=cfg.root_tokens
+                                            + cfg.depth * cfg.node_tokens, max_observers=1,
+                                            window=cfg.window, n_slice=len(st["slice_layers"])),
+                     dtype=torch.uint8, device="cuda")
+    stt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    tg = torch.tensor(targets, dtype=torch.int32, device="cuda")
+    margin = 2048
+    p = dict(st["params"])
+    v_in, u_in = st["v_sig"].cuda(), st["u_sig"].cuda()
+
+    def run(lo, hi):
+        rc = L.arbor_walk(kv, tg[lo:hi], st["budget"], p, A, s, k, delta, on_path, sel, stt, ws,
+                          host_k=st["host_k"], host_v=st["host_v"], pressure_margin=margin,
+                          q_win=q[lo:hi], window=cfg.window, slice_layers=st["slice_layers"],
+                          v_in=v_in, u_in=u_in, rows_seen=rows, a_out=a, stats=stats[lo:hi])
+        if rc != L.OK:
+            raise RuntimeError(f"arbor_walk failed on the host: {L.arbor_strerror(rc)}")
+
+    torch.cuda.synchronize()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record()
+    run(0, 1)
+    e[1].record()
+    run(1, len(targets))
+    e[2].record()
+    torch.cuda.synchronize()
+    code = int(stt)
+    if code < 0:
+        raise RuntimeError(f"device status {code}: {L.arbor_strerror(code)}")
+    t = stats.cpu().numpy()
+    first_ms = e[0].elapsed_time(e[1])
+    rest_ms = e[1].elapsed_time(e[2])
+    row_bytes = kv.layers * kv.kv_heads * kv.head_dim * 2 * 2
+    restored = int(t[1:, 1].sum())
+    res = {
+        "workload": config_label(cfg, kv) + f"; {len(targets)}-event walk, backtrack "
+                    f"{cfg.walk_backtrack:.0%}, pressure margin {margin} tokens",
+        "events": len(targets), "first_event_ms": first_ms,
+        "first_event_evicted_tokens": int(t[0, 2]),
+        "ms_per_transition": rest_ms / max(1, len(targets) - 1),
+        "transitions_per_s": (len(targets) - 1) / (rest_ms * 1e-3),
+        "tokens_restored": restored, "bytes_restored": restored * row_bytes,
+        "restore_gbs": restored * row_bytes / (rest_ms * 1e-3) / 1e9,
+        "tokens_evicted": int(t[1:, 2].sum()), "pressure_events": int(t[:, 3].sum()),
+        "resident_tokens_after": int(t[-1, 0]), "budget": st["budget"], "status": code,
+        "note": ("token-span record in device memory (2 x 82.7 GB exceeds the pinnable host "
+                 "memory): restore_gbs is HBM to HBM; the host-link rate is the pinned-host "
+                 "rehydrate leg of llama8b and dpts"),
+    }
+    del kv, st, q, A, sel
+    return res
 
 
 def main():
@@ -421,161 +759,35 @@ def main():
         sys.exit(2)
     cfg = synth.CONFIGS[args.config]
     torch.cuda.init()
-    st = synth.build_config(cfg, device="cuda")
-    kv = L.kv_state_from(st, "cuda")
-    pristine = kv.clone()
-    ev = Event(kv, st, cfg)
-    active = st["active"].cuda()
-    flush = torch.ones(128 << 20, dtype=torch.int32, device="cuda")  # 512 MiB
-
-    def restore():
-        kv.copy_from(pristine)
-        ev.reset_scores()
-        flush.sum()  # reads only: leaves the last-level cache clean
-    stages = ["score", "allocate", "select", "compact", "decode"]
-    # events around the rated kernels' own launches, recorded by the library
-    # during the breakdown pass only (one timing request per call)
-    kevents = {}
-    for name in STAGE_KERNEL:
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        e1.record()
-        kevents[name] = (e0, e1)
-    ktiming = {name: L.timing(STAGE_KERNEL[name][0], *kevents[name]) for name in STAGE_KERNEL}
-
-    # warmup
-    for _ in range(args.warmup):
-        restore()
-        ev.run(active)
-    torch.cuda.synchronize()
-    if int(ev.status) < 0:
-        raise RuntimeError(f"device status {int(ev.status)}: {L.arbor_strerror(int(ev.status))}")
-
-    # the step captured once as a HIP graph: its 15 launches replay without
-    # per-launch host work (the library enqueues kernels only: no host
-    # synchronisation, allocation or memset inside an entry point)
-    graph = None
-    if not args.no_graph:
-        restore()
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            ev.run(active)
-        torch.cuda.synchronize()
-
-    def timed_steps(n, replay):
-        times, wall = [], 0.0
-        for _ in range(n):
-            restore()
-            torch.cuda.synchronize()
-            e_start, e_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            t0 = time.perf_counter()
-            e_start.record()
-            if replay:
-                graph.replay()
-            else:
-                ev.run(active)
-            e_end.record()
-            torch.cuda.synchronize()
-            wall += time.perf_counter() - t0
-            times.append(e_start.elapsed_time(e_end))
-        return times, wall
-
-    # timed steps: one event pair around each whole step, nothing recorded inside
-    if graph is not None:
-        timed_steps(args.warmup, True)
-        if int(ev.status) < 0:
-            raise RuntimeError(f"device status {int(ev.status)}: {L.arbor_strerror(int(ev.status))}")
-    step_ms, wall = timed_steps(args.steps, graph is not None)
-    eager_ms = None
-    if graph is not None:
-        status = int(ev.status)
-        if status < 0:
-            raise RuntimeError(f"device status {status}: {L.arbor_strerror(status)}")
-        eager_ms = float(np.mean(timed_steps(args.steps, False)[0]))
-    status = int(ev.status)
-    if status < 0:
-        raise RuntimeError(f"device status {status}: {L.arbor_strerror(status)}")
-    # breakdown pass (as many steps again): events between the entry points and
-    # around the rated kernels' launches.  Kept apart from the timed steps
-    # because every recorded event also costs the stream a little time.
-    per_stage = {s: [] for s in stages}
-    per_kernel = {s: [] for s in STAGE_KERNEL}
-    for _ in range(args.steps):
-        restore()
-        torch.cuda.synchronize()
-        marks = []
-        ev.run(active, marks, ktiming)
-        torch.cuda.synchronize()
-        for si, s in enumerate(stages):
-            per_stage[s].append(marks[si].elapsed_time(marks[si + 1]))
-        for s, (e0, e1) in kevents.items():
-            per_kernel[s].append(e0.elapsed_time(e1))
-    status = int(ev.status)
-    if status < 0:
-        raise RuntimeError(f"device status {status}: {L.arbor_strerror(status)}")
-    ms = float(np.mean(step_ms))
-    N_event = int(pristine.n_kept.sum())
-    value = N_event / (ms * 1e-3)
-
-    # algorithmic work of this instance (from the last step's outputs)
-    k_after = ev.k.cpu().tolist()
-    st["_sel_cpu"] = ev.sel.cpu().numpy()
-    work = algorithmic_work(st, kv, k_after, pristine.n_kept.cpu().tolist(), st["active"].tolist())
-    mean = {s: float(np.mean(v)) for s, v in per_stage.items()}
-    kmean = {s: float(np.mean(v)) for s, v in per_kernel.items()}
-    # each rated kernel: the stage's algorithmic work over that kernel's own launch time
-    rates = {
-        "score": {"bound": "mfma", "achieved": work["score_flops"] / (kmean["score"] * 1e-3) / 1e12,
-                  "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"},
-        "compact": {"bound": "hbm",
-                    "achieved": work["compact_bytes"] / (kmean["compact"] * 1e-3) / 1e9,
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s"},
-        "decode": {"bound": "hbm", "achieved": work["decode_bytes"] / (kmean["decode"] * 1e-3) / 1e9,
-                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
-        "select": {"bound": "hbm", "achieved": work["select_bytes"] / (kmean["select"] * 1e-3) / 1e9,
-                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
-    }
-    entry = {"score": "arbor_score", "compact": "arbor_compact",
-             "decode": "arbor_tree_decode_attn", "select": "arbor_select"}
-    for st_name, r in rates.items():
-        _, kname, ksrc = STAGE_KERNEL[st_name]
-        r["frac"] = r["achieved"] / r["peak"]
-        r["kernel"] = kname
-        r["entry_point"] = entry[st_name]
-        r["ms_per_launch"] = kmean[st_name]
-        r["stage_ms"] = mean[st_name]
-        tr = stored_kernel_traffic(cfg.name, kname, ksrc)
-        r["traffic"] = None if tr is None else tr["read_bytes"] + tr["write_bytes"]
-        if tr is not None:
-            r["traffic_kernels"] = tr["kernels"]
-    dominant = max(STAGE_KERNEL, key=lambda s: kmean[s])
-    roof = dict(rates[dominant])
-
+    copy_gbs = copy_rate_gbs()
+    head, env = measure_event(cfg, args.steps, args.warmup, use_graph=not args.no_graph,
+                              copy_gbs=copy_gbs, rehydrate_leg=not args.no_rehydrate_leg)
+    rates = head["rates"]
+    dominant = max(STAGE_KERNEL, key=lambda x: rates[x]["ms_per_launch"])
     result = {
-        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": (f"{cfg.name}: {cfg.layers} layers, {cfg.kv_heads} KV heads, "
-                                f"{cfg.q_heads} q heads, head_dim {cfg.head_dim}, {cfg.dtype}; "
-                                f"root {cfg.root_tokens}, branching {cfg.branching}, depth "
-                                f"{cfg.depth}, {cfg.node_tokens} tokens/node "
-                                f"({kv.num_nodes} nodes, {kv.num_tokens} tokens); "
-                                f"{cfg.n_active} active leaves; budget {cfg.rho:.0%}; window "
-                                f"{cfg.window}"),
-                   "tokens_per_step": N_event, "parallelism": "single GPU"},
-        "roofline": roof,
-        "stages_ms": mean,
-        "rates": rates,
-        "decode_hbm_gbs": rates["decode"]["achieved"],
-        "decode_hbm_frac": rates["decode"]["frac"],
-        "decode_union_vs_naive_bytes": [work["decode_bytes"], work["decode_naive_bytes"]],
-        "compact_moved_rows": work["moved_rows"],
-        "wall_ms_per_step": wall / args.steps * 1e3,
-        "launch": "hip graph replay of the captured step" if graph is not None else "eager",
-        "eager_ms_per_step": eager_ms,
-        "status": status,
+        "metric": METRIC, "value": head["value"], "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": head["workload"], "tokens_per_step": head["tokens_per_step"],
+                   "parallelism": "single GPU"},
+        "roofline": dict(rates[dominant]),
+        "metric1": {"what": "resident KV tokens scored + evicted + compacted per second "
+                            "(score, allocate, select, compact; no decode)",
+                    "value": head["event_tokens_per_s"], "unit": "tokens/s",
+                    "ms": head["event_ms"]},
+        "copy_gbs": copy_gbs,
     }
+    for key in ("stages_ms", "rates", "entry_rates", "decode_union_vs_naive_bytes",
+                "compact_moved_rows", "wall_ms_per_step", "launch", "eager_ms_per_step",
+                "status", "rehydrate"):
+        if key in head:
+            result[key] = head[key]
+    result["decode_hbm_gbs"] = rates["decode"]["achieved"]
+    result["decode_hbm_frac"] = rates["decode"]["frac"]
+    st, kv, ev, active, flush, restore = (env[x] for x in ("st", "kv", "ev", "active", "flush",
+                                                          "restore"))
+    work = env["work"]
 
     # decode that also credits its slice-layer attention weights to A, on the
     # state the step leaves behind, beside the plain decode timed the same way
@@ -619,37 +831,6 @@ def main():
             "note": "arbor_tree_decode_attn_scored (decode + decode-time credit of A); "
                     "not part of value"}
 
-    # backtracking transition with lazy rehydration from pinned host memory
-    if not args.no_rehydrate_leg:
-        restore()
-        ev.run(active)
-        parent = st["parent"].tolist()
-        leaves = [i for i in range(kv.num_nodes) if i not in parent]
-        a0 = set(st["active"].tolist())
-        alt = [l for l in leaves if l not in a0]
-        a1 = torch.tensor([alt[(j * len(alt)) // len(a0) + 3] for j in range(len(a0))],
-                          dtype=torch.int32, device="cuda")
-        torch.cuda.synchronize()
-        n_kept_before = kv.n_kept.cpu().numpy()
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        e[0].record()
-        ev.check(L.arbor_allocate(kv, a1, st["budget"], ev.s, ev.params, ev.k, ev.delta,
-                                  ev.on_path, ev.status, ev.ws))
-        e[1].record()
-        ev.check(L.arbor_rehydrate(kv, ev.on_path, st["host_k"], st["host_v"], ev.status, ev.ws))
-        e[2].record()
-        torch.cuda.synchronize()
-        onp = ev.on_path.cpu().numpy().astype(bool)
-        nf = st["n_full"].numpy()
-        restored = int(np.sum((nf - n_kept_before)[onp]))
-        row_bytes = kv.layers * kv.kv_heads * kv.head_dim * 2 * 2
-        t_re = e[1].elapsed_time(e[2])
-        result["rehydrate"] = {"ms": t_re, "tokens_from_host": restored,
-                               "host_link_gbs": restored * row_bytes / (t_re * 1e-3) / 1e9,
-                               "nodes": int(np.sum(onp & (n_kept_before < nf))),
-                               "status": int(ev.status),
-                               "note": "pinned host -> HBM, PCIe-inclusive; not part of value"}
-
     # Eq. 1 uncertainty at the block boundaries: one logit row per block
     if not args.no_uncertainty_leg:
         vocab = 128256
@@ -671,8 +852,6 @@ def main():
                 if rep >= args.warmup:
                     ts.append(e0.elapsed_time(e1))
             t = float(np.mean(ts))
-            # algorithmic bytes: the logits once (the top-K variant reads them
-            # five times: stats, three radix passes, sums)
             nbytes = z.numel() * 2
             gbs = nbytes / (t * 1e-3) / 1e9
             leg["full" if top_k == 0 else f"top{top_k}"] = {
@@ -683,13 +862,32 @@ def main():
         result["uncertainty"] = leg
 
     if not args.no_cpu_baseline:
-        cpu_state = {k: (v.cpu() if isinstance(v, torch.Tensor) else v) for k, v in st.items()
-                     if k not in ("host_k", "host_v")}
+        pristine = env["pristine"]
+        cpu_state = {k_: (v_.cpu() if isinstance(v_, torch.Tensor) else v_) for k_, v_ in st.items()
+                     if k_ not in ("host_k", "host_v")}
         cpu_state.update(k=pristine.k.cpu(), v=pristine.v.cpu(), n_kept=pristine.n_kept.cpu(),
                          page_table=pristine.page_table.cpu(), slot_pos=pristine.slot_pos.cpu(),
                          free_stack=pristine.free_stack.cpu(), free_top=pristine.free_top.cpu())
         result["cpu_baseline"] = cpu_baseline(st, cpu_state, (st["active"].tolist(), st["budget"],
                                                                 st["params"]), work)
+    del env, st, kv, ev, active, flush, restore
+    torch.cuda.empty_cache()
+
+    # the other configurations: extra keys, never part of value
+    legs = {}
+    names = [] if args.no_legs else [x for x in args.legs.split(",") if x]
+    for name in names:
+        if name == "deep":
+            legs[name] = walk_leg()
+        else:
+            leg, env = measure_event(synth.CONFIGS[name], min(args.steps, 5),
+                                     min(args.warmup, 2), use_graph=not args.no_graph,
+                                     copy_gbs=copy_gbs, rehydrate_leg=(name == "dpts"))
+            legs[name] = leg
+            del env
+        torch.cuda.empty_cache()
+    if legs:
+        result["legs"] = legs
     if args.copy_calibration_mib > 0:
         n = args.copy_calibration_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")
