@@ -71,6 +71,14 @@ struct CreditArgs {
   int64_t *rows_seen;
 };
 
+// Plan of one call, in one workgroup: each active leaf's chain (root first),
+// the leaves below every node (in leaf order), the work units (chunks of the
+// chain nodes' slots, per class of row count), each unit's partial rows and
+// each leaf's list of partials, root first.  The per-node and per-leaf state
+// sits in LDS for trees of up to kPlanLds nodes and up to kPlanLeaves leaves,
+// so the chain walks, ranks and scans wait on global memory only for the
+// tree's arrays.
+constexpr int kPlanLeaves = 64;
 __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, int32_t *cls_items,
                                                     int32_t *item_node, int32_t *item_chunk,
                                                     int32_t *item_rowbase, int32_t *node_nl,
@@ -81,9 +89,9 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
                                                     int32_t *leaf_part) {
   __shared__ int64_t sm[6 * 16];
   __shared__ int s_err;
-  // parent links and leaf counts in LDS for trees of up to kPlanLds nodes, so
-  // the chain walks and the counting do not wait on global memory
-  __shared__ int32_t s_par[kPlanLds], s_nl[kPlanLds];
+  __shared__ int32_t s_par[kPlanLds], s_nl[kPlanLds], s_kept[kPlanLds], s_loff[kPlanLds],
+      s_rbase[kPlanLds], s_item0[kPlanLds];
+  __shared__ int32_t s_lanc[kPlanLeaves * MAXD], s_lrank[kPlanLeaves * MAXD], s_ldep[kPlanLeaves];
   if (status_failed(a.status)) {
     if (threadIdx.x == 0) meta[0] = meta[1] = meta[2] = 0;
     return;
@@ -91,20 +99,33 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   const Tree &t = a.t;
   const int V = t.V;
   const int G = a.pl.G;
+  const int nt = blockDim.x;
+  const int tid = threadIdx.x;
   const bool small = V <= kPlanLds;
+  const bool few = a.n_leaves <= kPlanLeaves;
   const int32_t *par = small ? s_par : t.parent;
+  const int32_t *kept = small ? s_kept : t.n_kept;
   int32_t *nlp = small ? s_nl : node_nl;
-  if (threadIdx.x == 0) s_err = 0;
-  for (int i = threadIdx.x; i < V; i += blockDim.x) {
+  int32_t *loffp = small ? s_loff : node_leaf_off;
+  int32_t *rbasep = small ? s_rbase : node_rowbase;
+  int32_t *item0p = small ? s_item0 : node_item0;
+  int32_t *lancp = few ? s_lanc : lanc;
+  int32_t *lrankp = few ? s_lrank : lrank;
+  int32_t *ldepp = few ? s_ldep : ldepth;
+  if (tid == 0) s_err = 0;
+  for (int i = tid; i < V; i += nt) {
     nlp[i] = 0;
-    if (small) s_par[i] = t.parent[i];
+    if (small) {
+      s_par[i] = t.parent[i];
+      s_kept[i] = t.n_kept[i];
+    }
   }
   __syncthreads();
-  for (int b = threadIdx.x; b < a.n_leaves; b += blockDim.x) {
+  for (int b = tid; b < a.n_leaves; b += nt) {
     const int l = a.leaves[b];
     if (l < 0 || l >= V) {
       atomicOr(&s_err, 1);
-      ldepth[b] = -1;
+      ldepp[b] = -1;
       continue;
     }
     // validate and measure the chain, then write it root first (two walks up
@@ -122,41 +143,41 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     }
     if (bad) {
       atomicOr(&s_err, bad);
-      ldepth[b] = -1;
+      ldepp[b] = -1;
       continue;
     }
-    ldepth[b] = d - 1;
+    ldepp[b] = d - 1;
     int e = d - 1;
     for (int x = l; x >= 0; x = par[x], --e) {
-      lanc[(int64_t)b * MAXD + e] = x;
+      lancp[(int64_t)b * MAXD + e] = x;
       atomicAdd(&nlp[x], 1);
     }
   }
   __syncthreads();
   if (s_err) {
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       status_error(a.status, (s_err & 1) ? ARBOR_EINVAL : ARBOR_EUNSUPPORTED);
       meta[0] = meta[1] = meta[2] = 0;
     }
     return;
   }
   // rank of each leaf among the leaves below each of its chain nodes
-  for (int e = threadIdx.x; e < a.n_leaves * MAXD; e += blockDim.x) {
+  for (int e = tid; e < a.n_leaves * MAXD; e += nt) {
     const int b = e / MAXD, d = e % MAXD;
-    if (d > ldepth[b]) continue;
-    const int x = lanc[(int64_t)b * MAXD + d];
+    if (d > ldepp[b]) continue;
+    const int x = lancp[(int64_t)b * MAXD + d];
     int r = 0;
     for (int b2 = 0; b2 < b; ++b2)
-      if (ldepth[b2] >= d && lanc[(int64_t)b2 * MAXD + d] == x) ++r;
-    lrank[(int64_t)b * MAXD + d] = r;
+      if (ldepp[b2] >= d && lancp[(int64_t)b2 * MAXD + d] == x) ++r;
+    lrankp[(int64_t)b * MAXD + d] = r;
   }
   // per-node offsets: leaf lists, items, partial rows; and class lists
   int64_t run_leaf = 0, run_item = 0, run_rows = 0, run_cls[3] = {0, 0, 0};
-  for (int base = 0; base < V; base += blockDim.x) {
-    const int i = base + threadIdx.x;
+  for (int base = 0; base < V; base += nt) {
+    const int i = base + tid;
     const int nl = i < V ? nlp[i] : 0;
     if (small && i < V) node_nl[i] = nl;
-    const int c = (i < V && nl > 0) ? t.n_kept[i] : 0;
+    const int c = (i < V && nl > 0) ? kept[i] : 0;
     const int chunks = (c + CHUNK - 1) / CHUNK;
     const int rows = nl * G;
     const int nbr = (rows + 15) / 16;
@@ -165,66 +186,74 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
                            cls == 1 ? chunks : 0, cls == 2 ? chunks : 0};
     int64_t sx[6], stot[6];
     block_exclusive_scan_n<6>(sv, sx, stot, sm);
-    const int64_t el = sx[0], ei = sx[1], er = sx[2], e0 = sx[3], e1 = sx[4], e2 = sx[5];
-    const int64_t tl = stot[0], ti = stot[1], tr = stot[2], tc0 = stot[3], tc1 = stot[4],
-                  tc2 = stot[5];
     if (i < V) {
-      node_leaf_off[i] = (int32_t)(run_leaf + el);
-      node_item0[i] = (int32_t)(run_item + ei);
-      node_rowbase[i] = (int32_t)(run_rows + er);
-      const int64_t ce = cls == 0 ? run_cls[0] + e0 : (cls == 1 ? run_cls[1] + e1 : run_cls[2] + e2);
-      for (int s = 0; s < chunks; ++s) {
-        const int64_t it = run_item + ei + s;
+      const int lo = (int32_t)(run_leaf + sx[0]);
+      const int it0 = (int32_t)(run_item + sx[1]);
+      const int rb = (int32_t)(run_rows + sx[2]);
+      loffp[i] = lo;
+      item0p[i] = it0;
+      rbasep[i] = rb;
+      if (small) {
+        node_leaf_off[i] = lo;
+        node_item0[i] = it0;
+        node_rowbase[i] = rb;
+      }
+      const int64_t ce = cls == 0 ? run_cls[0] + sx[3]
+                                  : (cls == 1 ? run_cls[1] + sx[4] : run_cls[2] + sx[5]);
+      for (int q = 0; q < chunks; ++q) {
+        const int64_t it = it0 + q;
         item_node[it] = i;
-        item_chunk[it] = s;
-        item_rowbase[it] = (int32_t)(run_rows + er + (int64_t)s * rows);
-        cls_items[(int64_t)cls * a.max_items + ce + s] = (int32_t)it;
+        item_chunk[it] = q;
+        item_rowbase[it] = (int32_t)(rb + (int64_t)q * rows);
+        cls_items[(int64_t)cls * a.max_items + ce + q] = (int32_t)it;
       }
     }
-    run_leaf += tl;
-    run_item += ti;
-    run_rows += tr;
-    run_cls[0] += tc0;
-    run_cls[1] += tc1;
-    run_cls[2] += tc2;
+    run_leaf += stot[0];
+    run_item += stot[1];
+    run_rows += stot[2];
+    run_cls[0] += stot[3];
+    run_cls[1] += stot[4];
+    run_cls[2] += stot[5];
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < a.n_leaves * MAXD; e += blockDim.x) {
+  for (int e = tid; e < a.n_leaves * MAXD; e += nt) {
     const int b = e / MAXD, d = e % MAXD;
-    if (d > ldepth[b]) continue;
-    const int x = lanc[(int64_t)b * MAXD + d];
-    leaf_list[node_leaf_off[x] + lrank[(int64_t)b * MAXD + d]] = b;
+    if (d > ldepp[b]) continue;
+    const int x = lancp[(int64_t)b * MAXD + d];
+    leaf_list[loffp[x] + lrankp[(int64_t)b * MAXD + d]] = b;
+    if (few) lanc[(int64_t)b * MAXD + d] = x;
   }
-  __syncthreads();
+  if (few)
+    for (int b = tid; b < a.n_leaves; b += nt) ldepth[b] = s_ldep[b];
   // each leaf's partials, root first, so the merge needs no chain walk: one
   // thread per (leaf, chain depth); the offsets come from a per-leaf scan of
   // the chunk counts along the chain (at most MAXD entries)
-  for (int b0 = 0; b0 < a.n_leaves; b0 += blockDim.x / MAXD) {
-    const int b = b0 + (int)threadIdx.x / MAXD;
-    const int d = (int)threadIdx.x % MAXD;
-    const bool live = b < a.n_leaves && d <= ldepth[b];
+  for (int b0 = 0; b0 < a.n_leaves; b0 += nt / MAXD) {
+    const int b = b0 + tid / MAXD;
+    const int d = tid % MAXD;
+    const bool live = b < a.n_leaves && d <= ldepp[b];
     int x = 0, nch = 0;
     if (live) {
-      x = lanc[(int64_t)b * MAXD + d];
-      nch = (t.n_kept[x] + CHUNK - 1) / CHUNK;
+      x = lancp[(int64_t)b * MAXD + d];
+      nch = (kept[x] + CHUNK - 1) / CHUNK;
     }
     // inclusive scan over the MAXD threads of this leaf (MAXD = kWave)
     const int incl = wave_inclusive_scan<int>(nch);
     const int np = incl - nch;
     if (live) {
-      const int r = lrank[(int64_t)b * MAXD + d] * G;
-      const int it0 = node_item0[x];
+      const int r = lrankp[(int64_t)b * MAXD + d] * G;
+      const int rows = nlp[x] * G;
       if (incl > a.max_parts) {
         atomicOr(&s_err, 4);  // more resident tokens than the workspace was sized for
       } else {
-        for (int s = 0; s < nch; ++s)
-          leaf_part[(int64_t)b * a.max_parts + np + s] = item_rowbase[it0 + s] + r;
+        for (int q = 0; q < nch; ++q)
+          leaf_part[(int64_t)b * a.max_parts + np + q] = rbasep[x] + q * rows + r;
       }
-      if (d == ldepth[b]) leaf_np[b] = min(incl, a.max_parts);
+      if (d == ldepp[b]) leaf_np[b] = min(incl, a.max_parts);
     }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     const int64_t need = run_rows * a.Lr * a.pl.Hkv * (int64_t)(a.pl.D + 2);
     if (run_item > a.max_items || need > a.part_cap || s_err) {
       status_error(a.status, ARBOR_EWORKSPACE);
