@@ -373,10 +373,14 @@ typedef struct {
   int64_t *rows_seen;           /* device, int64 [V], in/out                         */
 } arbor_decode_credit_t;
 
-/* Errors: those of arbor_tree_decode_attn; EINVAL for a slice layer outside
+/* The attention units keep the logits of the slice layers (fp32, CHUNK = 256
+ * per unit row and kv head) in the workspace, and a second kernel turns them
+ * into the credited weights once the merge has each row's log-sum-exp: the
+ * workspace must be sized with arbor_sizes_t.n_slice >= n_slice.
+ * Errors: those of arbor_tree_decode_attn; EINVAL for a slice layer outside
  * [layer_begin, layer_end), n_slice outside 1..8, self_window not 0 or 1, or A /
- * rows_seen NULL with n_leaves > 0.  Needs the same workspace as
- * arbor_tree_decode_attn. */
+ * rows_seen NULL with n_leaves > 0; EWORKSPACE (device) when the workspace
+ * cannot hold the kept logits. */
 int arbor_tree_decode_attn_scored(const arbor_geom_t *geom, const arbor_tree_t *tree,
                                   const arbor_pool_t *pool, const int32_t *leaves,
                                   int32_t n_leaves, int32_t layer_begin, int32_t layer_end,

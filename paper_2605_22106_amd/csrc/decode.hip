@@ -58,6 +58,8 @@ struct DecArgs {
   float *part;
   int64_t part_cap;
   float *lse2;                // [n_leaves][Lr][Hq] log2-domain LSE (credit calls only)
+  int zS;                     // credit calls: slice layers whose logits the units keep
+  int zlr[8];                 //   (relative to l0); zS = 0 otherwise
   int32_t *status;
 };
 
@@ -66,6 +68,7 @@ struct DecArgs {
 struct CreditArgs {
   int S;
   int slice[8];
+  int zslot[8];   // kept-logit slot of slice e: the first entry with the same layer
   int self_window;
   float *A;
   int64_t *rows_seen;
@@ -254,8 +257,11 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   }
   __syncthreads();
   if (tid == 0) {
-    const int64_t need = run_rows * a.Lr * a.pl.Hkv * (int64_t)(a.pl.D + 2);
-    if (run_item > a.max_items || need > a.part_cap || s_err) {
+    // the partials, then (credit calls) the slice-layer logits of every unit
+    // row and slot: [slice][kv head][row][CHUNK]
+    const int64_t need_p = (run_rows * a.Lr * a.pl.Hkv * (int64_t)(a.pl.D + 2) + 3) & ~(int64_t)3;
+    const int64_t need = need_p + (int64_t)a.zS * a.pl.Hkv * run_rows * CHUNK;
+    if (run_item > a.max_items || need > a.part_cap || need_p > INT32_MAX || s_err) {
       status_error(a.status, ARBOR_EWORKSPACE);
       meta[0] = meta[1] = meta[2] = 0;
       return;
@@ -264,6 +270,7 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
     meta[1] = (int32_t)run_cls[1];
     meta[2] = (int32_t)run_cls[2];
     meta[3] = (int32_t)run_rows;
+    meta[4] = (int32_t)need_p;
   }
 }
 
@@ -322,11 +329,15 @@ __device__ __forceinline__ KVFrag<T, D, GSP> fetch_kv(const UnitAddr &ua, int pg
 // sub-page's resident count may hold anything: only a ragged sub-page (the
 // last of a node) masks its logits and zeroes its value rows.  The output is
 // rescaled only when some row's running max moved.
+// zrow (NULL: none) keeps the fragment's masked logits in log2 units, the
+// weights the decode-time credit normalises later: zrow + r * CHUNK + 16 sub
+// + key for query row r < zrows of the unit, sub-page sub0 + sp.
 template <class T, int D, int NB, int GSP>
 __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
                                        const typename Op<T>::reg (&q)[NB][KVFrag<T, D, GSP>::KS],
                                        float sl2, int g4, float (&m_run)[NB], float (&l_run)[NB],
-                                       f32x4 (&o)[NB][D / 16]) {
+                                       f32x4 (&o)[NB][D / 16], float *zrow = nullptr,
+                                       int zrows = 0, int sub0 = 0, int rbase = 0) {
   typedef KVFrag<T, D, GSP> F;
   constexpr int NC = F::NC;
   float sv[GSP][NB][4];
@@ -359,6 +370,19 @@ __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
     for (int nb = 0; nb < NB; ++nb)
       gmax[nb] = fmaxf(gmax[nb], fmaxf(fmaxf(sv[sp][nb][0], sv[sp][nb][1]),
                                        fmaxf(sv[sp][nb][2], sv[sp][nb][3])));
+    if (zrow && f.nval[sp] > 0) {
+      // lane (rr, g4) holds keys 4 g4 .. 4 g4 + 3 of the sub-page for row rr
+      const int rr = lane_id() & 15;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int r = rbase + nb * 16 + rr;
+        if (r < zrows) {
+          const float4 z4 = make_float4(sv[sp][nb][0], sv[sp][nb][1], sv[sp][nb][2],
+                                        sv[sp][nb][3]);
+          *reinterpret_cast<float4 *>(zrow + (int64_t)r * CHUNK + 16 * (sub0 + sp) + 4 * g4) = z4;
+        }
+      }
+    }
   }
   bool moved = false;
   float alpha[NB];
@@ -509,6 +533,14 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
     ua.koff = (uint32_t)(rr * D * esz + frag_col<T>(0, g4) * esz);
     ua.voff = (uint32_t)(4 * g4 * D * esz + F::NC * rr * esz);
   }
+  // a credited slice layer keeps its logits: [slice][kv head][unit row][slot]
+  float *zrow = nullptr;
+  for (int z = 0; z < a.zS; ++z)
+    if (a.zlr[z] == lr) {
+      zrow = a.part + a.meta[4] +
+             (((int64_t)z * pl.Hkv + g) * a.meta[3] + a.item_rowbase[item]) * CHUNK;
+      break;
+    }
   F cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, 0, pl.P);
   float m_run[NB], l_run[NB];
   f32x4 o[NB][NC];
@@ -526,16 +558,17 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
       F nxt = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 1) * GSP, pl.P);
       // keep the prefetch ahead of the work on the current fragment
       __builtin_amdgcn_sched_barrier(0);
-      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
+      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
       if (gi + 1 >= n_grp) break;
       cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 2) * GSP, pl.P);
       __builtin_amdgcn_sched_barrier(0);
-      attend<T, D, NB, GSP>(nxt, q, a.sl2, g4, m_run, l_run, o);
+      attend<T, D, NB, GSP>(nxt, q, a.sl2, g4, m_run, l_run, o, zrow, R, (gi + 1) * GSP,
+                            rbase);
     }
   } else {
     for (int gi = 0; gi < n_grp; ++gi) {
       if (gi > 0) cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
-      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o);
+      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
     }
   }
   // partial rows [m, l, o(0..D-1)] of this unit
@@ -683,25 +716,18 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 }
 
 // Decode-time credit (Sec. 4 Execution (iii)): the softmax weight exp2(z -
-// lse2) of every decode query row on every key of a unit, summed over the
+// lse2) of every decode query row on every key of a unit, from the logits z
+// the attention units kept for the credited slice layers, summed over the
 // rows whose leaf lies strictly below the unit's node (and, in the
-// self-window mode, the leaf's own rows on keys before its newest position),
-// over the slice layers and kv heads, and added to A at the key's token.
-// Workgroups stride over the 16-slot sub-pages of the units; the four waves
-// of a workgroup take the (slice layer, kv head) pairs of a sub-page in turn,
-// so each token's sum has one owner and a fixed order.  S = Q K^T puts query
-// rows along M and keys along N: lane (rr, g4) receives rows 4 g4 + e of key
-// rr, so a key's sum over 16 rows is an in-lane sum of four values and one
-// across-rows reduction.  Workgroup 0 also adds the row counts to rows_seen
-// (integer atomics: order-free).
-//
-// The credit of one sub-page (item, sub) of a unit.  Every return is uniform
-// over the workgroup.
-template <class T, int D>
+// self-window mode, the leaf's own rows on keys before its newest position)
+// and over the slice layers and kv heads, and added to A at the key's token.
+// One workgroup per 16-slot sub-page of a unit: thread (row lane j, key k)
+// sums rows j, j + 16, ... of key k over the (slice layer, kv head) pairs in
+// a fixed order, and the 16 row lanes are added in order, so each token's sum
+// has one owner and a fixed order.  Workgroup 0 also adds the row counts to
+// rows_seen (integer atomics: order-free).
 __device__ __forceinline__ void credit_subpage(const DecArgs &a, const CreditArgs &cr, int item,
-                                               int sub, float (&s_red)[4][16]) {
-  using O = Op<T>;
-  constexpr int KS = D / 4 / O::kPerStep;
+                                               int sub, float (&s_red)[16][16]) {
   const Tree &t = a.t;
   const Pool &pl = a.pl;
   const int G = pl.G;
@@ -713,90 +739,46 @@ __device__ __forceinline__ void credit_subpage(const DecArgs &a, const CreditArg
   const int R = a.node_nl[node] * G;
   const int loff = a.node_leaf_off[node];
   const int nval = min(16, c - s0);
-  const int lane = lane_id();
-  const int rr = lane & 15;
-  const int g4 = lane >> 4;
-  const int wave = threadIdx.x >> 6;
+  const int kk = threadIdx.x & 15;
+  const int rj = threadIdx.x >> 4;
+  const bool key_ok = kk < nval;
   const int page = t.page_table[t.page_off[node] + s0 / pl.P];
-  const int64_t slot = (int64_t)page * pl.P + s0 % pl.P + rr;
-  const bool key_ok = rr < nval;
-  const int pos = key_ok ? pl.slot_pos[slot] : 0;
+  const int pos = key_ok ? pl.slot_pos[(int64_t)page * pl.P + s0 % pl.P + kk] : 0;
   const int64_t tok = t.tok_off[node] + pos;
-  const float a_old = key_ok ? cr.A[tok] : 0.f;   // fetched early, added last
   // own rows (the node is the row's leaf) are credited only on earlier keys
   // in the self-window mode
   const bool own_ok = cr.self_window && key_ok && pos < t.n_full[node] - 1;
-  const int npairs = cr.S * pl.Hkv;
-  // pairs per wave per pass: the K and Q fragments of all of them are loaded
-  // before the first is used, so one memory round trip covers the pass
-  constexpr int PPW = KS >= 16 ? 1 : 16 / KS;
+  const float *z0 = a.part + a.meta[4];
+  const int64_t rows_total = a.meta[3];
+  const int rb = a.item_rowbase[item];
   float sum = 0.f;
-  for (int rb = 0; rb < R; rb += 16) {
-    // the query row this lane supplies, and the four output rows it receives
-    const int qr = rb + rr;
-    const int qb = qr < R ? a.leaf_list[loff + qr / G] : -1;
-    int ob[4];
-    bool ocr[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = rb + 4 * g4 + e;
-      ob[e] = row < R ? a.leaf_list[loff + row / G] : -1;
-      ocr[e] = ob[e] >= 0 && key_ok && (a.leaves[ob[e]] != node || own_ok);
-    }
-    for (int p0 = wave * PPW; p0 < npairs; p0 += 4 * PPW) {
-      typename O::reg kf[PPW][KS], qf[PPW][KS];
-      float l2[PPW][4];
-#pragma unroll
-      for (int j = 0; j < PPW; ++j) {
-        const int pr = min(p0 + j, npairs - 1);   // clamped: every load stays in bounds
-        const int lr = cr.slice[pr / pl.Hkv];
-        const int g = pr % pl.Hkv;
-        const T *kp = static_cast<const T *>(pl.k) +
-                      (((int64_t)(a.l0 + lr) * pl.num_pages + page) * pl.Hkv + g) * pl.P * D +
-                      (int64_t)(s0 % pl.P + rr) * D;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kf[j][ks] = O::load(kp + frag_col<T>(ks, g4));
-        if (qb >= 0) {
-          const T *qp = static_cast<const T *>(a.q) +
-                        (((int64_t)qb * a.Lr + lr) * Hq + g * G + qr % G) * D;
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) qf[j][ks] = O::load(qp + frag_col<T>(ks, g4));
-        } else {
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) qf[j][ks] = O::zero();
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int row = rb + 4 * g4 + e;
-          l2[j][e] = ocr[e] ? a.lse2[((int64_t)ob[e] * a.Lr + lr) * Hq + g * G + row % G] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < PPW; ++j) {
-        if (p0 + j >= npairs) break;             // wave-uniform
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) acc = O::mma(qf[j][ks], kf[j][ks], acc);
-        float part = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          part += ocr[e] ? __builtin_amdgcn_exp2f(acc[e] * a.sl2 - l2[j][e]) : 0.f;
-        sum += across_rows(part, [](float x, float y) { return x + y; });
+  for (int r = rj; r < R; r += 16) {
+    const int b = a.leaf_list[loff + r / G];
+    if (!key_ok || (a.leaves[b] == node && !own_ok)) continue;
+    for (int z = 0; z < cr.S; ++z) {
+      const int lr = cr.slice[z];
+      for (int g = 0; g < pl.Hkv; ++g) {
+        const float zv = z0[(((int64_t)cr.zslot[z] * pl.Hkv + g) * rows_total + rb + r) * CHUNK +
+                            (s0 - a.item_chunk[item] * CHUNK) + kk];
+        const float l2 = a.lse2[((int64_t)b * a.Lr + lr) * Hq + g * G + r % G];
+        sum += __builtin_amdgcn_exp2f(zv - l2);
       }
     }
   }
-  if (g4 == 0) s_red[wave][rr] = sum;
+  s_red[rj][kk] = sum;
   __syncthreads();
   if (threadIdx.x < 16 && key_ok) {
-    const float tot = ((s_red[0][rr] + s_red[1][rr]) + s_red[2][rr]) + s_red[3][rr];
-    cr.A[tok] = a_old + tot;
+    float tot = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) tot += s_red[j][kk];
+    cr.A[tok] = cr.A[tok] + tot;
   }
 }
 
 template <class T, int D>
 __global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
   constexpr int SUBS = CHUNK / 16;
-  __shared__ float s_red[4][16];
+  __shared__ float s_red[16][16];
   if (status_failed(a.status)) return;
   const int Hq = a.pl.Hkv * a.pl.G;
   if (blockIdx.x == 0) {
@@ -812,7 +794,7 @@ __global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
   }
   const int n_items = a.meta[0] + a.meta[1] + a.meta[2];
   for (int w = blockIdx.x; w < n_items * SUBS; w += gridDim.x) {
-    credit_subpage<T, D>(a, cr, w / SUBS, w % SUBS, s_red);
+    credit_subpage(a, cr, w / SUBS, w % SUBS, s_red);
     __syncthreads();                        // s_red is reused by the next sub-page
   }
 }
@@ -866,6 +848,8 @@ size_t decode_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   b += nl * (size_t)sz->max_layers * g->num_kv_heads * g->q_per_kv * 4;   // log2 LSE
   b += nl * 4 + nl * decode_max_parts(sz) * 4;
   b += rows * (size_t)sz->max_layers * g->num_kv_heads * (g->head_dim + 2) * 4;
+  // logits of the credited slice layers (scored decode)
+  b += rows * (size_t)(sz->n_slice > 0 ? sz->n_slice : 0) * g->num_kv_heads * CHUNK * 4 + 16;
   return b;
 }
 
@@ -920,10 +904,20 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
     for (int e = 0; e < 8; ++e)
       cr.slice[e] = e < credit->n_slice ? credit->slice_layers[e] - layer_begin : 0;
     cr.self_window = credit->self_window;
+    for (int e = 0; e < 8; ++e) {
+      cr.zslot[e] = e;
+      for (int f = 0; f < e && e < credit->n_slice; ++f)
+        if (cr.slice[f] == cr.slice[e]) {
+          cr.zslot[e] = f;
+          break;
+        }
+    }
     cr.A = credit->A;
     cr.rows_seen = credit->rows_seen;
   }
   a.lse2 = credit ? lse2 : nullptr;
+  a.zS = credit ? cr.S : 0;
+  for (int e = 0; e < 8; ++e) a.zlr[e] = credit && e < cr.S ? cr.slice[e] : -1;
   a.meta = meta;
   a.cls_items = cls_items;
   a.item_node = item_node;

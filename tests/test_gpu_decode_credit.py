@@ -23,7 +23,7 @@ def _scored(st, kv, leaves, l0, l1, q, slice_layers, self_window, A0, r0, out_dt
     A = torch.tensor(A0, device="cuda")
     rows = torch.tensor(r0, device="cuda")
     stt = status()
-    ws = workspace(kv, max_leaves=max(n, 1), max_layers=l1 - l0)
+    ws = workspace(kv, max_leaves=max(n, 1), max_layers=l1 - l0, n_slice=len(slice_layers))
     check_rc(L.arbor_tree_decode_attn_scored(kv, leaves.cuda(), l0, l1, q.cuda().contiguous(),
                                              out, lse, 0.0, slice_layers, self_window, A, rows,
                                              stt, ws))
@@ -114,7 +114,7 @@ def test_scored_decode_rejects_bad_slices():
     out = torch.empty((lt.numel(), 2, Hq, kv.head_dim), device="cuda")
     A = torch.zeros(st["num_tokens"], device="cuda")
     rows = torch.zeros(kv.num_nodes, dtype=torch.int64, device="cuda")
-    ws = workspace(kv, max_leaves=lt.numel(), max_layers=2)
+    ws = workspace(kv, max_leaves=lt.numel(), max_layers=2, n_slice=8)
     q = st["q_dec"][:, 1:3].cuda().contiguous()
     for sl, sw in (([0], 0), ([3], 0), ([], 0), ([1] * 9, 0), ([1], 2)):
         rc = L.arbor_tree_decode_attn_scored(kv, lt.cuda(), 1, 3, q, out, None, 0.0, sl, sw, A,
@@ -137,7 +137,7 @@ def test_incremental_scores_drive_an_eviction():
     r_o = np.zeros(V, np.int64)
     A_g = torch.zeros(N, device="cuda")
     r_g = torch.zeros(V, dtype=torch.int64, device="cuda")
-    ws = workspace(kv, max_leaves=len(leaves), max_layers=2)
+    ws = workspace(kv, max_leaves=len(leaves), max_layers=2, n_slice=1)
     gen = torch.Generator().manual_seed(21)
     for step in range(3):
         q = torch.randn((len(leaves), 2, Hq, kv.head_dim), generator=gen).to(torch.bfloat16)
