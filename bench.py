@@ -194,6 +194,8 @@ def parse():
     ap.add_argument("--legs", default="dpts,llama70b,deep",
                     help="other configurations measured after the headline one")
     ap.add_argument("--no-legs", action="store_true")
+    ap.add_argument("--walk-only", action="store_true",
+                    help="run only the deep-tree walk leg and print its record")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch the timed steps eagerly instead of replaying a captured HIP graph")
     ap.add_argument("--summarize-trace", metavar="DB",
@@ -759,6 +761,9 @@ def main():
         sys.exit(2)
     cfg = synth.CONFIGS[args.config]
     torch.cuda.init()
+    if args.walk_only:
+        print(json.dumps({"deep_walk": walk_leg()}))
+        return
     copy_gbs = copy_rate_gbs()
     head, env = measure_event(cfg, args.steps, args.warmup, use_graph=not args.no_graph,
                               copy_gbs=copy_gbs, rehydrate_leg=not args.no_rehydrate_leg)

@@ -33,6 +33,7 @@ namespace {
 
 constexpr int AT = 1024;
 constexpr int kLdsNodes = 512;    // per-node state in LDS up to this many nodes
+constexpr int kGeoNodes = 10240;  // parent, depth and down links in LDS up to this many
 constexpr int kCandLds = 1536;    // listed prices selected in LDS up to this many
 constexpr int kNodeBytes = 2 * 8 + 8 * 4 + 1;
 constexpr int kSearchWaves = AT / kWave / 2;   // waves per bracket end
@@ -293,10 +294,11 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   }
 
   // listed prices: LDS after the node state when few enough, else workspace
-  uint64_t *const cand_lds =
-      reinterpret_cast<uint64_t *>(dyn + (in_lds ? ((size_t)V * kNodeBytes + 15) / 16 * 16 : 0));
+  const size_t node_lds = in_lds == 1 ? ((size_t)V * kNodeBytes + 15) / 16 * 16
+                                      : (in_lds == 2 ? ((size_t)V * 12 + 15) / 16 * 16 : 0);
+  uint64_t *const cand_lds = reinterpret_cast<uint64_t *>(dyn + node_lds);
   Nodes nd;
-  if (in_lds) {
+  if (in_lds == 1) {
     double *dp = reinterpret_cast<double *>(dyn);
     nd.W = dp;
     nd.w = dp + V;
@@ -322,6 +324,15 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     nd.n_kept = t.n_kept;
     nd.depth = ws.depth;
     nd.down = ws.down;
+    if (in_lds == 2) {
+      // the chain walks of the geometry (and the listing that later reuses
+      // depth / down) run on LDS copies
+      int32_t *ip = reinterpret_cast<int32_t *>(dyn);
+      nd.parent = ip;
+      nd.depth = ip + V;
+      nd.down = ip + 2 * V;
+      for (int i = tid; i < V; i += AT) nd.parent[i] = t.parent[i];
+    }
     nd.F = ws.F;
     nd.cnt = ws.cnt;
     nd.cap = ws.cap;
@@ -387,7 +398,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     const int n = nd.n_full[i];
     const int c = nd.n_kept[i];
     const bool on = nd.path[i] != 0;
-    if (in_lds) on_path[i] = nd.path[i];
+    if (in_lds == 1) on_path[i] = nd.path[i];
     // the most a block can keep: a Path* block is restored to n_i by
     // rehydration (or keeps c_i when evicted tokens stay lost), any other
     // block only ever loses tokens
@@ -786,9 +797,16 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
     p.dexp[i] = exp(-params->lambda_d * (double)i);
     p.texp[i] = exp(-params->lambda_delta * (double)i);
   }
-  const int in_lds = t.V <= kLdsNodes ? 1 : 0;
-  const size_t lds = (in_lds ? ((size_t)t.V * kNodeBytes + 15) / 16 * 16 : 0) +
+  const int in_lds = t.V <= kLdsNodes ? 1 : (t.V <= kGeoNodes ? 2 : 0);
+  const size_t lds = (in_lds == 1 ? ((size_t)t.V * kNodeBytes + 15) / 16 * 16
+                                  : (in_lds == 2 ? ((size_t)t.V * 12 + 15) / 16 * 16 : 0)) +
                      2 * (size_t)kCandLds * sizeof(uint64_t);
+  // more than 64 KiB of dynamic LDS has to be allowed explicitly
+  static_assert(kGeoNodes * 12 + 2 * kCandLds * 8 <= 150 * 1024, "within the LDS of a CU");
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute(reinterpret_cast<const void *>(&allocate_kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return ARBOR_EHIP;
   hipLaunchKernelGGL(allocate_kernel, dim3(1), dim3(AT), lds, stream, t, active, n_active,
                      (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws,
                      in_lds, gate);

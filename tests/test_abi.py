@@ -29,7 +29,8 @@ def test_library_exports_every_symbol():
 
 STRUCTS = {"Geom": "arbor_geom_t", "TreeS": "arbor_tree_t", "PoolS": "arbor_pool_t",
            "Params": "arbor_params_t", "Sizes": "arbor_sizes_t",
-           "DecodeCredit": "arbor_decode_credit_t", "Timing": "arbor_timing_t"}
+           "DecodeCredit": "arbor_decode_credit_t", "Timing": "arbor_timing_t",
+           "Walk": "arbor_walk_t"}
 
 
 def test_struct_layouts(tmp_path):

@@ -89,13 +89,15 @@ def run_allocate_bit_exact(seed, base):
         assert np.array_equal(onp.cpu().numpy(), on_o)
 
 
-@pytest.mark.parametrize("V,max_n,seed", [(300, 400, 0), (300, 400, 1), (1500, 100, 2)])
+@pytest.mark.parametrize("V,max_n,seed", [(300, 400, 0), (300, 400, 1), (1500, 100, 2),
+                                           (10240, 20, 4), (12000, 40, 3)])
 def test_allocate_large_bracketed(V, max_n, seed):
     """Tens of thousands of prices, so the order statistic is bracketed by the
     rounded counts before the prices in the bracket are listed.  Node sizes come
     from a small set and weights are rounded to 1/8, so whole runs of prices tie
     exactly; alpha_max both open and binding.  V = 300 keeps the per-node state
-    in LDS, V = 1500 in the workspace."""
+    in LDS; V = 1500 and V = 10240 (the largest such tree) keep only the tree's
+    geometry there; V = 12000 keeps everything in the workspace."""
     parent, _ = synth.random_tree(V, max_n, seed)
     rng = np.random.default_rng(seed)
     sizes = np.array([max_n // 4, max_n // 2, max_n])
