@@ -102,13 +102,46 @@ __device__ int count_prefix(int F, int c, double W, Pred pred) {
 
 // Largest m in [F, F + cnt] with price(m) <= x (m = F: none), starting from
 // the rounded estimate floor(x W) and correcting it by exact comparisons.
+// The product y = x W carries a relative error of at most 2^-53, and so does
+// each quotient j / W: an integer j with j > y (1 + 2^-50) has a price above
+// x, one with j < y (1 - 2^-50) a price below it.  Only an estimate that close
+// to the boundary needs the divisions.
 __device__ int last_le(double x, int F, int cnt, double W) {
-  double y = __builtin_floor(x * W);
-  y = y < (double)F ? (double)F : (y > (double)(F + cnt) ? (double)(F + cnt) : y);
+  const double yr = x * W;
+  double y = __builtin_floor(yr);
+  // (a NaN estimate, 0 * inf, starts from F)
+  y = !(y >= (double)F) ? (double)F : (y > (double)(F + cnt) ? (double)(F + cnt) : y);
   int m = (int)y;
+  const bool up_ok = m == F + cnt || (double)(m + 1) > yr * (1.0 + 0x1p-50);
+  const bool down_ok = m == F || (double)m < yr * (1.0 - 0x1p-50);
+  if (up_ok && down_ok && yr < __builtin_inf()) return m;
   while (m < F + cnt && price(m + 1, W) <= x) ++m;
   while (m > F && price(m, W) > x) --m;
   return m;
+}
+
+// Largest m in [F, F + cnt] with price(m) < x (m = F: none), as last_le.
+__device__ int last_lt(double x, int F, int cnt, double W) {
+  const double yr = x * W;
+  double y = __builtin_floor(yr);
+  y = !(y >= (double)F) ? (double)F : (y > (double)(F + cnt) ? (double)(F + cnt) : y);
+  int m = (int)y;
+  const bool up_ok = m == F + cnt || (double)(m + 1) > yr * (1.0 + 0x1p-50);
+  const bool down_ok = m == F || (double)m < yr * (1.0 - 0x1p-50);
+  if (up_ok && down_ok && yr < __builtin_inf()) return m;
+  while (m < F + cnt && price(m + 1, W) < x) ++m;
+  while (m > F && !(price(m, W) < x)) --m;
+  return m;
+}
+
+// Eligible prices of a block: those in (F, cap] that are finite and at most
+// amax.  Prices ascend with j, so when the last one qualifies they all do.
+__device__ int eligible(int F, int cap, double W, double amax) {
+  if (cap <= F || !(W > 0.0)) return 0;
+  const double last = price(cap, W);
+  if (last <= amax && last < __builtin_inf()) return cap - F;
+  if (last < __builtin_inf()) return last_le(amax, F, cap - F, W) - F;
+  return count_prefix(F, cap, W, [amax](double x) { return x <= amax && x < __builtin_inf(); });
 }
 
 // Rounded count of prices <= x of one node (exact up to one price at each end).
@@ -133,6 +166,37 @@ __device__ void block_sum3(int64_t (&v)[3], int64_t *sm) {
 
 __device__ __forceinline__ int64_t wave_min_i64(int64_t v) {
   return wave_allreduce(v, [](int64_t a, int64_t b) { return a < b ? a : b; });
+}
+
+// block-wide sums of v[0..NS) and minima of v[NS..N) in one exchange; sm
+// holds 16 N values
+// Threads from `live` on hold the identities, so their waves skip the
+// wave-level reductions; the wave totals are combined by wave 0 alone, which
+// hands the results back through sm.
+template <int NS, int N>
+__device__ void block_reduce_n(int64_t (&v)[N], int64_t *sm, int live) {
+  const int lane = lane_id(), w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  if (w * kWave < live) {
+#pragma unroll
+    for (int q = 0; q < N; ++q) v[q] = q < NS ? wave_sum(v[q]) : wave_min_i64(v[q]);
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int q = 0; q < N; ++q) sm[16 * q + w] = v[q];
+  __syncthreads();
+  if (w == 0) {
+    const bool in = lane < nw;
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+      const int64_t r = q < NS ? wave_sum(in ? sm[16 * q + lane] : (int64_t)0)
+                               : wave_min_i64(in ? sm[16 * q + lane] : INT64_MAX);
+      if (lane == 0) sm[16 * q] = r;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < N; ++q) v[q] = sm[16 * q];
+  __syncthreads();
 }
 
 // block-wide sum of v[0] and minima of v[1], v[2] in one exchange
@@ -160,7 +224,8 @@ __device__ void block_min_sum3(int64_t (&v)[3], int64_t *sm) {
 // (room for n keys) may be LDS or global memory; both are overwritten.
 // Called by the whole block; contains __syncthreads.
 __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t rank,
-                                int64_t *sm) {
+                                int64_t *sm, bool known = false, uint64_t kmin = 0,
+                                uint64_t kmax = 0) {
   __shared__ unsigned hist4[4 * 256];
   __shared__ int64_t s_wtot[4];
   __shared__ int s_chosen;
@@ -168,13 +233,15 @@ __device__ uint64_t select_rank(uint64_t *src, uint64_t *dst, int64_t n, int64_t
   __shared__ unsigned s_ncand;
   __shared__ uint64_t s_key;
   const int tid = threadIdx.x, lane = lane_id();
-  uint64_t cmin = ~0ull, cmax = 0ull;
-  for (int64_t e = tid; e < n; e += blockDim.x) {
-    const uint64_t key = src[e];
-    cmin = key < cmin ? key : cmin;
-    cmax = key > cmax ? key : cmax;
-  }
-  {
+  uint64_t cmin = kmin, cmax = kmax;
+  if (!known) {
+    cmin = ~0ull;
+    cmax = 0ull;
+    for (int64_t e = tid; e < n; e += blockDim.x) {
+      const uint64_t key = src[e];
+      cmin = key < cmin ? key : cmin;
+      cmax = key > cmax ? key : cmax;
+    }
     // both extremes in one exchange (keys of finite positive doubles < 2^63)
     int64_t v3[3] = {0, cmin == ~0ull ? INT64_MAX : (int64_t)cmin, INT64_MAX - (int64_t)cmax};
     block_min_sum3(v3, sm);
@@ -262,33 +329,58 @@ __device__ __forceinline__ uint64_t split_point(uint64_t lo, uint64_t span, int 
   return lo + (span / (N + 1)) * m + ((span % (N + 1)) * m) / (N + 1);
 }
 
+// MODE 1: all per-node state in LDS; 2: the geometry (parent, depth, down)
+// in LDS, the rest in the workspace; 0: everything in the workspace.  The
+// mode is a template argument so that every access compiles to an LDS or a
+// global instruction rather than a flat one.
+template <int MODE>
 __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__restrict__ active,
                                                       int n_active, int64_t budget,
                                                       const float *__restrict__ s_in, AllocParams p,
                                                       int32_t *__restrict__ k_out,
                                                       int32_t *__restrict__ delta_out,
                                                       uint8_t *__restrict__ on_path,
-                                                      int32_t *status, AllocWs ws, int in_lds,
-                                                      int gate) {
+                                                      int32_t *status, AllocWs ws, int gate) {
+  constexpr int in_lds = MODE;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
-  __shared__ int64_t sm[3 * 16];
+  __shared__ int64_t sm[7 * 16];
   __shared__ int s_err;
   __shared__ unsigned long long hist64[256];
   __shared__ double s_cnt[2][2 * kSearchPts];
   __shared__ uint64_t s_x[2][2 * kSearchPts];
-  if (status_failed(status)) return;
+  __shared__ double s_dexp[kDecay], s_texp[kDecay];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = lane_id();
   const int V = t.V;
+  // each thread's first node, its score and the decay tables: loads issued
+  // together, ahead of the status check, so they cost one round trip
+  int par0 = 0, nf0 = 0, nk0 = 0;
+  float s0 = 0.f;
+  if (tid < V) {
+    par0 = t.parent[tid];
+    nf0 = t.n_full[tid];
+    nk0 = t.n_kept[tid];
+    s0 = s_in[tid];
+  }
+  double dx = 0.0, tx = 0.0;
+  if (tid < kDecay) {
+    dx = p.dexp[tid];
+    tx = p.texp[tid];
+  }
+  if (status_failed(status)) return;
+  if (tid < kDecay) {
+    s_dexp[tid] = dx;
+    s_texp[tid] = tx;
+  }
   if (tid == 0) s_err = 0;
   if (gate) {
     // a Pressure event (Alg. 2): it fires only when the resident tokens
     // reach the budget it is given; otherwise every count stays as it is
     int64_t m = 0;
-    for (int i = tid; i < V; i += AT) m += t.n_kept[i];
+    for (int i = tid; i < V; i += AT) m += i == tid ? nk0 : t.n_kept[i];
     m = block_sum<int64_t>(m, sm);
     if (m < budget) {
-      for (int i = tid; i < V; i += AT) k_out[i] = t.n_kept[i];
+      for (int i = tid; i < V; i += AT) k_out[i] = i == tid ? nk0 : t.n_kept[i];
       return;
     }
   }
@@ -297,6 +389,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   const size_t node_lds = in_lds == 1 ? ((size_t)V * kNodeBytes + 15) / 16 * 16
                                       : (in_lds == 2 ? ((size_t)V * 12 + 15) / 16 * 16 : 0);
   uint64_t *const cand_lds = reinterpret_cast<uint64_t *>(dyn + node_lds);
+  // per-wave counts of the search (in LDS mode only)
+  double *const s_part = reinterpret_cast<double *>(cand_lds + 2 * kCandLds);
   Nodes nd;
   if (in_lds == 1) {
     double *dp = reinterpret_cast<double *>(dyn);
@@ -314,9 +408,9 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     nd.path = reinterpret_cast<uint8_t *>(ip + 8 * V);
 
     for (int i = tid; i < V; i += AT) {
-      nd.parent[i] = t.parent[i];
-      nd.n_full[i] = t.n_full[i];
-      nd.n_kept[i] = t.n_kept[i];
+      nd.parent[i] = i == tid ? par0 : t.parent[i];
+      nd.n_full[i] = i == tid ? nf0 : t.n_full[i];
+      nd.n_kept[i] = i == tid ? nk0 : t.n_kept[i];
     }
   } else {
     nd.parent = const_cast<int32_t *>(t.parent);
@@ -331,7 +425,7 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       nd.parent = ip;
       nd.depth = ip + V;
       nd.down = ip + 2 * V;
-      for (int i = tid; i < V; i += AT) nd.parent[i] = t.parent[i];
+      for (int i = tid; i < V; i += AT) nd.parent[i] = i == tid ? par0 : t.parent[i];
     }
     nd.F = ws.F;
     nd.cnt = ws.cnt;
@@ -344,9 +438,9 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
 
   // ---- geometry: validation, depth d_i, Path*, Delta_i (Sec. 3) ----------
   for (int i = tid; i < V; i += AT) {
-    const int par = nd.parent[i];
-    const int n = nd.n_full[i];
-    const int c = nd.n_kept[i];
+    const int par = i == tid ? par0 : nd.parent[i];
+    const int n = i == tid ? nf0 : nd.n_full[i];
+    const int c = i == tid ? nk0 : nd.n_kept[i];
     bool ok = (i == 0) ? (par == -1) : (par >= 0 && par < i);
     ok = ok && n >= 0 && c >= 0 && c <= n;
     int d = 0;
@@ -386,7 +480,11 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   }
   // Delta_i = min over ancestors a (incl. i) of (d_i - d_a) + (distance from a
   // down to its nearest active leaf)
-  int64_t path_tok = 0, sum_F = 0, sum_red = 0;
+  // The eligible prices of each block (finite, at most alpha_max) and their
+  // key range are counted here too, so one exchange gives every total.
+  const double amax = p.alpha_max;
+  int64_t path_tok = 0, sum_F = 0, sum_red = 0, total = 0, n_elig = 0;
+  uint64_t kmin = ~0ull, kmax = 0ull;
   for (int i = tid; i < V; i += AT) {
     int best = 0x7fffffff;
     const int di = nd.depth[i];
@@ -395,8 +493,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       if (dn != 0x7fffffff) best = min(best, di - nd.depth[a] + dn);
     }
     delta_out[i] = best;
-    const int n = nd.n_full[i];
-    const int c = nd.n_kept[i];
+    const int n = i == tid ? nf0 : nd.n_full[i];
+    const int c = i == tid ? nk0 : nd.n_kept[i];
     const bool on = nd.path[i] != 0;
     if (in_lds == 1) on_path[i] = nd.path[i];
     // the most a block can keep: a Path* block is restored to n_i by
@@ -411,10 +509,11 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       nd.F[i] = 0;
       nd.W[i] = 0.0;
       nd.w[i] = 0.0;
+      nd.cnt[i] = 0;
       continue;
     }
     // s_i = clip(sigmoid(.), 0, 1) lies in [0, 1]
-    const float sf = s_in[i];
+    const float sf = i == tid ? s0 : s_in[i];
     if (!(sf == sf)) atomicOr(&s_err, 2);
     else if (!(sf >= 0.f && sf <= 1.f)) atomicOr(&s_err, 4);
     const double s = (double)sf;
@@ -428,23 +527,41 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     // the Eq. 2 weight without alpha, in the same operation order as
     // ((eta^[off path] * s^gamma) * e^{-lambda_d d}) * e^{-lambda_Delta Delta}
     double w = (on ? 1.0 : p.eta) * pow_gamma(s, p.gamma);
-    w = w * (di < kDecay ? p.dexp[di] : exp(-p.lambda_d * (double)di));
-    w = w * (best < kDecay ? p.texp[best] : exp(-p.lambda_delta * (double)best));
+    w = w * (di < kDecay ? s_dexp[di] : exp(-p.lambda_d * (double)di));
+    w = w * (best < kDecay ? s_texp[best] : exp(-p.lambda_delta * (double)best));
     // -0 (s = -0 with an odd gamma) as +0: the Pressure order compares bit
     // patterns, in which -0 would rank above every positive weight
     w = w == 0.0 ? 0.0 : w;
     nd.w[i] = w;
-    nd.W[i] = w * (double)n;
+    const double W = w * (double)n;
+    nd.W[i] = W;
     sum_F += f;
     // Pressure lowers only off-path blocks
     if (!on) sum_red += f - min(p.k_min, c);
+    const int cnt = eligible(f, cap, W, amax);
+    nd.cnt[i] = cnt;
+    total += cnt;
+    if (cnt > 0) {
+      const uint64_t lo = (uint64_t)__double_as_longlong(price(f + 1, W));
+      const uint64_t hi = (uint64_t)__double_as_longlong(price(f + cnt, W));
+      kmin = lo < kmin ? lo : kmin;
+      kmax = hi > kmax ? hi : kmax;
+      ++n_elig;
+    }
   }
   {
-    int64_t v3[3] = {path_tok, sum_F, sum_red};
-    block_sum3(v3, sm);
-    path_tok = v3[0];
-    sum_F = v3[1];
-    sum_red = v3[2];
+    // five sums and two minima in one exchange (finite positive keys are
+    // below 2^63: the maximum is taken as the minimum of INT64_MAX - key)
+    int64_t v[7] = {path_tok, sum_F, sum_red, total, n_elig,
+                    kmin == ~0ull ? INT64_MAX : (int64_t)kmin, INT64_MAX - (int64_t)kmax};
+    block_reduce_n<5>(v, sm, V);
+    path_tok = v[0];
+    sum_F = v[1];
+    sum_red = v[2];
+    total = v[3];
+    n_elig = v[4];
+    kmin = (uint64_t)v[5];
+    kmax = (uint64_t)(INT64_MAX - v[6]);
   }
   if (s_err) {
     if (tid == 0) status_error(status, (s_err & 2) ? ARBOR_ENONFINITE : ARBOR_EINVAL);
@@ -455,43 +572,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
   if (sum_F <= b_off) {
     // ---- budget mode: alpha from the price order statistic ---------------
     const int64_t E = b_off - sum_F;
-    const double amax = p.alpha_max;
-    // eligible prices of each node (finite, at most alpha_max) and their range
-    int64_t total = 0, n_elig = 0;
-    uint64_t kmin = ~0ull, kmax = 0ull;
-    for (int i = tid; i < V; i += AT) {
-      int cnt = 0;
-      if (!(nd.path[i] && p.k_protect == 0)) {
-        const double W = nd.W[i];
-        const int F = nd.F[i];
-        cnt = count_prefix(F, nd.cap[i], W,
-                           [amax](double x) { return x <= amax && x < __builtin_inf(); });
-        if (cnt > 0) {
-          const uint64_t lo = (uint64_t)__double_as_longlong(price(F + 1, W));
-          const uint64_t hi = (uint64_t)__double_as_longlong(price(F + cnt, W));
-          kmin = lo < kmin ? lo : kmin;
-          kmax = hi > kmax ? hi : kmax;
-          ++n_elig;
-        }
-      }
-      nd.cnt[i] = cnt;
-      total += cnt;
-    }
-    total = block_sum<int64_t>(total, sm);
     if (total <= E) {
       for (int i = tid; i < V; i += AT)
         if (!(nd.path[i] && p.k_protect == 0)) k_out[i] = nd.F[i] + nd.cnt[i];
       return;
-    }
-    {
-      // n_elig, kmin and kmax in one exchange (finite positive keys are below
-      // 2^63: the maximum is taken as the minimum of INT64_MAX - key)
-      int64_t v3[3] = {n_elig, kmin == ~0ull ? INT64_MAX : (int64_t)kmin,
-                       INT64_MAX - (int64_t)kmax};
-      block_min_sum3(v3, sm);
-      n_elig = v3[0];
-      kmin = (uint64_t)v3[1];
-      kmax = (uint64_t)(INT64_MAX - v3[2]);
     }
 
     // -- bracket: keys a (few prices <= a) and b (enough prices <= b) --------
@@ -515,7 +599,9 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     // another round
     const double enough = 256.0 + 4.0 * (double)n_elig;
     static_assert(2 * kSearchPts == kWave, "one lane per test point in the narrowing");
-    for (int round = 0; !(a_done && b_done) && cb - ca > enough; ++round) {
+    // (trees held in LDS skip this search: their exact counts below cost
+    // about as much as the rounded ones)
+    for (int round = 0; MODE != 1 && !(a_done && b_done) && cb - ca > enough; ++round) {
       const bool end_b = wave >= kSearchWaves;
       const int q0 = (wave % kSearchWaves) * kPtsPerWave;
       const uint64_t lo = end_b ? b_lo : a_lo;
@@ -592,6 +678,110 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     }
     const uint64_t a = a_lo, b = b_hi;
 
+    if constexpr (MODE == 1) {
+      // -- few nodes: narrow on exact counts --------------------------------
+      // Keys ka < kb with count(<= ka) <= E < count(<= kb), from ka = the
+      // smallest price's key - 1 (-1 when that price is 0: below every
+      // price) and kb = the largest one's.  Each round tests ka, kb and 62
+      // keys between them, one key per lane; the waves split the blocks,
+      // whose exact counts (last_le) are added in wave order.  It stops when
+      // kb - ka = 1 (the answer is kb) or when at most 64 prices lie in
+      // (ka, kb], which are then listed and ranked by one wave.
+      int64_t ka = a_none ? -1 : (int64_t)a, kb = (int64_t)b;
+      int64_t cA = 0, cB = 0;
+      bool counted = false;
+      uint64_t answer = 0;
+      bool found = false;
+      for (int round = 0;; ++round) {
+        if (kb - ka <= 1) {
+          answer = (uint64_t)kb;
+          found = true;
+          break;
+        }
+        if (counted && cB - cA <= kWave) break;
+        const uint64_t span = (uint64_t)(kb - ka);
+        const uint64_t m = (uint64_t)lane;
+        const int64_t x = lane == kWave - 1
+                              ? kb
+                              : ka + (int64_t)((span / (kWave - 1)) * m +
+                                               ((span % (kWave - 1)) * m) / (kWave - 1));
+        double c = 0.0;
+        if (x >= 0) {
+          const double xv = key_value((uint64_t)x);
+#pragma unroll 4
+          for (int i = wave; i < V; i += AT / kWave) {
+            const int cnt = nd.cnt[i];
+            const int F = nd.F[i];
+            const int mm = cnt > 0 ? last_le(xv, F, cnt, nd.W[i]) : F;
+            c += (double)(mm - F);
+          }
+        }
+        s_part[tid] = c;
+        __syncthreads();
+        if (tid < kWave) {
+          double sum = 0.0;
+          for (int w = 0; w < AT / kWave; ++w) sum += s_part[w * kWave + tid];
+          s_cnt[round & 1][tid] = sum;
+          s_x[round & 1][tid] = (uint64_t)x;
+        }
+        __syncthreads();
+        // the keys ascend and their counts with them: the last one with
+        // count <= E is the new ka (lane 0 at least), the first one above E
+        // the new kb (lane 63 at least)
+        const double cq = s_cnt[round & 1][lane];
+        const int64_t xq = (int64_t)s_x[round & 1][lane];
+        const uint64_t le = ballot(cq <= (double)E);
+        const int qa = 63 - __builtin_clzll(le);
+        const int qb = __builtin_ctzll(~le);
+        ka = lane_value(xq, qa);
+        kb = lane_value(xq, qb);
+        cA = (int64_t)lane_value(cq, qa);
+        cB = (int64_t)lane_value(cq, qb);
+        counted = true;
+      }
+      if (!found) {
+        // the cB - cA <= 64 prices in (ka, kb], placed by a block scan and
+        // ranked by one wave
+        uint64_t *const lst = cand_lds;
+        const double av1 = ka >= 0 ? key_value((uint64_t)ka) : 0.0, bv1 = key_value((uint64_t)kb);
+        int m_lo = 0, m_hi = 0;
+        double Wt = 0.0;
+        if (tid < V && nd.cnt[tid] > 0) {
+          const int F = nd.F[tid], cnt = nd.cnt[tid];
+          Wt = nd.W[tid];
+          m_lo = ka >= 0 ? last_le(av1, F, cnt, Wt) : F;
+          m_hi = last_le(bv1, F, cnt, Wt);
+        }
+        int64_t tot;
+        const int64_t off = block_exclusive_scan<int64_t>((int64_t)(m_hi - m_lo), sm, &tot);
+        for (int j = m_lo; j < m_hi; ++j)
+          lst[off + (j - m_lo)] = (uint64_t)__double_as_longlong(price(j + 1, Wt));
+        __syncthreads();
+        if (wave == 0) {
+          const int n = (int)tot;
+          const int64_t r = E - cA;
+          const uint64_t key = lane < n ? lst[lane] : ~0ull;
+          int less = 0, leq = 0;
+          for (int q = 0; q < n; ++q) {
+            const uint64_t kq = lane_value(key, q);
+            less += kq < key ? 1 : 0;
+            leq += kq <= key ? 1 : 0;
+          }
+          if (lane < n && less <= r && r < leq) s_x[0][0] = key;
+        }
+        __syncthreads();
+        answer = s_x[0][0];
+      }
+      const double cut = key_value(answer);
+      for (int i = tid; i < V; i += AT) {
+        if (nd.path[i] && p.k_protect == 0) continue;
+        const int F = nd.F[i];
+        const double W = nd.W[i];
+        k_out[i] = W > 0.0 ? last_lt(cut, F, nd.cap[i] - F, W) : F;
+      }
+      return;
+    }
+
     // -- list the prices in (a, b] and count those <= a exactly -------------
     // per node: first listed j - 1 in depth[], how many in down[], offset in
     // cnt[] (the geometry fields are no longer needed)
@@ -599,54 +789,58 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     int64_t below = 0, run = 0;
     for (int base = 0; base < V; base += AT) {
       const int i = base + tid;
-      int m_lo = 0, m_hi = 0;
+      int m_lo = 0, m_hi = 0, F = 0;
       if (i < V) {
         const int cnt = nd.cnt[i];
         if (cnt > 0) {
-          const int F = nd.F[i];
+          F = nd.F[i];
           const double W = nd.W[i];
           m_lo = a_none ? F : last_le(av, F, cnt, W);
           m_hi = last_le(bv, F, cnt, W);
-          below += m_lo - F;
         }
       }
-      int64_t tot;
-      const int64_t ex = block_exclusive_scan<int64_t>((int64_t)(m_hi - m_lo), sm, &tot);
+      // offsets of the listed prices, and the count of prices <= a
+      const int64_t v2[2] = {(int64_t)(m_hi - m_lo), (int64_t)(m_lo - F)};
+      int64_t ex[2], tot[2];
+      block_exclusive_scan_n<2>(v2, ex, tot, sm, V - base);
       if (i < V) {
         nd.depth[i] = m_lo;
         nd.down[i] = m_hi - m_lo;
-        nd.cnt[i] = (int)(run + ex);
+        nd.cnt[i] = (int)(run + ex[0]);
       }
-      run += tot;
+      run += tot[0];
+      below += tot[1];
     }
-    below = block_sum<int64_t>(below, sm);
     const int64_t total_c = run;
     if (total_c > ws.buf_cap || total_c > 0x7fffffff) {
       if (tid == 0) status_error(status, ARBOR_EWORKSPACE);
       return;
     }
-    const bool c_lds = total_c <= kCandLds;
-    uint64_t *const cand = c_lds ? cand_lds : ws.buf0;
-    uint64_t *const cand2 = c_lds ? cand_lds + kCandLds : ws.buf1;
-    // one wave per node, lanes over its listed prices
-    for (int i = wave; i < V; i += AT / kWave) {
-      const int nl = nd.down[i];
-      if (nl <= 0) continue;
-      const int m_lo = nd.depth[i], o = nd.cnt[i];
-      const double W = nd.W[i];
-      for (int j = lane; j < nl; j += kWave)
-        cand[o + j] = (uint64_t)__double_as_longlong(price(m_lo + 1 + j, W));
-    }
-    __syncthreads();
-
-    // -- the order statistic among the listed prices -------------------------
-    const uint64_t prefix = select_rank(cand, cand2, total_c, E - below, sm);
+    // the listed prices and their order statistic (every listed key lies in
+    // (a, b]); LDS and workspace buffers take separate code paths, so that
+    // each compiles to its own kind of memory instruction
+    auto order_stat = [&](uint64_t *cand, uint64_t *cand2) __attribute__((always_inline)) {
+      // one wave per node, lanes over its listed prices
+      for (int i = wave; i < V; i += AT / kWave) {
+        const int nl = nd.down[i];
+        if (nl <= 0) continue;
+        const int m_lo = nd.depth[i], o = nd.cnt[i];
+        const double W = nd.W[i];
+        for (int j = lane; j < nl; j += kWave)
+          cand[o + j] = (uint64_t)__double_as_longlong(price(m_lo + 1 + j, W));
+      }
+      __syncthreads();
+      return select_rank(cand, cand2, total_c, E - below, sm, true, a_none ? 0 : a + 1, b);
+    };
+    const uint64_t prefix = total_c <= kCandLds ? order_stat(cand_lds, cand_lds + kCandLds)
+                                                : order_stat(ws.buf0, ws.buf1);
     const double cut = key_value(prefix);
     for (int i = tid; i < V; i += AT) {
       if (nd.path[i] && p.k_protect == 0) continue;
-      const int kept = count_prefix(nd.F[i], nd.cap[i], nd.W[i],
-                                    [cut](double x) { return x < cut; });
-      k_out[i] = nd.F[i] + kept;
+      const int F = nd.F[i];
+      const double W = nd.W[i];
+      // the prices below the cut (none when W_i = 0: all infinite)
+      k_out[i] = W > 0.0 ? last_lt(cut, F, nd.cap[i] - F, W) : F;
     }
     return;
   }
@@ -798,18 +992,24 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
     p.texp[i] = exp(-params->lambda_delta * (double)i);
   }
   const int in_lds = t.V <= kLdsNodes ? 1 : (t.V <= kGeoNodes ? 2 : 0);
-  const size_t lds = (in_lds == 1 ? ((size_t)t.V * kNodeBytes + 15) / 16 * 16
+  const void *fn = in_lds == 1 ? reinterpret_cast<const void *>(&allocate_kernel<1>)
+                               : (in_lds == 2 ? reinterpret_cast<const void *>(&allocate_kernel<2>)
+                                              : reinterpret_cast<const void *>(&allocate_kernel<0>));
+  const size_t lds = (in_lds == 1 ? ((size_t)t.V * kNodeBytes + 15) / 16 * 16 + AT * 8
                                   : (in_lds == 2 ? ((size_t)t.V * 12 + 15) / 16 * 16 : 0)) +
                      2 * (size_t)kCandLds * sizeof(uint64_t);
   // more than 64 KiB of dynamic LDS has to be allowed explicitly
   static_assert(kGeoNodes * 12 + 2 * kCandLds * 8 <= 150 * 1024, "within the LDS of a CU");
   if (lds > 64 * 1024 &&
-      hipFuncSetAttribute(reinterpret_cast<const void *>(&allocate_kernel),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return ARBOR_EHIP;
-  hipLaunchKernelGGL(allocate_kernel, dim3(1), dim3(AT), lds, stream, t, active, n_active,
-                     (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws,
-                     in_lds, gate);
+#define ARBOR_ALLOC_LAUNCH(M)                                                                   \
+  hipLaunchKernelGGL(allocate_kernel<M>, dim3(1), dim3(AT), lds, stream, t, active, n_active,    \
+                     (int64_t)budget_tokens, s, p, k_out, delta_out, on_path_out, status, ws, gate)
+  if (in_lds == 1) ARBOR_ALLOC_LAUNCH(1);
+  else if (in_lds == 2) ARBOR_ALLOC_LAUNCH(2);
+  else ARBOR_ALLOC_LAUNCH(0);
+#undef ARBOR_ALLOC_LAUNCH
   return hip_ok(hipGetLastError());
 }
 

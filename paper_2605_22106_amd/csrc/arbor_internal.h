@@ -64,7 +64,9 @@ __device__ __forceinline__ void store16_nt(void *dst, uint4 v) {
 }
 
 __device__ __forceinline__ bool status_failed(const int32_t *st) {
-  return *reinterpret_cast<const volatile int32_t *>(st) < 0;
+  // (the status word is device-accessible global memory: a global load, not
+  // a flat one)
+  return *(const __attribute__((address_space(1))) volatile int32_t *)st < 0;
 }
 __device__ __forceinline__ void status_error(int32_t *st, int32_t code) { atomicMin(st, code); }
 __device__ __forceinline__ void status_warn(int32_t *st, int32_t code) { atomicCAS(st, 0, code); }
@@ -227,17 +229,20 @@ __device__ T block_exclusive_scan(T v, T *smem, T *total) {
 }
 
 // N exclusive scans over the block in one exchange (two barriers in all);
-// smem holds N * 16 values.
+// smem holds N * 16 values.  Threads from `live` on contribute zeros, so
+// their waves skip the wave-level scans.
 template <int N>
 __device__ void block_exclusive_scan_n(const int64_t (&v)[N], int64_t (&ex)[N],
-                                       int64_t (&total)[N], int64_t *smem) {
+                                       int64_t (&total)[N], int64_t *smem,
+                                       int live = 1 << 30) {
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
   const int nw = blockDim.x >> 6;
+  const bool scan = w * kWave < live;
   int64_t inc[N];
 #pragma unroll
   for (int k = 0; k < N; ++k) {
-    inc[k] = wave_inclusive_scan(v[k]);
+    inc[k] = scan ? wave_inclusive_scan(v[k]) : (int64_t)0;
     if (lane == kWave - 1) smem[k * 16 + w] = inc[k];
   }
   __syncthreads();

@@ -80,8 +80,10 @@ struct CreditArgs {
 // each leaf's list of partials, root first.  The per-node and per-leaf state
 // sits in LDS for trees of up to kPlanLds nodes and up to kPlanLeaves leaves,
 // so the chain walks, ranks and scans wait on global memory only for the
-// tree's arrays.
+// tree's arrays.  SMALL / FEW are template arguments, so that every access
+// compiles to an LDS or a global instruction rather than a flat one.
 constexpr int kPlanLeaves = 64;
+template <bool SMALL, bool FEW>
 __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, int32_t *cls_items,
                                                     int32_t *item_node, int32_t *item_chunk,
                                                     int32_t *item_rowbase, int32_t *node_nl,
@@ -104,8 +106,8 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   const int G = a.pl.G;
   const int nt = blockDim.x;
   const int tid = threadIdx.x;
-  const bool small = V <= kPlanLds;
-  const bool few = a.n_leaves <= kPlanLeaves;
+  constexpr bool small = SMALL;
+  constexpr bool few = FEW;
   const int32_t *par = small ? s_par : t.parent;
   const int32_t *kept = small ? s_kept : t.n_kept;
   int32_t *nlp = small ? s_nl : node_nl;
@@ -936,9 +938,16 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   a.max_parts = max_parts;
   a.part = reinterpret_cast<float *>(cv.rest());
   a.part_cap = (int64_t)(cv.remaining() / 4);
-  hipLaunchKernelGGL(decode_plan, dim3(1), dim3(1024), 0, stream, a, meta, cls_items, item_node,
-                     item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list, node_item0,
-                     node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part);
+#define ARBOR_PLAN_LAUNCH(S, F)                                                                \
+  hipLaunchKernelGGL((decode_plan<S, F>), dim3(1), dim3(1024), 0, stream, a, meta, cls_items,     \
+                     item_node, item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list,      \
+                     node_item0, node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part)
+  const bool small = t.V <= kPlanLds, few = n_leaves <= kPlanLeaves;
+  if (small && few) ARBOR_PLAN_LAUNCH(true, true);
+  else if (small) ARBOR_PLAN_LAUNCH(true, false);
+  else if (few) ARBOR_PLAN_LAUNCH(false, true);
+  else ARBOR_PLAN_LAUNCH(false, false);
+#undef ARBOR_PLAN_LAUNCH
   const CreditArgs *crp = credit ? &cr : nullptr;
   if (geom->dtype == ARBOR_BF16) {
     if (geom->head_dim == 128)

@@ -651,6 +651,9 @@ __device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
 // mode) in ascending id, so that the reduction visits only those.
 // fbase / tbase hold the prefixes of the chain lengths and sub-page counts
 // until the totals are known.
+// IN_LDS (trees of up to kSetupLds nodes) is a template argument, so that the
+// tree's arrays are read with LDS or global instructions rather than flat ones.
+template <bool IN_LDS>
 __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_cap,
                                                     int64_t *__restrict__ pbase,
                                                     int64_t *__restrict__ fbase,
@@ -674,7 +677,7 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
   const int tid = threadIdx.x;
   const int nt = blockDim.x;
   if (tid == 0) s_err = 0;
-  const bool in_lds = t.V <= kSetupLds;
+  constexpr bool in_lds = IN_LDS;
   for (int i = tid; i < t.V; i += nt) {
     const int par = t.parent[i];
     const int nf = t.n_full[i];
@@ -1064,8 +1067,12 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.anc = anc;
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
-    hipLaunchKernelGGL(score_setup, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase, fbase,
-                       tbase, nsp, ctxlen, odepth, anc, flag, cred);
+    if (t.V <= kSetupLds)
+      hipLaunchKernelGGL(score_setup<true>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
+                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, cred);
+    else
+      hipLaunchKernelGGL(score_setup<false>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
+                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, cred);
     hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
