@@ -42,19 +42,20 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
   // each wave's node positions, slot order, when the node holds at most
   // kPlanPos resident tokens: the binary searches then run in LDS
   __shared__ int s_pos[4][kPlanPos];
-  if (status_failed(status)) return;
   const int lane = lane_id();
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= t.V) return;
+  // the node's scalars are loaded together with the status word
   const int c = t.n_kept[i];
   const int ki = k[i];
+  const int n = t.n_full[i];
+  const int64_t tb = t.tok_off[i];
+  const int64_t po = t.page_off[i];
+  if (status_failed(status)) return;
   if (ki >= c) {
     if (lane == 0) freed[i] = 0;
     return;
   }
-  const int n = t.n_full[i];
-  const int64_t tb = t.tok_off[i];
-  const int64_t po = t.page_off[i];
   bool bad = ki < 0;
   int *lp = s_pos[threadIdx.x >> 6];
   const bool in_lds = c <= kPlanPos;
@@ -113,7 +114,13 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
                                                      int32_t *__restrict__ push_base,
                                                      int32_t *__restrict__ changed,
                                                      int32_t *__restrict__ meta, int32_t *status) {
-  __shared__ int64_t sm[17];
+  __shared__ int64_t sm[2 * 16];
+  // the first nodes' counts and the free-stack top are loaded together with
+  // the status word
+  const int i0 = threadIdx.x;
+  const bool in0 = i0 < t.V;
+  const int k0 = in0 ? k[i0] : 0, c0 = in0 ? t.n_kept[i0] : 0, f0 = in0 ? freed[i0] : 0;
+  const int top = threadIdx.x == 0 ? *pl.free_top : 0;
   if (status_failed(status)) {
     if (threadIdx.x == 0) meta[0] = 0;
     return;
@@ -122,20 +129,18 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
   for (int base = 0; base < t.V; base += blockDim.x) {
     const int i = base + threadIdx.x;
     const bool in = i < t.V;
-    const bool ch = in && k[i] < t.n_kept[i];
-    const int64_t f = ch ? freed[i] : 0;
-    int64_t tot_p, tot_n;
-    const int64_t exp = block_exclusive_scan<int64_t>(f, sm, &tot_p);
-    const int64_t exn = block_exclusive_scan<int64_t>(ch ? 1 : 0, sm, &tot_n);
+    const bool ch = in && (base == 0 ? k0 < c0 : k[i] < t.n_kept[i]);
+    const int64_t v2[2] = {ch ? (base == 0 ? f0 : freed[i]) : 0, ch ? 1 : 0};
+    int64_t ex[2], tot[2];
+    block_exclusive_scan_n<2>(v2, ex, tot, sm, t.V - base);
     if (ch) {
-      push_base[i] = (int32_t)(run_pages + exp);
-      changed[run_nodes + exn] = i;
+      push_base[i] = (int32_t)(run_pages + ex[0]);
+      changed[run_nodes + ex[1]] = i;
     }
-    run_pages += tot_p;
-    run_nodes += tot_n;
+    run_pages += tot[0];
+    run_nodes += tot[1];
   }
   if (threadIdx.x == 0) {
-    const int top = *pl.free_top;
     if (top < 0 || (int64_t)top + run_pages > pl.num_pages) {
       status_error(status, ARBOR_ECORRUPT);
       meta[0] = 0;
@@ -290,8 +295,10 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   const dim3 node_grid((t.V + 3) / 4);
   hipLaunchKernelGGL(compact_plan, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos, src_slot,
                      mv_src, mv_dst, first_moved, freed, status);
-  hipLaunchKernelGGL(compact_scan, dim3(1), dim3(1024), 0, stream, t, pl, k, freed, push_base,
-                     changed, meta, status);
+  // (a workgroup no wider than the tree needs: the scans cost per wave)
+  const int scan_threads = t.V <= 256 ? 256 : 1024;
+  hipLaunchKernelGGL(compact_scan, dim3(1), dim3(scan_threads), 0, stream, t, pl, k, freed,
+                     push_base, changed, meta, status);
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
   const int fin_blocks = (t.V + 3) / 4;

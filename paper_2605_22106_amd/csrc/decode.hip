@@ -97,15 +97,18 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   __shared__ int32_t s_par[kPlanLds], s_nl[kPlanLds], s_kept[kPlanLds], s_loff[kPlanLds],
       s_rbase[kPlanLds], s_item0[kPlanLds];
   __shared__ int32_t s_lanc[kPlanLeaves * MAXD], s_lrank[kPlanLeaves * MAXD], s_ldep[kPlanLeaves];
-  if (status_failed(a.status)) {
-    if (threadIdx.x == 0) meta[0] = meta[1] = meta[2] = 0;
-    return;
-  }
   const Tree &t = a.t;
   const int V = t.V;
   const int G = a.pl.G;
   const int nt = blockDim.x;
   const int tid = threadIdx.x;
+  // each thread's first node and leaf are loaded together with the status word
+  const int par0 = tid < V ? t.parent[tid] : 0, kept0 = tid < V ? t.n_kept[tid] : 0;
+  const int leaf0 = tid < a.n_leaves ? a.leaves[tid] : 0;
+  if (status_failed(a.status)) {
+    if (threadIdx.x == 0) meta[0] = meta[1] = meta[2] = 0;
+    return;
+  }
   constexpr bool small = SMALL;
   constexpr bool few = FEW;
   const int32_t *par = small ? s_par : t.parent;
@@ -121,13 +124,13 @@ __global__ __launch_bounds__(1024) void decode_plan(DecArgs a, int32_t *meta, in
   for (int i = tid; i < V; i += nt) {
     nlp[i] = 0;
     if (small) {
-      s_par[i] = t.parent[i];
-      s_kept[i] = t.n_kept[i];
+      s_par[i] = i == tid ? par0 : t.parent[i];
+      s_kept[i] = i == tid ? kept0 : t.n_kept[i];
     }
   }
   __syncthreads();
   for (int b = tid; b < a.n_leaves; b += nt) {
-    const int l = a.leaves[b];
+    const int l = b == tid ? leaf0 : a.leaves[b];
     if (l < 0 || l >= V) {
       atomicOr(&s_err, 1);
       ldepp[b] = -1;

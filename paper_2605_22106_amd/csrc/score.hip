@@ -53,6 +53,8 @@ struct ScoreArgs {
   const int32_t *ctxlen;  // [n_obs]
   const int32_t *odepth;  // [n_obs]
   const int32_t *anc;     // [n_obs][MAXD]
+  const int32_t *nctx;    // [V]: context offset of each chain node's first token (setup)
+  const int32_t *ndep;    // [V]: its depth
   int32_t *status;
 };
 
@@ -663,25 +665,32 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
                                                     int32_t *__restrict__ odepth,
                                                     int32_t *__restrict__ anc,
                                                     int32_t *__restrict__ flag,
+                                                    int32_t *__restrict__ nctx,
+                                                    int32_t *__restrict__ ndep,
                                                     int32_t *__restrict__ cred) {
   __shared__ int64_t sm[17];
   __shared__ int s_err;
   // parent links and block sizes in LDS for trees of up to kSetupLds nodes, so
   // the chain walks do not wait on global memory at every step
   __shared__ int32_t s_par[kSetupLds], s_full[kSetupLds], s_kept[kSetupLds];
+  Tree t = a.t;
+  const int tid = threadIdx.x;
+  const int nt = blockDim.x;
+  // each thread's first node and observer, loaded together with the status
+  const bool n0 = tid < t.V;
+  const int par0 = n0 ? t.parent[tid] : 0, nf0 = n0 ? t.n_full[tid] : 0,
+            c0 = n0 ? t.n_kept[tid] : 0;
+  const int obs0 = tid < a.n_obs ? a.obs[tid] : 0;
   if (status_failed(a.status)) {
     if (threadIdx.x == 0) cred[0] = 0;
     return;
   }
-  Tree t = a.t;
-  const int tid = threadIdx.x;
-  const int nt = blockDim.x;
   if (tid == 0) s_err = 0;
   constexpr bool in_lds = IN_LDS;
   for (int i = tid; i < t.V; i += nt) {
-    const int par = t.parent[i];
-    const int nf = t.n_full[i];
-    const int c = t.n_kept[i];
+    const int par = i == tid ? par0 : t.parent[i];
+    const int nf = i == tid ? nf0 : t.n_full[i];
+    const int c = i == tid ? c0 : t.n_kept[i];
     const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
     if (!ok || c < 0 || c > nf) atomicOr(&s_err, 1);
     if (in_lds) {
@@ -703,7 +712,7 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
     const int o = base + tid;
     int64_t len = 0, subs = 0;
     if (o < a.n_obs) {
-      const int j = a.obs[o];
+      const int j = base == 0 ? obs0 : a.obs[o];
       if (j < 0 || j >= t.V) {
         atomicOr(&s_err, 1);
         odepth[o] = -1;
@@ -721,8 +730,17 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
         nsp[2 * o + 1] = r.ok ? (int32_t)(a.self_window ? subs : subs - own) : 0;
         ctxlen[o] = (int32_t)len;
         if (r.ok) {
-          // blocks this observer credits (benign races: every writer stores 1)
-          for (int e = 0; e < r.depth; ++e) flag[ao[e]] = 1;
+          // blocks this observer credits, and the depth and context offset
+          // of each block of its chain (benign races: every writer of an
+          // entry stores the same value)
+          int ctx = 0;
+          for (int e = 0; e <= r.depth; ++e) {
+            const int x = ao[e];
+            if (e < r.depth) flag[x] = 1;
+            nctx[x] = ctx;
+            ndep[x] = e;
+            ctx += t.n_kept[x];
+          }
           if (a.self_window) flag[j] = 1;
         }
       }
@@ -773,12 +791,13 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
 // registers.
 __global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
   __shared__ ChainLds ch;
-  if (status_failed(a.status)) return;   // also set by the setup on any error
   const Tree &t = a.t;
   const int o = blockIdx.x;
   const int tid = threadIdx.x;
+  // (loaded together with the status word)
   const int j = a.obs[o];
   const int depth = a.odepth[o];
+  if (status_failed(a.status)) return;   // also set by the setup on any error
   if (tid == 0) ch.depth = depth;
   if (tid <= depth) {
     const int x = a.anc[(int64_t)o * MAXD + tid];
@@ -820,14 +839,17 @@ __global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
 // Fold the (slice layer, kv head, row group) slabs of every observer: one
 // column sum per (observer, credited context key), summed in slab order.
 __global__ __launch_bounds__(256) void score_fold(ScoreArgs a, const int64_t *__restrict__ fbase) {
-  if (status_failed(a.status)) return;
   const int o = blockIdx.x;
+  // (loaded together with the status word)
   const int len = a.ctxlen[o];
-  const int own_c = a.t.n_kept[a.obs[o]];
+  const int jo = a.obs[o];
+  const int64_t pb = a.pbase[o], fb = fbase[o];
+  if (status_failed(a.status)) return;
+  const int own_c = a.t.n_kept[jo];
   const int credited = a.self_window ? len : len - own_c;
   const int nslab = a.S * a.pl.Hkv * a.n_rg;
-  const float *src = a.part + a.pbase[o];
-  float *dst = a.part + fbase[o];
+  const float *src = a.part + pb;
+  float *dst = a.part + fb;
   for (int x = blockIdx.y * blockDim.x + threadIdx.x; x < credited; x += gridDim.y * blockDim.x) {
     // eight loads in flight, added in slab order
     float acc = 0.f;
@@ -883,20 +905,21 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
   __shared__ int64_t hbase[256];
   __shared__ int s_wcnt[4];
   __shared__ double s_acc[4][64];
+  // (loaded together with the status word; the list entry past its end is
+  // allocated, and unused then)
+  const int ncred = cred[0];
+  const int i = cred[1 + blockIdx.x];
   if (status_failed(a.status)) return;
-  if ((int)blockIdx.x >= cred[0]) return;
+  if ((int)blockIdx.x >= ncred) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
-  const int i = cred[1 + blockIdx.x];
   const int c = t.n_kept[i];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const float *fold = a.part;
-  int di = 0, ctxoff = 0;
-  for (int x = t.parent[i]; x >= 0 && di < MAXD; x = t.parent[x]) {
-    ++di;
-    ctxoff += t.n_kept[x];
-  }
+  // (every credited block lies on an observer's chain, whose depth and
+  // context offset the setup recorded)
+  const int di = a.ndep[i], ctxoff = a.nctx[i];
   const int64_t tb = t.tok_off[i];
   const int64_t po = t.page_off[i];
   int64_t rows_add = 0;
@@ -1009,7 +1032,7 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   size_t b = 0;
   // offsets, counts, chains, credited-block flags and list (each carve
   // rounds up to 256 B)
-  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + (size_t)sz->num_nodes * 8 + 12 * 256;
+  b += nobs * (8 * 3 + 4 * 4) + nobs * MAXD * 4 + (size_t)sz->num_nodes * 16 + 14 * 256;
   // partials and their folded sums
   b += nobs * (slabs + 1) * (size_t)sz->max_context * 4 + 256;
   // sub-page tables: at most one ragged sub-page per chain node
@@ -1054,6 +1077,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   int32_t *odepth = cv.take<int32_t>(nobs);
   int32_t *anc = cv.take<int32_t>(nobs * MAXD);
   int32_t *flag = cv.take<int32_t>((size_t)t.V);
+  int32_t *nctx = cv.take<int32_t>((size_t)t.V);
+  int32_t *ndep = cv.take<int32_t>((size_t)t.V);
   int32_t *cred = cv.take<int32_t>((size_t)t.V + 1);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   float *part = reinterpret_cast<float *>(cv.rest());
@@ -1065,14 +1090,16 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.ctxlen = ctxlen;
   a.odepth = odepth;
   a.anc = anc;
+  a.nctx = nctx;
+  a.ndep = ndep;
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
     if (t.V <= kSetupLds)
       hipLaunchKernelGGL(score_setup<true>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
-                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, cred);
+                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
     else
       hipLaunchKernelGGL(score_setup<false>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
-                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, cred);
+                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
     hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     const int n_planes = n_slice * pl.Hkv * a.n_rg;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));

@@ -80,21 +80,43 @@ __device__ __forceinline__ bool recency_only(int mode, int ki, int c, const Rang
 }
 
 // Nodes with at most 64 * kCached resident slots: keys and positions stay in
-// registers for every radix pass.
+// registers for every radix pass.  When the block's n <= kStageA positions fit,
+// its whole row of A is first copied to LDS with loads issued together with
+// the page-table loads, so the keys are read from LDS once the positions are
+// known (one global round trip fewer).
+constexpr int kStageA = 512;
 __device__ void select_cached(const NodeView &nv, const float *__restrict__ A, int c, int ki,
                               int thr, int sk, int mode, int32_t *__restrict__ out,
-                              int32_t *status, int lane, const Hist &hist) {
+                              int32_t *status, int lane, const Hist &hist, int n,
+                              float *__restrict__ a_lds) {
   uint32_t key[kCached];
   int pos[kCached];
   bool nan = false;
   Ranges rg{0, 0};
   const int hthr = thr > sk ? thr : sk;
+  const bool staged = n <= kStageA;
+  int page[kCached];
+#pragma unroll
+  for (int r = 0; r < kCached; ++r) {
+    const int s = r * kWave + lane;
+    page[r] = s < c ? nv.page_table[nv.po + s / nv.P] : 0;
+  }
+  if (staged) {
+#pragma unroll
+    for (int r = 0; r < kStageA / kWave; ++r) {
+      const int p = r * kWave + lane;
+      if (p < n) a_lds[p] = A[p];
+    }
+    // LDS operations of one wave complete in order; this keeps the compiler
+    // from moving the reads below above these writes
+    __builtin_amdgcn_wave_barrier();
+  }
 #pragma unroll
   for (int r = 0; r < kCached; ++r) {
     const int s = r * kWave + lane;
     const bool v = s < c;
-    const int p = v ? nv.pos(s) : 0;
-    const float a = v ? A[p] : 0.f;
+    const int p = v ? nv.slot_pos[(int64_t)page[r] * nv.P + (s % nv.P)] : 0;
+    const float a = v ? (staged ? a_lds[p] : A[p]) : 0.f;
     nan |= v && (a != a);
     key[r] = ordered_key(a);
     pos[r] = p;
@@ -219,26 +241,30 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
                                                      int32_t *__restrict__ sel_pos,
                                                      int32_t *status) {
   __shared__ unsigned s_hist[4][256];
-  if (status_failed(status)) return;
+  __shared__ float s_a[4][kStageA];
   const int lane = lane_id();
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const Hist hist{s_hist[threadIdx.x >> 6]};
   if (i >= t.V) return;
+  // the node's scalars are loaded together with the status word
   const int c = t.n_kept[i];
   const int ki = k[i];
+  const int n = t.n_full[i];
+  const int64_t tb = t.tok_off[i];
+  const int64_t po = t.page_off[i];
+  if (status_failed(status)) return;
   if (ki >= c) return;
   if (ki < 0) {
     if (lane == 0) status_error(status, ARBOR_EINVAL);
     return;
   }
-  const int n = t.n_full[i];
-  const int64_t tb = t.tok_off[i];
-  const NodeView nv{t.page_table, pl.slot_pos, t.page_off[i], pl.P};
+  const NodeView nv{t.page_table, pl.slot_pos, po, pl.P};
   int32_t *out = sel_pos + tb;
   // the global sinks are the first positions of the root block (the prompt)
   const int sk = (i == 0 && mode != ARBOR_SELECT_TAIL_ONLY) ? n_sinks : 0;
   if (c <= kWave * kCached)
-    select_cached(nv, A + tb, c, ki, n - l_tail, sk, mode, out, status, lane, hist);
+    select_cached(nv, A + tb, c, ki, n - l_tail, sk, mode, out, status, lane, hist, n,
+                  s_a[threadIdx.x >> 6]);
   else
     select_streamed(nv, A + tb, c, ki, n - l_tail, sk, mode, out, status, lane, hist);
 }
