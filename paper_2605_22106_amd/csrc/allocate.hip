@@ -615,13 +615,17 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
         c[p] = 0.0;
       }
       if (!(end_b ? b_done : a_done)) {
+        // (selects rather than a branch, so that the loads of several nodes
+        // are in flight together; blocks without prices add 0)
+#pragma unroll 4
         for (int i = lane; i < V; i += kWave) {
           const int cnt = nd.cnt[i];
-          if (cnt > 0) {
-            const int F = nd.F[i];
-            const double W = nd.W[i];
+          const int F = nd.F[i];
+          const double W = nd.W[i];
 #pragma unroll
-            for (int p = 0; p < kPtsPerWave; ++p) c[p] += approx_le(xv[p], F, cnt, W);
+          for (int p = 0; p < kPtsPerWave; ++p) {
+            const double y = approx_le(xv[p], F, cnt, W);
+            c[p] += cnt > 0 ? y : 0.0;
           }
         }
 #pragma unroll
@@ -820,13 +824,13 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     // (a, b]); LDS and workspace buffers take separate code paths, so that
     // each compiles to its own kind of memory instruction
     auto order_stat = [&](uint64_t *cand, uint64_t *cand2) __attribute__((always_inline)) {
-      // one wave per node, lanes over its listed prices
-      for (int i = wave; i < V; i += AT / kWave) {
+      // one thread per node over its listed prices (a few per node: the
+      // bracket holds a few hundred in all)
+      for (int i = tid; i < V; i += AT) {
         const int nl = nd.down[i];
-        if (nl <= 0) continue;
         const int m_lo = nd.depth[i], o = nd.cnt[i];
         const double W = nd.W[i];
-        for (int j = lane; j < nl; j += kWave)
+        for (int j = 0; j < nl; ++j)
           cand[o + j] = (uint64_t)__double_as_longlong(price(m_lo + 1 + j, W));
       }
       __syncthreads();
@@ -934,6 +938,7 @@ __global__ __launch_bounds__(AT) void walk_stats(Tree t, const int32_t *__restri
   __shared__ int64_t sm[3 * 16];
   if (status_failed(status)) return;
   int64_t v[3] = {0, 0, 0};   // sum k, evicted, restored or resident
+#pragma unroll 4
   for (int i = threadIdx.x; i < t.V; i += AT) {
     const int c = t.n_kept[i], ki = k[i], n = t.n_full[i];
     v[0] += ki;

@@ -115,31 +115,39 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
                                                      int32_t *__restrict__ changed,
                                                      int32_t *__restrict__ meta, int32_t *status) {
   __shared__ int64_t sm[2 * 16];
-  // the first nodes' counts and the free-stack top are loaded together with
-  // the status word
-  const int i0 = threadIdx.x;
-  const bool in0 = i0 < t.V;
-  const int k0 = in0 ? k[i0] : 0, c0 = in0 ? t.n_kept[i0] : 0, f0 = in0 ? freed[i0] : 0;
-  const int top = threadIdx.x == 0 ? *pl.free_top : 0;
+  const int V = t.V;
+  const int nt = blockDim.x, tid = threadIdx.x;
+  // each thread takes a run of consecutive nodes, so its loads are issued
+  // together and one exchange gives every offset
+  const int per = (V + nt - 1) / nt;
+  const int i0 = min(V, tid * per), i1 = min(V, i0 + per);
+  const int top = tid == 0 ? *pl.free_top : 0;
+  int64_t pages = 0, nodes = 0;
+#pragma unroll 4
+  for (int i = i0; i < i1; ++i) {
+    const bool ch = k[i] < t.n_kept[i];
+    const int f = freed[i];
+    pages += ch ? f : 0;
+    nodes += ch ? 1 : 0;
+  }
   if (status_failed(status)) {
     if (threadIdx.x == 0) meta[0] = 0;
     return;
   }
-  int64_t run_pages = 0, run_nodes = 0;
-  for (int base = 0; base < t.V; base += blockDim.x) {
-    const int i = base + threadIdx.x;
-    const bool in = i < t.V;
-    const bool ch = in && (base == 0 ? k0 < c0 : k[i] < t.n_kept[i]);
-    const int64_t v2[2] = {ch ? (base == 0 ? f0 : freed[i]) : 0, ch ? 1 : 0};
-    int64_t ex[2], tot[2];
-    block_exclusive_scan_n<2>(v2, ex, tot, sm, t.V - base);
-    if (ch) {
-      push_base[i] = (int32_t)(run_pages + ex[0]);
-      changed[run_nodes + ex[1]] = i;
+  const int64_t v2[2] = {pages, nodes};
+  int64_t ex[2], tot[2];
+  block_exclusive_scan_n<2>(v2, ex, tot, sm);
+  int64_t run_pages = ex[0], run_nodes = ex[1];
+  for (int i = i0; i < i1; ++i) {
+    if (k[i] < t.n_kept[i]) {
+      push_base[i] = (int32_t)run_pages;
+      changed[run_nodes] = i;
+      run_pages += freed[i];
+      ++run_nodes;
     }
-    run_pages += tot[0];
-    run_nodes += tot[1];
   }
+  run_pages = tot[0];
+  run_nodes = tot[1];
   if (threadIdx.x == 0) {
     if (top < 0 || (int64_t)top + run_pages > pl.num_pages) {
       status_error(status, ARBOR_ECORRUPT);
