@@ -78,6 +78,8 @@ struct AllocWs {
   double *W, *w;
   uint64_t *buf0, *buf1;
   int64_t buf_cap;
+  int32_t *eF, *eC;     // the blocks with eligible prices: F, count
+  double *eW;            // and W, side by side (trees beyond LDS mode)
 };
 
 __device__ __forceinline__ double price(int j, double W) {
@@ -578,6 +580,37 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       return;
     }
 
+    // Beyond LDS mode the blocks with eligible prices are listed once (F,
+    // cnt, W side by side in the workspace), so that the search rounds, the
+    // listing and the fill below visit only them.
+    const int32_t *eF = nd.F;
+    int32_t *eC = nd.cnt;
+    const double *eW = nd.W;
+    int ne = V;
+    if constexpr (MODE != 1) {
+      const int per = (V + AT - 1) / AT;
+      const int i0 = min(V, tid * per), i1 = min(V, i0 + per);
+      int64_t mine = 0;
+#pragma unroll 4
+      for (int i = i0; i < i1; ++i) mine += nd.cnt[i] > 0 ? 1 : 0;
+      int64_t tot;
+      int64_t off = block_exclusive_scan<int64_t>(mine, sm, &tot);
+      for (int i = i0; i < i1; ++i) {
+        const int cnt = nd.cnt[i];
+        if (cnt > 0) {
+          ws.eF[off] = nd.F[i];
+          ws.eC[off] = cnt;
+          ws.eW[off] = nd.W[i];
+          ++off;
+        }
+      }
+      __syncthreads();
+      eF = ws.eF;
+      eC = ws.eC;
+      eW = ws.eW;
+      ne = (int)tot;
+    }
+
     // -- bracket: keys a (few prices <= a) and b (enough prices <= b) --------
     // The rounded count is off by at most two prices per node, so
     //   approx(a) <= E - 2 n_elig - 1  ->  exact(a) <= E - 1, and
@@ -618,10 +651,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
         // (selects rather than a branch, so that the loads of several nodes
         // are in flight together; blocks without prices add 0)
 #pragma unroll 4
-        for (int i = lane; i < V; i += kWave) {
-          const int cnt = nd.cnt[i];
-          const int F = nd.F[i];
-          const double W = nd.W[i];
+        for (int e = lane; e < ne; e += kWave) {
+          const int cnt = eC[e];
+          const int F = eF[e];
+          const double W = eW[e];
 #pragma unroll
           for (int p = 0; p < kPtsPerWave; ++p) {
             const double y = approx_le(xv[p], F, cnt, W);
@@ -787,18 +820,18 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     }
 
     // -- list the prices in (a, b] and count those <= a exactly -------------
-    // per node: first listed j - 1 in depth[], how many in down[], offset in
-    // cnt[] (the geometry fields are no longer needed)
+    // per listed block e: first listed j - 1 in depth[e], how many in
+    // down[e], offset in eC[e] (the geometry fields are no longer needed)
     const double av = key_value(a), bv = key_value(b);
     int64_t below = 0, run = 0;
-    for (int base = 0; base < V; base += AT) {
-      const int i = base + tid;
+    for (int base = 0; base < ne; base += AT) {
+      const int e = base + tid;
       int m_lo = 0, m_hi = 0, F = 0;
-      if (i < V) {
-        const int cnt = nd.cnt[i];
+      if (e < ne) {
+        const int cnt = eC[e];
         if (cnt > 0) {
-          F = nd.F[i];
-          const double W = nd.W[i];
+          F = eF[e];
+          const double W = eW[e];
           m_lo = a_none ? F : last_le(av, F, cnt, W);
           m_hi = last_le(bv, F, cnt, W);
         }
@@ -806,11 +839,11 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
       // offsets of the listed prices, and the count of prices <= a
       const int64_t v2[2] = {(int64_t)(m_hi - m_lo), (int64_t)(m_lo - F)};
       int64_t ex[2], tot[2];
-      block_exclusive_scan_n<2>(v2, ex, tot, sm, V - base);
-      if (i < V) {
-        nd.depth[i] = m_lo;
-        nd.down[i] = m_hi - m_lo;
-        nd.cnt[i] = (int)(run + ex[0]);
+      block_exclusive_scan_n<2>(v2, ex, tot, sm, ne - base);
+      if (e < ne) {
+        nd.depth[e] = m_lo;
+        nd.down[e] = m_hi - m_lo;
+        eC[e] = (int)(run + ex[0]);
       }
       run += tot[0];
       below += tot[1];
@@ -826,10 +859,10 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
     auto order_stat = [&](uint64_t *cand, uint64_t *cand2) __attribute__((always_inline)) {
       // one thread per node over its listed prices (a few per node: the
       // bracket holds a few hundred in all)
-      for (int i = tid; i < V; i += AT) {
-        const int nl = nd.down[i];
-        const int m_lo = nd.depth[i], o = nd.cnt[i];
-        const double W = nd.W[i];
+      for (int e = tid; e < ne; e += AT) {
+        const int nl = nd.down[e];
+        const int m_lo = nd.depth[e], o = eC[e];
+        const double W = eW[e];
         for (int j = 0; j < nl; ++j)
           cand[o + j] = (uint64_t)__double_as_longlong(price(m_lo + 1 + j, W));
       }
@@ -921,7 +954,8 @@ __global__ __launch_bounds__(AT) void allocate_kernel(Tree t, const int32_t *__r
 }  // namespace
 
 size_t allocate_workspace(const arbor_sizes_t *sz) {
-  return (size_t)sz->num_nodes * (5 * 4 + 8 * 2 + 64) + (size_t)sz->num_tokens * 16 + 8192;
+  return (size_t)sz->num_nodes * (5 * 4 + 8 * 2 + 2 * 4 + 8 + 64) +
+         (size_t)sz->num_tokens * 16 + 8192;
 }
 
 // Per-event statistics of the device-side controller (arbor_walk): one
@@ -985,6 +1019,9 @@ int launch_allocate(const arbor_tree_t *tree, const int32_t *active, int32_t n_a
   ws.cap = cv.take<int32_t>(t.V);
   ws.W = cv.take<double>(t.V);
   ws.w = cv.take<double>(t.V);
+  ws.eF = cv.take<int32_t>(t.V);
+  ws.eC = cv.take<int32_t>(t.V);
+  ws.eW = cv.take<double>(t.V);
   ws.buf0 = cv.take<uint64_t>((size_t)t.N);
   ws.buf1 = cv.take<uint64_t>((size_t)t.N);
   ws.buf_cap = t.N;
