@@ -83,7 +83,8 @@ typedef enum {
   ARBOR_KERNEL_SELECT = 1,        /* the selection kernel of arbor_select          */
   ARBOR_KERNEL_COMPACT_MOVE = 2,  /* the row-move kernel of arbor_compact          */
   ARBOR_KERNEL_DECODE_ATTN = 3,   /* the attention kernels of arbor_tree_decode_attn */
-  ARBOR_KERNEL_DECODE_CREDIT = 4, /* the credit kernel of arbor_tree_decode_attn_scored */
+  ARBOR_KERNEL_DECODE_CREDIT = 4, /* the merge-and-credit kernel of
+                                     arbor_tree_decode_attn_scored                 */
   ARBOR_KERNEL_COUNT = 5
 } arbor_kernel_t;
 
@@ -373,10 +374,12 @@ typedef struct {
   int64_t *rows_seen;           /* device, int64 [V], in/out                         */
 } arbor_decode_credit_t;
 
-/* The attention units keep the logits of the slice layers (fp32, CHUNK = 256
- * per unit row and kv head) in the workspace, and a second kernel turns them
- * into the credited weights once the merge has each row's log-sum-exp: the
- * workspace must be sized with arbor_sizes_t.n_slice >= n_slice.
+/* The attention units keep the logits of the distinct slice layers (fp32,
+ * CHUNK = 256 per unit row and kv head) in the workspace; the launch that
+ * merges the partials also turns them into the credited weights, its credit
+ * workgroups forming each row's log-sum-exp from the chain's partials
+ * themselves.  The workspace must be sized with arbor_sizes_t.n_slice >=
+ * n_slice.
  * Errors: those of arbor_tree_decode_attn; EINVAL for a slice layer outside
  * [layer_begin, layer_end), n_slice outside 1..8, self_window not 0 or 1, or A /
  * rows_seen NULL with n_leaves > 0; EWORKSPACE (device) when the workspace

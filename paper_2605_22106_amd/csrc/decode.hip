@@ -57,8 +57,7 @@ struct DecArgs {
   int max_parts;
   float *part;
   int64_t part_cap;
-  float *lse2;                // [n_leaves][Lr][Hq] log2-domain LSE (credit calls only)
-  int zS;                     // credit calls: slice layers whose logits the units keep
+  int zS;                     // credit calls: distinct slice layers whose logits the units keep
   int zlr[8];                 //   (relative to l0); zS = 0 otherwise
   int32_t *status;
 };
@@ -66,9 +65,10 @@ struct DecArgs {
 // The decode-time credit of accumulated attention: slice layers relative to
 // the call's first layer, the crediting mode and the caller's A / rows_seen.
 struct CreditArgs {
-  int S;
-  int slice[8];
-  int zslot[8];   // kept-logit slot of slice e: the first entry with the same layer
+  int S;          // slice entries (a layer may be listed more than once)
+  int U;          // distinct slice layers: the units keep logits for these
+  int slice[8];   // distinct slice layers
+  int mult[8];    //   and how often each is listed
   int self_window;
   float *A;
   int64_t *rows_seen;
@@ -621,21 +621,22 @@ __global__ __launch_bounds__(256) void decode_attn(DecArgs a, int cls) {
 // One wave per (leaf, layer, query head): merge the partials of the leaf's
 // chain.  Lane k holds partial k's (max, sum); the running max and the weights
 // come from fixed-order wave reductions, and o is accumulated in partial order,
-// so the result does not depend on scheduling.
+// so the result does not depend on scheduling.  Workgroups blk of nblk take
+// the rows in turn.
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int out_dtype,
-                                                    float *lse_out) {
+__device__ __forceinline__ void merge_rows(const DecArgs &a, void *out, int out_dtype,
+                                           float *lse_out, int blk, int nblk) {
   constexpr int EPL = D / 64;  // output columns per lane
   constexpr int U = 4;         // partial rows loaded together
-  if (status_failed(a.status)) return;
   const Pool &pl = a.pl;
   const int lane = lane_id();
   const int G = pl.G;
   const int Hq = pl.Hkv * G;
   const int64_t total = (int64_t)a.n_leaves * a.Lr * Hq;
   const int64_t stride = D + 2;
-  for (int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); w < total;
-       w += (int64_t)gridDim.x * 4) {
+  const int wpb = blockDim.x / kWave;
+  for (int64_t w = (int64_t)blk * wpb + threadIdx.x / kWave; w < total;
+       w += (int64_t)nblk * wpb) {
     const int b = (int)(w / (a.Lr * Hq));
     const int rem = (int)(w % (a.Lr * Hq));
     const int lr = rem / Hq;
@@ -715,7 +716,6 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
       const float l2 = L > 0.f ? M + __log2f(L) : -__builtin_inff();
       const int64_t li = ((int64_t)b * a.Lr + lr) * Hq + h;
       if (lse_out) lse_out[li] = L > 0.f ? l2 * kLn2 : -__builtin_inff();
-      if (a.lse2) a.lse2[li] = l2;
     }
   }
 }
@@ -725,68 +725,109 @@ __global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int ou
 // the attention units kept for the credited slice layers, summed over the
 // rows whose leaf lies strictly below the unit's node (and, in the
 // self-window mode, the leaf's own rows on keys before its newest position)
-// and over the slice layers and kv heads, and added to A at the key's token.
-// One workgroup per 16-slot sub-page of a unit: thread (row lane j, key k)
-// sums rows j, j + 16, ... of key k over the (slice layer, kv head) pairs in
-// a fixed order, and the 16 row lanes are added in order, so each token's sum
-// has one owner and a fixed order.  Workgroup 0 also adds the row counts to
-// rows_seen (integer atomics: order-free).
-__device__ __forceinline__ void credit_subpage(const DecArgs &a, const CreditArgs &cr, int item,
-                                               int sub, float (&s_red)[16][16]) {
-  const Tree &t = a.t;
-  const Pool &pl = a.pl;
-  const int G = pl.G;
-  const int Hq = pl.Hkv * G;
-  const int node = a.item_node[item];
-  const int c = t.n_kept[node];
-  const int s0 = a.item_chunk[item] * CHUNK + sub * 16;
-  if (s0 >= c) return;                        // uniform over the workgroup
-  const int R = a.node_nl[node] * G;
-  const int loff = a.node_leaf_off[node];
-  const int nval = min(16, c - s0);
-  const int kk = threadIdx.x & 15;
-  const int rj = threadIdx.x >> 4;
-  const bool key_ok = kk < nval;
-  const int page = t.page_table[t.page_off[node] + s0 / pl.P];
-  const int pos = key_ok ? pl.slot_pos[(int64_t)page * pl.P + s0 % pl.P + kk] : 0;
-  const int64_t tok = t.tok_off[node] + pos;
-  // own rows (the node is the row's leaf) are credited only on earlier keys
-  // in the self-window mode
-  const bool own_ok = cr.self_window && key_ok && pos < t.n_full[node] - 1;
-  const float *z0 = a.part + a.meta[4];
-  const int64_t rows_total = a.meta[3];
-  const int rb = a.item_rowbase[item];
-  float sum = 0.f;
-  for (int r = rj; r < R; r += 16) {
-    const int b = a.leaf_list[loff + r / G];
-    if (!key_ok || (a.leaves[b] == node && !own_ok)) continue;
-    for (int z = 0; z < cr.S; ++z) {
-      const int lr = cr.slice[z];
-      for (int g = 0; g < pl.Hkv; ++g) {
-        const float zv = z0[(((int64_t)cr.zslot[z] * pl.Hkv + g) * rows_total + rb + r) * CHUNK +
-                            (s0 - a.item_chunk[item] * CHUNK) + kk];
-        const float l2 = a.lse2[((int64_t)b * a.Lr + lr) * Hq + g * G + r % G];
-        sum += __builtin_amdgcn_exp2f(zv - l2);
-      }
+// and over the slice layers (a layer listed m times counts m times) and kv
+// heads, and added to A at the key's token.  A row's log2 LSE, lse2 = M +
+// log2(sum_k l_k exp2(m_k - M)) over the (max m_k, sum l_k) of the partials of
+// its leaf's chain, is formed here from those partials, so the credit does not
+// wait for the merge and runs beside it in the same launch.
+// One workgroup of kCreditWaves waves per quarter (64 slots) of a unit, one
+// lane per slot.  The unit's (row, distinct slice layer, kv head) triples, in
+// the order (r * U + z) * Hkv + g, are staged in LDS up to kCreditTile at a
+// time (one thread per triple): each triple's lse2 and its weight, the layer's
+// multiplicity, negated when the row is the node's own leaf's.  Wave v takes
+// the triples v, v + kCreditWaves, ... in order, kCreditBatch logit loads at a
+// time, the next batch in flight while one is summed; the first batch is
+// issued before the tables are built (a triple's logit row, (z * Hkv + g) *
+// rows + r, is known without them), and for up to kCreditWaves * kCreditBatch
+// triples it is the only one.  The rows of other leaves and the node's own
+// rows are kept in two sums; the waves' sums are added in wave order, so each
+// token's sum has one owner and a fixed order.  Workgroup 0 also adds the row
+// counts to rows_seen (integer atomics: order-free).
+constexpr int kCreditWaves = 16;
+constexpr int kCreditThreads = kCreditWaves * kWave;
+constexpr int kCreditTile = 1024;
+constexpr int kCreditBatch = 16;
+constexpr int kQuarters = CHUNK / kWave;
+constexpr int kLsePar = 8;            // partials of a chain loaded together
+static_assert(CHUNK % kWave == 0, "a unit is a whole number of 64-slot quarters");
+static_assert(kCreditTile % (kCreditWaves * kCreditBatch) == 0, "batches do not straddle tiles");
+
+// a triple as (row r, zg = z * Hkv + g), stepped without divisions
+struct Triple {
+  int r, zg;
+  __device__ __forceinline__ void step(int k, int per) {
+    zg += k;
+    while (zg >= per) {
+      zg -= per;
+      ++r;
     }
   }
-  s_red[rj][kk] = sum;
-  __syncthreads();
-  if (threadIdx.x < 16 && key_ok) {
-    float tot = 0.f;
+};
+
+// logits of the batch of triples it, it + kCreditWaves, ... (it is left at
+// the next batch's first triple): zb points at the unit's first logit row and
+// the lane's slot; triples past the unit's R rows are not read
+__device__ __forceinline__ void credit_load(float (&zv)[kCreditBatch], const float *zb, Triple &it,
+                                            int R, int per, int64_t rows_total) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) tot += s_red[j][kk];
-    cr.A[tok] = cr.A[tok] + tot;
+  for (int u = 0; u < kCreditBatch; ++u) {
+    zv[u] = it.r < R ? zb[((int64_t)it.zg * rows_total + it.r) * CHUNK] : 0.f;
+    it.step(kCreditWaves, per);
   }
 }
 
-template <class T, int D>
-__global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
-  constexpr int SUBS = CHUNK / 16;
-  __shared__ float s_red[16][16];
+// log2 LSE of query row (leaf b, layer lr, head g * G + hl) over the partials
+// of b's chain, with the maximum taken kLsePar partials at a time
+template <int D>
+__device__ __forceinline__ float chain_lse2(const DecArgs &a, int b, int lr, int g, int hl) {
+  const int64_t stride = D + 2;
+  const float *base = a.part + (((int64_t)lr * a.pl.Hkv + g) * a.meta[3] + hl) * stride;
+  const int32_t *lp = a.leaf_part + (int64_t)b * a.max_parts;
+  const int np = a.leaf_np[b];
+  float M = -__builtin_inff(), L = 0.f;
+  for (int k0 = 0; k0 < np; k0 += kLsePar) {
+    float m[kLsePar], l[kLsePar];
+#pragma unroll
+    for (int u = 0; u < kLsePar; ++u) {
+      const int64_t off = k0 + u < np ? (int64_t)lp[k0 + u] * stride : 0;
+      m[u] = k0 + u < np ? base[off] : -__builtin_inff();
+      l[u] = k0 + u < np ? base[off + 1] : 0.f;
+    }
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < kLsePar; ++u) Mn = fmaxf(Mn, m[u]);
+    if (Mn == -__builtin_inff()) continue;
+    L = M > -__builtin_inff() ? L * __builtin_amdgcn_exp2f(M - Mn) : 0.f;
+#pragma unroll
+    for (int u = 0; u < kLsePar; ++u)
+      L += m[u] > -__builtin_inff() ? l[u] * __builtin_amdgcn_exp2f(m[u] - Mn) : 0.f;
+    M = Mn;
+  }
+  return L > 0.f ? M + __log2f(L) : -__builtin_inff();
+}
+
+// the credit of the quarters blk, blk + nblk, ... of the plan's units
+template <int D>
+__device__ __forceinline__ void credit_quarters(const DecArgs &a, const CreditArgs &cr, int blk,
+                                                int nblk) {
+  __shared__ float s_oth[kCreditWaves][kWave], s_own[kCreditWaves][kWave];
+  __shared__ float s_l2[kCreditTile], s_w[kCreditTile];
+  const Tree &t = a.t;
+  const Pool &pl = a.pl;
+  const int G = pl.G, Hkv = pl.Hkv;
+  const int Hq = Hkv * G;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  // the launch covers at most max_items units, so the first unit's fields can
+  // be read before the plan's unit count is known
+  const int n_items = a.meta[0] + a.meta[1] + a.meta[2];
+  const int64_t rows_total = a.meta[3];
+  const int item0 = blk / kQuarters;
+  const int node0 = a.item_node[item0];
+  const int chunk0 = a.item_chunk[item0];
+  const int rb0 = a.item_rowbase[item0];
   if (status_failed(a.status)) return;
-  const int Hq = a.pl.Hkv * a.pl.G;
-  if (blockIdx.x == 0) {
+  if (blk == 0) {
     const unsigned long long per = (unsigned long long)cr.S * Hq;
     for (int e = threadIdx.x; e < a.n_leaves * MAXD; e += blockDim.x) {
       const int b = e / MAXD, d = e % MAXD;
@@ -797,11 +838,121 @@ __global__ __launch_bounds__(256) void decode_credit(DecArgs a, CreditArgs cr) {
                   per);
     }
   }
-  const int n_items = a.meta[0] + a.meta[1] + a.meta[2];
-  for (int w = blockIdx.x; w < n_items * SUBS; w += gridDim.x) {
-    credit_subpage(a, cr, w / SUBS, w % SUBS, s_red);
-    __syncthreads();                        // s_red is reused by the next sub-page
+  const float *z0 = a.part + a.meta[4];
+  const int per = cr.U * Hkv;
+  constexpr int kLast = kCreditWaves - 1;
+  for (int w = blk; w < n_items * kQuarters; w += nblk) {
+    const int item = w / kQuarters;
+    const bool first = w == blk;
+    const int node = first ? node0 : a.item_node[item];
+    const int k0 = (first ? chunk0 : a.item_chunk[item]) * CHUNK;
+    const int rb = first ? rb0 : a.item_rowbase[item];
+    const int c = t.n_kept[node];
+    const int s0 = k0 + (w % kQuarters) * kWave;
+    if (s0 >= c) continue;                    // uniform over the workgroup
+    const int slot = s0 + lane;
+    const bool key_ok = slot < c;
+    const int R = a.node_nl[node] * G;
+    const int loff = a.node_leaf_off[node];
+    const int n = R * per;
+    // the leaf of this thread's first table entry, read before the logits so
+    // that waiting for it does not wait for them
+    const int b_first = (int)threadIdx.x < min(n, kCreditTile)
+                            ? a.leaf_list[loff + (int)threadIdx.x / per / G] : 0;
+    // logit rows hold CHUNK slots each, so the lane's slot is in bounds for
+    // every lane; lanes past the node's count are masked after the load
+    const float *zb = z0 + (int64_t)rb * CHUNK + (slot - k0);
+    float cur[kCreditBatch];
+    Triple it{0, 0};
+    it.step(wv, per);
+    credit_load(cur, zb, it, R, per, rows_total);
+    // the last wave fetches the lane's token and its A entry meanwhile; each
+    // token has one owner, so A is read before the sums
+    int64_t tok = 0;
+    float a_old = 0.f;
+    bool own_ok = false;
+    if (wv == kLast && key_ok) {
+      const int page = t.page_table[t.page_off[node] + slot / pl.P];
+      const int pos = pl.slot_pos[(int64_t)page * pl.P + slot % pl.P];
+      tok = t.tok_off[node] + pos;
+      a_old = cr.A[tok];
+      // own rows (the node is the row's leaf) are credited only on earlier
+      // keys in the self-window mode
+      own_ok = cr.self_window && pos < t.n_full[node] - 1;
+    }
+    float oth = 0.f, own = 0.f;
+    int e0 = wv;
+    for (int t0 = 0; t0 < n; t0 += kCreditTile) {
+      const int nt = min(kCreditTile, n - t0);
+      for (int i = threadIdx.x; i < nt; i += blockDim.x) {
+        const int e = t0 + i;
+        const int r = e / per, zg = e % per;
+        const int z = zg / Hkv, g = zg % Hkv;
+        const int b = t0 == 0 && i == (int)threadIdx.x ? b_first : a.leaf_list[loff + r / G];
+        s_l2[i] = chain_lse2<D>(a, b, cr.slice[z], g, r % G);
+        const float m = (float)cr.mult[z];
+        s_w[i] = a.leaves[b] == node ? -m : m;
+      }
+      __syncthreads();
+      for (; e0 < t0 + nt; e0 += kCreditWaves * kCreditBatch) {
+        float nxt[kCreditBatch];
+        const bool more = e0 + kCreditWaves * kCreditBatch < n;
+        if (more) credit_load(nxt, zb, it, R, per, rows_total);
+#pragma unroll
+        for (int u = 0; u < kCreditBatch; ++u) {
+          const int i = e0 + kCreditWaves * u - t0;
+          if (i < nt) {
+            const float p = key_ok ? __builtin_amdgcn_exp2f(cur[u] - s_l2[i]) : 0.f;
+            const float wt = s_w[i];
+            if (wt < 0.f) own += -wt * p;
+            else oth += wt * p;
+          }
+        }
+        if (more) {
+#pragma unroll
+          for (int u = 0; u < kCreditBatch; ++u) cur[u] = nxt[u];
+        }
+      }
+      __syncthreads();                        // the tables are reused by the next tile
+    }
+    s_oth[wv][lane] = oth;
+    s_own[wv][lane] = own;
+    __syncthreads();
+    if (wv == kLast && key_ok) {
+      float tot = 0.f;
+#pragma unroll
+      for (int v = 0; v < kCreditWaves; ++v) tot += s_oth[v][lane];
+      if (own_ok) {
+#pragma unroll
+        for (int v = 0; v < kCreditWaves; ++v) tot += s_own[v][lane];
+      }
+      cr.A[tok] = a_old + tot;
+    }
+    __syncthreads();                          // the sums are reused by the next quarter
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge(DecArgs a, void *out, int out_dtype,
+                                                    float *lse_out) {
+  if (status_failed(a.status)) return;
+  merge_rows<D>(a, out, out_dtype, lse_out, blockIdx.x, gridDim.x);
+}
+
+// scored calls: the first credit_blocks workgroups credit (their chain of
+// loads is the longer one, so they are dispatched first), the rest merge
+template <int D>
+__global__ __launch_bounds__(kCreditThreads) void decode_merge_credit(DecArgs a, CreditArgs cr,
+                                                                      void *out, int out_dtype,
+                                                                      float *lse_out,
+                                                                      int credit_blocks) {
+  if ((int)blockIdx.x < credit_blocks) {
+    credit_quarters<D>(a, cr, blockIdx.x, credit_blocks);
+    return;
+  }
+  if (status_failed(a.status)) return;
+  merge_rows<D>(a, out, out_dtype, lse_out, blockIdx.x - credit_blocks,
+                gridDim.x - credit_blocks);
 }
 
 template <class T, int D>
@@ -819,16 +970,22 @@ void launch_decode_kernels(const arbor_geom_t *geom, const DecArgs &a, void *out
     hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
   timing_end(geom, ARBOR_KERNEL_DECODE_ATTN, stream);
   const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv * a.pl.G;
-  const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
-  hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
-                     lse_out);
-  if (cr) {
-    // workgroups stride over the sub-pages of the plan's units
-    timing_begin(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
-    const int cgrid = std::min(a.max_items * (CHUNK / 16), 1024);
-    hipLaunchKernelGGL((decode_credit<T, D>), dim3(cgrid), dim3(256), 0, stream, a, *cr);
-    timing_end(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
+  if (!cr) {
+    const int mgrid = (int)((mw + 3) / 4 < 8192 ? (mw + 3) / 4 : 8192);
+    hipLaunchKernelGGL((decode_merge<D>), dim3(mgrid), dim3(256), 0, stream, a, out, out_dtype,
+                       lse_out);
+    return;
   }
+  // credit workgroups stride over the quarters of the plan's units (at most
+  // half the chip's wave slots, so that the merge workgroups start beside
+  // them); merge workgroups hold kCreditWaves rows each
+  const int cgrid = std::min(a.max_items * kQuarters, 256);
+  const int64_t mb = (mw + kCreditWaves - 1) / kCreditWaves;
+  const int mgrid = (int)(mb < 2048 ? mb : 2048);
+  timing_begin(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
+  hipLaunchKernelGGL((decode_merge_credit<D>), dim3(cgrid + mgrid), dim3(kCreditThreads), 0,
+                     stream, a, *cr, out, out_dtype, lse_out, cgrid);
+  timing_end(geom, ARBOR_KERNEL_DECODE_CREDIT, stream);
 }
 
 }  // namespace
@@ -850,7 +1007,6 @@ size_t decode_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const size_t rows = nl * per_leaf * g->q_per_kv;
   size_t b = 19 * 256;
   b += 3 * items * 4 + 3 * items * 4 + V * 4 * 4 + nl * MAXD * 4 * 3 + nl * 4 + nl * MAXD * 4;
-  b += nl * (size_t)sz->max_layers * g->num_kv_heads * g->q_per_kv * 4;   // log2 LSE
   b += nl * 4 + nl * decode_max_parts(sz) * 4;
   b += rows * (size_t)sz->max_layers * g->num_kv_heads * (g->head_dim + 2) * 4;
   // logits of the credited slice layers (scored decode)
@@ -901,28 +1057,23 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   const int max_parts = (int)decode_max_parts(&sz);
   int32_t *leaf_np = cv.take<int32_t>(n_leaves);
   int32_t *leaf_part = cv.take<int32_t>((size_t)n_leaves * max_parts);
-  float *lse2 = cv.take<float>((size_t)n_leaves * a.Lr * pl.Hkv * pl.G);
   if (!cv.ok) return ARBOR_EWORKSPACE;
   CreditArgs cr{};
   if (credit) {
     cr.S = credit->n_slice;
-    for (int e = 0; e < 8; ++e)
-      cr.slice[e] = e < credit->n_slice ? credit->slice_layers[e] - layer_begin : 0;
-    cr.self_window = credit->self_window;
-    for (int e = 0; e < 8; ++e) {
-      cr.zslot[e] = e;
-      for (int f = 0; f < e && e < credit->n_slice; ++f)
-        if (cr.slice[f] == cr.slice[e]) {
-          cr.zslot[e] = f;
-          break;
-        }
+    for (int e = 0; e < credit->n_slice; ++e) {
+      const int lr = credit->slice_layers[e] - layer_begin;
+      int u = 0;
+      while (u < cr.U && cr.slice[u] != lr) ++u;
+      if (u == cr.U) cr.slice[cr.U++] = lr;
+      ++cr.mult[u];
     }
+    cr.self_window = credit->self_window;
     cr.A = credit->A;
     cr.rows_seen = credit->rows_seen;
   }
-  a.lse2 = credit ? lse2 : nullptr;
-  a.zS = credit ? cr.S : 0;
-  for (int e = 0; e < 8; ++e) a.zlr[e] = credit && e < cr.S ? cr.slice[e] : -1;
+  a.zS = credit ? cr.U : 0;
+  for (int e = 0; e < 8; ++e) a.zlr[e] = credit && e < cr.U ? cr.slice[e] : -1;
   a.meta = meta;
   a.cls_items = cls_items;
   a.item_node = item_node;
