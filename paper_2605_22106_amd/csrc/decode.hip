@@ -6,7 +6,7 @@
 // kv head).  Its rows are the G query heads of every active leaf below a, so a
 // shared ancestor is streamed from HBM once for all leaves that need it.  A
 // wave computes S = K Q^T with bf16 MFMA (keys along M, so each lane owns one
-// query row), an online softmax at 64-key granularity, and O += P V.  For
+// query row), an online softmax per fragment of keys, and O += P V.  For
 // bf16 pools P is split into a bf16 high part and a bf16 remainder, both
 // multiplied with the exact bf16 V by bf16 MFMAs (fp32-level accuracy of P);
 // fp32 pools use the fp32 MFMA (16x16x4).  The key order inside each MFMA
@@ -412,41 +412,47 @@ __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
     }
   }
   if constexpr (sizeof(T) == 2) {
-    // bf16 values: O += P V as one bf16 MFMA (16x16x32) per 16 output columns
-    // over the fragment's keys, element t = 4 sp + e of a lane's k-slice being
-    // key 4 g4 + e of sub-page sp (zero past GSP sub-pages).  P is split into
-    // a bf16 high part and a bf16 remainder, p = hi + lo to about 2^-17
-    // relative, and both are multiplied by the exact bf16 V, so the product
-    // keeps fp32-level accuracy at a quarter of the fp32 MFMA's issue time.
-    bf16x8 ph[NB], pl[NB];
+    // bf16 values: O += P V as bf16 MFMAs (16x16x32), one per 16 output
+    // columns and pair of sub-pages sp0, sp0 + 1 of the fragment, element t =
+    // 4 (sp - sp0) + e of a lane's k-slice being key 4 g4 + e of sub-page sp
+    // (zero past GSP sub-pages).  P is split into a bf16 high part and a bf16
+    // remainder, p = hi + lo to about 2^-17 relative, and both are multiplied
+    // by the exact bf16 V, so the product keeps fp32-level accuracy at a
+    // quarter of the fp32 MFMA's issue time.
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int sp = t / 4, e = t % 4;
-        if (sp < GSP) {
-          const float p = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
-          l_run[nb] += p;
-          const __bf16 hi = (__bf16)p;
-          ph[nb][t] = hi;
-          pl[nb][t] = (__bf16)(p - (float)hi);
-        } else {
-          ph[nb][t] = (__bf16)0.f;
-          pl[nb][t] = (__bf16)0.f;
-        }
-      }
-    }
-#pragma unroll
-    for (int cc = 0; cc < NC; ++cc) {
-      bf16x8 vv;
-#pragma unroll
-      for (int t = 0; t < 8; ++t)
-        vv[t] = t / 4 < GSP ? (__bf16)f.v[t / 4 < GSP ? t / 4 : 0][t % 4][cc] : (__bf16)0.f;
+    for (int sp0 = 0; sp0 < GSP; sp0 += 2) {
+      bf16x8 ph[NB], pl[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        o[nb][cc] = Op<__bf16>::mma(ph[nb], vv, o[nb][cc]);
-        o[nb][cc] = Op<__bf16>::mma(pl[nb], vv, o[nb][cc]);
+        const float nm = m_run[nb] > -__builtin_inff() ? -m_run[nb] : 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int sp = sp0 + t / 4, e = t % 4;
+          if (sp < GSP) {
+            const float p = __builtin_amdgcn_exp2f(sv[sp][nb][e] + nm);
+            l_run[nb] += p;
+            const __bf16 hi = (__bf16)p;
+            ph[nb][t] = hi;
+            pl[nb][t] = (__bf16)(p - (float)hi);
+          } else {
+            ph[nb][t] = (__bf16)0.f;
+            pl[nb][t] = (__bf16)0.f;
+          }
+        }
+      }
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) {
+        bf16x8 vv;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const int sp = sp0 + t / 4;
+          vv[t] = sp < GSP ? (__bf16)f.v[sp < GSP ? sp : 0][t % 4][cc] : (__bf16)0.f;
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          o[nb][cc] = Op<__bf16>::mma(ph[nb], vv, o[nb][cc]);
+          o[nb][cc] = Op<__bf16>::mma(pl[nb], vv, o[nb][cc]);
+        }
       }
     }
   } else {
@@ -471,15 +477,26 @@ __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
   }
 }
 
+// Sub-pages a wave loads at once: 16 KB of K and V in flight per wave, one
+// fragment at a time.  Measured on the llama8b and dpts trees: with a single
+// buffer the 16-row waves fit three to a SIMD, whose loads overlap one
+// another's work; double-buffered fragments, or larger ones, leave one or
+// two waves per SIMD and stream HBM more slowly.
+template <class T, int D, int NB>
+constexpr int sub_pages_per_fetch() {
+  constexpr int per = 32 * D * (int)sizeof(T);   // K and V of one 16-slot sub-page
+  return (16 << 10) / per < 1 ? 1 : (16 << 10) / per;
+}
+
 // One wave: one work unit (a CHUNK of a chain node's slots, one layer, one kv
 // head), rows [rbase, rbase + 16 NB).  The unit's sub-pages are taken GSP at
-// a time; with DB the next fragment is in flight while the current one is
-// attended, so HBM streaming overlaps the MFMA work.
+// a time (the last fragment of a unit re-reads its last sub-page in the
+// unused places, which the cache serves); other waves of the SIMD attend
+// while one waits for its fragment.
 template <class T, int D, int NB>
 __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase) {
   using O = Op<T>;
-  constexpr int GSP = NB == 1 ? 2 : 1;
-  constexpr bool DB = NB <= 2;
+  constexpr int GSP = sub_pages_per_fetch<T, D, NB>();
   typedef KVFrag<T, D, GSP> F;
   constexpr int KS = F::KS;
   constexpr int NC = F::NC;
@@ -556,25 +573,9 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) o[nb][cc] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  if (DB) {
-    // two fragments alternate; the last prefetch of an odd count is a clamped
-    // re-read of the final sub-pages with no valid slots
-    for (int gi = 0; gi < n_grp; gi += 2) {
-      F nxt = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 1) * GSP, pl.P);
-      // keep the prefetch ahead of the work on the current fragment
-      __builtin_amdgcn_sched_barrier(0);
-      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
-      if (gi + 1 >= n_grp) break;
-      cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 2) * GSP, pl.P);
-      __builtin_amdgcn_sched_barrier(0);
-      attend<T, D, NB, GSP>(nxt, q, a.sl2, g4, m_run, l_run, o, zrow, R, (gi + 1) * GSP,
-                            rbase);
-    }
-  } else {
-    for (int gi = 0; gi < n_grp; ++gi) {
-      if (gi > 0) cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
-      attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
-    }
+  for (int gi = 0; gi < n_grp; ++gi) {
+    if (gi > 0) cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
+    attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
   }
   // partial rows [m, l, o(0..D-1)] of this unit
   const int64_t stride = D + 2;
