@@ -334,15 +334,14 @@ __device__ __forceinline__ KVFrag<T, D, GSP> fetch_kv(const UnitAddr &ua, int pg
 // sub-page's resident count may hold anything: only a ragged sub-page (the
 // last of a node) masks its logits and zeroes its value rows.  The output is
 // rescaled only when some row's running max moved.
-// zrow (NULL: none) keeps the fragment's masked logits in log2 units, the
-// weights the decode-time credit normalises later: zrow + r * CHUNK + 16 sub
-// + key for query row r < zrows of the unit, sub-page sub0 + sp.
+// zs (when keep_z) receives the fragment's masked logits in log2 units, the
+// weights the decode-time credit normalises later; the caller stores them.
 template <class T, int D, int NB, int GSP>
 __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
                                        const typename Op<T>::reg (&q)[NB][KVFrag<T, D, GSP>::KS],
                                        float sl2, int g4, float (&m_run)[NB], float (&l_run)[NB],
-                                       f32x4 (&o)[NB][D / 16], float *zrow = nullptr,
-                                       int zrows = 0, int sub0 = 0, int rbase = 0) {
+                                       f32x4 (&o)[NB][D / 16], bool keep_z,
+                                       float (&zs)[GSP][NB][4]) {
   typedef KVFrag<T, D, GSP> F;
   constexpr int NC = F::NC;
   float sv[GSP][NB][4];
@@ -375,18 +374,11 @@ __device__ __forceinline__ void attend(KVFrag<T, D, GSP> &f,
     for (int nb = 0; nb < NB; ++nb)
       gmax[nb] = fmaxf(gmax[nb], fmaxf(fmaxf(sv[sp][nb][0], sv[sp][nb][1]),
                                        fmaxf(sv[sp][nb][2], sv[sp][nb][3])));
-    if (zrow && f.nval[sp] > 0) {
-      // lane (rr, g4) holds keys 4 g4 .. 4 g4 + 3 of the sub-page for row rr
-      const int rr = lane_id() & 15;
+    if (keep_z) {
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int r = rbase + nb * 16 + rr;
-        if (r < zrows) {
-          const float4 z4 = make_float4(sv[sp][nb][0], sv[sp][nb][1], sv[sp][nb][2],
-                                        sv[sp][nb][3]);
-          *reinterpret_cast<float4 *>(zrow + (int64_t)r * CHUNK + 16 * (sub0 + sp) + 4 * g4) = z4;
-        }
-      }
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) zs[sp][nb][e] = sv[sp][nb][e];
     }
   }
   bool moved = false;
@@ -574,8 +566,28 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
     for (int cc = 0; cc < NC; ++cc) o[nb][cc] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   for (int gi = 0; gi < n_grp; ++gi) {
-    if (gi > 0) cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
-    attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow, R, gi * GSP, rbase);
+    float zs[GSP][NB][4];
+    attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow != nullptr, zs);
+    // the next fragment's loads go out before this one's logits are stored:
+    // a wave's loads and stores share one counter, so a wait for loads
+    // issued after the stores would wait for the stores as well
+    if (gi + 1 < n_grp)
+      cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 1) * GSP, pl.P);
+    if (zrow) {
+      // lane (rr, g4) holds keys 4 g4 .. 4 g4 + 3 of each sub-page for row rr:
+      // zrow + r * CHUNK + 16 sub + key for query row r < R of the unit
+#pragma unroll
+      for (int sp = 0; sp < GSP; ++sp) {
+        if (gi * GSP + sp >= n_sub) continue;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          const int r = rbase + nb * 16 + rr;
+          if (r < R)
+            *reinterpret_cast<float4 *>(zrow + (int64_t)r * CHUNK + 16 * (gi * GSP + sp) + 4 * g4) =
+                make_float4(zs[sp][nb][0], zs[sp][nb][1], zs[sp][nb][2], zs[sp][nb][3]);
+        }
+      }
+    }
   }
   // partial rows [m, l, o(0..D-1)] of this unit
   const int64_t stride = D + 2;
