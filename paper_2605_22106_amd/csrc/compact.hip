@@ -2,17 +2,20 @@
 // K/V rows inside the paged tree KV pool (Sec. 4 Execution: retained entries
 // stay, the other entries are freed).
 //
-// Three launches on one stream:
+// Two launches on one stream:
 //   plan     one wave per node: validate the selection, locate each kept
-//            position's source slot, count the pages the node releases;
-//   scan     one workgroup: (node, page)-ordered free-stack offsets and the
-//            list of changed nodes;
+//            position's source slot; one more workgroup of the same launch
+//            scans the nodes for the (node, page)-ordered free-stack offsets
+//            and the list of changed nodes (a node releases ceil(c / P) -
+//            ceil(k / P) pages, so the scan needs nothing from the plan);
 //   move     one wave per (changed node, layer, kv head) plane: rows move to
 //            lower slots only, so a wave stages a chunk of rows in registers
 //            (all loads of the chunk retire before its stores issue) and walks
 //            the chunks in ascending slot order -- in-place safe; extra
 //            workgroups of the same launch finalize the changed nodes
-//            (slot_pos, page table, free stack, c_i).
+//            (slot_pos, page table, free stack and its top, c_i).
+// The plan and the scan only write the workspace (and the status word), so
+// an error either of them finds leaves the state unchanged.
 #include "arbor_internal.h"
 
 namespace arbor {
@@ -32,13 +35,10 @@ __device__ __forceinline__ int plane_row(const Tree &t, const Pool &pl, int64_t 
   return t.page_table[po + s / pl.P] * pl.Hkv * pl.P + s % pl.P;
 }
 
-__global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32_t *__restrict__ k,
-                                                    const int32_t *__restrict__ sel_pos,
-                                                    int32_t *__restrict__ src_slot,
-                                                    int32_t *__restrict__ mv_src,
-                                                    int32_t *__restrict__ mv_dst,
-                                                    int32_t *__restrict__ first_moved,
-                                                    int32_t *__restrict__ freed, int32_t *status) {
+__device__ void plan_node(const Tree &t, const Pool &pl, const int32_t *__restrict__ k,
+                          const int32_t *__restrict__ sel_pos, int32_t *__restrict__ src_slot,
+                          int32_t *__restrict__ mv_src, int32_t *__restrict__ mv_dst,
+                          int32_t *__restrict__ first_moved, int32_t *status) {
   // each wave's node positions, slot order, when the node holds at most
   // kPlanPos resident tokens: the binary searches then run in LDS
   __shared__ int s_pos[4][kPlanPos];
@@ -52,10 +52,7 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
   const int64_t tb = t.tok_off[i];
   const int64_t po = t.page_off[i];
   if (status_failed(status)) return;
-  if (ki >= c) {
-    if (lane == 0) freed[i] = 0;
-    return;
-  }
+  if (ki >= c) return;
   bool bad = ki < 0;
   int *lp = s_pos[threadIdx.x >> 6];
   const bool in_lds = c <= kPlanPos;
@@ -102,33 +99,30 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
       break;
     }
   }
-  if (lane == 0) {
-    freed[i] = (c + pl.P - 1) / pl.P - (ki + pl.P - 1) / pl.P;
-    first_moved[i] = s0;
-  }
+  if (lane == 0) first_moved[i] = s0;
 }
 
-// meta[0] = number of changed nodes, meta[1] = free-stack top before pushes
-__global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int32_t *__restrict__ k,
-                                                     const int32_t *__restrict__ freed,
-                                                     int32_t *__restrict__ push_base,
-                                                     int32_t *__restrict__ changed,
-                                                     int32_t *__restrict__ meta, int32_t *status) {
+// meta[0] = number of changed nodes, meta[1] = free-stack top before pushes,
+// meta[2] = pages pushed.  One workgroup.
+__device__ void scan_nodes(const Tree &t, const Pool &pl, const int32_t *__restrict__ k,
+                           int32_t *__restrict__ push_base, int32_t *__restrict__ changed,
+                           int32_t *__restrict__ meta, int32_t *status) {
   __shared__ int64_t sm[2 * 16];
   const int V = t.V;
   const int nt = blockDim.x, tid = threadIdx.x;
+  const int P = pl.P;
   // each thread takes a run of consecutive nodes, so its loads are issued
   // together and one exchange gives every offset
   const int per = (V + nt - 1) / nt;
   const int i0 = min(V, tid * per), i1 = min(V, i0 + per);
   const int top = tid == 0 ? *pl.free_top : 0;
+  auto freed = [&](int c, int ki) { return ki < c ? (c + P - 1) / P - (ki + P - 1) / P : 0; };
   int64_t pages = 0, nodes = 0;
 #pragma unroll 4
   for (int i = i0; i < i1; ++i) {
-    const bool ch = k[i] < t.n_kept[i];
-    const int f = freed[i];
-    pages += ch ? f : 0;
-    nodes += ch ? 1 : 0;
+    const int c = t.n_kept[i], ki = k[i];
+    pages += freed(c, ki);
+    nodes += ki < c ? 1 : 0;
   }
   if (status_failed(status)) {
     if (threadIdx.x == 0) meta[0] = 0;
@@ -139,25 +133,43 @@ __global__ __launch_bounds__(1024) void compact_scan(Tree t, Pool pl, const int3
   block_exclusive_scan_n<2>(v2, ex, tot, sm);
   int64_t run_pages = ex[0], run_nodes = ex[1];
   for (int i = i0; i < i1; ++i) {
-    if (k[i] < t.n_kept[i]) {
+    const int c = t.n_kept[i], ki = k[i];
+    if (ki < c) {
       push_base[i] = (int32_t)run_pages;
       changed[run_nodes] = i;
-      run_pages += freed[i];
+      run_pages += freed(c, ki);
       ++run_nodes;
     }
   }
-  run_pages = tot[0];
-  run_nodes = tot[1];
   if (threadIdx.x == 0) {
-    if (top < 0 || (int64_t)top + run_pages > pl.num_pages) {
+    if (top < 0 || (int64_t)top + tot[0] > pl.num_pages) {
       status_error(status, ARBOR_ECORRUPT);
       meta[0] = 0;
       return;
     }
-    meta[0] = (int32_t)run_nodes;
+    meta[0] = (int32_t)tot[1];
     meta[1] = top;
-    *pl.free_top = top + (int32_t)run_pages;
+    meta[2] = (int32_t)tot[0];
   }
+}
+
+// The plan: workgroups below node_blocks plan four nodes each, the last one
+// scans.
+__global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32_t *__restrict__ k,
+                                                    const int32_t *__restrict__ sel_pos,
+                                                    int32_t *__restrict__ src_slot,
+                                                    int32_t *__restrict__ mv_src,
+                                                    int32_t *__restrict__ mv_dst,
+                                                    int32_t *__restrict__ first_moved,
+                                                    int32_t *__restrict__ push_base,
+                                                    int32_t *__restrict__ changed,
+                                                    int32_t *__restrict__ meta, int node_blocks,
+                                                    int32_t *status) {
+  if ((int)blockIdx.x == node_blocks) {
+    scan_nodes(t, pl, k, push_base, changed, meta, status);
+    return;
+  }
+  plan_node(t, pl, k, sel_pos, src_slot, mv_src, mv_dst, first_moved, status);
 }
 
 // Node bookkeeping of the changed nodes: slot_pos, page table, free stack, c_i.
@@ -172,6 +184,7 @@ __device__ void finalize_nodes(const Tree &t, const Pool &pl, const int32_t *__r
   const int nch = meta[0];
   const int top = meta[1];
   const int P = pl.P;
+  if (wave0 == 0 && lane == 0 && nch > 0) *pl.free_top = top + meta[2];
   for (int w = wave0; w < nch; w += nwaves) {
     const int i = changed[w];
     const int ki = k[i];
@@ -295,18 +308,14 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   int32_t *mv_src = cv.take<int32_t>((size_t)t.N);
   int32_t *mv_dst = cv.take<int32_t>((size_t)t.N);
   int32_t *first_moved = cv.take<int32_t>(t.V);
-  int32_t *freed = cv.take<int32_t>(t.V);
   int32_t *push_base = cv.take<int32_t>(t.V);
   int32_t *changed = cv.take<int32_t>(t.V);
   int32_t *meta = cv.take<int32_t>(4);
   if (!cv.ok) return ARBOR_EWORKSPACE;
-  const dim3 node_grid((t.V + 3) / 4);
-  hipLaunchKernelGGL(compact_plan, node_grid, dim3(256), 0, stream, t, pl, k, sel_pos, src_slot,
-                     mv_src, mv_dst, first_moved, freed, status);
-  // (a workgroup no wider than the tree needs: the scans cost per wave)
-  const int scan_threads = t.V <= 256 ? 256 : 1024;
-  hipLaunchKernelGGL(compact_scan, dim3(1), dim3(scan_threads), 0, stream, t, pl, k, freed,
-                     push_base, changed, meta, status);
+  const int node_blocks = (t.V + 3) / 4;
+  hipLaunchKernelGGL(compact_plan, dim3(node_blocks + 1), dim3(256), 0, stream, t, pl, k, sel_pos,
+                     src_slot, mv_src, mv_dst, first_moved, push_base, changed, meta, node_blocks,
+                     status);
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
   const int fin_blocks = (t.V + 3) / 4;
