@@ -485,7 +485,9 @@ constexpr int sub_pages_per_fetch() {
 // a time (the last fragment of a unit re-reads its last sub-page in the
 // unused places, which the cache serves); other waves of the SIMD attend
 // while one waits for its fragment.
-template <class T, int D, int NB>
+// KZ: the call credits (some slice layers keep their logits); a plain call
+// compiles without that path and its registers.
+template <class T, int D, int NB, bool KZ>
 __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase) {
   using O = Op<T>;
   constexpr int GSP = sub_pages_per_fetch<T, D, NB>();
@@ -549,7 +551,7 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   }
   // a credited slice layer keeps its logits: [slice][kv head][unit row][slot]
   float *zrow = nullptr;
-  for (int z = 0; z < a.zS; ++z)
+  for (int z = 0; KZ && z < a.zS; ++z)
     if (a.zlr[z] == lr) {
       zrow = a.part + a.meta[4] +
              (((int64_t)z * pl.Hkv + g) * a.meta[3] + a.item_rowbase[item]) * CHUNK;
@@ -565,30 +567,33 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) o[nb][cc] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  for (int gi = 0; gi < n_grp; ++gi) {
-    float zs[GSP][NB][4];
-    attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, zrow != nullptr, zs);
-    // the next fragment's loads go out before this one's logits are stored:
-    // a wave's loads and stores share one counter, so a wait for loads
-    // issued after the stores would wait for the stores as well
-    if (gi + 1 < n_grp)
-      cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, (gi + 1) * GSP, pl.P);
-    if (zrow) {
-      // lane (rr, g4) holds keys 4 g4 .. 4 g4 + 3 of each sub-page for row rr:
-      // zrow + r * CHUNK + 16 sub + key for query row r < R of the unit
+  // the logits of fragment gi are stored after fragment gi + 1's loads are
+  // issued: a wave's loads and stores share one counter, so a wait for loads
+  // issued after the stores would wait for the stores as well
+  float zs[GSP][NB][4];
+  auto store_z = [&](int gz) __attribute__((always_inline)) {
+    // lane (rr, g4) holds keys 4 g4 .. 4 g4 + 3 of each sub-page for row rr:
+    // zrow + r * CHUNK + 16 sub + key for query row r < R of the unit
 #pragma unroll
-      for (int sp = 0; sp < GSP; ++sp) {
-        if (gi * GSP + sp >= n_sub) continue;
+    for (int sp = 0; sp < GSP; ++sp) {
+      if (gz * GSP + sp >= n_sub) continue;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int r = rbase + nb * 16 + rr;
-          if (r < R)
-            *reinterpret_cast<float4 *>(zrow + (int64_t)r * CHUNK + 16 * (gi * GSP + sp) + 4 * g4) =
-                make_float4(zs[sp][nb][0], zs[sp][nb][1], zs[sp][nb][2], zs[sp][nb][3]);
-        }
+      for (int nb = 0; nb < NB; ++nb) {
+        const int r = rbase + nb * 16 + rr;
+        if (r < R)
+          *reinterpret_cast<float4 *>(zrow + (int64_t)r * CHUNK + 16 * (gz * GSP + sp) + 4 * g4) =
+              make_float4(zs[sp][nb][0], zs[sp][nb][1], zs[sp][nb][2], zs[sp][nb][3]);
       }
     }
+  };
+  for (int gi = 0; gi < n_grp; ++gi) {
+    if (gi > 0) {
+      cur = fetch_kv<T, D, GSP>(ua, pg, s_begin, s_end, n_sub, gi * GSP, pl.P);
+      if (KZ && zrow) store_z(gi - 1);
+    }
+    attend<T, D, NB, GSP>(cur, q, a.sl2, g4, m_run, l_run, o, KZ && zrow != nullptr, zs);
   }
+  if (KZ && zrow && n_grp > 0) store_z(n_grp - 1);
   // partial rows [m, l, o(0..D-1)] of this unit
   const int64_t stride = D + 2;
   const int64_t slab = ((int64_t)lr * pl.Hkv + g) * a.meta[3];
@@ -613,7 +618,7 @@ __device__ void decode_unit(const DecArgs &a, int item, int lr, int g, int rbase
   }
 }
 
-template <class T, int D, int NB>
+template <class T, int D, int NB, bool KZ>
 __global__ __launch_bounds__(256) void decode_attn(DecArgs a, int cls) {
   if (status_failed(a.status)) return;
   const int n_items = a.meta[cls];
@@ -627,7 +632,7 @@ __global__ __launch_bounds__(256) void decode_attn(DecArgs a, int cls) {
     const int lr = rem / a.pl.Hkv;
     const int g = rem % a.pl.Hkv;
     const int R = a.node_nl[a.item_node[item]] * a.pl.G;
-    for (int rbase = 0; rbase < R; rbase += 16 * NB) decode_unit<T, D, NB>(a, item, lr, g, rbase);
+    for (int rbase = 0; rbase < R; rbase += 16 * NB) decode_unit<T, D, NB, KZ>(a, item, lr, g, rbase);
   }
 }
 
@@ -976,11 +981,19 @@ void launch_decode_kernels(const arbor_geom_t *geom, const DecArgs &a, void *out
   // can occur are launched
   const int max_rows = a.n_leaves * a.pl.G;
   timing_begin(geom, ARBOR_KERNEL_DECODE_ATTN, stream);
-  hipLaunchKernelGGL((decode_attn<T, D, 1>), dim3(grid), dim3(256), 0, stream, a, 0);
-  if (max_rows > 16)
-    hipLaunchKernelGGL((decode_attn<T, D, 2>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
-  if (max_rows > 32)
-    hipLaunchKernelGGL((decode_attn<T, D, 4>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
+  if (cr) {
+    hipLaunchKernelGGL((decode_attn<T, D, 1, true>), dim3(grid), dim3(256), 0, stream, a, 0);
+    if (max_rows > 16)
+      hipLaunchKernelGGL((decode_attn<T, D, 2, true>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
+    if (max_rows > 32)
+      hipLaunchKernelGGL((decode_attn<T, D, 4, true>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
+  } else {
+    hipLaunchKernelGGL((decode_attn<T, D, 1, false>), dim3(grid), dim3(256), 0, stream, a, 0);
+    if (max_rows > 16)
+      hipLaunchKernelGGL((decode_attn<T, D, 2, false>), dim3(grid / 2), dim3(256), 0, stream, a, 1);
+    if (max_rows > 32)
+      hipLaunchKernelGGL((decode_attn<T, D, 4, false>), dim3(grid / 4), dim3(256), 0, stream, a, 2);
+  }
   timing_end(geom, ARBOR_KERNEL_DECODE_ATTN, stream);
   const int64_t mw = (int64_t)a.n_leaves * a.Lr * a.pl.Hkv * a.pl.G;
   if (!cr) {
