@@ -160,7 +160,6 @@ def summarize_traffic(fetch_csv: str, write_csv: str, title: str, command: str,
 # the kernel of each rated stage whose launches are timed on their own
 # (a per-call timing request, arbor_timing_t) and rated against its roofline
 STAGE_KERNEL = {"score": (L.KERNEL_SCORE_ATTN, "score_attn", "score.hip"),
-                "select": (L.KERNEL_SELECT, "select_kernel", "select.hip"),
                 "compact": (L.KERNEL_COMPACT_MOVE, "compact_move", "compact.hip"),
                 "decode": (L.KERNEL_DECODE_ATTN, "decode_attn", "decode.hip")}
 
@@ -256,9 +255,10 @@ class Event:
         self.status.zero_()
 
     def run(self, active, marks=None, timings=None, decode=True):
-        """score -> allocate -> select -> compact -> decode; `marks` records events
-        between the entry points, `timings` ({stage: L.Timing}) asks each call to
-        time its rated kernel; decode=False stops after the compaction."""
+        """score -> allocate -> select + compact (arbor_select_compact) -> decode;
+        `marks` records events between the entry points, `timings` ({stage:
+        L.Timing}) asks each call to time its rated kernel; decode=False stops
+        after the compaction."""
         tm = timings or {}
         kv, st = self.kv, self.st
         ev = (lambda: marks.append(torch.cuda.Event(enable_timing=True))) if marks is not None else None
@@ -276,11 +276,8 @@ class Event:
         self.check(L.arbor_allocate(kv, active, st["budget"], self.s, self.params, self.k,
                                     self.delta, self.on_path, self.status, self.ws))
         mark()
-        self.check(L.arbor_select(kv, self.A, self.k, self.params, self.sel, self.status,
-                                  timing=tm.get("select")))
-        mark()
-        self.check(L.arbor_compact(kv, self.k, self.sel, self.status, self.ws,
-                                   timing=tm.get("compact")))
+        self.check(L.arbor_select_compact(kv, self.A, self.k, self.params, self.sel,
+                                          self.status, self.ws, timing=tm.get("compact")))
         mark()
         if not decode:
             return
@@ -545,7 +542,7 @@ def measure_event(cfg, steps, warmup, use_graph=True, copy_gbs=None, rehydrate_l
         e1.record()
         kevents[name] = (e0, e1)
     ktiming = {name: L.timing(STAGE_KERNEL[name][0], *kevents[name]) for name in STAGE_KERNEL}
-    stages = ["score", "allocate", "select", "compact", "decode"]
+    stages = ["score", "allocate", "select+compact", "decode"]
     per_stage = {x: [] for x in stages}
     per_kernel = {x: [] for x in STAGE_KERNEL}
     for _ in range(steps):
@@ -575,11 +572,9 @@ def measure_event(cfg, steps, warmup, use_graph=True, copy_gbs=None, rehydrate_l
                     "peak": HBM_PEAK_GBS, "unit": "GB/s"},
         "decode": {"bound": "hbm", "achieved": work["decode_bytes"] / (kmean["decode"] * 1e-3) / 1e9,
                    "peak": HBM_PEAK_GBS, "unit": "GB/s"},
-        "select": {"bound": "hbm", "achieved": work["select_bytes"] / (kmean["select"] * 1e-3) / 1e9,
-                   "peak": HBM_PEAK_GBS, "unit": "GB/s"},
     }
-    entry = {"score": "arbor_score", "compact": "arbor_compact",
-             "decode": "arbor_tree_decode_attn", "select": "arbor_select"}
+    entry = {"score": "arbor_score", "compact": "arbor_select_compact",
+             "decode": "arbor_tree_decode_attn"}
     for st_name, r in rates.items():
         _, kname, ksrc = STAGE_KERNEL[st_name]
         r["frac"] = r["achieved"] / r["peak"]
@@ -588,14 +583,14 @@ def measure_event(cfg, steps, warmup, use_graph=True, copy_gbs=None, rehydrate_l
         r["kernel"] = kname
         r["entry_point"] = entry[st_name]
         r["ms_per_launch"] = kmean[st_name]
-        r["stage_ms"] = mean[st_name]
+        r["stage_ms"] = mean["select+compact" if st_name == "compact" else st_name]
         tr = stored_kernel_traffic(cfg.name, kname, ksrc)
         r["traffic"] = None if tr is None else tr["read_bytes"] + tr["write_bytes"]
         if tr is not None:
             r["traffic_kernels"] = tr["kernels"]
-    # the entry points rated on their whole time: select + compact together
-    # (the eviction and compaction of the event), the decode entry point
-    sc_ms = mean["select"] + mean["compact"]
+    # the entry points rated on their whole time: select + compact (one entry
+    # point: the eviction and compaction of the event), the decode entry point
+    sc_ms = mean["select+compact"]
     entry_rates = {
         "select+compact": {"ms": sc_ms, "bytes": work["compact_bytes"] + work["select_bytes"],
                            "achieved": (work["compact_bytes"] + work["select_bytes"])

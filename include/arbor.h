@@ -11,6 +11,7 @@
  *                           Execution; Alg. 1 Evict).
  *   arbor_compact           token-extractive, order-preserving compaction of the
  *                           retained K/V inside a paged tree KV pool (Sec. 4).
+ *   arbor_select_compact    the two above on the same k, in fewer launches.
  *   arbor_rehydrate         lazy rehydration of Path* blocks (Sec. 4; Alg. 2).
  *   arbor_tree_decode_attn  decode attention of each active leaf over its
  *                           ancestor chain (Sec. 1 and Sec. 3: the next step
@@ -289,6 +290,22 @@ int arbor_select(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
 int arbor_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
                   const int32_t *k, const int32_t *sel_pos, int32_t *status, void *workspace,
                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * arbor_select_compact -- arbor_select followed by arbor_compact on the same
+ * k, in two launches instead of three to four (Sec. 4 Execution; Alg. 1
+ * Evict): the wave that selects a block's retained set also writes its
+ * compaction plan, as it knows the slot of every kept position, and the
+ * free-stack scan runs in the same launch.  Writes exactly what
+ * arbor_select then arbor_compact write (sel_pos included), from the same
+ * arguments; the workspace is sized as for arbor_compact.
+ * Errors: those of arbor_select (ENONFINITE, EINVAL) and ECORRUPT (free stack
+ * would overflow); every error leaves the tree and pool unchanged.
+ */
+int arbor_select_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                         const float *A, const int32_t *k, const arbor_params_t *params,
+                         int32_t *sel_pos, int32_t *status, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
 
 /*
  * arbor_compact_noalloc -- arbor_compact for callers that cannot allocate

@@ -111,6 +111,7 @@ def load() -> ctypes.CDLL:
             "arbor_select": (ctypes.c_int, [G, T, Pl, vp, vp, Pa, vp, vp, vp]),
             "arbor_compact": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, sz, vp]),
             "arbor_compact_noalloc": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp]),
+            "arbor_select_compact": (ctypes.c_int, [G, T, Pl, vp, vp, Pa, vp, vp, vp, sz, vp]),
             "arbor_rehydrate": (ctypes.c_int, [G, T, Pl, vp, vp, vp, vp, vp, sz, vp]),
             "arbor_tree_decode_attn": (ctypes.c_int, [G, T, Pl, vp, i32, i32, i32, vp, vp, i32,
                                                       vp, ctypes.c_float, vp, vp, sz, vp]),
@@ -133,7 +134,8 @@ def load() -> ctypes.CDLL:
 
 def exported_symbols():
     return ["arbor_workspace_size", "arbor_strerror", "arbor_score", "arbor_allocate",
-            "arbor_select", "arbor_compact", "arbor_compact_noalloc", "arbor_rehydrate", "arbor_tree_decode_attn",
+            "arbor_select", "arbor_compact", "arbor_compact_noalloc", "arbor_select_compact",
+            "arbor_rehydrate", "arbor_tree_decode_attn",
             "arbor_tree_decode_attn_scored", "arbor_uncertainty",
             "arbor_uncertainty_workspace_size", "arbor_walk"]
 
@@ -296,6 +298,18 @@ def arbor_compact(kv: KVState, k, sel_pos, status, workspace, stream=None, timin
                                 _dev(sel_pos, "sel_pos"), _dev(status, "status"),
                                 _dev(workspace, "workspace"), int(workspace.numel()),
                                 _stream(stream))
+
+
+def arbor_select_compact(kv: KVState, A, k, params: dict, sel_pos, status, workspace,
+                         stream=None, timing=None) -> int:
+    """arbor_select then arbor_compact on the same k, as one entry point."""
+    g, t, p = kv.geom(timing), kv.tree(), kv.pool()
+    pa = params_struct(params)
+    return load().arbor_select_compact(ctypes.byref(g), ctypes.byref(t), ctypes.byref(p),
+                                       _dev(A, "A"), _dev(k, "k"), ctypes.byref(pa),
+                                       _dev(sel_pos, "sel_pos"), _dev(status, "status"),
+                                       _dev(workspace, "workspace"), int(workspace.numel()),
+                                       _stream(stream))
 
 
 def arbor_compact_noalloc(kv: KVState, k, sel_pos, status, stream=None) -> int:

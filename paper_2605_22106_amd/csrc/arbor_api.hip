@@ -16,6 +16,9 @@ int launch_select(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t
                   const int32_t *, const arbor_params_t *, int32_t *, int32_t *, hipStream_t);
 int launch_compact(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const int32_t *,
                    const int32_t *, int32_t *, void *, size_t, hipStream_t);
+int launch_select_compact(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const float *,
+                          const int32_t *, const arbor_params_t *, int32_t *, int32_t *, void *,
+                          size_t, hipStream_t);
 int launch_rehydrate(const arbor_geom_t *, arbor_tree_t *, arbor_pool_t *, const uint8_t *,
                      const void *, const void *, int32_t *, void *, size_t, hipStream_t);
 int launch_decode(const arbor_geom_t *, const arbor_tree_t *, const arbor_pool_t *,
@@ -159,6 +162,23 @@ int arbor_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *po
   ARBOR_TRY(check_pool(pool));
   if (!status || !k || !sel_pos) return ARBOR_EINVAL;
   return launch_compact(geom, tree, pool, k, sel_pos, status, workspace, workspace_bytes, stream);
+}
+
+int arbor_select_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                         const float *A, const int32_t *k, const arbor_params_t *params,
+                         int32_t *sel_pos, int32_t *status, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  ARBOR_TRY(check_geom(geom));
+  ARBOR_TRY(check_tree(tree));
+  ARBOR_TRY(check_pool(pool));
+  if (!params || !status || !A || !k || !sel_pos) return ARBOR_EINVAL;
+  if (params->l_tail < 0 || params->n_sinks < 0) return ARBOR_EINVAL;
+  if (params->select_mode != ARBOR_SELECT_TAIL_HEAVY &&
+      params->select_mode != ARBOR_SELECT_TAIL_ONLY &&
+      params->select_mode != ARBOR_SELECT_SINKS_TAIL)
+    return ARBOR_EINVAL;
+  return launch_select_compact(geom, tree, pool, A, k, params, sel_pos, status, workspace,
+                               workspace_bytes, stream);
 }
 
 int arbor_rehydrate(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,

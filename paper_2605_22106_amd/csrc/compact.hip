@@ -16,7 +16,10 @@
 //            (slot_pos, page table, free stack and its top, c_i).
 // The plan and the scan only write the workspace (and the status word), so
 // an error either of them finds leaves the state unchanged.
+#include <climits>
+
 #include "arbor_internal.h"
+#include "select_impl.h"
 
 namespace arbor {
 
@@ -172,6 +175,57 @@ __global__ __launch_bounds__(256) void compact_plan(Tree t, Pool pl, const int32
   plan_node(t, pl, k, sel_pos, src_slot, mv_src, mv_dst, first_moved, status);
 }
 
+// The fused select-and-compact entry point: the wave that selects a block's
+// retained set also writes the block's plan, since it knows the source slot
+// of every kept position; the moving rows form a suffix of the destinations
+// (sources ascend and are at or after their destinations).
+struct PlanEmit {
+  int32_t *sel;                  // kept positions of the block
+  int32_t *mv_src, *mv_dst;      // plane rows of the moving slots
+  const int32_t *pt;             // the block's page table
+  int P, Hkv;
+  int &first;                    // this lane's first moving destination
+  __device__ __forceinline__ int row(int s) const { return pt[s / P] * Hkv * P + s % P; }
+  __device__ __forceinline__ void operator()(int dst, int src, int pos) const {
+    sel[dst] = pos;
+    if (src != dst) {
+      mv_src[dst] = row(src);
+      mv_dst[dst] = row(dst);
+      first = min(first, dst);
+    }
+  }
+};
+
+// workgroups below node_blocks select and plan four nodes each, the last one
+// scans
+__global__ __launch_bounds__(256) void select_plan(Tree t, Pool pl, const float *__restrict__ A,
+                                                   const int32_t *__restrict__ k, int l_tail,
+                                                   int n_sinks, int mode,
+                                                   int32_t *__restrict__ sel_pos,
+                                                   int32_t *__restrict__ mv_src,
+                                                   int32_t *__restrict__ mv_dst,
+                                                   int32_t *__restrict__ first_moved,
+                                                   int32_t *__restrict__ push_base,
+                                                   int32_t *__restrict__ changed,
+                                                   int32_t *__restrict__ meta, int node_blocks,
+                                                   int32_t *status) {
+  __shared__ SelectLds lds;
+  if ((int)blockIdx.x == node_blocks) {
+    scan_nodes(t, pl, k, push_base, changed, meta, status);
+    return;
+  }
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= t.V) return;
+  const int64_t tb = t.tok_off[i];
+  int first = INT_MAX;
+  const PlanEmit emit{sel_pos + tb, mv_src + tb, mv_dst + tb, t.page_table + t.page_off[i],
+                      pl.P, pl.Hkv, first};
+  if (select_node(t, pl, A, k, l_tail, n_sinks, mode, i, lds, emit, status)) {
+    first = wave_allreduce(first, [](int x, int y) { return min(x, y); });
+    if (lane_id() == 0) first_moved[i] = first == INT_MAX ? k[i] : first;
+  }
+}
+
 // Node bookkeeping of the changed nodes: slot_pos, page table, free stack, c_i.
 // It touches no K/V bytes and the moves read none of it (they use the plan's
 // tables), so it runs in the same launch as the moves.
@@ -316,6 +370,39 @@ int launch_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *p
   hipLaunchKernelGGL(compact_plan, dim3(node_blocks + 1), dim3(256), 0, stream, t, pl, k, sel_pos,
                      src_slot, mv_src, mv_dst, first_moved, push_base, changed, meta, node_blocks,
                      status);
+  const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
+  const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
+  const int fin_blocks = (t.V + 3) / 4;
+  timing_begin(geom, ARBOR_KERNEL_COMPACT_MOVE, stream);
+  hipLaunchKernelGGL(compact_move, dim3(move_blocks + fin_blocks), dim3(256), 0, stream, t, pl, k,
+                     mv_src, mv_dst, first_moved, sel_pos, push_base, changed, meta, move_blocks,
+                     status);
+  timing_end(geom, ARBOR_KERNEL_COMPACT_MOVE, stream);
+  return hip_ok(hipGetLastError());
+}
+
+int launch_select_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_pool_t *pool,
+                          const float *A, const int32_t *k, const arbor_params_t *params,
+                          int32_t *sel_pos, int32_t *status, void *workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  Tree t = make_tree(tree);
+  Pool pl = make_pool(geom, pool);
+  if (t.V <= 0) return ARBOR_OK;
+  Carve cv(workspace, workspace_bytes);
+  if ((int64_t)pl.num_pages * pl.Hkv * pl.P >= ((int64_t)1 << 31)) return ARBOR_EUNSUPPORTED;
+  int32_t *mv_src = cv.take<int32_t>((size_t)t.N);
+  int32_t *mv_dst = cv.take<int32_t>((size_t)t.N);
+  int32_t *first_moved = cv.take<int32_t>(t.V);
+  int32_t *push_base = cv.take<int32_t>(t.V);
+  int32_t *changed = cv.take<int32_t>(t.V);
+  int32_t *meta = cv.take<int32_t>(4);
+  if (!cv.ok) return ARBOR_EWORKSPACE;
+  const int node_blocks = (t.V + 3) / 4;
+  timing_begin(geom, ARBOR_KERNEL_SELECT, stream);
+  hipLaunchKernelGGL(select_plan, dim3(node_blocks + 1), dim3(256), 0, stream, t, pl, A, k,
+                     params->l_tail, params->n_sinks, params->select_mode, sel_pos, mv_src, mv_dst,
+                     first_moved, push_base, changed, meta, node_blocks, status);
+  timing_end(geom, ARBOR_KERNEL_SELECT, stream);
   const int64_t planes = (int64_t)t.V * pl.L * pl.Hkv;
   const int move_blocks = (int)((planes + 3) / 4 < 8192 ? (planes + 3) / 4 : 8192);
   const int fin_blocks = (t.V + 3) / 4;

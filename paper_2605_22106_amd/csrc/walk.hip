@@ -59,9 +59,8 @@ extern "C" int arbor_walk(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_po
                            static_cast<const char *>(w->q_win) + e * q_stride, w->window,
                            w->slice_layers, w->n_slice, w->v_in, w->u_in, w->A, w->rows_seen,
                            w->a_out, w->s, params, status, workspace, workspace_bytes, stream));
-    WALK_TRY(arbor_select(geom, tree, pool, w->A, w->k, params, w->sel_pos, status, stream));
-    WALK_TRY(arbor_compact(geom, tree, pool, w->k, w->sel_pos, status, workspace,
-                           workspace_bytes, stream));
+    WALK_TRY(arbor_select_compact(geom, tree, pool, w->A, w->k, params, w->sel_pos, status,
+                                  workspace, workspace_bytes, stream));
     if (w->pressure_margin > 0) {
       // RaisePressureEvent: fires on the device when M >= B - delta
       WALK_TRY(launch_allocate(tree, leaf, 1, b_p, w->s, params, w->k, w->delta, w->on_path,
@@ -69,9 +68,8 @@ extern "C" int arbor_walk(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_po
       if (row)
         WALK_TRY(launch_walk_stats(tree, w->k, w->on_path, b_p, 0, params->lazy_rehydration,
                                    row, status, stream));
-      WALK_TRY(arbor_select(geom, tree, pool, w->A, w->k, params, w->sel_pos, status, stream));
-      WALK_TRY(arbor_compact(geom, tree, pool, w->k, w->sel_pos, status, workspace,
-                             workspace_bytes, stream));
+      WALK_TRY(arbor_select_compact(geom, tree, pool, w->A, w->k, params, w->sel_pos, status,
+                                    workspace, workspace_bytes, stream));
     }
   }
   return ARBOR_OK;
