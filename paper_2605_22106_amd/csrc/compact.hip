@@ -196,9 +196,12 @@ struct PlanEmit {
   }
 };
 
-// workgroups below node_blocks select and plan four nodes each, the last one
-// scans
-__global__ __launch_bounds__(256) void select_plan(Tree t, Pool pl, const float *__restrict__ A,
+// workgroups below node_blocks select and plan kSelWaves nodes each (one per
+// wave; their other waves exit at once, so the selections spread over as many
+// CUs as with small workgroups), the last one scans with all kScanWaves waves
+constexpr int kSelWaves = 4;
+constexpr int kScanWaves = 16;
+__global__ __launch_bounds__(kScanWaves * kWave) void select_plan(Tree t, Pool pl, const float *__restrict__ A,
                                                    const int32_t *__restrict__ k, int l_tail,
                                                    int n_sinks, int mode,
                                                    int32_t *__restrict__ sel_pos,
@@ -209,12 +212,13 @@ __global__ __launch_bounds__(256) void select_plan(Tree t, Pool pl, const float 
                                                    int32_t *__restrict__ changed,
                                                    int32_t *__restrict__ meta, int node_blocks,
                                                    int32_t *status) {
-  __shared__ SelectLds lds;
+  __shared__ SelectLds<kSelWaves> lds;
   if ((int)blockIdx.x == node_blocks) {
     scan_nodes(t, pl, k, push_base, changed, meta, status);
     return;
   }
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if ((int)(threadIdx.x >> 6) >= kSelWaves) return;
+  const int i = blockIdx.x * kSelWaves + (threadIdx.x >> 6);
   if (i >= t.V) return;
   const int64_t tb = t.tok_off[i];
   int first = INT_MAX;
@@ -397,9 +401,10 @@ int launch_select_compact(const arbor_geom_t *geom, arbor_tree_t *tree, arbor_po
   int32_t *changed = cv.take<int32_t>(t.V);
   int32_t *meta = cv.take<int32_t>(4);
   if (!cv.ok) return ARBOR_EWORKSPACE;
-  const int node_blocks = (t.V + 3) / 4;
+  const int node_blocks = (t.V + kSelWaves - 1) / kSelWaves;
   timing_begin(geom, ARBOR_KERNEL_SELECT, stream);
-  hipLaunchKernelGGL(select_plan, dim3(node_blocks + 1), dim3(256), 0, stream, t, pl, A, k,
+  hipLaunchKernelGGL(select_plan, dim3(node_blocks + 1), dim3(kScanWaves * kWave), 0, stream, t,
+                     pl, A, k,
                      params->l_tail, params->n_sinks, params->select_mode, sel_pos, mv_src, mv_dst,
                      first_moved, push_base, changed, meta, node_blocks, status);
   timing_end(geom, ARBOR_KERNEL_SELECT, stream);

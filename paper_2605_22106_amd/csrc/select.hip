@@ -18,7 +18,7 @@ __global__ __launch_bounds__(256) void select_kernel(Tree t, Pool pl, const floa
                                                      int n_sinks, int mode,
                                                      int32_t *__restrict__ sel_pos,
                                                      int32_t *status) {
-  __shared__ SelectLds lds;
+  __shared__ SelectLds<4> lds;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (i >= t.V) return;
   const PosEmit emit{sel_pos + t.tok_off[i]};

@@ -243,18 +243,20 @@ __device__ void select_streamed(const NodeView &nv, const float *__restrict__ A,
   for (int s = lane; s < c - rg.hi; s += kWave) out(rg.lo + m + s, rg.hi + s, nv.pos(rg.hi + s));
 }
 
-// Per-wave LDS of the selection: a histogram and a staged row of A.
+// Per-wave LDS of the selection for workgroups of W waves: a histogram and a
+// staged row of A.
+template <int W>
 struct SelectLds {
-  unsigned hist[4][256];
-  float a[4][kStageA];
+  unsigned hist[W][256];
+  float a[W][kStageA];
 };
 
 // The retained set of node i (one wave); returns false when the node keeps
 // every resident slot (or on an error), having emitted nothing.
-template <class Emit>
+template <int W, class Emit>
 __device__ bool select_node(const Tree &t, const Pool &pl, const float *__restrict__ A,
                             const int32_t *__restrict__ k, int l_tail, int n_sinks, int mode, int i,
-                            SelectLds &lds, const Emit &emit, int32_t *status) {
+                            SelectLds<W> &lds, const Emit &emit, int32_t *status) {
   const int lane = lane_id();
   const int w = threadIdx.x >> 6;
   const Hist hist{lds.hist[w]};
