@@ -71,9 +71,15 @@ def short_kernel_name(name: str) -> str:
         rest = name[start + k:]
         if rest.startswith("I"):
             args = []
-            for tok in re.finditer(r"Li(\d+)E|DF16b|(?<=[IE])f(?=[LE])", rest[:rest.find("EEv") + 1]):
+            for tok in re.finditer(r"Li(\d+)E|Lb([01])E|DF16b|(?<=[IE])f(?=[LE])",
+                                   rest[:rest.find("EEv") + 1]):
                 t = tok.group(0)
-                args.append(tok.group(1) if tok.group(1) else ("bf16" if t == "DF16b" else "f32"))
+                if tok.group(1):
+                    args.append(tok.group(1))
+                elif tok.group(2):
+                    args.append("true" if tok.group(2) == "1" else "false")
+                else:
+                    args.append("bf16" if t == "DF16b" else "f32")
             return f"{ident}<{','.join(args)}>"
         return ident
     m = re.search(r"arbor::\(anonymous namespace\)::(?:void )?([A-Za-z_0-9]+(?:<[^>(]*>)?)\(", name)
@@ -171,7 +177,10 @@ def stored_kernel_traffic(workload: str, prefix: str, src: str):
     if not os.path.exists(path):
         return None
     rows = [json.loads(line) for line in open(path) if line.startswith("{")]
-    rows = [r for r in rows if r.get("kernel", "").startswith(prefix)]
+    # (the attention of a scored decode keeps its logits: a kernel of its own,
+    # never launched by the plain decode that the stage times)
+    rows = [r for r in rows if r.get("kernel", "").startswith(prefix)
+            and not r["kernel"].endswith(",true>")]
     if not rows or any(r["source_sha256"] != source_sha256(src) for r in rows):
         return None
     return {"read_bytes": sum(r["hbm_read_bytes"] for r in rows),
