@@ -646,6 +646,7 @@ __device__ __forceinline__ void merge_rows(const DecArgs &a, void *out, int out_
                                            float *lse_out, int blk, int nblk) {
   constexpr int EPL = D / 64;  // output columns per lane
   constexpr int U = 4;         // partial rows loaded together
+  constexpr int kPreO = 8;     // partial rows read ahead of the max
   const Pool &pl = a.pl;
   const int lane = lane_id();
   const int G = pl.G;
@@ -673,6 +674,15 @@ __device__ __forceinline__ void merge_rows(const DecArgs &a, void *out, int out_
       off0 = (int64_t)lp[lane] * stride;
       m0 = base[off0];
       l0 = base[off0 + 1];
+    }
+    // the output rows of the first kPreO partials are read together with
+    // their (max, sum), before the max is known
+    float xv0[kPreO][EPL];
+#pragma unroll
+    for (int u = 0; u < kPreO; ++u) {
+      const int64_t oj = lane_value(off0, u < np ? u : 0);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) xv0[u][e] = u < np ? base[oj + 2 + 64 * e + lane] : 0.f;
     }
     float M = m0;
     for (int k0 = kWave; k0 < np; k0 += kWave) {
@@ -702,7 +712,17 @@ __device__ __forceinline__ void merge_rows(const DecArgs &a, void *out, int out_
         }
         L += wave_sum(lk * f);
         const int nk = min(kWave, np - k0);
-        for (int j0 = 0; j0 < nk; j0 += U) {
+        int jstart = 0;
+        if (k0 == 0) {
+#pragma unroll
+          for (int u = 0; u < kPreO; ++u) {
+            const float fu = u < nk ? lane_value(f, u) : 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) ov[e] += (fu > 0.f ? xv0[u][e] * fu : 0.f);
+          }
+          jstart = kPreO;
+        }
+        for (int j0 = jstart; j0 < nk; j0 += U) {
           float xv[U][EPL], fj[U];
 #pragma unroll
           for (int u = 0; u < U; ++u) {
