@@ -1138,10 +1138,14 @@ int launch_decode(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbo
   a.max_parts = max_parts;
   a.part = reinterpret_cast<float *>(cv.rest());
   a.part_cap = (int64_t)(cv.remaining() / 4);
+  // one thread per node, and one wave per leaf for the per-leaf scans: a
+  // small tree takes a smaller workgroup, whose barriers are cheaper
+  const int64_t plan_need = std::max<int64_t>(t.V, (int64_t)n_leaves * MAXD);
+  const int plan_threads = (int)std::min<int64_t>(1024, (plan_need + kWave - 1) / kWave * kWave);
 #define ARBOR_PLAN_LAUNCH(S, F)                                                                \
-  hipLaunchKernelGGL((decode_plan<S, F>), dim3(1), dim3(1024), 0, stream, a, meta, cls_items,     \
-                     item_node, item_chunk, item_rowbase, node_nl, node_leaf_off, leaf_list,      \
-                     node_item0, node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part)
+  hipLaunchKernelGGL((decode_plan<S, F>), dim3(1), dim3(plan_threads), 0, stream, a, meta,       \
+                     cls_items, item_node, item_chunk, item_rowbase, node_nl, node_leaf_off,      \
+                     leaf_list, node_item0, node_rowbase, lanc, ldepth, lrank, leaf_np, leaf_part)
   const bool small = t.V <= kPlanLds, few = n_leaves <= kPlanLeaves;
   if (small && few) ARBOR_PLAN_LAUNCH(true, true);
   else if (small) ARBOR_PLAN_LAUNCH(true, false);

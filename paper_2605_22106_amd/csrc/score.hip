@@ -12,9 +12,10 @@
 //           (one thread per observer) for the partial / table offsets (prefix
 //           sums over observers) and lists the blocks that receive credit;
 //   tables  one workgroup per observer: its 16-slot sub-page table;
-//   attn    per (observer, slice layer, kv head, group of up to 64 rows),
-//           two passes over the same (row, key) pairs as MFMA tiles of 16
-//           keys x 16 rows, the four waves taking alternate 16-key sub-pages:
+//   attn    per (observer, slice layer, kv head, 1, 2 or 4 groups of up to
+//           64 rows), two passes over the same (row, key) pairs as MFMA tiles
+//           of 16 keys x 16 rows, one wave per (row group, key split), the
+//           waves of a row group taking alternate 16-key sub-pages:
 //           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
 //           sums of exp2(z - lse) -> one partial per credited context key;
 //   fold    per observer: sum its (slice layer, kv head, row group) partials;
@@ -122,21 +123,6 @@ __device__ __forceinline__ SubPage sub_page(const Tree &t, const Pool &pl, const
 }
 
 // ---------------------------------------------------------------------------
-// Streaming kernel.  One workgroup of four waves per (observer, slice layer,
-// kv head, group of up to 128 query rows).  The waves split the chain's 16-key
-// sub-pages round-robin (wave w takes sub-pages w, w + 4, ...), and every wave
-// holds the Q of all the group's rows in registers.  So each key tile is read
-// from LDS by one wave only, and a key's sum over the rows never leaves its
-// wave.
-//   pass 0  C = K Q^T: each lane keeps a running max / sum of one row over its
-//           keys; lanes, then waves, are merged into the row's log2-sum-exp;
-//   pass 1  C = Q K^T: per key, the sum over all rows of exp2(z - lse), stored
-//           as the row group's partial for that key.
-// Keys reach the wave's own ring of LDS buffers by direct global->LDS loads in
-// which each 16-lane group reads one whole 256-byte key row (coalesced).  The
-// 16-byte pieces of key r are stored XOR-permuted by r, so the sixteen lanes of
-// an MFMA operand read (keys 0..15, one piece each) hit distinct banks.  A wave
-// waits only for its own loads; neither pass has a barrier.
 template <class T, int D>
 struct KTile {
   static constexpr int R = D * (int)sizeof(T) / 16;   // 16-byte pieces of a key row
@@ -150,21 +136,24 @@ struct KTile {
 };
 
 typedef __attribute__((address_space(3))) void *LdsPtr;
-// NDMA direct loads (global -> LDS) of one BYTES-long tile at src: lane L's 16
-// bytes of load c land at lds + 1024 c + 16 L.  A buffer resource over the
+// This wave's part of the direct loads (global -> LDS) of one BYTES-long tile
+// at src: its loads m < n are the tile's loads c = c0 + step m, and lane L's
+// 16 bytes of load c land at lds + 1024 c + 16 L.  A buffer resource over the
 // tile (scalar registers) leaves each lane a 32-bit offset, and bounds every
 // access to the tile.
 // (host-device so the kernel's host-device lambdas can call it; the host
 // pass of the compiler never runs it)
-template <int NDMA, int BYTES>
-__host__ __device__ __forceinline__ void dma_tile(const char *src, char *lds,
-                                                  const int (&off)[NDMA]) {
+template <int NW, int BYTES>
+__host__ __device__ __forceinline__ void dma_part(const char *src, char *lds, int c0, int step,
+                                                  int n, const int (&off)[NW]) {
 #if defined(__HIP_DEVICE_COMPILE__)
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(src), 0, BYTES, 0x00020000);
 #pragma unroll
-  for (int c = 0; c < NDMA; ++c)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LdsPtr)(lds + 1024 * c), 16, off[c], 0, 0, 0);
+  for (int m = 0; m < NW; ++m)
+    if (m < n)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (LdsPtr)(lds + 1024 * (c0 + step * m)), 16,
+                                               off[m], 0, 0, 0);
 #endif
 }
 template <class T, int D>
@@ -223,27 +212,50 @@ __device__ __forceinline__ float piece_op<float>(const uint4 &p, int c) {
   return __uint_as_float(c == 0 ? p.x : (c == 1 ? p.y : (c == 2 ? p.z : p.w)));
 }
 
-template <class T, int D, int NRB>
+// Streaming kernel.  One workgroup of four waves per (observer, slice layer,
+// kv head, RGW groups of up to 16 NRB query rows), RGW = 1, 2 or 4.  Wave w
+// is (row group w % RGW, key split w / RGW): the 4 / RGW key splits take the
+// chain's 16-key sub-pages round-robin (split x takes sub-pages x, x + 4 /
+// RGW, ...), and every wave holds the Q of its row group in registers.  The
+// RGW waves of a key split work on the same sub-page at each step: each loads
+// a part of it into their shared ring of LDS slots and they meet at a barrier
+// before reading it, so a key tile moves from L2 to LDS once for RGW row
+// groups.  A key's sum over a row group never leaves its wave.
+//   pass 0  C = K Q^T: each lane keeps a running max / sum of one row over its
+//           keys; lanes, then the key splits, are merged into the row's
+//           log2-sum-exp;
+//   pass 1  C = Q K^T: per key, the sum over the group's rows of
+//           exp2(z - lse), stored as the row group's partial for that key.
+// Keys reach the ring by direct global->LDS loads in which each 16-lane group
+// reads one whole 256-byte key row (coalesced).  The 16-byte pieces of key r
+// are stored XOR-permuted by r, so the sixteen lanes of an MFMA operand read
+// (keys 0..15, one piece each) hit distinct banks.  A wave waits only for its
+// own loads; the barrier (RGW > 1 only) does not wait for memory.
+template <class T, int D, int NRB, int RGW>
 __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   using O = Op<T>;
   using KT = KTile<T, D>;
   using Buf = KBuf<T, D>;
   constexpr int R = KT::R, RQ = KT::RQ, KS = KT::KS, SPP = KT::SPP, ND = KT::ND;
-  constexpr int ROWS = 16 * NRB;            // rows of the workgroup
+  constexpr int ROWS = 16 * NRB;            // rows of one wave (a row group)
+  constexpr int KSW = 4 / RGW;              // key splits of the workgroup
+  constexpr int NDW = (ND + RGW - 1) / RGW; // direct loads of a wave per tile (at most)
+  static_assert(RGW == 1 || RGW == 2 || RGW == 4, "row groups per workgroup");
   constexpr float kFloor = -1e30f;
   // one ring slot per object, so the compiler can tell a buffer being filled
-  // from the one being read
-  __shared__ Buf b0[4], b1[4], b2[4];
-  __shared__ float2 s_ml[4][ROWS];
-  __shared__ __attribute__((aligned(16))) float s_lse[ROWS];
+  // from the one being read; slot [x] belongs to key split x
+  __shared__ Buf b0[KSW], b1[KSW], b2[KSW];
+  __shared__ float2 s_ml[KSW][RGW * ROWS];
+  __shared__ __attribute__((aligned(16))) float s_lse[RGW * ROWS];
   __shared__ int s_bad;
   // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
-  // (slice layer, kv head, row group) planes p = x, x + 8, ...; it runs the
+  // (slice layer, kv head, RGW row groups) planes p = x, x + 8, ...; it runs the
   // observers from the deepest (longest chain) down, each over all its
   // planes in turn -- the longest work starts first, so the grid ends on the
   // shortest, and siblings, which share their whole ancestor chain, run
   // together and read those keys from the XCD's L2
-  const int n_planes = a.S * a.pl.Hkv * a.n_rg;
+  const int n_rgp = (a.n_rg + RGW - 1) / RGW;
+  const int n_planes = a.S * a.pl.Hkv * n_rgp;
   const int xcd = (int)blockIdx.x % kXcds;
   const int idx = (int)blockIdx.x / kXcds;
   const int ppx = (n_planes + kXcds - 1) / kXcds;   // planes per XCD
@@ -255,8 +267,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   if (s_bad) return;
   const Tree &t = a.t;
   const Pool &pl = a.pl;
-  const int slg = plane / a.n_rg;
-  const int rg = plane % a.n_rg;
+  const int slg = plane / n_rgp;
   const int si = slg / pl.Hkv;
   const int g = slg % pl.Hkv;
   const int layer = a.slice[si];
@@ -266,6 +277,11 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // wave = (key split ksw, row group rgw of the workgroup): the RGW waves of
+  // a key split share its key tiles, each loading a part of every tile
+  const int rgw = wave % RGW;
+  const int ksw = wave / RGW;
+  const int rg = (plane % n_rgp) * RGW + rgw;   // may be >= n_rg: rows all invalid
   const int r = lane & 15;
   const int q = lane >> 4;
   const int G = pl.G;
@@ -297,14 +313,17 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   }
   const int64_t plane_row0 = (int64_t)layer * pl.num_pages * pl.Hkv * pl.P + (int64_t)g * pl.P;
   const char *kplane = static_cast<const char *>(pl.k) + plane_row0 * D * (int64_t)sizeof(T);
-  // byte offset, within a sub-page, of the piece lane L fetches for direct load c
-  int src_off[KT::NDMA];
+  // byte offset, within a sub-page, of the piece lane L fetches for this
+  // wave's direct load m (load c = rgw + RGW m of the tile, if c < ND)
+  int src_off[NDW];
 #pragma unroll
-  for (int c = 0; c < KT::NDMA; ++c) {
+  for (int m = 0; m < NDW; ++m) {
+    const int c = rgw + RGW * m;
     const int sig = 64 * c + lane;           // LDS slot: key sig / R, stored piece sig % R
     const int kr = sig / R;
-    src_off[c] = 16 * (R * kr + ((sig % R) ^ (kr & KT::XM)));
+    src_off[m] = 16 * (R * kr + ((sig % R) ^ (kr & KT::XM)));
   }
+  const int n_dma = ND >= RGW ? NDW : (rgw < ND ? 1 : 0);   // this wave's loads per tile
   // LDS byte offset of piece jp of this lane's quarter of key r
   const int lbase = 16 * (R * r + ((q * RQ) ^ (r & KT::XM)));
 
@@ -313,23 +332,26 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   // one sub-page: a buffer resource over its BYTES (set up in scalar
   // registers), so each lane supplies only a 32-bit offset
   auto issue = [&](Buf &B, int row) __attribute__((always_inline)) {
-    dma_tile<KT::NDMA, KT::BYTES>(kplane + (int64_t)row * (D * (int)sizeof(T)), B.k, src_off);
+    dma_part<NDW, KT::BYTES>(kplane + (int64_t)row * (D * (int)sizeof(T)), B.k, rgw, RGW, n_dma,
+                             src_off);
   };
-  // offsets of this lane's pieces from the start of a ring (slot `wave`
+  // offsets of this lane's pieces from the start of a ring (slot `ksw`
   // included), so a read addresses the ring's fixed LDS base plus a register
   int roff[RQ];
 #pragma unroll
-  for (int jp = 0; jp < RQ; ++jp) roff[jp] = wave * (int)sizeof(Buf) + (lbase ^ (16 * jp));
-  auto read_k = [&](const Buf (&ring)[4], uint4 (&kp)[RQ]) __attribute__((always_inline)) {
+  for (int jp = 0; jp < RQ; ++jp) roff[jp] = ksw * (int)sizeof(Buf) + (lbase ^ (16 * jp));
+  auto read_k = [&](const Buf (&ring)[KSW], uint4 (&kp)[RQ]) __attribute__((always_inline)) {
 #pragma unroll
     for (int jp = 0; jp < RQ; ++jp)
       kp[jp] = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(ring) + roff[jp]);
   };
 
-  // One pass over this wave's sub-pages sp = wave + 4 i (i < cnt) of the
-  // first n_sp of the chain, software-pipelined over a ring of three LDS
-  // slots.  Step i waits for its own sub-page (the next one may stay in
-  // flight), refills the slot of sub-page i - 1 with sub-page i + 2, reads its
+  // One pass over this key split's sub-pages sp = ksw + KSW i of the first
+  // n_sp of the chain, software-pipelined over a ring of three LDS slots.
+  // Step i waits for this wave's part of sub-page i (the next one may stay in
+  // flight) and, when RGW waves share the tiles, meets them at a barrier, so
+  // every part has landed and every wave is done with sub-page i - 1; it
+  // refills the slot of sub-page i - 1 with sub-page i + 2, reads its
   // operands, then runs
   //   fix(prev)  rare, branchy corrections of sub-page i - 1 (key masks);
   //   mm(kp)     the MFMAs of sub-page i, interleaved in one straight-line
@@ -338,17 +360,34 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   //   post(prev) rare corrections after the fact, and stores.
   // The table entries of a window of up to 64 steps sit in registers (lane L
   // holds step L) and are read with readlane, so the loop has no scalar loads.
+  // Every wave of the workgroup runs the same steps (those of key split 0):
+  // a split with one sub-page fewer runs its last step on a copy of its
+  // previous entry with no valid slots (masked in pass 0, not stored in
+  // pass 1), so the barriers pair up.
   struct StepState {
     f32x4 acc[NRB];
     int meta, ctx, slot;
   };
+  // the barrier of the waves sharing a tile (the whole workgroup), without
+  // the wait for all memory operations that a fenced barrier would add
+  auto tile_sync = [&]() __attribute__((always_inline)) {
+    if constexpr (RGW > 1) asm volatile("s_barrier" ::: "memory");
+  };
   auto run = [&](int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post)
                  __attribute__((always_inline)) {
-    const int cnt = n_sp > wave ? (n_sp - wave + 3) / 4 : 0;
+    const int cnt = (n_sp + KSW - 1) / KSW;
     for (int base = 0; base < cnt; base += 64) {
       const int wc = min(64, cnt - base);
       int4 e = make_int4(0, 0, 0, 0);
-      if (lane < wc) e = tabv[wave + 4 * (base + lane)];
+      if (lane < wc) {
+        const int sp = ksw + KSW * (base + lane);
+        if (sp < n_sp) {
+          e = tabv[sp];
+        } else {
+          e = tabv[n_sp - 1];
+          e.w = kMask0;
+        }
+      }
       // a field of window step i (clamped to the last step)
       auto ent = [&](int i, int v) __attribute__((always_inline)) -> int {
         return __builtin_amdgcn_readlane(v, min(i, wc - 1));
@@ -356,17 +395,18 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       auto issue_i = [&](Buf &B, int i) __attribute__((always_inline)) {
         issue(B, ent(i, e.x));
       };
-      issue_i(b0[wave], 0);
-      issue_i(b1[wave], 1);
+      issue_i(b0[ksw], 0);
+      issue_i(b1[ksw], 1);
       StepState prev;
       {
-        wait_vm<ND>();
+        wait_vm<NDW>();
+        tile_sync();
         uint4 kp[RQ];
         read_k(b0, kp);
-        issue_i(b2[wave], 2);
+        issue_i(b2[ksw], 2);
         prev = mm(kp, ent(0, e.y), ent(0, e.w), ent(0, e.z));
       }
-      auto body = [&](const Buf (&ring)[4], int i) __attribute__((always_inline)) {
+      auto body = [&](const Buf (&ring)[KSW], int i) __attribute__((always_inline)) {
         uint4 kp[RQ];
         read_k(ring, kp);
         fix(prev);
@@ -382,30 +422,37 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       };
       int i = 1;
       for (; i + 3 <= wc; i += 3) {
-        wait_vm<ND>();
-        issue_i(b0[wave], i + 2);
+        wait_vm<NDW>();
+        tile_sync();
+        issue_i(b0[ksw], i + 2);
         body(b1, i);
-        wait_vm<ND>();
-        issue_i(b1[wave], i + 3);
+        wait_vm<NDW>();
+        tile_sync();
+        issue_i(b1[ksw], i + 3);
         body(b2, i + 1);
-        wait_vm<ND>();
-        issue_i(b2[wave], i + 4);
+        wait_vm<NDW>();
+        tile_sync();
+        issue_i(b2[ksw], i + 4);
         body(b0, i + 2);
       }
       // the last one or two sub-pages (i in slot 1, i + 1 in slot 2)
       if (i < wc) {
-        wait_vm<ND>();
+        wait_vm<NDW>();
+        tile_sync();
         body(b1, i);
         if (i + 1 < wc) {
           wait_vm<0>();
+          tile_sync();
           body(b2, i + 1);
         }
       }
       fix(prev);
       hot(prev);
       post(prev);
-      // drain (the clamped reloads past the end) before the ring is reused
+      // drain (the clamped reloads past the end), and let every wave finish
+      // reading, before the ring is reused
       wait_vm<0>();
+      tile_sync();
     }
   };
 
@@ -525,30 +572,31 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       mm = mn;
       ll = ln;
     }
-    if (lane < 16) s_ml[wave][rb * 16 + lane] = make_float2(mm, ll);
+    if (lane < 16) s_ml[ksw][rgw * ROWS + rb * 16 + lane] = make_float2(mm, ll);
   }
   __syncthreads();
-  for (int row = tid; row < ROWS; row += blockDim.x) {
+  for (int x = tid; x < RGW * ROWS; x += blockDim.x) {
     float mm = -__builtin_inff();
 #pragma unroll
-    for (int w = 0; w < 4; ++w) mm = fmaxf(mm, s_ml[w][row].x);
+    for (int w = 0; w < KSW; ++w) mm = fmaxf(mm, s_ml[w][x].x);
     float ll = 0.f;
     if (mm > -__builtin_inff()) {
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float2 v = s_ml[w][row];
+      for (int w = 0; w < KSW; ++w) {
+        const float2 v = s_ml[w][x];
         ll += v.x > -__builtin_inff() ? v.y * __builtin_amdgcn_exp2f(v.x - mm) : 0.f;
       }
     }
-    const bool valid = urow(row) >= 0 && ll > 0.f;
-    s_lse[row] = valid ? mm + __log2f(ll) : __builtin_inff();
+    // (urow counts rows from this wave's group: re-base to group x / ROWS)
+    const bool valid = urow(x - rgw * ROWS) >= 0 && ll > 0.f;
+    s_lse[x] = valid ? mm + __log2f(ll) : __builtin_inff();
   }
   __syncthreads();
   // pass-1 layout: this lane holds rows 16 rb + 4 q + e of its key
   float nlse[NRB][4];
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
-    const float4 v = *reinterpret_cast<const float4 *>(&s_lse[rb * 16 + 4 * q]);
+    const float4 v = *reinterpret_cast<const float4 *>(&s_lse[rgw * ROWS + rb * 16 + 4 * q]);
     nlse[rb][0] = -v.x;
     nlse[rb][1] = -v.y;
     nlse[rb][2] = -v.z;
@@ -600,7 +648,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       [&](const StepState &st) __attribute__((always_inline)) {
         // wave-uniform base (scalar registers) plus the lane's offset
         float *const dst = pout + st.ctx;
-        if (lane < (st.meta & 255)) dst[lane] = colsum;
+        if (rg < a.n_rg && lane < (st.meta & 255)) dst[lane] = colsum;
       });
 }
 
@@ -988,25 +1036,35 @@ __global__ __launch_bounds__(256) void score_final(Tree t, const float *__restri
   block_final(t, i, A, rows_seen, fa.v_in, fa.u_in, fa.th0, fa.th1, fa.th2, fa.a_out, fa.s_out);
 }
 
-template <class T, int D>
-void launch_attn_nb(int NRB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
-  switch (NRB) {
-    case 1: hipLaunchKernelGGL((score_attn<T, D, 1>), grid, dim3(256), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((score_attn<T, D, 2>), grid, dim3(256), 0, stream, a); break;
-    default:
-      if constexpr (sizeof(T) == 2)
-        hipLaunchKernelGGL((score_attn<T, D, 4>), grid, dim3(256), 0, stream, a);
-      break;
+template <class T, int D, int NRB>
+void launch_attn_rg(int RGW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  switch (RGW) {
+    case 1: hipLaunchKernelGGL((score_attn<T, D, NRB, 1>), grid, dim3(256), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((score_attn<T, D, NRB, 2>), grid, dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL((score_attn<T, D, NRB, 4>), grid, dim3(256), 0, stream, a); break;
   }
 }
 
-void launch_attn(int dtype, int D, int NRB, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+// Fewer than the full 16 NRB rows fit in one row group: one group, no sharing.
+template <class T, int D>
+void launch_attn_nb(int NRB, int RGW, dim3 grid, hipStream_t stream, const ScoreArgs &a) {
+  constexpr int cap = sizeof(T) == 2 ? 4 : 2;
+  if (NRB < cap) {
+    if (NRB == 1) hipLaunchKernelGGL((score_attn<T, D, 1, 1>), grid, dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((score_attn<T, D, 2, 1>), grid, dim3(256), 0, stream, a);
+    return;
+  }
+  launch_attn_rg<T, D, cap>(RGW, grid, stream, a);
+}
+
+void launch_attn(int dtype, int D, int NRB, int RGW, dim3 grid, hipStream_t stream,
+                 const ScoreArgs &a) {
   if (dtype == ARBOR_BF16) {
-    if (D == 128) launch_attn_nb<__bf16, 128>(NRB, grid, stream, a);
-    else launch_attn_nb<__bf16, 64>(NRB, grid, stream, a);
+    if (D == 128) launch_attn_nb<__bf16, 128>(NRB, RGW, grid, stream, a);
+    else launch_attn_nb<__bf16, 64>(NRB, RGW, grid, stream, a);
   } else {
-    if (D == 128) launch_attn_nb<float, 128>(NRB, grid, stream, a);
-    else launch_attn_nb<float, 64>(NRB, grid, stream, a);
+    if (D == 128) launch_attn_nb<float, 128>(NRB, RGW, grid, stream, a);
+    else launch_attn_nb<float, 64>(NRB, RGW, grid, stream, a);
   }
 }
 
@@ -1094,17 +1152,24 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   a.ndep = ndep;
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
+    // one thread per node and per observer, in one workgroup (a small tree
+    // takes a smaller one, whose barriers are cheaper)
+    const int64_t need = std::max<int64_t>(t.V, n_obs);
+    const dim3 st((unsigned)std::min<int64_t>(1024, (need + kWave - 1) / kWave * kWave));
     if (t.V <= kSetupLds)
-      hipLaunchKernelGGL(score_setup<true>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
-                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+      hipLaunchKernelGGL(score_setup<true>, dim3(1), st, 0, stream, a, part_cap, pbase, fbase,
+                         tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
     else
-      hipLaunchKernelGGL(score_setup<false>, dim3(1), dim3(1024), 0, stream, a, part_cap, pbase,
-                         fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+      hipLaunchKernelGGL(score_setup<false>, dim3(1), st, 0, stream, a, part_cap, pbase, fbase,
+                         tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
     hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
-    const int n_planes = n_slice * pl.Hkv * a.n_rg;
+    // row groups of one workgroup, which share its key tiles (the same
+    // power of two as in the kernel's template)
+    const int RGW = a.n_rg >= 4 ? 4 : (a.n_rg >= 2 ? 2 : 1);
+    const int n_planes = n_slice * pl.Hkv * ((a.n_rg + RGW - 1) / RGW);
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     timing_begin(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
-    launch_attn(geom->dtype, geom->head_dim, NRB, grid, stream, a);
+    launch_attn(geom->dtype, geom->head_dim, NRB, RGW, grid, stream, a);
     timing_end(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
     // at most V credited blocks, and at most MAXD per observer

@@ -358,6 +358,34 @@ def test_score_random_trees(seed, self_window, dtype):
     assert np.array_equal(A.view(np.uint32), A2.view(np.uint32))
 
 
+# rows per (observer, slice layer, kv head) = G * W; a row group holds 64 rows
+# (bf16) or 32 (fp32), and a workgroup covers 2 or 4 groups that share its key
+# tiles: 3 and 5 groups leave empty groups in the last workgroup, and chains of
+# one to a few sub-pages give key splits with a step fewer than the others
+@pytest.mark.parametrize("seed,dtype,d,G,W", [(20, "bf16", 128, 4, 32),    # 2 groups
+                                              (21, "bf16", 128, 4, 40),    # 3 groups
+                                              (22, "bf16", 64, 8, 32),     # 4 groups
+                                              (23, "bf16", 128, 8, 36),    # 5 groups
+                                              (24, "f32", 64, 4, 20),      # 3 groups
+                                              (25, "f32", 128, 4, 40)])    # 5 groups
+def test_score_shared_key_tiles(seed, dtype, d, G, W):
+    st = rand_tree_state(seed, V=16, max_n=90, min_n=1, G=G, d=d, dtype=dtype, window=W)
+    kv = to_gpu(st)
+    ost = oracle_state(st)
+    p = dict(PARAMS, score_self_window=seed % 2, theta=(0.5, -1.0, 2.0))
+    A0 = (np.random.default_rng(seed).random(st["num_tokens"]) * 3).astype(np.float32)
+    r0 = np.arange(16, dtype=np.int64)
+    A, rows, a, s, sg = _gpu_score(st, kv, p, A0, r0)
+    Ao, ro, ao, so = _oracle_score(st, ost, p, A0, r0)
+    assert sg == L.OK
+    _close(A, Ao)
+    assert np.array_equal(rows, ro)
+    _close(a, ao)
+    _close(s, so)
+    A2, *_ = _gpu_score(st, kv, p, A0, r0)
+    assert np.array_equal(A.view(np.uint32), A2.view(np.uint32))
+
+
 def test_score_after_eviction():
     st = rand_tree_state(7, V=12, max_n=60, min_n=10, G=4, window=16)
     kv = to_gpu(st)
