@@ -53,6 +53,7 @@ ENTRY_KERNELS = {
     "arbor_allocate": ("allocate_", "allocate.hip"),
     "arbor_select": ("select_", "select.hip"),
     "arbor_compact": ("compact_", "compact.hip"),
+    "arbor_select_compact": ("select_plan", "compact.hip"),
     "arbor_tree_decode_attn": ("decode_", "decode.hip"),
     "arbor_rehydrate": ("rehyd_", "rehydrate.hip"),
     "arbor_uncertainty": ("uncert_", "uncertainty.hip"),
@@ -152,7 +153,10 @@ def summarize_traffic(fetch_csv: str, write_csv: str, title: str, command: str,
     for name in sorted(set(fk) | set(wk)):
         fkib = float(np.mean(fk.get(name, [0.0])))
         wkib = float(np.mean(wk.get(name, [0.0])))
-        src = next((s for pre, s in src_of.items() if name.startswith(pre)), None)
+        # the longest matching prefix ("select_plan" of arbor_select_compact
+        # lives in compact.hip, the other "select_" kernels in select.hip)
+        pres = sorted((pre for pre in src_of if name.startswith(pre)), key=len)
+        src = src_of[pres[-1]] if pres else None
         lines.append(json.dumps({
             "kernel": name, "fetch_kib": round(fkib, 3), "write_kib": round(wkib, 3),
             "hbm_read_bytes": round(fkib * ff * 1024), "hbm_write_bytes": round(wkib * wf * 1024),
