@@ -1068,10 +1068,9 @@ void launch_attn(int dtype, int D, int NRB, int RGW, dim3 grid, hipStream_t stre
   }
 }
 
-// 16-row blocks of a workgroup: enough for all the rows up to 64 (32 for fp32,
-// whose operands take four times the registers), a power of two.  Every wave
-// holds the Q of all the group's rows; 64 rows keep it within the registers
-// of two waves per SIMD.
+// 16-row blocks of a row group: enough for all the rows up to 64 (32 for fp32,
+// whose operands take four times the registers), a power of two.  A wave
+// holds the Q of its group's rows; 64 rows (bf16) keep three waves per SIMD.
 int row_blocks(int rows_total, int dtype) {
   const int cap = dtype == ARBOR_BF16 ? 4 : 2;
   int nrb = 1;
