@@ -386,6 +386,26 @@ def test_score_shared_key_tiles(seed, dtype, d, G, W):
     assert np.array_equal(A.view(np.uint32), A2.view(np.uint32))
 
 
+@pytest.mark.parametrize("dtype,d,G", [("bf16", 128, 4), ("bf16", 128, 8), ("f32", 64, 2)])
+def test_score_shared_key_tiles_long_chain(dtype, d, G):
+    """Chains of more than 64 steps per key split: the sub-page table is read
+    in windows of 64 steps, and the waves sharing the tiles meet at the end
+    of each window before the ring is reused."""
+    parent, n_full = [-1, 0, 1], [2500, 1700, 300]
+    st = synth.build_state(parent, n_full, layers=2, kv_heads=2, q_per_kv=G, head_dim=d,
+                           dtype=dtype, seed=31, shuffle_pages=True, page_size=16, window=32,
+                           active=[2], heavy_frac=0.01)
+    kv = to_gpu(st)
+    ost = oracle_state(st)
+    p = dict(PARAMS, score_self_window=1 if G == 8 else 0)
+    A, rows, a, s, sg = _gpu_score(st, kv, p)
+    Ao, ro, ao, so = _oracle_score(st, ost, p)
+    assert sg == L.OK
+    _close(A, Ao)
+    assert np.array_equal(rows, ro)
+    _close(s, so)
+
+
 def test_score_after_eviction():
     st = rand_tree_state(7, V=12, max_n=60, min_n=10, G=4, window=16)
     kv = to_gpu(st)
