@@ -11,7 +11,9 @@
 //   setup   one workgroup: validates the tree, walks every observer chain
 //           (one thread per observer) for the partial / table offsets (prefix
 //           sums over observers) and lists the blocks that receive credit;
-//   tables  one workgroup per observer: its 16-slot sub-page table;
+//   tables  one workgroup per observer: its 16-slot sub-page table (up to
+//           512 observers, in the setup's launch: each table workgroup walks
+//           the observer chains itself for its offset);
 //   attn    per (observer, slice layer, kv head, 1, 2 or 4 groups of up to
 //           64 rows), two passes over the same (row, key) pairs as MFMA tiles
 //           of 16 keys x 16 rows, one wave per (row group, key split), the
@@ -704,7 +706,7 @@ __device__ ObsChain walk_chain(const Tree &t, int j, int32_t *anc_out) {
 // IN_LDS (trees of up to kSetupLds nodes) is a template argument, so that the
 // tree's arrays are read with LDS or global instructions rather than flat ones.
 template <bool IN_LDS>
-__global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_cap,
+__device__ __forceinline__ void setup_body(const ScoreArgs &a, int64_t part_cap,
                                                     int64_t *__restrict__ pbase,
                                                     int64_t *__restrict__ fbase,
                                                     int64_t *__restrict__ tbase,
@@ -833,23 +835,32 @@ __global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_ca
   if (tid == 0) cred[0] = (s_err || !fits) ? 0 : (int32_t)crun;
 }
 
-// One workgroup per observer: its chain (root first, from the setup's walk)
-// and its sub-page table as 16-byte entries (plane row, slot, context offset,
-// valid slots | own << 8 | mask flags) that the streaming kernel reads into
-// registers.
-__global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
-  __shared__ ChainLds ch;
+template <bool IN_LDS>
+__global__ __launch_bounds__(1024) void score_setup(ScoreArgs a, int64_t part_cap,
+                                                    int64_t *__restrict__ pbase,
+                                                    int64_t *__restrict__ fbase,
+                                                    int64_t *__restrict__ tbase,
+                                                    int32_t *__restrict__ nsp,
+                                                    int32_t *__restrict__ ctxlen,
+                                                    int32_t *__restrict__ odepth,
+                                                    int32_t *__restrict__ anc,
+                                                    int32_t *__restrict__ flag,
+                                                    int32_t *__restrict__ nctx,
+                                                    int32_t *__restrict__ ndep,
+                                                    int32_t *__restrict__ cred) {
+  setup_body<IN_LDS>(a, part_cap, pbase, fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx,
+                     ndep, cred);
+}
+
+// The sub-page table of observer o at tab, as 16-byte entries (plane row,
+// slot, context offset, valid slots | own << 8 | mask flags) that the
+// streaming kernel reads into registers; ch holds o's chain (node, depth).
+__device__ __forceinline__ void table_body(const ScoreArgs &a, ChainLds &ch, int j, int4 *tab) {
   const Tree &t = a.t;
-  const int o = blockIdx.x;
   const int tid = threadIdx.x;
-  // (loaded together with the status word)
-  const int j = a.obs[o];
-  const int depth = a.odepth[o];
-  if (status_failed(a.status)) return;   // also set by the setup on any error
-  if (tid == 0) ch.depth = depth;
+  const int depth = ch.depth;
   if (tid <= depth) {
-    const int x = a.anc[(int64_t)o * MAXD + tid];
-    ch.node[tid] = x;
+    const int x = ch.node[tid];
     ch.c[tid] = t.n_kept[x];
     ch.po[tid] = t.page_off[x];
   }
@@ -868,7 +879,6 @@ __global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
   __syncthreads();
   const int n = ch.sp_off[depth + 1];
   fill_table(t, a.pl, ch, n);
-  int4 *tab = reinterpret_cast<int4 *>(a.part + a.tbase[o]);
   // the window rows see own positions up to u >= u_min: an own sub-page whose
   // last position is above u_min needs per-key masking in pass 0; in the
   // self-window mode, one whose last position reaches u_min needs it in pass 1
@@ -882,6 +892,93 @@ __global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
     tab[sp] = make_int4(e.row, e.slot, e.ctx,
                         e.nvalid | (own ? 1 << 8 : 0) | (m0 ? kMask0 : 0) | (m1 ? kMask1 : 0));
   }
+}
+
+// One workgroup per observer: its chain (root first, from the setup's walk)
+// and its sub-page table.
+__global__ __launch_bounds__(256) void score_tables(ScoreArgs a) {
+  __shared__ ChainLds ch;
+  const int o = blockIdx.x;
+  const int tid = threadIdx.x;
+  // (loaded together with the status word)
+  const int j = a.obs[o];
+  const int depth = a.odepth[o];
+  if (status_failed(a.status)) return;   // also set by the setup on any error
+  if (tid == 0) ch.depth = depth;
+  if (tid <= depth) ch.node[tid] = a.anc[(int64_t)o * MAXD + tid];
+  __syncthreads();
+  table_body(a, ch, j, reinterpret_cast<int4 *>(a.part + a.tbase[o]));
+}
+
+// Setup and tables in one launch (up to kPrepObs observers): workgroup 0 runs
+// the setup; workgroup 1 + o builds observer o's table without waiting for
+// it.  It walks every observer's chain itself (one thread per observer, the
+// setup's checks) for the sums that place the tables after the partials and
+// folded sums, and the prefix of the sub-page counts that places o's table:
+// the same integers the setup computes, so the offsets agree.  A malformed
+// chain or a workspace too small leaves o's table unwritten (the setup
+// reports the error, and no later kernel runs).
+constexpr int kPrepObs = 512;
+template <bool IN_LDS>
+__global__ __launch_bounds__(1024) void score_prep(ScoreArgs a, int64_t part_cap,
+                                                   int64_t *__restrict__ pbase,
+                                                   int64_t *__restrict__ fbase,
+                                                   int64_t *__restrict__ tbase,
+                                                   int32_t *__restrict__ nsp,
+                                                   int32_t *__restrict__ ctxlen,
+                                                   int32_t *__restrict__ odepth,
+                                                   int32_t *__restrict__ anc,
+                                                   int32_t *__restrict__ flag,
+                                                   int32_t *__restrict__ nctx,
+                                                   int32_t *__restrict__ ndep,
+                                                   int32_t *__restrict__ cred) {
+  if (blockIdx.x == 0) {
+    setup_body<IN_LDS>(a, part_cap, pbase, fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx,
+                       ndep, cred);
+    return;
+  }
+  __shared__ ChainLds ch;
+  __shared__ int64_t sm[17];
+  __shared__ int64_t s_pre;
+  __shared__ int s_bad;
+  const Tree &t = a.t;
+  const int o = (int)blockIdx.x - 1;
+  const int tid = threadIdx.x;
+  const int nt = blockDim.x;
+  const int j = a.obs[o];
+  if (status_failed(a.status)) return;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  const int slabs = a.S * a.pl.Hkv * a.n_rg;
+  int64_t run = 0, frun = 0, trun = 0;
+  for (int base = 0; base < a.n_obs; base += nt) {
+    const int oo = base + tid;
+    int64_t len = 0, subs = 0;
+    if (oo < a.n_obs) {
+      const int jj = a.obs[oo];
+      if (jj < 0 || jj >= t.V) {
+        s_bad = 1;
+      } else {
+        const ObsChain r = walk_chain(t, jj, oo == o ? ch.node : nullptr);
+        if (!r.ok) s_bad = 1;
+        len = r.len;
+        subs = r.subs;
+        if (oo == o) ch.depth = r.depth;
+      }
+    }
+    int64_t tot, ftot, ttot;
+    block_exclusive_scan<int64_t>(len * slabs, sm, &tot);
+    block_exclusive_scan<int64_t>(len, sm, &ftot);
+    const int64_t tx = block_exclusive_scan<int64_t>(subs, sm, &ttot);
+    if (oo == o) s_pre = trun + tx;
+    run += tot;
+    frun += ftot;
+    trun += ttot;
+  }
+  __syncthreads();
+  const int64_t tab0 = (run + frun + 3) & ~(int64_t)3;
+  if (s_bad || tab0 + 4 * trun > part_cap) return;
+  table_body(a, ch, j, reinterpret_cast<int4 *>(a.part + tab0 + 4 * s_pre));
 }
 
 // Fold the (slice layer, kv head, row group) slabs of every observer: one
@@ -1152,16 +1249,27 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   const FinalArgs fa{v_in, u_in, params->theta[0], params->theta[1], params->theta[2], a_out, s_out};
   if (n_obs > 0) {
     // one thread per node and per observer, in one workgroup (a small tree
-    // takes a smaller one, whose barriers are cheaper)
+    // takes a smaller one, whose barriers are cheaper); with few observers
+    // the tables are built in the same launch
     const int64_t need = std::max<int64_t>(t.V, n_obs);
-    const dim3 st((unsigned)std::min<int64_t>(1024, (need + kWave - 1) / kWave * kWave));
-    if (t.V <= kSetupLds)
-      hipLaunchKernelGGL(score_setup<true>, dim3(1), st, 0, stream, a, part_cap, pbase, fbase,
-                         tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
-    else
-      hipLaunchKernelGGL(score_setup<false>, dim3(1), st, 0, stream, a, part_cap, pbase, fbase,
-                         tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
-    hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
+    const int st = (int)std::min<int64_t>(1024, (need + kWave - 1) / kWave * kWave);
+    if (n_obs <= kPrepObs) {
+      const dim3 grid((unsigned)n_obs + 1), blk((unsigned)std::max(st, 256));
+      if (t.V <= kSetupLds)
+        hipLaunchKernelGGL(score_prep<true>, grid, blk, 0, stream, a, part_cap, pbase, fbase,
+                           tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+      else
+        hipLaunchKernelGGL(score_prep<false>, grid, blk, 0, stream, a, part_cap, pbase, fbase,
+                           tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+    } else {
+      if (t.V <= kSetupLds)
+        hipLaunchKernelGGL(score_setup<true>, dim3(1), dim3(st), 0, stream, a, part_cap, pbase,
+                           fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+      else
+        hipLaunchKernelGGL(score_setup<false>, dim3(1), dim3(st), 0, stream, a, part_cap, pbase,
+                           fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
+      hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
+    }
     // row groups of one workgroup, which share its key tiles (the same
     // power of two as in the kernel's template)
     const int RGW = a.n_rg >= 4 ? 4 : (a.n_rg >= 2 ? 2 : 1);

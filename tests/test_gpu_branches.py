@@ -170,6 +170,42 @@ def deep_tree():
     return st, kv, obs, leaves
 
 
+@pytest.mark.parametrize("V", [700, 2600])
+def test_score_more_observers_than_one_prep_launch(V):
+    """More than 512 observers: the setup and the sub-page tables run as two
+    launches (the setup walking the tree from LDS up to 2,048 nodes, from
+    global memory beyond)."""
+    parent, n_full = synth.random_tree(V, 12, 40 + V, min_tokens=1)
+    rng = np.random.default_rng(V)
+    obs = sorted(rng.choice(V, 600, replace=False).tolist())
+    st = synth.build_state(parent, n_full, layers=1, kv_heads=1, q_per_kv=1, head_dim=64,
+                           dtype="bf16", seed=V, shuffle_pages=True, page_size=16, window=4,
+                           observers=obs, active=[obs[-1]], host_store=False,
+                           decode_queries=False)
+    kv = to_gpu(st)
+    ost = oracle_state(st)
+    p = dict(PARAMS, theta=(0.5, -1.0, 2.0))
+    N = st["num_tokens"]
+    ws = workspace(kv, max_observers=len(obs), window=4, n_slice=len(st["slice_layers"]))
+    A = torch.zeros(N, device="cuda")
+    rows = torch.zeros(V, dtype=torch.int64, device="cuda")
+    a = torch.empty(V, device="cuda")
+    s = torch.empty(V, device="cuda")
+    stt = status()
+    check_rc(L.arbor_score(kv, st["observers"].cuda(), st["q_win"].cuda().contiguous(), 4,
+                           st["slice_layers"], st["v_sig"].cuda(), st["u_sig"].cuda(), A, rows,
+                           a, s, p, stt, ws))
+    torch.cuda.synchronize()
+    assert int(stt) == L.OK
+    Ao, ro, ao, so = O.score(ost, obs, np_float(st["q_win"]), 4, st["slice_layers"], 1,
+                             st["v_sig"].numpy(), st["u_sig"].numpy(), np.zeros(N, np.float32),
+                             np.zeros(V, np.int64), theta=p["theta"])
+    _close(A.cpu().numpy(), Ao)
+    assert np.array_equal(rows.cpu().numpy(), ro)
+    _close(a.cpu().numpy(), ao)
+    _close(s.cpu().numpy(), so)
+
+
 def test_deep_tree_score_sampled_observers(deep_tree):
     st, kv, obs, _ = deep_tree
     V, N = kv.num_nodes, kv.num_tokens
