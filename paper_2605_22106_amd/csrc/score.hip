@@ -252,10 +252,12 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   __shared__ int s_bad;
   // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
   // (slice layer, kv head, RGW row groups) planes p = x, x + 8, ...; it runs the
-  // observers from the deepest (longest chain) down, each over all its
-  // planes in turn -- the longest work starts first, so the grid ends on the
-  // shortest, and siblings, which share their whole ancestor chain, run
-  // together and read those keys from the XCD's L2
+  // observers in reverse list order, each over all its planes in turn.  For
+  // observers listed in id order of a tree numbered level by level (children
+  // after their parents) that is deepest first: the longest work starts
+  // first, so the grid ends on the shortest, and siblings, which share their
+  // whole ancestor chain, run together and read those keys from the XCD's L2
+  // (any other order is as correct, only slower)
   const int n_rgp = (a.n_rg + RGW - 1) / RGW;
   const int n_planes = a.S * a.pl.Hkv * n_rgp;
   const int xcd = (int)blockIdx.x % kXcds;
