@@ -419,7 +419,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
 #pragma unroll
         for (int k = 0; k < KS * NRB; ++k) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
         }
         post(prev);
         prev = cur;
