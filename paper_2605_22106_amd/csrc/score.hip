@@ -1019,15 +1019,26 @@ __device__ void block_final(const Tree &t, int i, const float *__restrict__ A,
                             const float *__restrict__ u_in, float th0, float th1, float th2,
                             float *__restrict__ a_out, float *__restrict__ s_out) {
   const int lane = lane_id();
+  // the block's fields and signals in one round trip, then its A eight loads
+  // at a time (added in the same order as one at a time)
   const int64_t tb = t.tok_off[i];
   const int n = t.n_full[i];
+  const int64_t rs = rows_seen[i];
+  const float vi = v_in[i], ui = u_in[i];
   double sum = 0.0;
-  for (int p = lane; p < n; p += kWave) sum += (double)A[tb + p];
+  int p = lane;
+  for (; p + 7 * kWave < n; p += 8 * kWave) {
+    float x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = A[tb + p + u * kWave];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sum += (double)x[u];
+  }
+  for (; p < n; p += kWave) sum += (double)A[tb + p];
   sum = wave_sum<double>(sum);
   if (lane == 0) {
-    const int64_t rs = rows_seen[i];
     const double av = rs > 0 ? sum / (double)rs : 0.0;
-    const double x = (double)th0 * (double)v_in[i] + (double)th1 * (double)u_in[i] + (double)th2 * av;
+    const double x = (double)th0 * (double)vi + (double)th1 * (double)ui + (double)th2 * av;
     double sv = 1.0 / (1.0 + exp(-x));
     sv = fmin(1.0, fmax(0.0, sv));
     a_out[i] = (float)av;
