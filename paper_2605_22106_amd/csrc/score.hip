@@ -1064,9 +1064,14 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
   __shared__ int s_wcnt[4];
   __shared__ double s_acc[4][64];
   // (loaded together with the status word; the list entry past its end is
-  // allocated, and unused then)
+  // allocated, and unused then; so are the first 256 observers' depths and
+  // window sizes, which do not depend on the block)
   const int ncred = cred[0];
   const int i = cred[1 + blockIdx.x];
+  const bool o0 = (int)threadIdx.x < a.n_obs;
+  const int od0 = o0 ? a.odepth[threadIdx.x] : -1;
+  const int64_t fb0 = o0 ? fbase[threadIdx.x] : 0;
+  const int wn0 = o0 ? min(a.W, a.t.n_full[a.obs[threadIdx.x]]) : 0;
   if (status_failed(a.status)) return;
   if ((int)blockIdx.x >= ncred) return;
   const Tree &t = a.t;
@@ -1086,7 +1091,7 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
     const int o = ob + threadIdx.x;
     bool hit = false;
     if (o < a.n_obs) {
-      const int od = a.odepth[o];
+      const int od = ob == 0 ? od0 : a.odepth[o];
       hit = (od > di && a.anc[(int64_t)o * MAXD + di] == i) || (a.self_window && a.obs[o] == i);
     }
     const uint64_t bm = ballot(hit);
@@ -1096,8 +1101,10 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
     for (int w = 0; w < wave; ++w) before += s_wcnt[w];
     const int nh = s_wcnt[0] + s_wcnt[1] + s_wcnt[2] + s_wcnt[3];
     if (hit) {
-      hbase[before + rank_below(bm, lane)] = fbase[o] + ctxoff;
-      if (blockIdx.y == 0) rows_add += (int64_t)a.S * pl.Hkv * pl.G * min(a.W, t.n_full[a.obs[o]]);
+      hbase[before + rank_below(bm, lane)] = (ob == 0 ? fb0 : fbase[o]) + ctxoff;
+      if (blockIdx.y == 0)
+        rows_add += (int64_t)a.S * pl.Hkv * pl.G *
+                    (ob == 0 ? wn0 : min(a.W, t.n_full[a.obs[o]]));
     }
     __syncthreads();
     if (nh > 0) {
