@@ -739,18 +739,37 @@ __device__ __forceinline__ void setup_body(const ScoreArgs &a, int64_t part_cap,
   }
   if (tid == 0) s_err = 0;
   constexpr bool in_lds = IN_LDS;
-  for (int i = tid; i < t.V; i += nt) {
-    const int par = i == tid ? par0 : t.parent[i];
-    const int nf = i == tid ? nf0 : t.n_full[i];
-    const int c = i == tid ? c0 : t.n_kept[i];
-    const bool ok = (i == 0) ? par == -1 : (par >= 0 && par < i);
-    if (!ok || c < 0 || c > nf) atomicOr(&s_err, 1);
-    if (in_lds) {
-      s_par[i] = par;
-      s_full[i] = nf;
-      s_kept[i] = c;
+  // trees beyond LDS take eight of the thread's nodes at a time: their loads
+  // in flight together (the flag stores of one node would otherwise hold up
+  // the next node's loads, which share the counter of outstanding memory
+  // operations); a tree in LDS takes at most two nodes per thread
+  constexpr int kGrp = IN_LDS ? 1 : 8;
+  for (int ib = tid; ib < t.V; ib += kGrp * nt) {
+    int par[kGrp], nf[kGrp], c[kGrp];
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const int i = ib + u * nt;
+      par[u] = nf[u] = c[u] = 0;
+      if (i < t.V) {
+        par[u] = i == tid ? par0 : t.parent[i];
+        nf[u] = i == tid ? nf0 : t.n_full[i];
+        c[u] = i == tid ? c0 : t.n_kept[i];
+      }
     }
-    flag[i] = 0;
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      const int i = ib + u * nt;
+      if (i < t.V) {
+        const bool ok = (i == 0) ? par[u] == -1 : (par[u] >= 0 && par[u] < i);
+        if (!ok || c[u] < 0 || c[u] > nf[u]) atomicOr(&s_err, 1);
+        if (in_lds) {
+          s_par[i] = par[u];
+          s_full[i] = nf[u];
+          s_kept[i] = c[u];
+        }
+        flag[i] = 0;
+      }
+    }
   }
   if (in_lds) {
     t.parent = s_par;
@@ -826,13 +845,37 @@ __device__ __forceinline__ void setup_body(const ScoreArgs &a, int64_t part_cap,
   }
   // the credited blocks in ascending id
   int64_t crun = 0;
-  for (int base = 0; base < t.V; base += nt) {
-    const int i = base + tid;
-    const int f = i < t.V ? flag[i] : 0;
-    int64_t ctot;
-    const int64_t cx = block_exclusive_scan<int64_t>(f, sm, &ctot);
-    if (f) cred[1 + crun + cx] = i;
-    crun += ctot;
+  if constexpr (IN_LDS) {
+    for (int base = 0; base < t.V; base += nt) {
+      const int i = base + tid;
+      const int f = i < t.V ? flag[i] : 0;
+      int64_t ctot;
+      const int64_t cx = block_exclusive_scan<int64_t>(f, sm, &ctot);
+      if (f) cred[1 + crun + cx] = i;
+      crun += ctot;
+    }
+  } else {
+    // each thread takes a run of consecutive blocks (their flags loaded eight
+    // at a time), and one scan places the runs
+    const int per = (t.V + nt - 1) / nt;
+    const int r0 = min(t.V, tid * per), r1 = min(t.V, r0 + per);
+    int64_t mine = 0;
+    for (int ib = r0; ib < r1; ib += kGrp) {
+      int f[kGrp];
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u) f[u] = ib + u < r1 ? flag[ib + u] : 0;
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u) mine += f[u];
+    }
+    int64_t off = block_exclusive_scan<int64_t>(mine, sm, &crun);
+    for (int ib = r0; ib < r1 && mine > 0; ib += kGrp) {
+      int f[kGrp];
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u) f[u] = ib + u < r1 ? flag[ib + u] : 0;
+#pragma unroll
+      for (int u = 0; u < kGrp; ++u)
+        if (f[u]) cred[1 + off++] = ib + u;
+    }
   }
   if (tid == 0) cred[0] = (s_err || !fits) ? 0 : (int32_t)crun;
 }
