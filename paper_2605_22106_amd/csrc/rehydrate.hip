@@ -23,31 +23,60 @@ __global__ __launch_bounds__(1024) void rehyd_plan(Tree t, Pool pl, const uint8_
                                                    int32_t *__restrict__ pop_base,
                                                    int32_t *__restrict__ todo,
                                                    int32_t *__restrict__ meta, int32_t *status) {
-  __shared__ int64_t sm[17];
+  __shared__ int64_t sm[2 * 16];
   if (status_failed(status)) {
     if (threadIdx.x == 0) meta[0] = 0;
     return;
   }
   const int P = pl.P;
-  int64_t run_pages = 0, run_nodes = 0;
-  for (int base = 0; base < t.V; base += blockDim.x) {
-    const int i = base + threadIdx.x;
-    bool rh = false;
-    int64_t need = 0;
-    if (i < t.V && on_path[i]) {
-      const int n = t.n_full[i], c = t.n_kept[i];
-      rh = c < n;
-      need = rh ? (n + P - 1) / P - (c + P - 1) / P : 0;
+  // each thread takes a run of consecutive blocks (their path flags loaded
+  // eight at a time; only Path* blocks load their sizes), and one scan
+  // places the runs, so the blocks are listed in ascending id
+  constexpr int kGrp = 8;
+  const int nt = blockDim.x;
+  const int per = (t.V + nt - 1) / nt;
+  const int r0 = min(t.V, (int)threadIdx.x * per), r1 = min(t.V, r0 + per);
+  auto need_of = [&](int i) -> int64_t {
+    const int n = t.n_full[i], c = t.n_kept[i];
+    return c < n ? (int64_t)((n + P - 1) / P - (c + P - 1) / P) : -1;   // -1: nothing to restore
+  };
+  int64_t my_pages = 0, my_nodes = 0;
+  for (int ib = r0; ib < r1; ib += kGrp) {
+    uint8_t f[kGrp];
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) f[u] = ib + u < r1 ? on_path[ib + u] : 0;
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      if (f[u]) {
+        const int64_t nd = need_of(ib + u);
+        if (nd >= 0) {
+          my_pages += nd;
+          ++my_nodes;
+        }
+      }
     }
-    int64_t tp, tn;
-    const int64_t ep = block_exclusive_scan<int64_t>(need, sm, &tp);
-    const int64_t en = block_exclusive_scan<int64_t>(rh ? 1 : 0, sm, &tn);
-    if (rh) {
-      pop_base[i] = (int32_t)(run_pages + ep);
-      todo[run_nodes + en] = i;
+  }
+  const int64_t v[2] = {my_pages, my_nodes};
+  int64_t ex[2], tot[2];
+  block_exclusive_scan_n<2>(v, ex, tot, sm);
+  const int64_t run_pages = tot[0], run_nodes = tot[1];
+  int64_t op = ex[0], on = ex[1];
+  for (int ib = r0; ib < r1 && my_nodes > 0; ib += kGrp) {
+    uint8_t f[kGrp];
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) f[u] = ib + u < r1 ? on_path[ib + u] : 0;
+#pragma unroll
+    for (int u = 0; u < kGrp; ++u) {
+      if (f[u]) {
+        const int64_t nd = need_of(ib + u);
+        if (nd >= 0) {
+          pop_base[ib + u] = (int32_t)op;
+          todo[on] = ib + u;
+          op += nd;
+          ++on;
+        }
+      }
     }
-    run_pages += tp;
-    run_nodes += tn;
   }
   if (threadIdx.x == 0) {
     const int top = *pl.free_top;
