@@ -19,8 +19,9 @@
 //           of 16 keys x 16 rows, one wave per (row group, key split), the
 //           waves of a row group taking alternate 16-key sub-pages:
 //           C = K Q^T for the row log-sum-exp, then C = Q K^T for per-key
-//           sums of exp2(z - lse) -> one partial per credited context key;
-//   fold    per observer: sum its (slice layer, kv head, row group) partials;
+//           sums of exp2(z - lse) -> one partial per credited context key
+//           and workgroup (its row groups added in order);
+//   fold    per observer: sum its (slice layer, kv head, workgroup) partials;
 //   reduce  per credited block i and 64-slot chunk: sum the folded partials of
 //           every observer below i in observer order (fp64) into A, rows_seen;
 //   final   a_i = sum_p A_i(p) / rows_seen_i, s_i = clip(sigmoid(theta.phi)).
@@ -47,6 +48,7 @@ struct ScoreArgs {
   int S;
   int slice[8];
   int n_rg;
+  int n_slab;       // partial slabs per (slice layer, kv head): one per workgroup's row groups
   float sl2;        // softmax scale * log2(e)
   int self_window;
   float *part;      // partial column sums
@@ -222,12 +224,14 @@ __device__ __forceinline__ float piece_op<float>(const uint4 &p, int c) {
 // RGW waves of a key split work on the same sub-page at each step: each loads
 // a part of it into their shared ring of LDS slots and they meet at a barrier
 // before reading it, so a key tile moves from L2 to LDS once for RGW row
-// groups.  A key's sum over a row group never leaves its wave.
+// groups.  A key's sum over a row group never leaves its wave; the RGW sums
+// of a key meet in LDS and are stored as one partial.
 //   pass 0  C = K Q^T: each lane keeps a running max / sum of one row over its
 //           keys; lanes, then the key splits, are merged into the row's
 //           log2-sum-exp;
 //   pass 1  C = Q K^T: per key, the sum over the group's rows of
-//           exp2(z - lse), stored as the row group's partial for that key.
+//           exp2(z - lse); the workgroup's partial for that key is the sum
+//           of its row groups' values, in row-group order.
 // Keys reach the ring by direct global->LDS loads in which each 16-lane group
 // reads one whole 256-byte key row (coalesced).  The 16-byte pieces of key r
 // are stored XOR-permuted by r, so the sixteen lanes of an MFMA operand read
@@ -249,6 +253,9 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   __shared__ Buf b0[KSW], b1[KSW], b2[KSW];
   __shared__ float2 s_ml[KSW][RGW * ROWS];
   __shared__ __attribute__((aligned(16))) float s_lse[RGW * ROWS];
+  // pass 1: the key sums of the last four steps, per key split, key and row
+  // group (used when RGW > 1)
+  __shared__ __attribute__((aligned(16))) float s_cs[KSW][4][16 * RGW];
   __shared__ int s_bad;
   // XCD-aware order: workgroup n runs on XCD n % 8, so XCD x takes the
   // (slice layer, kv head, RGW row groups) planes p = x, x + 8, ...; it runs the
@@ -361,7 +368,9 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   //   mm(kp)     the MFMAs of sub-page i, interleaved in one straight-line
   //   hot(prev)  block with the VALU work of sub-page i - 1, so the matrix
   //              core and the VALU work side by side within the wave;
-  //   post(prev) rare corrections after the fact, and stores.
+  //   post(prev) rare corrections after the fact, and stores;
+  // flush() runs once a window's last barrier has passed (empty unless
+  // results are combined across the waves of a key split).
   // The table entries of a window of up to 64 steps sit in registers (lane L
   // holds step L) and are read with readlane, so the loop has no scalar loads.
   // Every wave of the workgroup runs the same steps (those of key split 0):
@@ -377,7 +386,8 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   auto tile_sync = [&]() __attribute__((always_inline)) {
     if constexpr (RGW > 1) asm volatile("s_barrier" ::: "memory");
   };
-  auto run = [&](int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post)
+  auto run = [&](int n_sp, auto &&mm, auto &&fix, auto &&hot, auto &&post,
+                 auto &&flush)
                  __attribute__((always_inline)) {
     const int cnt = (n_sp + KSW - 1) / KSW;
     for (int base = 0; base < cnt; base += 64) {
@@ -421,7 +431,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
         }
-        post(prev);
+        post(prev, false);
         prev = cur;
       };
       int i = 1;
@@ -452,11 +462,14 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
       }
       fix(prev);
       hot(prev);
-      post(prev);
+      post(prev, true);
       // drain (the clamped reloads past the end), and let every wave finish
-      // reading, before the ring is reused
+      // reading, before the ring is reused; the LDS writes of the last steps
+      // complete before the barrier, so flush() sees them
       wait_vm<0>();
+      if constexpr (RGW > 1) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       tile_sync();
+      flush();
     }
   };
 
@@ -536,7 +549,7 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
           grow |= !(lt[rb] <= kGrow);          // also true for +inf
         }
       },
-      [&](const StepState &st) __attribute__((always_inline)) {
+      [&](const StepState &st, bool) __attribute__((always_inline)) {
         if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
           for (int rb = 0; rb < NRB; ++rb) {
@@ -558,7 +571,8 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
 #pragma unroll
           for (int rb = 0; rb < NRB; ++rb) l[rb] += lt[rb];
         }
-      });
+      },
+      []() {});
   // merge the four lane groups (log2 units), then the four waves, in order
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
@@ -608,8 +622,35 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
   }
 
   // ---- pass 1: credited column sums ----
-  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_rg + rg) * a.ctxlen[o];
+  // With RGW row groups per workgroup, the waves of a key split add their sums
+  // of a key into one slab: each wave writes its sums of step m into a ring of
+  // four LDS slots, and two steps later (after two barriers, by which every
+  // wave's write has completed) the wave rgw = m mod RGW adds the RGW values
+  // in row-group order and stores them; a window's last three steps are
+  // stored after its final barrier.
+  float *pout = a.part + a.pbase[o] + (int64_t)(slg * a.n_slab + rg / RGW) * a.ctxlen[o];
   float colsum = 0.f;
+  int m = 0;                            // step of the window (stores pending)
+  int ctx1 = 0, ctx2 = 0, ctx3 = 0;     // context offsets of steps m-1, m-2, m-3
+  int nv1 = 0, nv2 = 0, nv3 = 0;        // and their valid slots
+  auto load_sums = [&](int step, float (&v)[RGW]) __attribute__((always_inline)) {
+    const float *src = &s_cs[ksw][step & 3][(lane & 15) * RGW];
+    if constexpr (RGW == 4) {
+      const float4 x = *reinterpret_cast<const float4 *>(src);
+      v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    } else if constexpr (RGW == 2) {
+      const float2 x = *reinterpret_cast<const float2 *>(src);
+      v[0] = x.x; v[1] = x.y;
+    } else {
+      v[0] = src[0];
+    }
+  };
+  auto store_sums = [&](const float (&v)[RGW], int ctx, int nv) __attribute__((always_inline)) {
+    float x = v[0];
+#pragma unroll
+    for (int u = 1; u < RGW; ++u) x += v[u];
+    if (lane < nv) pout[ctx + lane] = x;
+  };
   run(a.nsp[2 * o + 1],
       [&](const uint4 (&kp)[RQ], int slot, int meta, int ctx) __attribute__((always_inline)) {
         StepState st;
@@ -649,10 +690,45 @@ __global__ __launch_bounds__(256, 3) void score_attn(ScoreArgs a) {
         colsum = group_sum(tree_sum(pz));
         asm volatile("" : "+v"(colsum));
       },
-      [&](const StepState &st) __attribute__((always_inline)) {
-        // wave-uniform base (scalar registers) plus the lane's offset
-        float *const dst = pout + st.ctx;
-        if (rg < a.n_rg && lane < (st.meta & 255)) dst[lane] = colsum;
+      [&](const StepState &st, bool tail) __attribute__((always_inline)) {
+        if constexpr (RGW == 1) {
+          // wave-uniform base (scalar registers) plus the lane's offset
+          float *const dst = pout + st.ctx;
+          if (rg < a.n_rg && lane < (st.meta & 255)) dst[lane] = colsum;
+        } else {
+          if (lane < 16) s_cs[ksw][m & 3][lane * RGW + rgw] = colsum;
+          if (!tail && m >= 2 && (m - 2) % RGW == rgw) {
+            // (written before the barrier this step passed)
+            float v[RGW];
+            load_sums(m - 2, v);
+            store_sums(v, ctx2, nv2);
+          }
+          ctx3 = ctx2;
+          ctx2 = ctx1;
+          ctx1 = st.ctx;
+          nv3 = nv2;
+          nv2 = nv1;
+          nv1 = st.meta & 255;
+          ++m;
+        }
+      },
+      [&]() __attribute__((always_inline)) {
+        if constexpr (RGW > 1) {
+          float v[RGW];
+          if (m >= 3 && (m - 3) % RGW == rgw) {
+            load_sums(m - 3, v);
+            store_sums(v, ctx3, nv3);
+          }
+          if (m >= 2 && (m - 2) % RGW == rgw) {
+            load_sums(m - 2, v);
+            store_sums(v, ctx2, nv2);
+          }
+          if (m >= 1 && (m - 1) % RGW == rgw) {
+            load_sums(m - 1, v);
+            store_sums(v, ctx1, nv1);
+          }
+          m = 0;
+        }
       });
 }
 
@@ -777,7 +853,7 @@ __device__ __forceinline__ void setup_body(const ScoreArgs &a, int64_t part_cap,
     t.n_kept = s_kept;
   }
   __syncthreads();
-  const int slabs = a.S * a.pl.Hkv * a.n_rg;
+  const int slabs = a.S * a.pl.Hkv * a.n_slab;
   int64_t run = 0, frun = 0, trun = 0;
   for (int base = 0; base < a.n_obs; base += nt) {
     const int o = base + tid;
@@ -994,7 +1070,7 @@ __global__ __launch_bounds__(1024) void score_prep(ScoreArgs a, int64_t part_cap
   if (status_failed(a.status)) return;
   if (tid == 0) s_bad = 0;
   __syncthreads();
-  const int slabs = a.S * a.pl.Hkv * a.n_rg;
+  const int slabs = a.S * a.pl.Hkv * a.n_slab;
   int64_t run = 0, frun = 0, trun = 0;
   for (int base = 0; base < a.n_obs; base += nt) {
     const int oo = base + tid;
@@ -1026,7 +1102,7 @@ __global__ __launch_bounds__(1024) void score_prep(ScoreArgs a, int64_t part_cap
   table_body(a, ch, j, reinterpret_cast<int4 *>(a.part + tab0 + 4 * s_pre));
 }
 
-// Fold the (slice layer, kv head, row group) slabs of every observer: one
+// Fold the (slice layer, kv head, workgroup) slabs of every observer: one
 // column sum per (observer, credited context key), summed in slab order.
 __global__ __launch_bounds__(256) void score_fold(ScoreArgs a, const int64_t *__restrict__ fbase) {
   const int o = blockIdx.x;
@@ -1037,7 +1113,7 @@ __global__ __launch_bounds__(256) void score_fold(ScoreArgs a, const int64_t *__
   if (status_failed(a.status)) return;
   const int own_c = a.t.n_kept[jo];
   const int credited = a.self_window ? len : len - own_c;
-  const int nslab = a.S * a.pl.Hkv * a.n_rg;
+  const int nslab = a.S * a.pl.Hkv * a.n_slab;
   const float *src = a.part + pb;
   float *dst = a.part + fb;
   for (int x = blockIdx.y * blockDim.x + threadIdx.x; x < credited; x += gridDim.y * blockDim.x) {
@@ -1231,6 +1307,10 @@ void launch_attn(int dtype, int D, int NRB, int RGW, dim3 grid, hipStream_t stre
 // 16-row blocks of a row group: enough for all the rows up to 64 (32 for fp32,
 // whose operands take four times the registers), a power of two.  A wave
 // holds the Q of its group's rows; 64 rows (bf16) keep three waves per SIMD.
+// Row groups per workgroup: they share its key tiles and one partial slab (a
+// power of two, as in the kernel's template).
+int rg_per_wg(int n_rg) { return n_rg >= 4 ? 4 : (n_rg >= 2 ? 2 : 1); }
+
 int row_blocks(int rows_total, int dtype) {
   const int cap = dtype == ARBOR_BF16 ? 4 : 2;
   int nrb = 1;
@@ -1244,8 +1324,9 @@ size_t score_workspace(const arbor_geom_t *g, const arbor_sizes_t *sz) {
   const int rows_total = g->q_per_kv * sz->window;
   const int NRB = row_blocks(rows_total, g->dtype);
   const int n_rg = (rows_total + 16 * NRB - 1) / (16 * NRB);
+  const int RGW = rg_per_wg(n_rg);
   const size_t nobs = (size_t)(sz->max_observers > 0 ? sz->max_observers : 0);
-  const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * n_rg;
+  const size_t slabs = (size_t)sz->n_slice * g->num_kv_heads * ((n_rg + RGW - 1) / RGW);
   size_t b = 0;
   // offsets, counts, chains, credited-block flags and list (each carve
   // rounds up to 256 B)
@@ -1279,6 +1360,8 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
   const int rows_total = pl.G * window;
   const int NRB = row_blocks(rows_total, geom->dtype);
   a.n_rg = (rows_total + 16 * NRB - 1) / (16 * NRB);
+  const int RGW = rg_per_wg(a.n_rg);
+  a.n_slab = (a.n_rg + RGW - 1) / RGW;
   const float scale = params->softmax_scale > 0.f ? params->softmax_scale
                                                   : 1.0f / sqrtf((float)geom->head_dim);
   a.sl2 = scale * kLog2e;
@@ -1333,10 +1416,7 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
                            fbase, tbase, nsp, ctxlen, odepth, anc, flag, nctx, ndep, cred);
       hipLaunchKernelGGL(score_tables, dim3(n_obs), dim3(256), 0, stream, a);
     }
-    // row groups of one workgroup, which share its key tiles (the same
-    // power of two as in the kernel's template)
-    const int RGW = a.n_rg >= 4 ? 4 : (a.n_rg >= 2 ? 2 : 1);
-    const int n_planes = n_slice * pl.Hkv * ((a.n_rg + RGW - 1) / RGW);
+    const int n_planes = n_slice * pl.Hkv * a.n_slab;
     const dim3 grid((unsigned)(((n_planes + kXcds - 1) / kXcds) * n_obs * kXcds));
     timing_begin(geom, ARBOR_KERNEL_SCORE_ATTN, stream);
     launch_attn(geom->dtype, geom->head_dim, NRB, RGW, grid, stream, a);
