@@ -1196,6 +1196,9 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
   const Tree &t = a.t;
   const Pool &pl = a.pl;
   const int c = t.n_kept[i];
+  // chunk splits past the block's last chunk have nothing to add (split 0
+  // still counts the rows)
+  if (blockIdx.y > 0 && (int)blockIdx.y * 64 >= c) return;
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const float *fold = a.part;
@@ -1231,7 +1234,15 @@ __global__ __launch_bounds__(256) void score_reduce(ScoreArgs a, const int64_t *
         const int s = chk * 64 + lane;
         double acc = 0.0;
         if (s < c) {
+          // (sixteen, then four loads in flight, added one by one in order)
           int h = wave;
+          for (; h + 60 < nh; h += 64) {
+            float f[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) f[u] = fold[hbase[h + 4 * u] + s];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) acc += (double)f[u];
+          }
           for (; h + 12 < nh; h += 16) {
             const float f0 = fold[hbase[h] + s];
             const float f1 = fold[hbase[h + 4] + s];
@@ -1424,8 +1435,11 @@ int launch_score(const arbor_geom_t *geom, const arbor_tree_t *tree, const arbor
     hipLaunchKernelGGL(score_fold, dim3(n_obs, 8), dim3(256), 0, stream, a, fbase);
     // at most V credited blocks, and at most MAXD per observer
     const int64_t max_cred = std::min<int64_t>(t.V, (int64_t)n_obs * MAXD);
-    hipLaunchKernelGGL(score_reduce, dim3((unsigned)max_cred, 16), dim3(256), 0, stream, a, fbase,
-                       cred, A, rows_seen);
+    // 64-slot chunk splits per block: 64 (one chunk each up to 4,096 kept
+    // slots) while the grid stays small, else 16
+    const unsigned ysplit = max_cred <= 512 ? 64u : 16u;
+    hipLaunchKernelGGL(score_reduce, dim3((unsigned)max_cred, ysplit), dim3(256), 0, stream, a,
+                       fbase, cred, A, rows_seen);
   }
   hipLaunchKernelGGL(score_final, dim3((t.V + 3) / 4), dim3(256), 0, stream, t, A, rows_seen, fa,
                      status);
